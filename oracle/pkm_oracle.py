@@ -1,0 +1,281 @@
+"""Plain fp64 CPU oracle for the product-key memory hot path.
+
+TEST INFRASTRUCTURE ONLY.  This module is the checker, not the product:
+only the test suite, the smoke check and the benchmark's CPU-baseline leg
+may import it.  It shares no code with the HIP library and never imports
+it.  It is deliberately slow and literal: per-token Python loops over
+NumPy float64 arrays, one library primitive per step (a dot product, a
+lexicographic sort, an exponential), no blocking, no fusion, no pruning.
+
+Paper: "Memory Layers at Scale" (arXiv 2412.09764).
+
+  Sec. 3, Eq. (1)              I = SelectTopkIndices(K q),
+                               s = Softmax(K_I q),  y = s V_I,
+                               each token independently.
+  Sec. 3.1.1 (Product-key lookup)
+                               K1, K2 in R^{sqrt(N) x n/2}; the full key set
+                               (never instantiated) is their product; split
+                               q into q1, q2; top-k per half; the result is
+                               the best k of the k x k sums s1[i1] + s2[i2].
+  Sec. 3.1.4 (Performance and stability improvements)
+                               the weighted sum is an EmbeddingBag; its
+                               backward propagates several output gradients
+                               into the same value-gradient row.
+
+Readings where the paper is silent (each is also listed in the design doc):
+  * heads: H independent (query, sub-key pair) per token, one shared value
+    table, per-head top-k and softmax, one bag of H*k rows summed;
+  * composed index i = i1 * S + i2, with q1 = q[:n/2] scored against
+    sub-key half 0, so full key row i is [K1[i // S]; K2[i % S]];
+  * "argmax over I1 x I2" means the top k of the k*k sums;
+  * order: score descending, index ascending (lower index wins a tie), at
+    both levels; outputs are in that rank order;
+  * raw dot-product scores: no scale, no temperature, no bias;
+  * softmax over the k selected scores of one (token, head);
+  * value gradients accumulate (+=) into the caller's table, because one
+    value pool is shared by several memory layers (Sec. 3.1.3).
+
+Function pins (tests under tests/test_oracle_*.py):
+  search           brute force over the instantiated full key set; all-equal
+                   sub-keys; k = 1 argmax; hand-worked golden fixture
+  softmax          closed form for two entries; sum/positivity/order/shift
+  bag_forward      torch embedding_bag (fp64, CPU); dense A @ V; one-hot rows
+  bag_backward     torch autograd (fp64, CPU); central finite differences;
+                   dense A.T @ dy; sum of score gradients is zero
+  invert_index     multiset and ordering invariants
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "rank_order",
+    "order_desc",
+    "topk_desc",
+    "half_scores",
+    "search",
+    "brute_force_search",
+    "softmax",
+    "bag_forward",
+    "bag_backward",
+    "bag_backward_rows",
+    "invert_index",
+]
+
+
+def _f64(a) -> np.ndarray:
+    """Exact widening of stored fp32 / bf16-in-fp32 values to fp64."""
+    return np.asarray(a, dtype=np.float64)
+
+
+def rank_order(scores: np.ndarray, ids: np.ndarray) -> np.ndarray:
+    """Positions sorted by (score descending, id ascending).
+
+    The tie rule (lower index first) is the reading taken for a point the
+    paper leaves open; it makes every selection unique.
+    """
+    scores = np.asarray(scores, dtype=np.float64)
+    # lexsort sorts by the last key first: primary -score, secondary id.
+    return np.lexsort((np.asarray(ids), -scores))
+
+
+def order_desc(scores: np.ndarray) -> np.ndarray:
+    """Positions of `scores` sorted by (score descending, position ascending)."""
+    return rank_order(scores, np.arange(np.asarray(scores).shape[0]))
+
+
+def topk_desc(scores: np.ndarray, k: int) -> np.ndarray:
+    """First k positions of order_desc(scores) (Sec. 3, Eq. (1): top-k)."""
+    return order_desc(scores)[:k]
+
+
+def half_scores(q_half: np.ndarray, subkeys_half: np.ndarray) -> np.ndarray:
+    """Scores of one query half against one sub-key table (Sec. 3.1.1).
+
+    q_half: [d]; subkeys_half: [S, d].  Returns [S] = subkeys_half @ q_half.
+    """
+    return _f64(subkeys_half) @ _f64(q_half)
+
+
+def softmax(z: np.ndarray) -> np.ndarray:
+    """Softmax over the selected scores (Sec. 3, Eq. (1)), max-subtracted."""
+    z = _f64(z)
+    e = np.exp(z - z.max())
+    return e / e.sum()
+
+
+def search(q: np.ndarray, subkeys: np.ndarray, k: int) -> dict:
+    """Multi-head product-key search (Sec. 3.1.1) followed by softmax (Eq. (1)).
+
+    q:       [T, H, n] query per token and head, n even, d = n / 2.
+    subkeys: [H, 2, S, d]; subkeys[h, 0] is K1 (paired with q[..., :d]),
+             subkeys[h, 1] is K2 (paired with q[..., d:]).
+    k:       1 <= k <= S.
+
+    Returns a dict of
+      idx        [T, H, k] int64   composed index i1 * S + i2, rank order
+      score      [T, H, k] fp64    s1[i1] + s2[i2] = full-key score K_I q
+      w          [T, H, k] fp64    softmax of `score` over k
+      half_idx   [T, H, 2, k] int64  per-half top-k, rank order
+      half_score [T, H, 2, k] fp64
+    """
+    q = _f64(q)
+    K = _f64(subkeys)
+    T, H, n = q.shape
+    assert n % 2 == 0, "query dim must be even"
+    d = n // 2
+    assert K.shape[0] == H and K.shape[1] == 2 and K.shape[3] == d
+    S = K.shape[2]
+    assert 1 <= k <= S
+    assert np.all(np.isfinite(q)) and np.all(np.isfinite(K))
+
+    idx = np.zeros((T, H, k), dtype=np.int64)
+    score = np.zeros((T, H, k))
+    w = np.zeros((T, H, k))
+    half_idx = np.zeros((T, H, 2, k), dtype=np.int64)
+    half_score = np.zeros((T, H, 2, k))
+    for t in range(T):
+        for h in range(H):
+            # Split the query into its two halves.
+            q1 = q[t, h, :d]
+            q2 = q[t, h, d:]
+            # Score each half against its own sqrt(N) sub-keys.
+            s1 = half_scores(q1, K[h, 0])
+            s2 = half_scores(q2, K[h, 1])
+            # Top-k of each half.
+            I1 = topk_desc(s1, k)
+            I2 = topk_desc(s2, k)
+            half_idx[t, h, 0] = I1
+            half_idx[t, h, 1] = I2
+            half_score[t, h, 0] = s1[I1]
+            half_score[t, h, 1] = s2[I2]
+            # All k*k combinations: summed score and composed index.
+            cand_score = (s1[I1][:, None] + s2[I2][None, :]).ravel()
+            cand_idx = (I1[:, None] * S + I2[None, :]).ravel()
+            # Best k by (score desc, composed index asc).
+            order = rank_order(cand_score, cand_idx)[:k]
+            idx[t, h] = cand_idx[order]
+            score[t, h] = cand_score[order]
+            # Softmax over the k selected scores.
+            w[t, h] = softmax(score[t, h])
+    return dict(idx=idx, score=score, w=w, half_idx=half_idx, half_score=half_score)
+
+
+def brute_force_search(q: np.ndarray, subkeys: np.ndarray, k: int) -> dict:
+    """Eq. (1) taken literally: instantiate all N = S^2 full keys.
+
+    Full key row i = concat(K1[i // S], K2[i % S]).  Only for tiny inputs;
+    this is the definition that the product-key search must reproduce.
+    Returns idx [T, H, k] and score [T, H, k].
+    """
+    q = _f64(q)
+    K = _f64(subkeys)
+    T, H, n = q.shape
+    d = n // 2
+    S = K.shape[2]
+    N = S * S
+    idx = np.zeros((T, H, k), dtype=np.int64)
+    score = np.zeros((T, H, k))
+    for h in range(H):
+        full = np.zeros((N, n))
+        for i in range(N):
+            full[i, :d] = K[h, 0, i // S]
+            full[i, d:] = K[h, 1, i % S]
+        for t in range(T):
+            f = full @ q[t, h]
+            sel = topk_desc(f, k)
+            idx[t, h] = sel
+            score[t, h] = f[sel]
+    return dict(idx=idx, score=score)
+
+
+def bag_forward(values: np.ndarray, idx: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """Weighted EmbeddingBag, sum mode (Eq. (1) y = s V_I; Sec. 3.1.4).
+
+    values: [N, D]; idx, w: [T, B] with B = H * k lookups per token (any
+    leading shape that flattens to T rows).  y[t] = sum_j w[t, j] V[idx[t, j]].
+    A row chosen by two heads contributes twice.
+    """
+    V = _f64(values)
+    idx = np.asarray(idx).reshape(idx.shape[0], -1)
+    w = _f64(w).reshape(idx.shape[0], -1)
+    T, B = idx.shape
+    y = np.zeros((T, V.shape[1]))
+    for t in range(T):
+        for j in range(B):
+            y[t] += w[t, j] * V[idx[t, j]]
+    return y
+
+
+def bag_backward_rows(dy: np.ndarray, values: np.ndarray, idx: np.ndarray,
+                      w: np.ndarray, H: int, k: int) -> dict:
+    """Backward of bag_forward and of the softmax in front of it.
+
+    Differentiates y[t] = sum_{h,j} w[t,h,j] V[idx[t,h,j]] with
+    w[t,h,:] = softmax(z[t,h,:]) (Sec. 3, Eq. (1); Sec. 3.1.4):
+      grad_w[t,h,j]  = dy[t] . V[idx[t,h,j]]
+      grad_z[t,h,j]  = w[t,h,j] * (grad_w[t,h,j] - sum_j' w[t,h,j'] grad_w[t,h,j'])
+      grad_V[r]     += sum over lookups (t,h,j) with idx = r of w[t,h,j] dy[t]
+
+    Returns grad_w [T,H,k], grad_z [T,H,k] and the value gradient as
+    touched rows only: rows (ascending int64) and grad_rows [U, D].
+    """
+    dy = _f64(dy)
+    V = _f64(values)
+    T = dy.shape[0]
+    idx = np.asarray(idx).reshape(T, H, k)
+    w = _f64(w).reshape(T, H, k)
+    grad_w = np.zeros((T, H, k))
+    grad_z = np.zeros((T, H, k))
+    acc: dict[int, np.ndarray] = {}
+    for t in range(T):
+        for h in range(H):
+            for j in range(k):
+                r = int(idx[t, h, j])
+                grad_w[t, h, j] = dy[t] @ V[r]
+                if r not in acc:
+                    acc[r] = np.zeros(V.shape[1])
+                acc[r] += w[t, h, j] * dy[t]
+            # Softmax backward: Jacobian diag(w) - w w^T applied to grad_w.
+            inner = w[t, h] @ grad_w[t, h]
+            grad_z[t, h] = w[t, h] * (grad_w[t, h] - inner)
+    rows = np.array(sorted(acc), dtype=np.int64)
+    grad_rows = np.stack([acc[int(r)] for r in rows]) if len(rows) else np.zeros((0, V.shape[1]))
+    return dict(grad_w=grad_w, grad_z=grad_z, rows=rows, grad_rows=grad_rows)
+
+
+def bag_backward(dy: np.ndarray, values: np.ndarray, idx: np.ndarray,
+                 w: np.ndarray, H: int, k: int, grad_values_in=None) -> dict:
+    """bag_backward_rows with a dense [N, D] value gradient.
+
+    The dense gradient is grad_values_in (default zeros) plus the touched
+    rows' sums: accumulate semantics, as for a value pool shared by layers.
+    """
+    out = bag_backward_rows(dy, values, idx, w, H, k)
+    N, D = np.asarray(values).shape
+    gV = np.zeros((N, D)) if grad_values_in is None else _f64(grad_values_in).copy()
+    for r, g in zip(out["rows"], out["grad_rows"]):
+        gV[int(r)] += g
+    out["grad_values"] = gV
+    return out
+
+
+def invert_index(idx: np.ndarray) -> dict:
+    """Invert the lookup -> row mapping (Sec. 3.1.4, "reverse indices").
+
+    idx: [L] rows of the flattened lookups l = 0..L-1.  Returns
+      rows     [U]   distinct rows, ascending
+      row_ptr  [U+1] CSR offsets into `lookups`
+      lookups  [L]   lookup ids grouped by row, ascending within a row
+    """
+    idx = np.asarray(idx).ravel().astype(np.int64)
+    groups: dict[int, list[int]] = {}
+    for l, r in enumerate(idx.tolist()):
+        groups.setdefault(r, []).append(l)
+    rows = np.array(sorted(groups), dtype=np.int64)
+    row_ptr = np.zeros(len(rows) + 1, dtype=np.int64)
+    lookups = []
+    for u, r in enumerate(rows.tolist()):
+        lookups.extend(groups[r])
+        row_ptr[u + 1] = len(lookups)
+    return dict(rows=rows, row_ptr=row_ptr, lookups=np.array(lookups, dtype=np.int64))
