@@ -1,0 +1,156 @@
+/*
+ * pkmem.h - C ABI of the product-key memory hot path on MI355X (gfx950).
+ *
+ * Paper: "Memory Layers at Scale" (arXiv 2412.09764).
+ *   Sec. 3, Eq. (1):  I = SelectTopkIndices(K q), s = Softmax(K_I q), y = s V_I,
+ *                     every token independently.
+ *   Sec. 3.1.1:       product keys: K1, K2 of sqrt(N) rows of n/2; split q into
+ *                     q1, q2; top-k per half; best k of the k*k sums.
+ *   Sec. 3.1.4:       the weighted sum is an EmbeddingBag; its backward adds many
+ *                     output gradients into the same value-gradient row, either
+ *                     with atomics or after inverting the lookup -> row mapping.
+ *
+ * Conventions for every entry point
+ *   - Pointers are DEVICE pointers unless marked "host".  All device buffers are
+ *     allocated and owned by the caller; the library never allocates or frees
+ *     device memory and keeps no device state between calls.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = null stream) and
+ *     return once the work is enqueued.  mem_bag_backward_sparse is the only call
+ *     that waits on the stream (it must report a row count to the host).
+ *   - Inputs are read-only.  Outputs are written, except grad_values, which is
+ *     accumulated (+=): one value pool may be shared by several memory layers.
+ *   - Layouts are dense row-major with the last dimension contiguous.
+ *   - A non-zero return means nothing was enqueued (argument errors are found on
+ *     the host before any launch) or a HIP error (PKMEM_ERR_HIP).  No call aborts
+ *     or throws; mem_last_error() gives a message for the calling thread.
+ *   - Inputs must be finite.  Indices passed to the bag calls must lie in [0, N)
+ *     and are not range-checked (they normally come from mem_search).
+ *
+ * Readings where the paper is silent:
+ *   - H heads: per token, H independent queries and sub-key pairs; each head
+ *     selects its own k values from ONE shared value table; the output sums the
+ *     H*k weighted rows (one bag).  A row chosen by two heads counts twice.
+ *   - q[t,h,0:d] (d = n/2) is scored against subkeys[h,0], q[t,h,d:n] against
+ *     subkeys[h,1]; the composed value index is i = i1 * S + i2.
+ *   - Order: score descending, index ascending (lower index wins ties), for the
+ *     per-half lists and for the final selection.  Outputs are in rank order.
+ *   - Scores are raw dot products (no scale or temperature); the softmax runs
+ *     over the k selected scores of one (token, head).
+ *   - Arithmetic: fp32 accumulation everywhere; bf16 outputs are rounded to
+ *     nearest even from the fp32 value.
+ */
+#ifndef PKMEM_H
+#define PKMEM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { PKMEM_F32 = 0, PKMEM_BF16 = 1 } pkmem_dtype;
+
+typedef enum {
+  PKMEM_OK = 0,
+  PKMEM_ERR_INVALID = -1,     /* null pointer, bad size, inconsistent shapes */
+  PKMEM_ERR_UNSUPPORTED = -2, /* valid request outside the supported limits  */
+  PKMEM_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required  */
+  PKMEM_ERR_HIP = -4          /* a HIP call or kernel launch failed          */
+} pkmem_status;
+
+/* Value-gradient strategies of the EmbeddingBag backward (Sec. 3.1.4). */
+typedef enum {
+  PKMEM_BWD_AUTO = 0,   /* library's choice (sorted when D > 128, else atomic) */
+  PKMEM_BWD_ATOMIC = 1, /* fp32 atomic adds straight into grad_values          */
+  PKMEM_BWD_SORTED = 2  /* lookups sorted by row, one read-modify-write per
+                           touched row, contributors summed in lookup order:
+                           bitwise deterministic run to run                    */
+} pkmem_bwd_mode;
+
+typedef void* pkmem_stream_t; /* a hipStream_t */
+
+/* Limits (checked on the host; exceeding them gives PKMEM_ERR_UNSUPPORTED). */
+#define PKMEM_KMAX 64       /* k per half and overall                       */
+#define PKMEM_SMAX 8192     /* sub-keys per half, so N = S*S <= 2^26        */
+#define PKMEM_DHALF_MAX 256 /* d = n/2 for bf16 queries; 64 for fp32        */
+
+/* ------------------------------------------------------------------------ *
+ * Product-key search (Sec. 3.1.1) and softmax (Sec. 3, Eq. (1)).
+ *
+ *   q        [T, H, n]      queries, dtype q_dt (PKMEM_F32 or PKMEM_BF16); n even.
+ *   subkeys  [H, 2, S, n/2] sub-key tables, same dtype as q.
+ *   k        1 <= k <= min(S, PKMEM_KMAX).
+ * Outputs (written):
+ *   idx_out      [T, H, k] int64  composed index i1*S + i2 of the selected values.
+ *   w_out        [T, H, k] fp32   softmax of the selected scores (the bag weights).
+ *   score_out    [T, H, k] fp32   selected scores s1[i1] + s2[i2]; may be NULL.
+ *   half_idx_out [T, H, 2, k] int32 per-half top-k (half 0 then half 1); may be NULL.
+ * Workspace: ws of at least mem_search_workspace_size(T, H, S, k) bytes, 256-byte
+ *   aligned, used only during the call (contents on entry are ignored).
+ * T = 0 is a valid no-op.
+ * ------------------------------------------------------------------------ */
+size_t mem_search_workspace_size(int64_t T, int H, int S, int k);
+
+int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+               int64_t T, int H, int n, int S, int k,
+               int64_t* idx_out, float* w_out, float* score_out, int32_t* half_idx_out,
+               void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * Weighted EmbeddingBag forward, sum mode (Sec. 3, Eq. (1) y = s V_I; Sec. 3.1.4).
+ *
+ *   values [N, D]   value table, dtype v_dt; D % 8 == 0.
+ *   idx    [T, bag] int64 rows in [0, N); w [T, bag] fp32 weights.
+ *   y_out  [T, D]   dtype v_dt, written: y[t] = sum_j w[t,j] * values[idx[t,j]],
+ *                   accumulated in fp32 in the order j = 0..bag-1.
+ * For the memory layer bag = H*k and idx / w are mem_search's outputs.
+ * ------------------------------------------------------------------------ */
+int mem_bag_forward(const void* values, pkmem_dtype v_dt, int64_t N, int D,
+                    const int64_t* idx, const float* w, int64_t T, int bag,
+                    void* y_out, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * EmbeddingBag backward and softmax backward (Sec. 3.1.4; Eq. (1)).
+ *
+ *   dy     [T, D]      upstream gradient of y, dtype v_dt.
+ *   values [N, D]      dtype v_dt.   idx, w [T, H, k] as from mem_search.
+ * Outputs (all optional; NULL skips the output, not the work it depends on):
+ *   grad_values [N, D] fp32, ACCUMULATED: += sum over lookups with idx = r of
+ *                      w * dy[t].
+ *   grad_w      [T, H, k] fp32, written: dy[t] . values[idx[t,h,j]].
+ *   grad_scores [T, H, k] fp32, written: w * (grad_w - sum_j w_j grad_w_j), the
+ *                      gradient with respect to the selected scores.
+ * mode: pkmem_bwd_mode.  Workspace: mem_bag_backward_workspace_size(...) bytes.
+ * ------------------------------------------------------------------------ */
+size_t mem_bag_backward_workspace_size(int64_t T, int H, int k, int64_t N, int D, int mode);
+
+int mem_bag_backward(const void* dy, const void* values, pkmem_dtype v_dt, int64_t N, int D,
+                     const int64_t* idx, const float* w, int64_t T, int H, int k,
+                     float* grad_values, float* grad_w, float* grad_scores,
+                     int mode, void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* Sparse form of the value gradient, for tables too large for a dense fp32
+ * gradient: the touched rows only.  Same arguments and other outputs as
+ * mem_bag_backward (always the sorted strategy), except
+ *   rows_out      [cap] int64  touched rows, ascending (cap >= T*H*k is enough).
+ *   grad_rows_out [cap, D] fp32, written: row u is the gradient of rows_out[u].
+ *   num_rows_out  host int64*: number of touched rows U.  Written after the call
+ *                 waits for `stream`.  Entries at and beyond U are not written.
+ * Workspace: mem_bag_backward_workspace_size(T, H, k, N, D, PKMEM_BWD_SORTED). */
+int mem_bag_backward_sparse(const void* dy, const void* values, pkmem_dtype v_dt, int64_t N,
+                            int D, const int64_t* idx, const float* w, int64_t T, int H, int k,
+                            int64_t* rows_out, float* grad_rows_out, int64_t cap,
+                            int64_t* num_rows_out, float* grad_w, float* grad_scores,
+                            void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* Message for the last non-OK status returned to the calling thread. */
+const char* mem_last_error(void);
+
+/* Library version, for the binding's sanity check. */
+int mem_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PKMEM_H */

@@ -1,0 +1,224 @@
+"""Product-key memory hot path on MI355X: thin binding of libpkmem.so.
+
+The library (include/pkmem.h) implements the product-key search of Sec. 3.1.1
+of "Memory Layers at Scale" (arXiv 2412.09764) followed by the softmax of
+Sec. 3, Eq. (1), and the weighted EmbeddingBag forward and backward of
+Sec. 3.1.4, as hand-written HIP kernels for gfx950.
+
+This module only marshals arguments: it checks tensor placement and dtype,
+allocates outputs and workspaces with torch on the current device, passes raw
+pointers and the current HIP stream through the C ABI, and turns a non-zero
+status into PkmemError.  Every step of the computation runs in the library;
+there is no fallback: without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # noqa: F401  (first: the library binds to the HIP runtime torch loads)
+
+__all__ = [
+    "PkmemError", "load", "lib_path", "mem_search", "mem_bag_forward", "mem_bag_backward",
+    "mem_bag_backward_sparse", "mem_search_workspace_size", "mem_bag_backward_workspace_size",
+    "BWD_MODES", "F32", "BF16",
+]
+
+F32, BF16 = 0, 1
+BWD_MODES = {"auto": 0, "atomic": 1, "sorted": 2}
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+
+class PkmemError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"pkmem status {code}: {msg}")
+        self.code = code
+
+
+def lib_path() -> str:
+    return os.environ.get("PKMEM_LIB", os.path.join(_HERE, "libpkmem.so"))
+
+
+def load() -> ctypes.CDLL:
+    """Load libpkmem.so (raises if it has not been built)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = lib_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2412_09764_amd.build`")
+    L = ctypes.CDLL(path)
+    P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+    L.mem_search_workspace_size.argtypes = [I64, I32, I32, I32]
+    L.mem_search_workspace_size.restype = SZ
+    L.mem_search.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, SZ, P]
+    L.mem_search.restype = I32
+    L.mem_bag_forward.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P]
+    L.mem_bag_forward.restype = I32
+    L.mem_bag_backward_workspace_size.argtypes = [I64, I32, I32, I64, I32, I32]
+    L.mem_bag_backward_workspace_size.restype = SZ
+    L.mem_bag_backward.argtypes = [P, P, I32, I64, I32, P, P, I64, I32, I32, P, P, P, I32, P, SZ, P]
+    L.mem_bag_backward.restype = I32
+    L.mem_bag_backward_sparse.argtypes = [P, P, I32, I64, I32, P, P, I64, I32, I32, P, P, I64, P,
+                                          P, P, P, SZ, P]
+    L.mem_bag_backward_sparse.restype = I32
+    L.mem_last_error.argtypes = []
+    L.mem_last_error.restype = ctypes.c_char_p
+    L.mem_version.argtypes = []
+    L.mem_version.restype = I32
+    _LIB = L
+    return L
+
+
+def _check(rc: int) -> None:
+    if rc != 0:
+        raise PkmemError(rc, load().mem_last_error().decode(errors="replace"))
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _dev(*ts: torch.Tensor) -> None:
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("tensors must be on the GPU")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _workspace(nbytes: int, device, ws):
+    if ws is not None:
+        if ws.numel() * ws.element_size() < nbytes:
+            raise ValueError(f"workspace too small: {nbytes} bytes needed")
+        return ws
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def mem_search_workspace_size(T: int, H: int, S: int, k: int) -> int:
+    return int(load().mem_search_workspace_size(T, H, S, k))
+
+
+def mem_bag_backward_workspace_size(T: int, H: int, k: int, N: int, D: int, mode="auto") -> int:
+    m = BWD_MODES[mode] if isinstance(mode, str) else int(mode)
+    return int(load().mem_bag_backward_workspace_size(T, H, k, N, D, m))
+
+
+def mem_search(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None, w_out=None,
+               score_out=None, half_idx_out=None, want_score: bool = True,
+               want_half: bool = False, workspace=None, stream=None):
+    """Product-key search + softmax.  q [T, H, n], subkeys [H, 2, S, n/2].
+
+    Returns (idx int64 [T,H,k], w fp32 [T,H,k], score fp32 [T,H,k] or None,
+    half_idx int32 [T,H,2,k] or None).
+    """
+    L = load()
+    _dev(q, subkeys)
+    T, H, n = q.shape
+    S = subkeys.shape[2]
+    dev = q.device
+    if idx_out is None:
+        idx_out = torch.empty((T, H, k), dtype=torch.int64, device=dev)
+    if w_out is None:
+        w_out = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    if score_out is None and want_score:
+        score_out = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    if half_idx_out is None and want_half:
+        half_idx_out = torch.empty((T, H, 2, k), dtype=torch.int32, device=dev)
+    _dev(idx_out, w_out, score_out, half_idx_out)
+    nbytes = mem_search_workspace_size(T, H, S, k)
+    ws = _workspace(nbytes, dev, workspace)
+    _check(L.mem_search(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
+                        _ptr(idx_out), _ptr(w_out), _ptr(score_out), _ptr(half_idx_out),
+                        _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+    return idx_out, w_out, score_out, half_idx_out
+
+
+def mem_bag_forward(values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor, *, y_out=None,
+                    stream=None):
+    """y[t] = sum_j w[t, j] values[idx[t, j]]; idx, w of shape [T, ...] (bag = rest)."""
+    L = load()
+    _dev(values, idx, w)
+    N, D = values.shape
+    T = idx.shape[0]
+    bag = idx.numel() // T if T else (idx[0].numel() if idx.dim() > 1 else 1)
+    if idx.dtype != torch.int64 or w.dtype != torch.float32:
+        raise TypeError("idx must be int64 and w float32")
+    if y_out is None:
+        y_out = torch.empty((T, D), dtype=values.dtype, device=values.device)
+    _dev(y_out)
+    _check(L.mem_bag_forward(_ptr(values), _dt(values), N, D, _ptr(idx), _ptr(w), T, bag,
+                             _ptr(y_out), _stream(stream)))
+    return y_out
+
+
+def mem_bag_backward(dy: torch.Tensor, values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor,
+                     *, grad_values=None, grad_w=None, grad_scores=None, want_grad_values=True,
+                     want_grad_w=True, want_grad_scores=True, mode="auto", workspace=None,
+                     stream=None):
+    """EmbeddingBag + softmax backward.  idx, w [T, H, k].  grad_values is
+    ACCUMULATED into (a zero table is allocated if none is given)."""
+    Lb = load()
+    _dev(dy, values, idx, w)
+    N, D = values.shape
+    T, H, k = idx.shape
+    dev = values.device
+    if grad_values is None and want_grad_values:
+        grad_values = torch.zeros((N, D), dtype=torch.float32, device=dev)
+    if grad_w is None and want_grad_w:
+        grad_w = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    if grad_scores is None and want_grad_scores:
+        grad_scores = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    _dev(grad_values, grad_w, grad_scores)
+    m = BWD_MODES[mode] if isinstance(mode, str) else int(mode)
+    nbytes = int(Lb.mem_bag_backward_workspace_size(T, H, k, N, D, m))
+    ws = _workspace(nbytes, dev, workspace)
+    _check(Lb.mem_bag_backward(_ptr(dy), _ptr(values), _dt(values), N, D, _ptr(idx), _ptr(w), T,
+                               H, k, _ptr(grad_values), _ptr(grad_w), _ptr(grad_scores), m,
+                               _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+    return grad_values, grad_w, grad_scores
+
+
+def mem_bag_backward_sparse(dy: torch.Tensor, values: torch.Tensor, idx: torch.Tensor,
+                            w: torch.Tensor, *, want_grad_w=True, want_grad_scores=True,
+                            workspace=None, stream=None):
+    """Backward with the value gradient as touched rows only.
+
+    Returns (rows int64 [U], grad_rows fp32 [U, D], grad_w, grad_scores); waits
+    for the stream to learn U.
+    """
+    Lb = load()
+    _dev(dy, values, idx, w)
+    N, D = values.shape
+    T, H, k = idx.shape
+    dev = values.device
+    cap = max(1, min(T * H * k, N))
+    rows = torch.empty((cap,), dtype=torch.int64, device=dev)
+    grad_rows = torch.empty((cap, D), dtype=torch.float32, device=dev)
+    grad_w = torch.empty((T, H, k), dtype=torch.float32, device=dev) if want_grad_w else None
+    grad_scores = torch.empty((T, H, k), dtype=torch.float32, device=dev) if want_grad_scores else None
+    nbytes = int(Lb.mem_bag_backward_workspace_size(T, H, k, N, D, BWD_MODES["sorted"]))
+    ws = _workspace(nbytes, dev, workspace)
+    U = ctypes.c_int64(0)
+    _check(Lb.mem_bag_backward_sparse(_ptr(dy), _ptr(values), _dt(values), N, D, _ptr(idx),
+                                      _ptr(w), T, H, k, _ptr(rows), _ptr(grad_rows), cap,
+                                      ctypes.addressof(U), _ptr(grad_w), _ptr(grad_scores),
+                                      _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+    u = int(U.value)
+    return rows[:u], grad_rows[:u], grad_w, grad_scores

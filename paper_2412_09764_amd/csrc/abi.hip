@@ -1,0 +1,241 @@
+// C ABI of the product-key memory hot path: argument checks on the host,
+// workspace carving, dispatch to the kernels.  Declared in include/pkmem.h.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "../../include/pkmem.h"
+#include "pk_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int hip_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return PKMEM_OK;
+  return fail(PKMEM_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+inline size_t esize(pkmem_dtype t) { return t == PKMEM_BF16 ? 2 : 4; }
+inline bool dtype_ok(int t) { return t == PKMEM_F32 || t == PKMEM_BF16; }
+
+struct SearchWs {
+  uint64_t* cand;
+  int32_t* half_idx;
+  float* half_score;
+  uint32_t* ovf;
+  size_t bytes;
+};
+
+SearchWs search_ws(void* base, int64_t T, int H, int k) {
+  const size_t rows = (size_t)T * H * 2;
+  char* p = reinterpret_cast<char*>(base);
+  SearchWs w;
+  size_t off = 0;
+  w.cand = reinterpret_cast<uint64_t*>(p + off);
+  off += align256(rows * pk::CAND_CAP * sizeof(uint64_t));
+  w.half_idx = reinterpret_cast<int32_t*>(p + off);
+  off += align256(rows * k * sizeof(int32_t));
+  w.half_score = reinterpret_cast<float*>(p + off);
+  off += align256(rows * k * sizeof(float));
+  w.ovf = reinterpret_cast<uint32_t*>(p + off);
+  off += align256((rows + 1) * sizeof(uint32_t));
+  w.bytes = off;
+  return w;
+}
+
+int check_bag_shapes(const char* fn, pkmem_dtype v_dt, int64_t N, int D, int64_t T, int bag) {
+  if (!dtype_ok(v_dt)) return fail(PKMEM_ERR_INVALID, "%s: unknown value dtype %d", fn, (int)v_dt);
+  if (N < 1) return fail(PKMEM_ERR_INVALID, "%s: N must be >= 1 (got %lld)", fn, (long long)N);
+  if (N > (int64_t(1) << 32)) return fail(PKMEM_ERR_UNSUPPORTED, "%s: N > 2^32 rows", fn);
+  if (T < 0) return fail(PKMEM_ERR_INVALID, "%s: T must be >= 0", fn);
+  if (bag < 1) return fail(PKMEM_ERR_INVALID, "%s: bag (H*k) must be >= 1", fn);
+  if (D < 8 || D % 8 != 0) return fail(PKMEM_ERR_UNSUPPORTED, "%s: D must be a positive multiple of 8 (got %d)", fn, D);
+  const int chunks = (int)(D * esize(v_dt) / 16);
+  if (chunks > 512) return fail(PKMEM_ERR_UNSUPPORTED, "%s: rows wider than 8 KiB are not supported (D=%d)", fn, D);
+  if ((T * (int64_t)bag) > (int64_t)0xFFFFFFFF) return fail(PKMEM_ERR_UNSUPPORTED, "%s: T*bag must be < 2^32", fn);
+  return PKMEM_OK;
+}
+
+size_t bwd_ws_bytes(int64_t T, int H, int k, int mode) {
+  const int64_t L = T * H * k;
+  size_t b = align256((size_t)L * sizeof(float));  // grad_w when the caller passes none
+  if (mode == PKMEM_BWD_SORTED) b += pk::sorted_workspace_bytes(L);
+  return b;
+}
+
+int resolve_mode(int mode, int D) {
+  if (mode == PKMEM_BWD_AUTO) return D > 128 ? PKMEM_BWD_SORTED : PKMEM_BWD_ATOMIC;
+  return mode;
+}
+
+int bag_backward_common(const char* fn, const void* dy, const void* values, pkmem_dtype v_dt,
+                        int64_t N, int D, const int64_t* idx, const float* w, int64_t T, int H,
+                        int k, float* grad_values, int64_t* rows_out, float* grad_rows_out,
+                        int64_t cap, int64_t* num_rows_out, float* grad_w, float* grad_scores,
+                        int mode, void* ws, size_t ws_bytes, hipStream_t st) {
+  if (H < 1 || k < 1) return fail(PKMEM_ERR_INVALID, "%s: H and k must be >= 1", fn);
+  int rc = check_bag_shapes(fn, v_dt, N, D, T, H * k);
+  if (rc) return rc;
+  if (mode != PKMEM_BWD_AUTO && mode != PKMEM_BWD_ATOMIC && mode != PKMEM_BWD_SORTED)
+    return fail(PKMEM_ERR_INVALID, "%s: unknown mode %d", fn, mode);
+  const bool sparse = rows_out != nullptr || num_rows_out != nullptr;
+  const int m = sparse ? PKMEM_BWD_SORTED : resolve_mode(mode, D);
+  if (T > 0 && (!dy || !values || !idx || !w))
+    return fail(PKMEM_ERR_INVALID, "%s: null input pointer", fn);
+  if (!aligned(dy, 16) || !aligned(values, 16))
+    return fail(PKMEM_ERR_INVALID, "%s: dy and values must be 16-byte aligned", fn);
+  if (grad_values && !aligned(grad_values, 16))
+    return fail(PKMEM_ERR_INVALID, "%s: grad_values must be 16-byte aligned", fn);
+  const int64_t L = T * H * k;
+  if (sparse) {
+    if (!rows_out || !grad_rows_out || !num_rows_out)
+      return fail(PKMEM_ERR_INVALID, "%s: rows_out, grad_rows_out and num_rows_out are required", fn);
+    if (!aligned(grad_rows_out, 16)) return fail(PKMEM_ERR_INVALID, "%s: grad_rows_out must be 16-byte aligned", fn);
+    const int64_t need = L < N ? L : N;
+    if (cap < need)
+      return fail(PKMEM_ERR_INVALID, "%s: cap %lld < min(T*H*k, N) = %lld", fn, (long long)cap, (long long)need);
+  }
+  const size_t need_ws = bwd_ws_bytes(T, H, k, m);
+  if (!ws || ws_bytes < need_ws)
+    return fail(PKMEM_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need_ws, ws ? ws_bytes : (size_t)0);
+  if (!aligned(ws, 256)) return fail(PKMEM_ERR_INVALID, "%s: workspace must be 256-byte aligned", fn);
+  if (sparse) *num_rows_out = 0;
+  if (T == 0) return PKMEM_OK;
+
+  char* p = reinterpret_cast<char*>(ws);
+  float* gw = grad_w ? grad_w : reinterpret_cast<float*>(p);
+  p += align256((size_t)L * sizeof(float));
+  const bool bf16 = v_dt == PKMEM_BF16;
+  hipError_t e;
+  if (m == PKMEM_BWD_ATOMIC) {
+    e = pk::launch_bag_backward_atomic(bf16, dy, values, D, idx, w, T, H * k, grad_values, gw, st);
+    if (e != hipSuccess) return hip_status(e, fn);
+  } else {
+    uint32_t* nrows_dev = nullptr;
+    e = pk::launch_bag_backward_sorted(bf16, dy, values, N, D, idx, w, T, H * k,
+                                       sparse ? nullptr : grad_values, sparse ? rows_out : nullptr,
+                                       grad_rows_out, gw, p, &nrows_dev, st);
+    if (e != hipSuccess) return hip_status(e, fn);
+    if (sparse) {
+      uint32_t U = 0;
+      e = hipMemcpyAsync(&U, nrows_dev, sizeof(U), hipMemcpyDeviceToHost, st);
+      if (e == hipSuccess) e = hipStreamSynchronize(st);
+      if (e != hipSuccess) return hip_status(e, fn);
+      *num_rows_out = U;
+    }
+  }
+  if (grad_scores) {
+    e = pk::launch_softmax_backward(w, gw, T * H, k, grad_scores, st);
+    if (e != hipSuccess) return hip_status(e, fn);
+  }
+  return PKMEM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mem_last_error(void) { return g_last_error.c_str(); }
+
+int mem_version(void) { return 1; }
+
+size_t mem_search_workspace_size(int64_t T, int H, int S, int k) {
+  (void)S;
+  if (T < 0 || H < 1 || k < 1) return 0;
+  return search_ws(nullptr, T, H, k).bytes;
+}
+
+int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt, int64_t T,
+               int H, int n, int S, int k, int64_t* idx_out, float* w_out, float* score_out,
+               int32_t* half_idx_out, void* ws, size_t ws_bytes, pkmem_stream_t stream) {
+  const char* fn = "mem_search";
+  if (!dtype_ok(q_dt) || !dtype_ok(k_dt)) return fail(PKMEM_ERR_INVALID, "%s: unknown dtype", fn);
+  if (q_dt != k_dt) return fail(PKMEM_ERR_UNSUPPORTED, "%s: queries and sub-keys must share a dtype", fn);
+  if (T < 0) return fail(PKMEM_ERR_INVALID, "%s: T must be >= 0", fn);
+  if (H < 1) return fail(PKMEM_ERR_INVALID, "%s: H must be >= 1", fn);
+  if (n < 2 || n % 2 != 0) return fail(PKMEM_ERR_INVALID, "%s: n must be even and >= 2 (got %d)", fn, n);
+  const int d = n / 2;
+  if (q_dt == PKMEM_BF16 && (d % 8 != 0 || d > PKMEM_DHALF_MAX))
+    return fail(PKMEM_ERR_UNSUPPORTED, "%s: bf16 needs n/2 a multiple of 8 and <= %d (got %d)", fn, PKMEM_DHALF_MAX, d);
+  if (q_dt == PKMEM_F32 && (d % 4 != 0 || d > 64))
+    return fail(PKMEM_ERR_UNSUPPORTED, "%s: fp32 needs n/2 a multiple of 4 and <= 64 (got %d)", fn, d);
+  if (S < 1) return fail(PKMEM_ERR_INVALID, "%s: S must be >= 1", fn);
+  if (S > PKMEM_SMAX) return fail(PKMEM_ERR_UNSUPPORTED, "%s: S > %d", fn, PKMEM_SMAX);
+  if (k < 1 || k > S) return fail(PKMEM_ERR_INVALID, "%s: need 1 <= k <= S (k=%d, S=%d)", fn, k, S);
+  if (k > PKMEM_KMAX) return fail(PKMEM_ERR_UNSUPPORTED, "%s: k > %d", fn, PKMEM_KMAX);
+  if ((T * H * 2) > (int64_t)0xFFFFFFFF) return fail(PKMEM_ERR_UNSUPPORTED, "%s: T*H*2 must be < 2^32", fn);
+  if (T > 0 && (!q || !subkeys || !idx_out || !w_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (!aligned(q, 16) || !aligned(subkeys, 16)) return fail(PKMEM_ERR_INVALID, "%s: q and subkeys must be 16-byte aligned", fn);
+  const SearchWs need = search_ws(nullptr, T, H, k);
+  if (!ws || ws_bytes < need.bytes)
+    return fail(PKMEM_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need.bytes, ws ? ws_bytes : (size_t)0);
+  if (!aligned(ws, 256)) return fail(PKMEM_ERR_INVALID, "%s: workspace must be 256-byte aligned", fn);
+  if (T == 0) return PKMEM_OK;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  SearchWs w = search_ws(ws, T, H, k);
+  int32_t* hidx = half_idx_out ? half_idx_out : w.half_idx;
+  hipError_t e = pk::launch_search_half(q_dt == PKMEM_BF16, q, subkeys, T, H, n, S, k, w.cand, hidx,
+                                        w.half_score, w.ovf, st);
+  if (e != hipSuccess) return hip_status(e, fn);
+  e = pk::launch_cartesian(hidx, w.half_score, T, H, S, k, idx_out, w_out, score_out, st);
+  if (e != hipSuccess) return hip_status(e, fn);
+  return PKMEM_OK;
+}
+
+int mem_bag_forward(const void* values, pkmem_dtype v_dt, int64_t N, int D, const int64_t* idx,
+                    const float* w, int64_t T, int bag, void* y_out, pkmem_stream_t stream) {
+  const char* fn = "mem_bag_forward";
+  int rc = check_bag_shapes(fn, v_dt, N, D, T, bag);
+  if (rc) return rc;
+  if (T > 0 && (!values || !idx || !w || !y_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (!aligned(values, 16) || !aligned(y_out, 16)) return fail(PKMEM_ERR_INVALID, "%s: values and y_out must be 16-byte aligned", fn);
+  if (T == 0) return PKMEM_OK;
+  hipError_t e = pk::launch_bag_forward(v_dt == PKMEM_BF16, values, D, idx, w, T, bag, y_out,
+                                        reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, fn);
+}
+
+size_t mem_bag_backward_workspace_size(int64_t T, int H, int k, int64_t N, int D, int mode) {
+  (void)N;
+  if (T < 0 || H < 1 || k < 1) return 0;
+  return bwd_ws_bytes(T, H, k, resolve_mode(mode, D));
+}
+
+int mem_bag_backward(const void* dy, const void* values, pkmem_dtype v_dt, int64_t N, int D,
+                     const int64_t* idx, const float* w, int64_t T, int H, int k,
+                     float* grad_values, float* grad_w, float* grad_scores, int mode, void* ws,
+                     size_t ws_bytes, pkmem_stream_t stream) {
+  const char* fn = "mem_bag_backward";
+  return bag_backward_common(fn, dy, values, v_dt, N, D, idx, w, T, H, k, grad_values, nullptr,
+                             nullptr, 0, nullptr, grad_w, grad_scores, mode, ws, ws_bytes,
+                             reinterpret_cast<hipStream_t>(stream));
+}
+
+int mem_bag_backward_sparse(const void* dy, const void* values, pkmem_dtype v_dt, int64_t N, int D,
+                            const int64_t* idx, const float* w, int64_t T, int H, int k,
+                            int64_t* rows_out, float* grad_rows_out, int64_t cap,
+                            int64_t* num_rows_out, float* grad_w, float* grad_scores, void* ws,
+                            size_t ws_bytes, pkmem_stream_t stream) {
+  const char* fn = "mem_bag_backward_sparse";
+  if (!rows_out || !grad_rows_out || !num_rows_out)
+    return fail(PKMEM_ERR_INVALID, "%s: rows_out, grad_rows_out and num_rows_out are required", fn);
+  return bag_backward_common(fn, dy, values, v_dt, N, D, idx, w, T, H, k, nullptr, rows_out,
+                             grad_rows_out, cap, num_rows_out, grad_w, grad_scores,
+                             PKMEM_BWD_SORTED, ws, ws_bytes, reinterpret_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

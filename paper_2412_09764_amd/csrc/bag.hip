@@ -1,0 +1,274 @@
+// Weighted EmbeddingBag on gfx950 (Sec. 3, Eq. (1) y = s V_I; Sec. 3.1.4 of
+// "Memory Layers at Scale").
+//
+// Row mapping shared by the kernels here and in sorted.hip: a value row of D
+// elements is cut into C = D * esize / 16 chunks of 16 bytes.  One wave owns
+// one bag (a token's H*k lookups).  For C >= 64 each lane holds CPL = C / 64
+// chunks i*64 + lane, so every load instruction of the wave reads 1 KiB of one
+// row contiguously.  For C < 64 the wave splits into G = 64 / CL groups of CL
+// lanes (CL = C rounded up to a power of two); group g takes the lookups
+// j = g, g + G, ... and the groups are summed at the end.
+#include "pk_device.h"
+#include "pk_internal.h"
+
+namespace pk {
+
+// 16-byte vector <-> fp32 lanes for the two value dtypes.
+template <typename V>
+struct Row16;
+
+template <>
+struct Row16<uint16_t> {  // bf16
+  static constexpr int N = 8;
+  __device__ static __forceinline__ void unpack(const uint4& v, float (&f)[8]) {
+    f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
+    f[4] = bf16_lo(v.z); f[5] = bf16_hi(v.z); f[6] = bf16_lo(v.w); f[7] = bf16_hi(v.w);
+  }
+  __device__ static __forceinline__ uint4 pack(const float (&f)[8]) {
+    return uint4{pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
+                 pack_bf16x2(f[6], f[7])};
+  }
+};
+
+template <>
+struct Row16<float> {
+  static constexpr int N = 4;
+  __device__ static __forceinline__ void unpack(const uint4& v, float (&f)[4]) {
+    f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+  }
+  __device__ static __forceinline__ uint4 pack(const float (&f)[4]) {
+    return uint4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                 __float_as_uint(f[3])};
+  }
+};
+
+__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+// y[t] = sum_j w[t,j] V[idx[t,j]]; fp32 accumulation, one rounding at the end.
+template <typename V, int CPL, int CL, int U>
+__global__ __launch_bounds__(256) void k_bag_fwd(const V* __restrict__ values, int D,
+                                                 const int64_t* __restrict__ idx,
+                                                 const float* __restrict__ w, int64_t T, int bag,
+                                                 V* __restrict__ y) {
+  using R = Row16<V>;
+  constexpr int G = WAVE / CL;
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int C = D / R::N;
+  const int grp = lane / CL, cl = lane % CL;
+
+  float acc[CPL][R::N];
+#pragma unroll
+  for (int i = 0; i < CPL; ++i)
+#pragma unroll
+    for (int e = 0; e < R::N; ++e) acc[i][e] = 0.f;
+
+  bool ok[CPL];
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) ok[i] = (i * CL + cl) < C;
+
+  const int64_t* ti = idx + t * bag;
+  const float* tw = w + t * bag;
+  int j = grp;
+  for (; j + (U - 1) * G < bag; j += U * G) {
+    int64_t r[U];
+    float ww[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) { r[u] = ti[j + u * G]; ww[u] = tw[j + u * G]; }
+    uint4 v[U][CPL];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < CPL; ++i)
+        v[u][i] = ok[i] ? ld16(values + r[u] * D + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+        float f[R::N];
+        R::unpack(v[u][i], f);
+#pragma unroll
+        for (int e = 0; e < R::N; ++e) acc[i][e] = fmaf(ww[u], f[e], acc[i][e]);
+      }
+  }
+  for (; j < bag; j += G) {
+    const int64_t r = ti[j];
+    const float ww = tw[j];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      if (!ok[i]) continue;
+      float f[R::N];
+      R::unpack(ld16(values + r * D + (size_t)(i * CL + cl) * R::N), f);
+#pragma unroll
+      for (int e = 0; e < R::N; ++e) acc[i][e] = fmaf(ww, f[e], acc[i][e]);
+    }
+  }
+  if (G > 1) {
+#pragma unroll
+    for (int m = CL; m < WAVE; m <<= 1)
+#pragma unroll
+      for (int i = 0; i < CPL; ++i)
+#pragma unroll
+        for (int e = 0; e < R::N; ++e) acc[i][e] += __shfl_xor(acc[i][e], m, WAVE);
+  }
+  if (grp == 0) {
+#pragma unroll
+    for (int i = 0; i < CPL; ++i)
+      if (ok[i]) *reinterpret_cast<uint4*>(y + t * D + (size_t)(i * CL + cl) * R::N) = R::pack(acc[i]);
+  }
+}
+
+// Atomic strategy: per lookup, grad_w = dy . V[row] and grad_values[row] +=
+// w * dy with fp32 atomic adds (no return) resolved in L2.  The dot product
+// uses dy in the 16-byte chunk layout of the value loads; the atomics use a
+// second, lane-strided copy of dy (element cl + CL*m in slot m), so each
+// atomic instruction of a lane group covers CL consecutive floats.
+template <typename V, int CPL, int CL>
+__global__ __launch_bounds__(256) void k_bag_bwd_atomic(const V* __restrict__ dy,
+                                                        const V* __restrict__ values, int D,
+                                                        const int64_t* __restrict__ idx,
+                                                        const float* __restrict__ w, int64_t T,
+                                                        int bag, float* __restrict__ grad_values,
+                                                        float* __restrict__ grad_w) {
+  using R = Row16<V>;
+  constexpr int G = WAVE / CL;
+  constexpr int AM = CPL * R::N;  // strided elements per lane
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int C = D / R::N;
+  const int grp = lane / CL, cl = lane % CL;
+  const V* dyt = dy + t * D;
+
+  bool ok[CPL];
+  float g[CPL][R::N];
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) {
+    ok[i] = (i * CL + cl) < C;
+    const uint4 v = ok[i] ? ld16(dyt + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
+    R::unpack(v, g[i]);
+  }
+  float ga[AM];
+#pragma unroll
+  for (int m = 0; m < AM; ++m) {
+    const int e = cl + CL * m;
+    ga[m] = 0.f;
+    if (e < D) {
+      if constexpr (sizeof(V) == 2) ga[m] = bf16_to_f32(dyt[e]);
+      else ga[m] = (float)dyt[e];
+    }
+  }
+  const int64_t* ti = idx + t * bag;
+  const float* tw = w + t * bag;
+  for (int j = grp; j < bag; j += G) {
+    const int64_t r = ti[j];
+    const float ww = tw[j];
+    float part = 0.f;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      if (!ok[i]) continue;
+      float f[R::N];
+      R::unpack(ld16(values + r * D + (size_t)(i * CL + cl) * R::N), f);
+#pragma unroll
+      for (int e = 0; e < R::N; ++e) part = fmaf(g[i][e], f[e], part);
+    }
+    if (grad_values) {
+      float* gr = grad_values + r * D;
+#pragma unroll
+      for (int m = 0; m < AM; ++m) {
+        const int e = cl + CL * m;
+        if (e < D) unsafeAtomicAdd(gr + e, ww * ga[m]);
+      }
+    }
+    part = group_sum<CL>(part);
+    if (cl == 0 && grad_w) grad_w[t * bag + j] = part;
+  }
+}
+
+// grad_scores = w * (grad_w - sum_j w_j grad_w_j) per (token, head) row of k.
+__global__ __launch_bounds__(256) void k_softmax_bwd(const float* __restrict__ w,
+                                                     const float* __restrict__ gw, int64_t rows,
+                                                     int k, float* __restrict__ gz) {
+  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (r >= rows) return;
+  const float* wr = w + r * k;
+  const float* gr = gw + r * k;
+  float inner = 0.f;
+  for (int j = 0; j < k; ++j) inner = fmaf(wr[j], gr[j], inner);
+  for (int j = 0; j < k; ++j) gz[r * k + j] = wr[j] * (gr[j] - inner);
+}
+
+__global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t value, int64_t count) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < count) p[i] = value;
+}
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, p, value, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_softmax_backward(const float* w, const float* grad_w, int64_t rows, int k,
+                                   float* grad_scores, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_softmax_bwd, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, st, w,
+                     grad_w, rows, k, grad_scores);
+  return hipGetLastError();
+}
+
+// Dispatch on (dtype, chunks per row): CPL in {1,2,4,8} for C >= 64, CL in
+// {1..64} for C < 64.
+#define PK_ROW_DISPATCH(C, MACRO)                    \
+  do {                                               \
+    if ((C) > 256) { MACRO(8, 64); }                 \
+    else if ((C) > 128) { MACRO(4, 64); }            \
+    else if ((C) > 64) { MACRO(2, 64); }             \
+    else if ((C) > 32) { MACRO(1, 64); }             \
+    else if ((C) > 16) { MACRO(1, 32); }             \
+    else if ((C) > 8) { MACRO(1, 16); }              \
+    else if ((C) > 4) { MACRO(1, 8); }               \
+    else if ((C) > 2) { MACRO(1, 4); }               \
+    else if ((C) > 1) { MACRO(1, 2); }               \
+    else { MACRO(1, 1); }                            \
+  } while (0)
+
+hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_t* idx,
+                              const float* w, int64_t T, int bag, void* y, hipStream_t st) {
+  if (T <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((T + 3) / 4)), block(256);
+  const int C = D * (bf16 ? 2 : 4) / 16;
+#define PK_FWD(CPL, CL)                                                                            \
+  if (bf16)                                                                                        \
+    hipLaunchKernelGGL((k_bag_fwd<uint16_t, CPL, CL, 4>), grid, block, 0, st,                      \
+                       (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);                 \
+  else                                                                                             \
+    hipLaunchKernelGGL((k_bag_fwd<float, CPL, CL, 4>), grid, block, 0, st, (const float*)values, D, \
+                       idx, w, T, bag, (float*)y);
+  PK_ROW_DISPATCH(C, PK_FWD);
+#undef PK_FWD
+  return hipGetLastError();
+}
+
+hipError_t launch_bag_backward_atomic(bool bf16, const void* dy, const void* values, int D,
+                                      const int64_t* idx, const float* w, int64_t T, int bag,
+                                      float* grad_values, float* grad_w, hipStream_t st) {
+  if (T <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((T + 3) / 4)), block(256);
+  const int C = D * (bf16 ? 2 : 4) / 16;
+#define PK_BWD(CPL, CL)                                                                         \
+  if (bf16)                                                                                     \
+    hipLaunchKernelGGL((k_bag_bwd_atomic<uint16_t, CPL, CL>), grid, block, 0, st,               \
+                       (const uint16_t*)dy, (const uint16_t*)values, D, idx, w, T, bag,          \
+                       grad_values, grad_w);                                                    \
+  else                                                                                          \
+    hipLaunchKernelGGL((k_bag_bwd_atomic<float, CPL, CL>), grid, block, 0, st, (const float*)dy, \
+                       (const float*)values, D, idx, w, T, bag, grad_values, grad_w);
+  PK_ROW_DISPATCH(C, PK_BWD);
+#undef PK_BWD
+  return hipGetLastError();
+}
+
+}  // namespace pk

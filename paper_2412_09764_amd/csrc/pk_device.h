@@ -1,0 +1,144 @@
+// Device helpers shared by the product-key memory kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pk {
+
+constexpr int WAVE = 64;
+
+// ---------------------------------------------------------------- bf16 ----
+__device__ __forceinline__ float bf16_lo(uint32_t two) { return __uint_as_float(two << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t two) { return __uint_as_float(two & 0xFFFF0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
+
+// Round to nearest, ties to even (inputs are finite).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// --------------------------------------------------- ordered 64-bit keys ----
+// A selection key orders (score descending, index ascending) as one unsigned
+// 64-bit integer, larger = better: the high word is the score mapped to an
+// order-preserving unsigned value (-0 folded onto +0), the low word is the
+// bitwise complement of the index.  Key 0 is never produced by a finite or
+// infinite score and serves as "empty".
+__device__ __forceinline__ uint32_t f32_to_ordered(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float ordered_to_f32(uint32_t o) {
+  uint32_t u = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
+  return __uint_as_float(u);
+}
+__device__ __forceinline__ uint64_t make_key(float score, uint32_t index) {
+  return (uint64_t(f32_to_ordered(score)) << 32) | uint64_t(~index);
+}
+__device__ __forceinline__ float key_score(uint64_t key) { return ordered_to_f32(uint32_t(key >> 32)); }
+__device__ __forceinline__ uint32_t key_index(uint64_t key) { return ~uint32_t(key); }
+
+// ---------------------------------------------------------- shuffles ----
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
+  uint32_t lo = __shfl_xor(uint32_t(v), mask, WAVE);
+  uint32_t hi = __shfl_xor(uint32_t(v >> 32), mask, WAVE);
+  return (uint64_t(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  uint32_t lo = __shfl(uint32_t(v), src, WAVE);
+  uint32_t hi = __shfl(uint32_t(v >> 32), src, WAVE);
+  return (uint64_t(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+
+// Sum over groups of G consecutive lanes (G a power of two <= 64); every lane
+// of a group ends with the group's sum.
+template <int G>
+__device__ __forceinline__ float group_sum(float v) {
+#pragma unroll
+  for (int m = G / 2; m >= 1; m >>= 1) v += __shfl_xor(v, m, WAVE);
+  return v;
+}
+
+// --------------------------------------------------- sorting networks ----
+// Bitonic sort of a register array, descending (element 0 largest).
+template <int N>
+__device__ __forceinline__ void sort_desc_regs(float (&v)[N]) {
+#pragma unroll
+  for (int size = 2; size <= N; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int j = i ^ stride;
+        if (j > i) {
+          const bool desc = (i & size) == 0;
+          const float a = v[i], b = v[j];
+          v[i] = desc ? fmaxf(a, b) : fminf(a, b);
+          v[j] = desc ? fminf(a, b) : fmaxf(a, b);
+        }
+      }
+    }
+  }
+}
+
+// Bitonic merge of a register array that is already bitonic, descending.
+template <int N>
+__device__ __forceinline__ void merge_desc_regs(float (&v)[N]) {
+#pragma unroll
+  for (int stride = N >> 1; stride > 0; stride >>= 1) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int j = i ^ stride;
+      if (j > i) {
+        const float a = v[i], b = v[j];
+        v[i] = fmaxf(a, b);
+        v[j] = fminf(a, b);
+      }
+    }
+  }
+}
+
+// Bitonic sort, descending, of 64*E keys held by one wave: element
+// e = r * 64 + lane lives in v[r] of that lane.  Afterwards element 0
+// (lane 0, v[0]) is the largest.
+template <int E>
+__device__ __forceinline__ void wave_sort_desc(uint64_t (&v)[E], int lane) {
+#pragma unroll
+  for (int size = 2; size <= WAVE * E; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      if (stride >= WAVE) {
+        const int rs = stride / WAVE;
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+          const int r2 = r ^ rs;
+          if (r2 > r) {
+            const bool desc = ((r * WAVE + lane) & size) == 0;
+            const uint64_t a = v[r], b = v[r2];
+            const bool swap = desc ? (a < b) : (a > b);
+            v[r] = swap ? b : a;
+            v[r2] = swap ? a : b;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+          const uint64_t p = shfl_xor_u64(v[r], stride);
+          const bool desc = ((r * WAVE + lane) & size) == 0;
+          const bool lower = (lane & stride) == 0;
+          v[r] = (lower == desc) ? umax64(v[r], p) : umin64(v[r], p);
+        }
+      }
+    }
+  }
+}
+
+}  // namespace pk

@@ -1,0 +1,51 @@
+// Host-side launchers shared between the kernel files and the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pk {
+
+// Candidate slots kept per (token, head, half) between the filter pass and the
+// per-row sort of the search kernel.
+constexpr int CAND_CAP = 128;
+// Tokens per workgroup of the scoring kernel (4 waves x 32 tokens).
+constexpr int SEARCH_TOK = 128;
+
+// Number of (i1, i2) rank pairs with (i1 + 1) * (i2 + 1) <= k: only these can
+// reach the top k of the k*k sums when both half lists are sorted.
+int cartesian_pairs(int k);
+
+// ---- search (search.hip) -------------------------------------------------
+// rows = T*H*2 (token, head, half) rows; cand = [rows, CAND_CAP] u64;
+// ovf = [1 + rows] u32 (count, then overflowed row ids).
+hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
+                              int n, int S, int k, uint64_t* cand, int32_t* half_idx,
+                              float* half_score, uint32_t* ovf, hipStream_t st);
+hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T, int H,
+                            int S, int k, int64_t* idx_out, float* w_out, float* score_out,
+                            hipStream_t st);
+
+// ---- bag (bag.hip) ---------------------------------------------------------
+hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_t* idx,
+                              const float* w, int64_t T, int bag, void* y, hipStream_t st);
+hipError_t launch_bag_backward_atomic(bool bf16, const void* dy, const void* values, int D,
+                                      const int64_t* idx, const float* w, int64_t T, int bag,
+                                      float* grad_values, float* grad_w, hipStream_t st);
+hipError_t launch_softmax_backward(const float* w, const float* grad_w, int64_t rows, int k,
+                                   float* grad_scores, hipStream_t st);
+hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream_t st);
+
+// ---- sorted backward (sorted.hip) ------------------------------------------
+size_t sorted_workspace_bytes(int64_t L);
+// Sorts the L lookups by row (stable), finds the touched rows, and per row
+// computes grad_w of its lookups and the row's gradient sum.  Dense mode adds
+// the sum into grad_values[row]; sparse mode writes rows_out / grad_rows_out.
+hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* values, int64_t N,
+                                      int D, const int64_t* idx, const float* w, int64_t T,
+                                      int bag, float* grad_values, int64_t* rows_out,
+                                      float* grad_rows_out, float* grad_w, void* ws,
+                                      uint32_t** num_rows_dev, hipStream_t st);
+
+}  // namespace pk

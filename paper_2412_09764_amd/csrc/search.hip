@@ -1,0 +1,433 @@
+// Product-key search on gfx950 (Sec. 3.1.1 of "Memory Layers at Scale";
+// softmax of Sec. 3, Eq. (1)).
+//
+// Step 1, k_score_topk: for every (token, head, half) row, the top k of the S
+// half-key scores s[i] = q_half . K_half[i], ordered (score desc, index asc).
+//   * A workgroup owns 128 tokens of one (head, half); the (head, half) index is
+//     blockIdx % (2H), so with 2H = 8 each XCD streams only its own 1 MiB sub-key
+//     table and keeps it in its L2.
+//   * Scores come from v_mfma_f32_32x32x16_bf16 (fp32 inputs: 32x32x2 f32) with
+//     sub-keys as the A operand (M = 32 sub-keys) and the wave's 32 queries as
+//     the register-resident B operand (N = 32 tokens); sub-key chunks of 32 rows
+//     are staged through LDS, double buffered.  Scores never leave registers.
+//   * Pass 1 keeps, per token, the maximum of each of 64 interleaved groups of
+//     sub-keys (group = row mod 64).  The k-th largest of those 64 maxima is a
+//     threshold with at least k distinct scores at or above it.
+//   * Pass 2 recomputes the same tiles (bitwise identical) and appends every
+//     score >= threshold, as a 64-bit (score, index) key, to the row's candidate
+//     list (typically about 43 of 2048 at k = 32).
+//   * Pass 3 sorts each row's candidates with a wave bitonic sort and writes the
+//     first k.  A row with more than CAND_CAP candidates (heavy ties) is listed
+//     for k_topk_fallback, which rescans it exactly.
+// Step 2, k_cartesian: per (token, head) the top k of the sums s1[a] + s2[b]
+//   over rank pairs with (a+1)(b+1) <= k (every other pair is beaten by at
+//   least k pairs), ordered (sum desc, composed index i1*S + i2 asc), then the
+//   softmax over the k selected sums.
+#include "pk_device.h"
+#include "pk_internal.h"
+
+namespace pk {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+
+constexpr int CHUNK_ROWS = 32;  // sub-keys per LDS chunk = one MFMA tile
+
+template <typename T>
+struct MfmaOp;
+
+template <>
+struct MfmaOp<uint16_t> {  // bf16 storage
+  static constexpr int KSTEP = 16;  // reduction elements per instruction
+  static constexpr int LANE_K = 8;  // reduction elements supplied per lane
+  static constexpr int ESIZE = 2;
+  using frag = bf16x8_t;
+  __device__ static __forceinline__ f32x16_t mma(frag a, frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ frag load(const void* p) {
+    return __builtin_bit_cast(frag, *reinterpret_cast<const uint4*>(p));
+  }
+  __device__ static __forceinline__ frag zero() { return __builtin_bit_cast(frag, uint4{0, 0, 0, 0}); }
+  __device__ static __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
+};
+
+template <>
+struct MfmaOp<float> {
+  static constexpr int KSTEP = 2;
+  static constexpr int LANE_K = 1;
+  static constexpr int ESIZE = 4;
+  using frag = float;
+  __device__ static __forceinline__ f32x16_t mma(frag a, frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ frag load(const void* p) { return *reinterpret_cast<const float*>(p); }
+  __device__ static __forceinline__ frag zero() { return 0.f; }
+  __device__ static __forceinline__ float to_f32(float v) { return v; }
+};
+
+// Row of the 32x32 MFMA result held in accumulator slot j of a lane whose
+// upper-half bit is kh (columns are lane & 31).
+__device__ __forceinline__ int acc_row(int j, int kh) { return 8 * (j >> 2) + 4 * kh + (j & 3); }
+
+template <typename T, int NSTEP>
+__global__ __launch_bounds__(256) void k_score_topk(
+    const T* __restrict__ q, const T* __restrict__ subkeys, int64_t ntok, int H, int n, int S,
+    int k, uint64_t* __restrict__ cand, int32_t* __restrict__ half_idx,
+    float* __restrict__ half_score, uint32_t* __restrict__ ovf) {
+  using M = MfmaOp<T>;
+  constexpr int DPAD = NSTEP * M::KSTEP;                   // padded half dim
+  constexpr int ROW_BYTES = DPAD * M::ESIZE + 16;          // +16 B: LDS bank skew
+  constexpr int CHUNK_BYTES = CHUNK_ROWS * ROW_BYTES;
+  constexpr int SEGS_PER_ROW = DPAD * M::ESIZE / 16;       // 16-byte segments per row
+  constexpr int SEGS = CHUNK_ROWS * SEGS_PER_ROW;
+  constexpr int SPT = (SEGS + 255) / 256;                  // segments per thread
+  constexpr int ELEMS_PER_SEG = 16 / M::ESIZE;
+
+  __shared__ __align__(16) unsigned char kbuf[2][CHUNK_BYTES];
+  __shared__ int cnt[SEARCH_TOK];
+
+  const int d = n >> 1;
+  const int HP = 2 * H;
+  const int hp = blockIdx.x % HP;
+  const int64_t tile = blockIdx.x / HP;
+  const int h = hp >> 1, p = hp & 1;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kh = lane >> 5;
+  const int col = lane & 31;
+  const int64_t tok = tile * SEARCH_TOK + wave * 32 + col;
+  const bool tok_ok = tok < ntok;
+  const T* kbase = subkeys + (size_t)hp * S * d;
+
+  // Queries of this lane's token, as B fragments: lane supplies reduction
+  // elements [s*KSTEP + kh*LANE_K, +LANE_K) of column `col`.
+  typename M::frag bq[NSTEP];
+  {
+    const T* qrow = q + ((size_t)(tok_ok ? tok : 0) * H + h) * n + (size_t)p * d;
+#pragma unroll
+    for (int s = 0; s < NSTEP; ++s) {
+      const int e0 = s * M::KSTEP + kh * M::LANE_K;
+      bq[s] = (tok_ok && e0 + M::LANE_K <= d) ? M::load(qrow + e0) : M::zero();
+    }
+  }
+
+  uint4 pre[SPT];
+  auto load_chunk = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+      const int seg = tid + i * 256;
+      uint4 v = {0, 0, 0, 0};
+      if (seg < SEGS) {
+        const int r = seg / SEGS_PER_ROW, cs = seg % SEGS_PER_ROW;
+        const int row = c * CHUNK_ROWS + r;
+        const int e0 = cs * ELEMS_PER_SEG;
+        if (row < S && e0 < d) v = *reinterpret_cast<const uint4*>(kbase + (size_t)row * d + e0);
+      }
+      pre[i] = v;
+    }
+  };
+  auto store_chunk = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+      const int seg = tid + i * 256;
+      if (seg < SEGS) {
+        const int r = seg / SEGS_PER_ROW, cs = seg % SEGS_PER_ROW;
+        *reinterpret_cast<uint4*>(&kbuf[b][r * ROW_BYTES + cs * 16]) = pre[i];
+      }
+    }
+  };
+  auto tile_mma = [&](int b) {
+    f32x16_t acc = {};
+    const unsigned char* base = &kbuf[b][col * ROW_BYTES + kh * M::LANE_K * M::ESIZE];
+#pragma unroll
+    for (int s = 0; s < NSTEP; ++s) acc = M::mma(M::load(base + s * M::KSTEP * M::ESIZE), bq[s], acc);
+    return acc;
+  };
+
+  const int nch = (S + CHUNK_ROWS - 1) / CHUNK_ROWS;
+
+  // ---- pass 1: maxima of the 64 interleaved groups -------------------------
+  float mx[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) mx[i] = -INFINITY;
+
+  auto group_max = [&](const f32x16_t& acc, int c, int half) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int row = c * CHUNK_ROWS + acc_row(j, kh);
+      const float v = row < S ? acc[j] : -INFINITY;
+      mx[half * 16 + j] = fmaxf(mx[half * 16 + j], v);
+    }
+  };
+
+  load_chunk(0);
+  store_chunk(0);
+  __syncthreads();
+  for (int c = 0; c < nch; c += 2) {
+    if (c + 1 < nch) load_chunk(c + 1);
+    group_max(tile_mma(0), c, 0);
+    if (c + 1 < nch) store_chunk(1);
+    __syncthreads();
+    if (c + 1 < nch) {
+      if (c + 2 < nch) load_chunk(c + 2);
+      group_max(tile_mma(1), c + 1, 1);
+      if (c + 2 < nch) store_chunk(0);
+      __syncthreads();
+    }
+  }
+
+  // Threshold = k-th largest of this token's 64 group maxima (32 in this lane,
+  // 32 in lane ^ 32).  Sort both halves, form the bitonic half-cleaner of the
+  // 64-element sequence (mine descending, partner's reversed) and merge.
+  float th;
+  {
+    sort_desc_regs<32>(mx);
+    float part[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) part[i] = __shfl_xor(mx[31 - i], 32, WAVE);
+    float sel[32];
+    if (k <= 32) {
+#pragma unroll
+      for (int i = 0; i < 32; ++i) sel[i] = fmaxf(mx[i], part[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 32; ++i) sel[i] = fminf(mx[i], part[i]);
+    }
+    merge_desc_regs<32>(sel);
+    const int want = (k <= 32) ? k - 1 : k - 33;
+    th = sel[0];
+#pragma unroll
+    for (int i = 1; i < 32; ++i) th = (i == want) ? sel[i] : th;
+  }
+
+  // ---- pass 2: collect candidates >= threshold ------------------------------
+  if (tid < SEARCH_TOK) cnt[tid] = 0;
+  const size_t rid = ((size_t)(tok_ok ? tok : 0) * H + h) * 2 + p;
+  uint64_t* my_cand = cand + rid * CAND_CAP;
+  int* my_cnt = &cnt[wave * 32 + col];
+
+  auto collect = [&](const f32x16_t& acc, int c) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int row = c * CHUNK_ROWS + acc_row(j, kh);
+      if (row < S && acc[j] >= th) m |= 1u << j;
+    }
+    if (!tok_ok) m = 0;
+    if (__ballot(m != 0) == 0) return;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if (m & (1u << j)) {
+        const int pos = atomicAdd(my_cnt, 1);
+        if (pos < CAND_CAP) my_cand[pos] = make_key(acc[j], (uint32_t)(c * CHUNK_ROWS + acc_row(j, kh)));
+      }
+    }
+  };
+
+  load_chunk(0);
+  store_chunk(0);
+  __syncthreads();
+  for (int c = 0; c < nch; c += 2) {
+    if (c + 1 < nch) load_chunk(c + 1);
+    collect(tile_mma(0), c);
+    if (c + 1 < nch) store_chunk(1);
+    __syncthreads();
+    if (c + 1 < nch) {
+      if (c + 2 < nch) load_chunk(c + 2);
+      collect(tile_mma(1), c + 1);
+      if (c + 2 < nch) store_chunk(0);
+      __syncthreads();
+    }
+  }
+
+  // ---- pass 3: sort each row's candidates, keep the first k ---------------
+  for (int i = 0; i < 32; ++i) {
+    const int64_t t = tile * SEARCH_TOK + wave * 32 + i;
+    if (t >= ntok) break;
+    const int c = cnt[wave * 32 + i];
+    const size_t r = ((size_t)t * H + h) * 2 + p;
+    if (c > CAND_CAP) {
+      if (lane == 0) {
+        const uint32_t slot = atomicAdd(&ovf[0], 1u);
+        ovf[1 + slot] = (uint32_t)r;
+      }
+      continue;
+    }
+    const uint64_t* rc = cand + r * CAND_CAP;
+    uint64_t key;
+    if (c <= WAVE) {
+      uint64_t v[1] = {lane < c ? rc[lane] : 0ull};
+      wave_sort_desc<1>(v, lane);
+      key = v[0];
+    } else {
+      uint64_t v[2] = {rc[lane], lane + WAVE < c ? rc[lane + WAVE] : 0ull};
+      wave_sort_desc<2>(v, lane);
+      key = v[0];
+    }
+    if (lane < k) {
+      half_idx[r * k + lane] = (int32_t)key_index(key);
+      half_score[r * k + lane] = key_score(key);
+    }
+  }
+}
+
+// Exact rescan of rows whose candidate list overflowed: all S scores of the row
+// in LDS, then k rounds of workgroup arg-max over the (score, index) keys, each
+// round restricted to keys below the previous winner (keys are distinct).
+template <typename T>
+__global__ __launch_bounds__(256) void k_topk_fallback(const T* __restrict__ q,
+                                                       const T* __restrict__ subkeys, int H, int n,
+                                                       int S, int k, const uint32_t* __restrict__ ovf,
+                                                       int32_t* __restrict__ half_idx,
+                                                       float* __restrict__ half_score) {
+  extern __shared__ float sc[];  // S scores
+  __shared__ uint64_t red[4];
+  using M = MfmaOp<T>;
+  const int d = n >> 1;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint32_t count = ovf[0];
+  for (uint32_t it = blockIdx.x; it < count; it += gridDim.x) {
+    const size_t r = ovf[1 + it];
+    const int p = (int)(r & 1);
+    const int h = (int)((r >> 1) % (size_t)H);
+    const size_t t = (r >> 1) / (size_t)H;
+    const T* qrow = q + (t * H + h) * (size_t)n + (size_t)p * d;
+    const T* kb = subkeys + (size_t)(h * 2 + p) * S * d;
+    for (int s = tid; s < S; s += 256) {
+      float acc = 0.f;
+      for (int e = 0; e < d; ++e) acc = fmaf(M::to_f32(qrow[e]), M::to_f32(kb[(size_t)s * d + e]), acc);
+      sc[s] = acc;
+    }
+    __syncthreads();
+    uint64_t prev = ~0ull;
+    for (int kk = 0; kk < k; ++kk) {
+      uint64_t best = 0;
+      for (int s = tid; s < S; s += 256) {
+        const uint64_t key = make_key(sc[s], (uint32_t)s);
+        if (key < prev) best = umax64(best, key);
+      }
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) best = umax64(best, shfl_xor_u64(best, m));
+      if (lane == 0) red[wave] = best;
+      __syncthreads();
+      best = umax64(umax64(red[0], red[1]), umax64(red[2], red[3]));
+      if (tid == 0) {
+        half_idx[r * k + kk] = (int32_t)key_index(best);
+        half_score[r * k + kk] = key_score(best);
+      }
+      prev = best;
+      __syncthreads();
+    }
+  }
+}
+
+template <int E>
+__global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ half_idx,
+                                                   const float* __restrict__ half_score,
+                                                   int64_t rows, int S, int k, int npairs,
+                                                   int64_t* __restrict__ idx_out,
+                                                   float* __restrict__ w_out,
+                                                   float* __restrict__ score_out) {
+  __shared__ uint32_t pairs[WAVE * E];
+  if (threadIdx.x == 0) {
+    int m = 0;
+    for (int a = 0; a < k; ++a)
+      for (int b = 0; b < k / (a + 1); ++b) pairs[m++] = (uint32_t(a) << 16) | uint32_t(b);
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < rows; r += (int64_t)gridDim.x * 4) {
+    const int32_t* i1 = half_idx + (size_t)r * 2 * k;
+    const int32_t* i2 = i1 + k;
+    const float* s1 = half_score + (size_t)r * 2 * k;
+    const float* s2 = s1 + k;
+    const float s1v = lane < k ? s1[lane] : 0.f;
+    const float s2v = lane < k ? s2[lane] : 0.f;
+    const int i1v = lane < k ? i1[lane] : 0;
+    const int i2v = lane < k ? i2[lane] : 0;
+    uint64_t v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int m = e * WAVE + lane;
+      const uint32_t pr = pairs[m < npairs ? m : 0];
+      const int a = (int)(pr >> 16), b = (int)(pr & 0xFFFFu);
+      const float sa = __shfl(s1v, a, WAVE), sb = __shfl(s2v, b, WAVE);
+      const int ia = __shfl(i1v, a, WAVE), ib = __shfl(i2v, b, WAVE);
+      v[e] = m < npairs ? make_key(sa + sb, (uint32_t)ia * (uint32_t)S + (uint32_t)ib) : 0ull;
+    }
+    wave_sort_desc<E>(v, lane);
+    const float z = key_score(v[0]);
+    const uint32_t ci = key_index(v[0]);
+    const float zmax = __shfl(z, 0, WAVE);
+    const float ex = lane < k ? expf(z - zmax) : 0.f;
+    const float sum = group_sum<WAVE>(ex);
+    if (lane < k) {
+      const size_t o = (size_t)r * k + lane;
+      idx_out[o] = (int64_t)ci;
+      w_out[o] = ex / sum;
+      if (score_out) score_out[o] = z;
+    }
+  }
+}
+
+int cartesian_pairs(int k) {
+  int m = 0;
+  for (int a = 0; a < k; ++a) m += k / (a + 1);
+  return m;
+}
+
+template <typename T, int NSTEP>
+static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, int H, int n, int S,
+                               int k, uint64_t* cand, int32_t* half_idx, float* half_score,
+                               uint32_t* ovf, hipStream_t st) {
+  const int64_t tiles = (T_ + SEARCH_TOK - 1) / SEARCH_TOK;
+  const int64_t blocks = tiles * 2 * H;
+  hipLaunchKernelGGL((k_score_topk<T, NSTEP>), dim3((unsigned)blocks), dim3(256), 0, st,
+                     (const T*)q, (const T*)subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t lds = (size_t)S * sizeof(float);
+  hipLaunchKernelGGL((k_topk_fallback<T>), dim3(256), dim3(256), lds, st, (const T*)q,
+                     (const T*)subkeys, H, n, S, k, (const uint32_t*)ovf, half_idx, half_score);
+  return hipGetLastError();
+}
+
+hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T_, int H,
+                              int n, int S, int k, uint64_t* cand, int32_t* half_idx,
+                              float* half_score, uint32_t* ovf, hipStream_t st) {
+  hipError_t e = launch_fill_u32(ovf, 0u, 1, st);
+  if (e != hipSuccess) return e;
+  const int d = n / 2;
+  if (bf16) {
+    const int steps = (d + 15) / 16;
+    if (steps <= 1) return launch_score<uint16_t, 1>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+    if (steps <= 2) return launch_score<uint16_t, 2>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+    if (steps <= 4) return launch_score<uint16_t, 4>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+    if (steps <= 8) return launch_score<uint16_t, 8>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+    return launch_score<uint16_t, 16>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+  }
+  const int steps = (d + 1) / 2;
+  if (steps <= 2) return launch_score<float, 2>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+  if (steps <= 4) return launch_score<float, 4>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+  if (steps <= 8) return launch_score<float, 8>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+  if (steps <= 16) return launch_score<float, 16>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+  return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+}
+
+hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T_, int H,
+                            int S, int k, int64_t* idx_out, float* w_out, float* score_out,
+                            hipStream_t st) {
+  const int64_t rows = T_ * H;
+  const int np = cartesian_pairs(k);
+  int64_t blocks = (rows + 3) / 4;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  const dim3 g((unsigned)blocks), b(256);
+  if (np <= 64) hipLaunchKernelGGL(k_cartesian<1>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
+  else if (np <= 128) hipLaunchKernelGGL(k_cartesian<2>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
+  else if (np <= 256) hipLaunchKernelGGL(k_cartesian<4>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
+  else hipLaunchKernelGGL(k_cartesian<8>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
+  return hipGetLastError();
+}
+
+}  // namespace pk

@@ -1,0 +1,419 @@
+// Atomic-free EmbeddingBag backward on gfx950 ("reverse indices" of Sec. 3.1.4
+// of "Memory Layers at Scale": invert the lookup -> row mapping so that each
+// gradient row knows which lookups contribute to it).
+//
+//   1. Stable LSD radix sort of the L = T*H*k lookups by row: 8-bit digits,
+//      per pass a tile histogram, a device-wide exclusive scan of the
+//      digit-major histogram, and a stable scatter whose in-tile ranks come
+//      from wave ballots.  Keys are rows (< 2^26), values lookup ids.
+//   2. Segment heads (first lookup of each distinct row) -> seg_start[U + 1].
+//   3. One lane group per touched row: read the value row once, then for each
+//      contributing lookup (in lookup order) read dy[t], add w * dy into a
+//      register accumulator and write grad_w = dy . V[row]; finally one
+//      read-modify-write of the fp32 gradient row (dense) or one write of the
+//      row's gradient (sparse).  Rows are visited in ascending order, so the
+//      value and gradient tables are streamed nearly sequentially, and the
+//      result is bitwise deterministic.
+#include "pk_device.h"
+#include "pk_internal.h"
+
+namespace pk {
+
+constexpr int RADIX_BITS = 8;
+constexpr int RADIX = 1 << RADIX_BITS;
+constexpr int SORT_ITEMS = 16;                 // keys per thread per tile
+constexpr int SORT_TILE = 256 * SORT_ITEMS;    // keys per workgroup tile
+constexpr int SCAN_ITEMS = 8;
+constexpr int SCAN_TILE = 256 * SCAN_ITEMS;
+
+static inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ------------------------------------------------------------------ scan ----
+// Exclusive prefix sum of u32, any length, in three launches.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum, uint32_t& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int o = 1; o < WAVE; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, WAVE);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  uint32_t before = 0;
+  for (int w = 0; w < wave; ++w) before += wsum[w];
+  total = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+  __syncthreads();
+  return before + x - v;
+}
+
+__global__ __launch_bounds__(256) void k_scan_reduce(const uint32_t* __restrict__ in, int64_t n,
+                                                     uint32_t* __restrict__ sums) {
+  __shared__ uint32_t wsum[4];
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
+  uint32_t s = 0;
+#pragma unroll
+  for (int i = 0; i < SCAN_ITEMS; ++i)
+    if (base + i < n) s += in[base + i];
+  uint32_t total;
+  block_exclusive_scan(s, wsum, total);
+  if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+// Single workgroup: exclusive scan of the tile sums, in place, any count.
+__global__ __launch_bounds__(256) void k_scan_top(uint32_t* __restrict__ sums, int64_t nb) {
+  __shared__ uint32_t wsum[4];
+  uint32_t carry = 0;
+  for (int64_t base = 0; base < nb; base += SCAN_TILE) {
+    const int64_t b0 = base + threadIdx.x * SCAN_ITEMS;
+    uint32_t v[SCAN_ITEMS];
+    uint32_t s = 0;
+#pragma unroll
+    for (int i = 0; i < SCAN_ITEMS; ++i) {
+      v[i] = (b0 + i < nb) ? sums[b0 + i] : 0u;
+      s += v[i];
+    }
+    uint32_t total;
+    uint32_t run = carry + block_exclusive_scan(s, wsum, total);
+#pragma unroll
+    for (int i = 0; i < SCAN_ITEMS; ++i) {
+      if (b0 + i < nb) sums[b0 + i] = run;
+      run += v[i];
+    }
+    carry += total;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_scan_down(const uint32_t* __restrict__ in,
+                                                   uint32_t* __restrict__ out, int64_t n,
+                                                   const uint32_t* __restrict__ sums) {
+  __shared__ uint32_t wsum[4];
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
+  uint32_t v[SCAN_ITEMS];
+  uint32_t s = 0;
+#pragma unroll
+  for (int i = 0; i < SCAN_ITEMS; ++i) {
+    v[i] = (base + i < n) ? in[base + i] : 0u;
+    s += v[i];
+  }
+  uint32_t total;
+  uint32_t run = sums[blockIdx.x] + block_exclusive_scan(s, wsum, total);
+#pragma unroll
+  for (int i = 0; i < SCAN_ITEMS; ++i) {
+    if (base + i < n) out[base + i] = run;
+    run += v[i];
+  }
+}
+
+static hipError_t exclusive_scan(uint32_t* data, int64_t n, uint32_t* sums, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int64_t nb = cdiv(n, SCAN_TILE);
+  hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(256), 0, st, data, n, sums);
+  hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(256), 0, st, sums, nb);
+  hipLaunchKernelGGL(k_scan_down, dim3((unsigned)nb), dim3(256), 0, st, data, data, n, sums);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------- radix sort ----
+// Keys of the first pass come straight from the int64 lookup rows, values are
+// the lookup ids themselves.
+template <bool FIRST>
+__device__ __forceinline__ uint32_t sort_key(const void* keys, int64_t i) {
+  if constexpr (FIRST) return (uint32_t)reinterpret_cast<const int64_t*>(keys)[i];
+  else return reinterpret_cast<const uint32_t*>(keys)[i];
+}
+
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_radix_hist(const void* __restrict__ keys, int64_t L,
+                                                    int shift, int bits, int64_t nblk,
+                                                    uint32_t* __restrict__ hist) {
+  __shared__ uint32_t h[RADIX];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const uint32_t mask = (1u << bits) - 1u;
+  const int64_t tile = (int64_t)blockIdx.x * SORT_TILE;
+#pragma unroll 4
+  for (int i = 0; i < SORT_ITEMS; ++i) {
+    const int64_t pos = tile + i * 256 + threadIdx.x;
+    if (pos < L) atomicAdd(&h[(sort_key<FIRST>(keys, pos) >> shift) & mask], 1u);
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
+}
+
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ keys_in,
+                                                       const uint32_t* __restrict__ vals_in,
+                                                       int64_t L, int shift, int bits, int64_t nblk,
+                                                       const uint32_t* __restrict__ offsets,
+                                                       uint32_t* __restrict__ keys_out,
+                                                       uint32_t* __restrict__ vals_out) {
+  __shared__ uint32_t run[RADIX];
+  __shared__ uint32_t wcnt[4][RADIX];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  run[tid] = offsets[(int64_t)tid * nblk + blockIdx.x];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) wcnt[w][tid] = 0;
+  __syncthreads();
+  const uint32_t mask = (1u << bits) - 1u;
+  const uint64_t below = (1ull << lane) - 1ull;
+  const int64_t tile = (int64_t)blockIdx.x * SORT_TILE;
+  for (int i = 0; i < SORT_ITEMS; ++i) {
+    // Items are taken in position order: slot-major, then thread order.
+    const int64_t pos = tile + i * 256 + tid;
+    const bool valid = pos < L;
+    const uint32_t key = valid ? sort_key<FIRST>(keys_in, pos) : 0u;
+    const uint32_t val = valid ? (FIRST ? (uint32_t)pos : vals_in[pos]) : 0u;
+    const uint32_t dig = (key >> shift) & mask;
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < bits; ++b) {
+      const bool bit = (dig >> b) & 1u;
+      const uint64_t set = __ballot(bit);
+      peers &= bit ? set : ~set;
+    }
+    const uint32_t rank = (uint32_t)__popcll(peers & below);
+    const uint32_t total = (uint32_t)__popcll(peers);
+    const bool leader = valid && rank == 0;
+    if (leader) wcnt[wave][dig] = total;
+    __syncthreads();
+    if (valid) {
+      uint32_t dst = run[dig] + rank;
+      for (int w = 0; w < wave; ++w) dst += wcnt[w][dig];
+      keys_out[dst] = key;
+      vals_out[dst] = val;
+    }
+    __syncthreads();
+    if (leader) {
+      atomicAdd(&run[dig], total);
+      wcnt[wave][dig] = 0;
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------- segments ----
+__global__ __launch_bounds__(256) void k_seg_flags(const uint32_t* __restrict__ keys, int64_t L,
+                                                   uint32_t* __restrict__ flags) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < L) flags[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1u : 0u;
+}
+
+__global__ __launch_bounds__(256) void k_seg_starts(const uint32_t* __restrict__ keys, int64_t L,
+                                                    const uint32_t* __restrict__ excl,
+                                                    uint32_t* __restrict__ seg_start,
+                                                    uint32_t* __restrict__ nseg) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= L) return;
+  const bool head = (i == 0 || keys[i] != keys[i - 1]);
+  if (head) seg_start[excl[i]] = (uint32_t)i;
+  if (i == L - 1) {
+    const uint32_t U = excl[i] + (head ? 1u : 0u);
+    seg_start[U] = (uint32_t)L;
+    *nseg = U;
+  }
+}
+
+// ------------------------------------------------------- per-row backward ----
+template <typename V>
+struct Row16s;
+template <>
+struct Row16s<uint16_t> {
+  static constexpr int N = 8;
+  __device__ static __forceinline__ void unpack(const uint4& v, float (&f)[8]) {
+    f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
+    f[4] = bf16_lo(v.z); f[5] = bf16_hi(v.z); f[6] = bf16_lo(v.w); f[7] = bf16_hi(v.w);
+  }
+};
+template <>
+struct Row16s<float> {
+  static constexpr int N = 4;
+  __device__ static __forceinline__ void unpack(const uint4& v, float (&f)[4]) {
+    f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+  }
+};
+
+__device__ __forceinline__ uint4 ldg16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+template <typename V, int CPL, int CL, bool SPARSE>
+__global__ __launch_bounds__(256) void k_bag_bwd_rows(
+    const V* __restrict__ dy, const V* __restrict__ values, int D, const float* __restrict__ w,
+    int bag, const uint32_t* __restrict__ rows_sorted, const uint32_t* __restrict__ lookups,
+    const uint32_t* __restrict__ seg_start, const uint32_t* __restrict__ nseg,
+    float* __restrict__ grad_values, int64_t* __restrict__ rows_out,
+    float* __restrict__ grad_rows_out, float* __restrict__ grad_w) {
+  using R = Row16s<V>;
+  constexpr int G = WAVE / CL;
+  const int lane = threadIdx.x & 63;
+  const int grp = lane / CL, cl = lane % CL;
+  const int C = D / R::N;
+  const uint32_t U = *nseg;
+  bool ok[CPL];
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) ok[i] = (i * CL + cl) < C;
+
+  const int64_t groups = (int64_t)gridDim.x * 4 * G;
+  for (int64_t u = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * G + grp; u < U; u += groups) {
+    const uint32_t s0 = seg_start[u], s1 = seg_start[u + 1];
+    const int64_t row = rows_sorted[s0];
+    float vr[CPL][R::N], acc[CPL][R::N];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const uint4 v = ok[i] ? ldg16(values + row * D + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
+      R::unpack(v, vr[i]);
+#pragma unroll
+      for (int e = 0; e < R::N; ++e) acc[i][e] = 0.f;
+    }
+    for (uint32_t s = s0; s < s1; ++s) {
+      const uint32_t l = lookups[s];
+      const int64_t t = l / (uint32_t)bag;
+      const float ww = w[l];
+      float part = 0.f;
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+        const uint4 v = ok[i] ? ldg16(dy + t * D + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
+        float g[R::N];
+        R::unpack(v, g);
+#pragma unroll
+        for (int e = 0; e < R::N; ++e) {
+          acc[i][e] = fmaf(ww, g[e], acc[i][e]);
+          part = fmaf(g[e], vr[i][e], part);
+        }
+      }
+      part = group_sum<CL>(part);
+      if (cl == 0) grad_w[l] = part;
+    }
+    if (!SPARSE && grad_values == nullptr) continue;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      if (!ok[i]) continue;
+      const size_t c0 = (size_t)(i * CL + cl) * R::N;
+      float* dst = SPARSE ? grad_rows_out + (size_t)u * D + c0 : grad_values + row * D + c0;
+#pragma unroll
+      for (int e0 = 0; e0 < R::N; e0 += 4) {
+        float4 o = make_float4(acc[i][e0], acc[i][e0 + 1], acc[i][e0 + 2], acc[i][e0 + 3]);
+        if (!SPARSE) {
+          const float4 old = *reinterpret_cast<const float4*>(dst + e0);
+          o.x += old.x; o.y += old.y; o.z += old.z; o.w += old.w;
+        }
+        *reinterpret_cast<float4*>(dst + e0) = o;
+      }
+    }
+    if (SPARSE && lane % CL == 0) rows_out[u] = row;
+  }
+}
+
+// -------------------------------------------------------------- launcher ----
+struct SortedWs {
+  uint32_t *keys_a, *vals_a, *keys_b, *vals_b, *hist, *sums, *seg, *misc;
+};
+
+static SortedWs carve(void* ws, int64_t L) {
+  const int64_t nblk = cdiv(L, SORT_TILE);
+  const int64_t hist_n = (int64_t)RADIX * nblk;
+  const int64_t scan_n = (hist_n > L + 1 ? hist_n : L + 1);
+  char* p = reinterpret_cast<char*>(ws);
+  SortedWs w;
+  auto take = [&](size_t bytes) { uint32_t* r = reinterpret_cast<uint32_t*>(p); p += align256(bytes); return r; };
+  w.keys_a = take(4 * (size_t)L);
+  w.vals_a = take(4 * (size_t)L);
+  w.keys_b = take(4 * (size_t)L);
+  w.vals_b = take(4 * (size_t)L);
+  w.hist = take(4 * (size_t)scan_n);
+  w.sums = take(4 * (size_t)(cdiv(scan_n, SCAN_TILE) + 1));
+  w.seg = take(4 * (size_t)(L + 1));
+  w.misc = take(256);
+  return w;
+}
+
+size_t sorted_workspace_bytes(int64_t L) {
+  const int64_t nblk = cdiv(L, SORT_TILE);
+  const int64_t hist_n = (int64_t)RADIX * nblk;
+  const int64_t scan_n = (hist_n > L + 1 ? hist_n : L + 1);
+  return 4 * align256(4 * (size_t)L) + align256(4 * (size_t)scan_n) +
+         align256(4 * (size_t)(cdiv(scan_n, SCAN_TILE) + 1)) + align256(4 * (size_t)(L + 1)) + 256;
+}
+
+hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* values, int64_t N,
+                                      int D, const int64_t* idx, const float* w, int64_t T,
+                                      int bag, float* grad_values, int64_t* rows_out,
+                                      float* grad_rows_out, float* grad_w, void* ws,
+                                      uint32_t** num_rows_dev, hipStream_t st) {
+  const int64_t L = T * bag;
+  SortedWs b = carve(ws, L);
+  if (num_rows_dev) *num_rows_dev = b.misc;
+  hipError_t e = launch_fill_u32(b.misc, 0u, 1, st);
+  if (e != hipSuccess || L == 0) return e;
+
+  // 1. radix sort of (row, lookup) by row
+  int key_bits = 1;
+  while (key_bits < 32 && (int64_t(1) << key_bits) < N) ++key_bits;
+  const int64_t nblk = cdiv(L, SORT_TILE);
+  const void* kin = idx;
+  const uint32_t* vin = nullptr;
+  uint32_t *kout = b.keys_a, *vout = b.vals_a;
+  for (int shift = 0, pass = 0; shift < key_bits; shift += RADIX_BITS, ++pass) {
+    const int bits = (key_bits - shift) < RADIX_BITS ? (key_bits - shift) : RADIX_BITS;
+    if (pass == 0)
+      hipLaunchKernelGGL(k_radix_hist<true>, dim3((unsigned)nblk), dim3(256), 0, st, kin, L, shift, bits, nblk, b.hist);
+    else
+      hipLaunchKernelGGL(k_radix_hist<false>, dim3((unsigned)nblk), dim3(256), 0, st, kin, L, shift, bits, nblk, b.hist);
+    e = exclusive_scan(b.hist, (int64_t)RADIX * nblk, b.sums, st);
+    if (e != hipSuccess) return e;
+    if (pass == 0)
+      hipLaunchKernelGGL(k_radix_scatter<true>, dim3((unsigned)nblk), dim3(256), 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+    else
+      hipLaunchKernelGGL(k_radix_scatter<false>, dim3((unsigned)nblk), dim3(256), 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+    kin = kout;
+    vin = vout;
+    if (kout == b.keys_a) { kout = b.keys_b; vout = b.vals_b; }
+    else { kout = b.keys_a; vout = b.vals_a; }
+  }
+  const uint32_t* ks = reinterpret_cast<const uint32_t*>(kin);
+  const uint32_t* vs = vin;
+
+  // 2. segments of equal rows
+  const unsigned lb = (unsigned)cdiv(L, 256);
+  hipLaunchKernelGGL(k_seg_flags, dim3(lb), dim3(256), 0, st, ks, L, b.hist);
+  e = exclusive_scan(b.hist, L, b.sums, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_seg_starts, dim3(lb), dim3(256), 0, st, ks, L, b.hist, b.seg, b.misc);
+
+  // 3. one lane group per touched row
+  const int C = D * (bf16 ? 2 : 4) / 16;
+  int64_t blocks = cdiv(L, 4);
+  if (blocks > 16384) blocks = 16384;
+  const dim3 grid((unsigned)blocks), block(256);
+  const bool sparse = rows_out != nullptr;
+#define PK_ROWS(CPL, CL)                                                                          \
+  if (bf16) {                                                                                     \
+    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, CPL, CL, true>), grid, block, 0, st,  \
+        (const uint16_t*)dy, (const uint16_t*)values, D, w, bag, ks, vs, b.seg, b.misc,            \
+        grad_values, rows_out, grad_rows_out, grad_w);                                            \
+    else hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, CPL, CL, false>), grid, block, 0, st,       \
+        (const uint16_t*)dy, (const uint16_t*)values, D, w, bag, ks, vs, b.seg, b.misc,            \
+        grad_values, rows_out, grad_rows_out, grad_w);                                            \
+  } else {                                                                                        \
+    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<float, CPL, CL, true>), grid, block, 0, st,     \
+        (const float*)dy, (const float*)values, D, w, bag, ks, vs, b.seg, b.misc, grad_values,     \
+        rows_out, grad_rows_out, grad_w);                                                         \
+    else hipLaunchKernelGGL((k_bag_bwd_rows<float, CPL, CL, false>), grid, block, 0, st,          \
+        (const float*)dy, (const float*)values, D, w, bag, ks, vs, b.seg, b.misc, grad_values,     \
+        rows_out, grad_rows_out, grad_w);                                                         \
+  }
+  if (C > 256) { PK_ROWS(8, 64); }
+  else if (C > 128) { PK_ROWS(4, 64); }
+  else if (C > 64) { PK_ROWS(2, 64); }
+  else if (C > 32) { PK_ROWS(1, 64); }
+  else if (C > 16) { PK_ROWS(1, 32); }
+  else if (C > 8) { PK_ROWS(1, 16); }
+  else if (C > 4) { PK_ROWS(1, 8); }
+  else if (C > 2) { PK_ROWS(1, 4); }
+  else if (C > 1) { PK_ROWS(1, 2); }
+  else { PK_ROWS(1, 1); }
+#undef PK_ROWS
+  return hipGetLastError();
+}
+
+}  // namespace pk

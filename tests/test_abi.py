@@ -1,0 +1,164 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+include/pkmem.h declares, and rejects bad arguments on the host with the
+documented status codes before any HIP call (pointer arguments here are fake,
+aligned addresses that are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2412_09764_amd as pk
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pkmem.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, -1, -2, -3
+F32, BF16 = 0, 1
+FAKE = 0x10000  # 256-byte aligned, never dereferenced
+BIG_WS = 1 << 40
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(mem_[a-z_]+)\s*\(", src, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(pk.lib_path()):
+        pytest.fail("libpkmem.so is not built (run __graft_entry__.build())")
+    return pk.load()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("mem_search", "mem_bag_forward", "mem_bag_backward", "mem_bag_backward_sparse",
+              "mem_search_workspace_size", "mem_bag_backward_workspace_size", "mem_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+    assert lib.mem_version() == 1
+
+
+def search(lib, q=FAKE, qdt=BF16, K=FAKE, kdt=BF16, T=8, H=2, n=64, S=16, k=4, idx=FAKE, w=FAKE,
+           ws=FAKE, ws_bytes=BIG_WS):
+    return lib.mem_search(q, qdt, K, kdt, T, H, n, S, k, idx, w, None, None, ws, ws_bytes, None)
+
+
+def msg(lib):
+    return lib.mem_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(n=63), INVALID, "even"),
+    (dict(n=0), INVALID, "even"),
+    (dict(k=0), INVALID, "k <= S"),
+    (dict(k=17), INVALID, "k <= S"),
+    (dict(S=100, k=65), UNSUPPORTED, "k >"),
+    (dict(S=8193), UNSUPPORTED, "S >"),
+    (dict(S=0), INVALID, "S must"),
+    (dict(H=0), INVALID, "H must"),
+    (dict(T=-1), INVALID, "T must"),
+    (dict(n=20), UNSUPPORTED, "multiple of 8"),
+    (dict(n=1024), UNSUPPORTED, "<= 256"),
+    (dict(qdt=F32, kdt=F32, n=256), UNSUPPORTED, "fp32"),
+    (dict(qdt=F32), UNSUPPORTED, "share a dtype"),
+    (dict(qdt=7, kdt=7), INVALID, "dtype"),
+    (dict(q=0), INVALID, "null"),
+    (dict(idx=0), INVALID, "null"),
+    (dict(q=FAKE + 8), INVALID, "aligned"),
+    (dict(ws=0), WORKSPACE, "workspace"),
+    (dict(ws_bytes=16), WORKSPACE, "workspace"),
+    (dict(ws=FAKE + 64), INVALID, "256-byte"),
+])
+def test_search_rejects(lib, kw, code, text):
+    assert search(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def test_search_empty_batch_is_a_noop(lib):
+    assert search(lib, T=0) == OK
+
+
+def test_workspace_sizes(lib):
+    a = lib.mem_search_workspace_size(1000, 4, 2048, 32)
+    b = lib.mem_search_workspace_size(2000, 4, 2048, 32)
+    assert 0 < a < b
+    assert lib.mem_search_workspace_size(-1, 4, 2048, 32) == 0
+    s = lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 2048, 2)
+    at = lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 2048, 1)
+    assert s > at >= 1000 * 4 * 32 * 4
+    # auto picks the sorted strategy for wide rows and atomics for narrow ones
+    assert lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 2048, 0) == s
+    assert lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 64, 0) == at
+
+
+def fwd(lib, V=FAKE, vdt=BF16, N=4096, D=64, idx=FAKE, w=FAKE, T=4, bag=8, y=FAKE):
+    return lib.mem_bag_forward(V, vdt, N, D, idx, w, T, bag, y, None)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(D=12), UNSUPPORTED, "multiple of 8"),
+    (dict(D=0), UNSUPPORTED, "multiple of 8"),
+    (dict(D=4104), UNSUPPORTED, "8 KiB"),
+    (dict(vdt=F32, D=2056), UNSUPPORTED, "8 KiB"),
+    (dict(N=0), INVALID, "N must"),
+    (dict(bag=0), INVALID, "bag"),
+    (dict(T=-2), INVALID, "T must"),
+    (dict(vdt=5), INVALID, "dtype"),
+    (dict(V=0), INVALID, "null"),
+    (dict(y=0), INVALID, "null"),
+    (dict(y=FAKE + 4), INVALID, "aligned"),
+])
+def test_bag_forward_rejects(lib, kw, code, text):
+    assert fwd(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def test_bag_forward_empty_batch_is_a_noop(lib):
+    assert fwd(lib, T=0) == OK
+
+
+def bwd(lib, dy=FAKE, V=FAKE, vdt=BF16, N=4096, D=64, idx=FAKE, w=FAKE, T=4, H=2, k=4, gv=FAKE,
+        gw=FAKE, gz=FAKE, mode=0, ws=FAKE, ws_bytes=BIG_WS):
+    return lib.mem_bag_backward(dy, V, vdt, N, D, idx, w, T, H, k, gv, gw, gz, mode, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(mode=3), INVALID, "mode"),
+    (dict(H=0), INVALID, "H and k"),
+    (dict(k=0), INVALID, "H and k"),
+    (dict(D=9), UNSUPPORTED, "multiple of 8"),
+    (dict(dy=0), INVALID, "null"),
+    (dict(ws=0), WORKSPACE, "workspace"),
+    (dict(ws_bytes=100), WORKSPACE, "workspace"),
+    (dict(ws=FAKE + 128), INVALID, "256-byte"),
+    (dict(gv=FAKE + 4), INVALID, "aligned"),
+])
+def test_bag_backward_rejects(lib, kw, code, text):
+    assert bwd(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def test_bag_backward_empty_batch_is_a_noop(lib):
+    assert bwd(lib, T=0) == OK
+
+
+def test_sparse_backward_rejects(lib):
+    nrows = ctypes.c_int64(-1)
+    f = lib.mem_bag_backward_sparse
+    # cap below min(T*H*k, N)
+    rc = f(FAKE, FAKE, BF16, 4096, 64, FAKE, FAKE, 4, 2, 4, FAKE, FAKE, 31, ctypes.addressof(nrows),
+           None, None, FAKE, BIG_WS, None)
+    assert rc == INVALID and "cap" in msg(lib)
+    rc = f(FAKE, FAKE, BF16, 4096, 64, FAKE, FAKE, 4, 2, 4, None, FAKE, 32, ctypes.addressof(nrows),
+           None, None, FAKE, BIG_WS, None)
+    assert rc == INVALID and "required" in msg(lib)
+    rc = f(FAKE, FAKE, BF16, 4096, 64, FAKE, FAKE, 0, 2, 4, FAKE, FAKE, 32, ctypes.addressof(nrows),
+           None, None, FAKE, BIG_WS, None)
+    assert rc == OK and nrows.value == 0

@@ -1,0 +1,264 @@
+"""GPU parity: every C-ABI entry point against the fp64 CPU oracle.
+
+Tolerances (normwise: max |gpu - ref| / max |ref|):
+  * indices: bit-exact (integer-valued queries and sub-keys make every score an
+    exact integer in fp32, so selection and tie-breaks are exact);
+  * fp32 outputs (scores, softmax weights, value / weight / score gradients):
+    1e-5;
+  * bf16 outputs (bag forward with bf16 values): 2e-2, the bound the workload
+    sets for bf16 values (the kernel's own error is one bf16 rounding, 2^-9).
+Float-valued queries can make two candidates tie to within fp32 rounding; there
+the oracle certifies each index mismatch by its own score gap.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2412_09764_amd.inputs import WORKLOADS
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32 = 1e-5
+TOL_BF16 = 2e-2
+
+
+def normwise(gpu, ref):
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.abs(ref).max()
+    return float(np.abs(gpu - ref).max() / (den if den > 0 else 1.0))
+
+
+def h64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def int_tensor(shape, seed, dtype, lo=-4, hi=4):
+    g = torch.Generator().manual_seed(seed)
+    return torch.randint(lo, hi + 1, shape, generator=g).to(dtype)
+
+
+def normal_tensor(shape, seed, dtype, std=1.0):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn(shape, generator=g) * std).to(dtype)
+
+
+SEARCH_CASES = [
+    # (name, S, H, n, k, T, dtype)
+    ("tiny_f32_S64_k8", 64, 1, 64, 8, 256, torch.float32),
+    ("bf16_S1024_H4_k32_ragged", 1024, 4, 512, 32, 200, torch.bfloat16),
+    ("bf16_S100_oddtile", 100, 2, 64, 16, 130, torch.bfloat16),
+    ("bf16_k_eq_S", 37, 3, 32, 37, 65, torch.bfloat16),
+    ("bf16_k1", 512, 1, 16, 1, 300, torch.bfloat16),
+    ("bf16_k64", 256, 2, 128, 64, 70, torch.bfloat16),
+    ("f32_d64_S200", 200, 2, 128, 20, 99, torch.float32),
+    ("bf16_S2048_d256", 2048, 4, 512, 32, 129, torch.bfloat16),
+]
+
+
+@pytest.mark.parametrize("case", SEARCH_CASES, ids=[c[0] for c in SEARCH_CASES])
+def test_search_integer_inputs_exact(gpu_lib, case):
+    name, S, H, n, k, T, dt = case
+    print(f"[search] {name}", flush=True)
+    q = int_tensor((T, H, n), 11, dt)
+    K = int_tensor((H, 2, S, n // 2), 12, dt)
+    idx, w, score, hidx = gpu_lib.mem_search(q.cuda(), K.cuda(), k, want_half=True)
+    torch.cuda.synchronize()
+    ref = oracle.search(h64(q), h64(K), k)
+    np.testing.assert_array_equal(hidx.cpu().numpy(), ref["half_idx"])
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    np.testing.assert_array_equal(h64(score), ref["score"])
+    assert normwise(h64(w), ref["w"]) <= TOL_F32
+
+
+def test_search_all_ties_use_the_exact_fallback(gpu_lib):
+    # every score equal: each row's candidate list overflows; the result is the
+    # k lowest composed indices
+    T, H, S, n, k = 70, 2, 300, 32, 16
+    q = torch.ones((T, H, n), dtype=torch.bfloat16).cuda()
+    K = torch.ones((H, 2, S, n // 2), dtype=torch.bfloat16).cuda()
+    idx, w, score, hidx = gpu_lib.mem_search(q, K, k, want_half=True)
+    torch.cuda.synchronize()
+    want = np.broadcast_to(np.arange(k), (T, H, k))
+    np.testing.assert_array_equal(idx.cpu().numpy(), want)
+    np.testing.assert_array_equal(hidx.cpu().numpy(), np.broadcast_to(np.arange(k), (T, H, 2, k)))
+    np.testing.assert_allclose(w.cpu().numpy(), 1.0 / k, rtol=1e-6)
+
+
+def _certify_near_ties(q, K, k, gpu_idx, ref, rel_gap=1e-4):
+    """Accept index mismatches only where the oracle's fp64 full scores of the
+    GPU's choice and of its own differ by at most rel_gap * max|score|."""
+    T, H, n = q.shape
+    d = n // 2
+    S = K.shape[2]
+    bad = 0
+    for t, h in zip(*np.nonzero((gpu_idx != ref["idx"]).any(-1))):
+        i = gpu_idx[t, h]
+        full = q[t, h, :d] @ K[h, 0, i // S].T + q[t, h, d:] @ K[h, 1, i % S].T
+        scale = np.abs(ref["score"][t, h]).max()
+        if not np.all(np.abs(np.sort(full)[::-1] - ref["score"][t, h]) <= rel_gap * scale):
+            bad += 1
+    return bad
+
+
+@pytest.mark.parametrize("wl_name", ["pk4k_d64_f32", "pk4m_d2048"])
+def test_search_float_inputs(gpu_lib, wl_name):
+    wl = WORKLOADS[wl_name]
+    T = min(wl.T, 256)
+    print(f"[search-float] {wl_name} T={T}", flush=True)
+    from paper_2412_09764_amd.inputs import gen_queries, gen_subkeys
+    q = gen_queries(wl, "cpu", T=T)
+    K = gen_subkeys(wl, "cpu")
+    idx, w, score, _ = gpu_lib.mem_search(q.cuda(), K.cuda(), wl.k)
+    torch.cuda.synchronize()
+    ref = oracle.search(h64(q), h64(K), wl.k)
+    gi = idx.cpu().numpy()
+    mism = (gi != ref["idx"]).any(-1).sum()
+    assert _certify_near_ties(h64(q), h64(K), wl.k, gi, ref) == 0
+    assert mism <= max(1, T * wl.H // 100)
+    ok = (gi == ref["idx"]).all(-1)
+    assert normwise(h64(score)[ok], ref["score"][ok]) <= TOL_F32
+    assert normwise(h64(w)[ok], ref["w"][ok]) <= TOL_F32
+
+
+def test_search_empty_batch(gpu_lib):
+    q = torch.zeros((0, 2, 64), dtype=torch.bfloat16).cuda()
+    K = torch.zeros((2, 2, 64, 32), dtype=torch.bfloat16).cuda()
+    idx, w, _, _ = gpu_lib.mem_search(q, K, 4)
+    torch.cuda.synchronize()
+    assert idx.shape == (0, 2, 4)
+
+
+BAG_CASES = [
+    # (name, N, D, T, H, k, dtype)
+    ("f32_D64", 4096, 64, 256, 1, 8, torch.float32),
+    ("bf16_D1024", 5000, 1024, 130, 4, 32, torch.bfloat16),
+    ("bf16_D2048", 3000, 2048, 67, 4, 32, torch.bfloat16),
+    ("bf16_D256", 9000, 256, 301, 4, 32, torch.bfloat16),
+    ("bf16_D24_nonpow2", 777, 24, 90, 2, 5, torch.bfloat16),
+    ("bf16_D8", 50, 8, 33, 3, 3, torch.bfloat16),
+    ("bf16_D4096", 700, 4096, 21, 2, 16, torch.bfloat16),
+    ("f32_D2048", 900, 2048, 40, 2, 8, torch.float32),
+]
+
+
+def bag_inputs(N, D, T, H, k, dt, seed=0, hot=None):
+    g = torch.Generator().manual_seed(seed)
+    V = (torch.randn((N, D), generator=g) * 0.02).to(dt)
+    if hot is None:
+        idx = torch.randint(0, N, (T, H, k), generator=g)
+    else:
+        idx = torch.randint(0, hot, (T, H, k), generator=g)
+    idx[0, -1] = idx[0, 0]  # a row chosen by two heads of one token
+    z = torch.randn((T, H, k), generator=g, dtype=torch.float64)
+    w = torch.softmax(z, -1).float()
+    dy = torch.randn((T, D), generator=g).to(dt)
+    return V, idx, w, dy
+
+
+@pytest.mark.parametrize("case", BAG_CASES, ids=[c[0] for c in BAG_CASES])
+def test_bag_forward(gpu_lib, case):
+    name, N, D, T, H, k, dt = case
+    print(f"[bag-fwd] {name}", flush=True)
+    V, idx, w, dy = bag_inputs(N, D, T, H, k, dt)
+    y = gpu_lib.mem_bag_forward(V.cuda(), idx.cuda(), w.cuda())
+    torch.cuda.synchronize()
+    ref = oracle.bag_forward(h64(V), idx.numpy(), h64(w))
+    tol = TOL_F32 if dt == torch.float32 else TOL_BF16
+    assert normwise(h64(y), ref) <= tol
+    if dt == torch.bfloat16:  # one bf16 rounding of the fp32 sum
+        assert np.all(np.abs(h64(y) - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-6 * np.abs(ref).max())
+
+
+@pytest.mark.parametrize("mode", ["atomic", "sorted"])
+@pytest.mark.parametrize("case", BAG_CASES, ids=[c[0] for c in BAG_CASES])
+def test_bag_backward(gpu_lib, case, mode):
+    name, N, D, T, H, k, dt = case
+    print(f"[bag-bwd] {name} {mode}", flush=True)
+    V, idx, w, dy = bag_inputs(N, D, T, H, k, dt, seed=1)
+    base = torch.randn((N, D), generator=torch.Generator().manual_seed(5))
+    gv = base.clone().cuda()
+    gv, gw, gz = gpu_lib.mem_bag_backward(dy.cuda(), V.cuda(), idx.cuda(), w.cuda(),
+                                          grad_values=gv, mode=mode)
+    torch.cuda.synchronize()
+    ref = oracle.bag_backward(h64(dy), h64(V), idx.numpy(), h64(w), H, k)
+    assert normwise(h64(gv) - h64(base), ref["grad_values"]) <= TOL_F32
+    assert normwise(h64(gw), ref["grad_w"]) <= TOL_F32
+    assert normwise(h64(gz), ref["grad_z"]) <= TOL_F32
+
+
+def test_sorted_backward_is_deterministic_and_matches_atomic(gpu_lib):
+    N, D, T, H, k = 20000, 1024, 512, 4, 32
+    V, idx, w, dy = bag_inputs(N, D, T, H, k, torch.bfloat16, seed=3, hot=3000)
+    args = (dy.cuda(), V.cuda(), idx.cuda(), w.cuda())
+    a = gpu_lib.mem_bag_backward(*args, mode="sorted")
+    b = gpu_lib.mem_bag_backward(*args, mode="sorted")
+    c = gpu_lib.mem_bag_backward(*args, mode="atomic")
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+    for x, y in zip(a, c):
+        assert normwise(h64(x), h64(y)) <= TOL_F32
+
+
+def test_hot_rows_long_segments(gpu_lib):
+    # every lookup hits one of 3 rows: segments thousands long
+    N, D, T, H, k = 1000, 256, 700, 4, 8
+    V, idx, w, dy = bag_inputs(N, D, T, H, k, torch.bfloat16, seed=4, hot=3)
+    ref = oracle.bag_backward(h64(dy), h64(V), idx.numpy(), h64(w), H, k)
+    for mode in ("sorted", "atomic"):
+        gv, gw, gz = gpu_lib.mem_bag_backward(dy.cuda(), V.cuda(), idx.cuda(), w.cuda(), mode=mode)
+        torch.cuda.synchronize()
+        assert normwise(h64(gv), ref["grad_values"]) <= TOL_F32
+        assert normwise(h64(gw), ref["grad_w"]) <= TOL_F32
+
+
+def test_three_pass_radix_sort_large_N(gpu_lib):
+    # N = 2^22 rows: 22-bit keys, three radix passes
+    N, D, T, H, k = 1 << 22, 8, 3000, 4, 32
+    V, idx, w, dy = bag_inputs(N, D, T, H, k, torch.bfloat16, seed=6)
+    rows, grows, gw, gz = gpu_lib.mem_bag_backward_sparse(dy.cuda(), V.cuda(), idx.cuda(), w.cuda())
+    torch.cuda.synchronize()
+    ref = oracle.bag_backward_rows(h64(dy), h64(V), idx.numpy(), h64(w), H, k)
+    np.testing.assert_array_equal(rows.cpu().numpy(), ref["rows"])
+    assert normwise(h64(grows), ref["grad_rows"]) <= TOL_F32
+    assert normwise(h64(gw), ref["grad_w"]) <= TOL_F32
+    assert normwise(h64(gz), ref["grad_z"]) <= TOL_F32
+
+
+@pytest.mark.parametrize("case", BAG_CASES[:4], ids=[c[0] for c in BAG_CASES[:4]])
+def test_sparse_backward(gpu_lib, case):
+    name, N, D, T, H, k, dt = case
+    V, idx, w, dy = bag_inputs(N, D, T, H, k, dt, seed=2)
+    rows, grows, gw, gz = gpu_lib.mem_bag_backward_sparse(dy.cuda(), V.cuda(), idx.cuda(), w.cuda())
+    torch.cuda.synchronize()
+    ref = oracle.bag_backward_rows(h64(dy), h64(V), idx.numpy(), h64(w), H, k)
+    np.testing.assert_array_equal(rows.cpu().numpy(), ref["rows"])
+    assert normwise(h64(grows), ref["grad_rows"]) <= TOL_F32
+    assert normwise(h64(gw), ref["grad_w"]) <= TOL_F32
+    assert normwise(h64(gz), ref["grad_z"]) <= TOL_F32
+
+
+def test_full_path_tiny_workload(gpu_lib):
+    """The 4096-key fp32 workload end to end (search -> bag fwd -> bag bwd), integer
+    queries / sub-keys so the selection is exact, in full."""
+    wl = WORKLOADS["pk4k_d64_f32"]
+    from paper_2412_09764_amd.inputs import gen_dy, gen_queries, gen_subkeys, gen_values
+    q = gen_queries(wl, "cpu", integer=True)
+    K = gen_subkeys(wl, "cpu", integer=True)
+    V = gen_values(wl, "cpu")
+    dy = gen_dy(wl, "cpu")
+    idx, w, score, _ = gpu_lib.mem_search(q.cuda(), K.cuda(), wl.k)
+    y = gpu_lib.mem_bag_forward(V.cuda(), idx.view(wl.T, -1), w.view(wl.T, -1))
+    gv, gw, gz = gpu_lib.mem_bag_backward(dy.cuda(), V.cuda(), idx, w)
+    torch.cuda.synchronize()
+    s = oracle.search(h64(q), h64(K), wl.k)
+    np.testing.assert_array_equal(idx.cpu().numpy(), s["idx"])
+    assert normwise(h64(w), s["w"]) <= TOL_F32
+    yref = oracle.bag_forward(h64(V), s["idx"].reshape(wl.T, -1), s["w"].reshape(wl.T, -1))
+    assert normwise(h64(y), yref) <= TOL_F32
+    b = oracle.bag_backward(h64(dy), h64(V), s["idx"], s["w"], wl.H, wl.k)
+    assert normwise(h64(gv), b["grad_values"]) <= TOL_F32
+    assert normwise(h64(gw), b["grad_w"]) <= TOL_F32
+    assert normwise(h64(gz), b["grad_z"]) <= TOL_F32
