@@ -1,0 +1,315 @@
+#!/usr/bin/env python3
+"""Memory-layer hot path throughput on one MI355X.
+
+One step = one pass of the whole hot path over one batch of T tokens:
+product-key search + softmax (mem_search), weighted EmbeddingBag forward
+(mem_bag_forward) and backward with value / weight / score gradients
+(mem_bag_backward).  Inputs are seeded synthetic tensors already resident in
+HBM when the timed region starts; the value gradient accumulates across steps
+(zeroing it is the caller's job, outside the step).
+
+Prints one JSON line: throughput (tokens/s), per-stage and per-kernel times
+from HIP events recorded inside the timed steps, the roofline of the dominant
+kernel, the gather / scatter bandwidths, and the CPU oracle timed on a bounded
+sample of the same workload.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload pk4m_d2048]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "memory-layer tokens/s fwd+bwd (4M keys×2048 bf16); gather HBM GB/s vs peak"
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, 8 TB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
+MFMA_F32_PEAK_TFLOPS = 157.3
+
+KERNELS = ["score_topk", "cartesian", "bag_forward", "sort_by_row", "bag_backward_rows",
+           "bag_backward_atomic", "softmax_backward"]
+KERNEL_SOURCES = {
+    "score_topk": ["search.hip", "pk_device.h"],
+    "cartesian": ["search.hip", "pk_device.h"],
+    "bag_forward": ["bag.hip", "pk_device.h"],
+    "bag_backward_atomic": ["bag.hip", "pk_device.h"],
+    "softmax_backward": ["bag.hip"],
+    "sort_by_row": ["sorted.hip", "pk_device.h"],
+    "bag_backward_rows": ["sorted.hip", "pk_device.h"],
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def source_hash(kernel: str) -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2412_09764_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this
+    kernel and workload, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    m_src = re.search(r"^source_sha256_16:\s*(\S+)", txt, re.M)
+    m_b = re.search(r"^hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt, re.M)
+    if not m_src or not m_b or m_src.group(1) != source_hash(kernel):
+        return None
+    return float(m_b.group(1))
+
+
+def alg_cost(kernel: str, wl, U: int, esz: int):
+    """Algorithmic bytes (HBM-bound kernels) or flops (scoring) of one launch."""
+    T, H, k, D, S, d = wl.T, wl.H, wl.k, wl.D, wl.S, wl.d
+    L = T * H * k
+    if kernel == "bag_forward":
+        # selected value rows + output rows + (idx int64, w fp32) per lookup
+        return "hbm", L * D * esz + T * D * esz + L * 12
+    if kernel == "bag_backward_rows":
+        # per touched row: value row read, fp32 gradient row read + write, segment start;
+        # per token: dy row; per lookup: sorted row key, lookup id, w, grad_w
+        return "hbm", U * D * (esz + 8) + U * 4 + T * D * esz + L * 16
+    if kernel == "bag_backward_atomic":
+        # per lookup: value row read, fp32 gradient row read + write, (idx, w, grad_w); dy per token
+        return "hbm", L * D * (esz + 8) + T * D * esz + L * 16
+    if kernel == "score_topk":
+        return "mfma", 2.0 * T * H * 2 * S * d
+    if kernel == "sort_by_row":
+        return "hbm", None
+    return "hbm", None
+
+
+def run_cpu_baseline(wl, q, K, V, dy, budget_s: float):
+    """The fp64 oracle on the first tokens of the batch, until ~budget_s seconds
+    of oracle time have been spent (at least 8 tokens).  One BLAS thread."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+
+    Kh = K.float().cpu().double().numpy()
+    spent = 0.0
+    done = 0
+    chunk = 8
+    with threadpool_limits(limits=1):
+        while done < wl.T and (spent < budget_s or done < 8):
+            t0, t1 = done, min(wl.T, done + chunk)
+            qh = q[t0:t1].float().cpu().double().numpy()
+            dyh = dy[t0:t1].float().cpu().double().numpy()
+            c0 = time.perf_counter()
+            s = oracle.search(qh, Kh, wl.k)
+            spent += time.perf_counter() - c0
+            # the value rows this chunk selects (host copy, not timed)
+            rows, inv = np.unique(s["idx"], return_inverse=True)
+            Vh = V[torch.from_numpy(rows).to(V.device)].float().cpu().double().numpy()
+            local = inv.reshape(s["idx"].shape)
+            c0 = time.perf_counter()
+            oracle.bag_forward(Vh, local.reshape(t1 - t0, -1), s["w"].reshape(t1 - t0, -1))
+            oracle.bag_backward_rows(dyh, Vh, local, s["w"], wl.H, wl.k)
+            spent += time.perf_counter() - c0
+            done = t1
+    return {"value": done / spent, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": (f"first {done} of {wl.T} tokens of {wl.name}: search + softmax + bag "
+                       f"forward + bag backward (touched rows), fp64 NumPy, one BLAS thread, "
+                       f"{spent:.1f} s")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="pk4m_d2048")
+    ap.add_argument("--bwd-mode", default="auto", choices=["auto", "atomic", "sorted"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2412_09764_amd as pk
+    from paper_2412_09764_amd.inputs import WORKLOADS, gen_dy, gen_queries, gen_subkeys, gen_values
+
+    pk.load()
+    wl = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    esz = 2 if wl.value_dtype == "bf16" else 4
+    T, H, k, N, D = wl.T, wl.H, wl.k, wl.N, wl.D
+    log(f"[bench] workload {wl.name}: N={N} D={D} H={H} k={k} T={T}; generating inputs")
+
+    q = gen_queries(wl, dev)
+    K = gen_subkeys(wl, dev)
+    V = gen_values(wl, dev)
+    dy = gen_dy(wl, dev)
+    idx = torch.empty((T, H, k), dtype=torch.int64, device=dev)
+    w = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    score = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    y = torch.empty((T, D), dtype=V.dtype, device=dev)
+    gw = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    gz = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    ws_s = torch.empty(pk.mem_search_workspace_size(T, H, wl.S, k), dtype=torch.uint8, device=dev)
+    sparse = wl.sparse_grad
+    mode = "sorted" if sparse else args.bwd_mode
+    ws_b = torch.empty(max(1, pk.mem_bag_backward_workspace_size(T, H, k, N, D, mode)),
+                       dtype=torch.uint8, device=dev)
+    if sparse:
+        cap = min(T * H * k, N)
+        rows_out = torch.empty((cap,), dtype=torch.int64, device=dev)
+        grows = torch.empty((cap, D), dtype=torch.float32, device=dev)
+        gv = None
+    else:
+        gv = torch.zeros((N, D), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    log("[bench] inputs resident; warming up")
+
+    L = pk.load()
+    import ctypes
+    st = torch.cuda.current_stream().cuda_stream
+    BF = pk.BF16 if wl.value_dtype == "bf16" else pk.F32
+    KDT = pk.BF16 if wl.key_dtype == "bf16" else pk.F32
+    m = pk.BWD_MODES[mode]
+    nrows = ctypes.c_int64(0)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        pk._check(L.mem_search(q.data_ptr(), KDT, K.data_ptr(), KDT, T, H, wl.n, wl.S, k,
+                               idx.data_ptr(), w.data_ptr(), score.data_ptr(), None,
+                               ws_s.data_ptr(), ws_s.numel(), st))
+        if ev is not None:
+            ev[1].record()
+        pk._check(L.mem_bag_forward(V.data_ptr(), BF, N, D, idx.data_ptr(), w.data_ptr(), T,
+                                    H * k, y.data_ptr(), st))
+        if ev is not None:
+            ev[2].record()
+        if sparse:
+            pk._check(L.mem_bag_backward_sparse(dy.data_ptr(), V.data_ptr(), BF, N, D,
+                                                idx.data_ptr(), w.data_ptr(), T, H, k,
+                                                rows_out.data_ptr(), grows.data_ptr(), cap,
+                                                ctypes.addressof(nrows), gw.data_ptr(),
+                                                gz.data_ptr(), ws_b.data_ptr(), ws_b.numel(), st))
+        else:
+            pk._check(L.mem_bag_backward(dy.data_ptr(), V.data_ptr(), BF, N, D, idx.data_ptr(),
+                                         w.data_ptr(), T, H, k, gv.data_ptr(), gw.data_ptr(),
+                                         gz.data_ptr(), m, ws_b.data_ptr(), ws_b.numel(), st))
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    pk.mem_timer_start(*KERNELS)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    pk.mem_timer_stop()
+    launches = pk.mem_timer_read()
+    ms_per_step = elapsed * 1e3 / args.steps
+    log(f"[bench] {ms_per_step:.3f} ms/step")
+
+    stages = {"search": 0.0, "bag_forward": 0.0, "bag_backward": 0.0}
+    for e in evs:
+        stages["search"] += e[0].elapsed_time(e[1])
+        stages["bag_forward"] += e[1].elapsed_time(e[2])
+        stages["bag_backward"] += e[2].elapsed_time(e[3])
+    stages = {s: round(v / args.steps, 4) for s, v in stages.items()}
+    per_kernel = {}
+    for pos, ms in launches:
+        per_kernel.setdefault(KERNELS[pos], []).append(ms)
+    kernel_ms = {kname: round(sum(v) / len(v), 4) for kname, v in per_kernel.items()}
+
+    # touched rows of the last step's selection (outside the timed region)
+    uniq, counts = torch.unique(idx.view(-1), return_counts=True)
+    U = int(uniq.numel())
+    max_mult = int(counts.max().item())
+
+    def bw(kname):
+        if kname not in kernel_ms:
+            return None
+        bound, cost = alg_cost(kname, wl, U, esz)
+        if cost is None:
+            return None
+        sec = kernel_ms[kname] / 1e3
+        if bound == "mfma":
+            peak = MFMA_BF16_PEAK_TFLOPS if wl.key_dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
+            ach = cost / sec / 1e12
+            return {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                    "frac": round(ach / peak, 4), "flops_per_launch": cost, "ms": kernel_ms[kname]}
+        ach = cost / sec / 1e9
+        return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBPS, 4), "alg_bytes_per_launch": cost,
+                "ms": kernel_ms[kname]}
+
+    dominant = max((kn for kn in kernel_ms if alg_cost(kn, wl, U, esz)[1] is not None),
+                   key=lambda kn: kernel_ms[kn])
+    roof = bw(dominant)
+    traffic = measured_traffic(dominant, wl.name)
+    roofline = {"kernel": dominant, "bound": roof["bound"], "achieved": roof["achieved"],
+                "peak": roof["peak"], "unit": roof["unit"], "frac": roof["frac"],
+                "traffic": traffic}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample")
+        cpu = run_cpu_baseline(wl, q, K, V, dy, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": round(T / (ms_per_step / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.value_dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "keys": N, "sub_keys_per_half": wl.S, "heads": H,
+                   "query_dim": wl.n, "value_dim": D, "k": k, "tokens": T,
+                   "value_table_GiB": round(N * D * esz / 2**30, 2),
+                   "value_grad": "sparse rows" if sparse else "dense fp32", "bwd_mode": mode},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "stages_ms": stages,
+        "kernels_ms": kernel_ms,
+        "gather": bw("bag_forward"),
+        "scatter": bw("bag_backward_rows") or bw("bag_backward_atomic"),
+        "search": bw("score_topk"),
+        "touched_rows": U,
+        "max_row_multiplicity": max_mult,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -103,7 +103,7 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
  *   values [N, D]   value table, dtype v_dt; D % 8 == 0.
  *   idx    [T, bag] int64 rows in [0, N); w [T, bag] fp32 weights.
  *   y_out  [T, D]   dtype v_dt, written: y[t] = sum_j w[t,j] * values[idx[t,j]],
- *                   accumulated in fp32 in the order j = 0..bag-1.
+ *                   accumulated in fp32 and rounded once to v_dt.
  * For the memory layer bag = H*k and idx / w are mem_search's outputs.
  * ------------------------------------------------------------------------ */
 int mem_bag_forward(const void* values, pkmem_dtype v_dt, int64_t N, int D,
@@ -143,6 +143,27 @@ int mem_bag_backward_sparse(const void* dy, const void* values, pkmem_dtype v_dt
                             int64_t* rows_out, float* grad_rows_out, int64_t cap,
                             int64_t* num_rows_out, float* grad_w, float* grad_scores,
                             void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * Benchmark instrumentation (host-side state; not thread-safe).
+ * mem_timer_start(kernels) takes a comma-separated list of kernel names and
+ * makes the library record a HIP event pair on the launch stream around every
+ * following launch of a listed kernel:
+ *   "score_topk", "cartesian"              (mem_search)
+ *   "bag_forward"                          (mem_bag_forward)
+ *   "bag_backward_atomic", "sort_by_row",
+ *   "bag_backward_rows", "softmax_backward" (mem_bag_backward[_sparse])
+ * ("sort_by_row" spans the whole radix sort and segment pass.)
+ * mem_timer_stop() stops recording.  mem_timer_read(ms_out, kernel_out, cap)
+ * waits for the recorded events, writes up to cap entries in launch order to
+ * the host arrays ms_out (duration in milliseconds) and kernel_out (position
+ * of the kernel in the list; either array may be NULL), frees the events, and
+ * returns how many launches were recorded (or a negative status).  With no
+ * timer running the library creates no events.
+ * ------------------------------------------------------------------------ */
+int mem_timer_start(const char* kernels);
+int mem_timer_stop(void);
+int mem_timer_read(float* ms_out, int* kernel_out, int cap);
 
 /* Message for the last non-OK status returned to the calling thread. */
 const char* mem_last_error(void);

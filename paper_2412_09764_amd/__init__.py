@@ -21,7 +21,7 @@ import torch  # noqa: F401  (first: the library binds to the HIP runtime torch l
 __all__ = [
     "PkmemError", "load", "lib_path", "mem_search", "mem_bag_forward", "mem_bag_backward",
     "mem_bag_backward_sparse", "mem_search_workspace_size", "mem_bag_backward_workspace_size",
-    "BWD_MODES", "F32", "BF16",
+    "BWD_MODES", "F32", "BF16", "mem_timer_start", "mem_timer_stop", "mem_timer_read",
 ]
 
 F32, BF16 = 0, 1
@@ -67,6 +67,12 @@ def load() -> ctypes.CDLL:
     L.mem_last_error.restype = ctypes.c_char_p
     L.mem_version.argtypes = []
     L.mem_version.restype = I32
+    L.mem_timer_start.argtypes = [ctypes.c_char_p]
+    L.mem_timer_start.restype = I32
+    L.mem_timer_stop.argtypes = []
+    L.mem_timer_stop.restype = I32
+    L.mem_timer_read.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int), I32]
+    L.mem_timer_read.restype = I32
     _LIB = L
     return L
 
@@ -109,6 +115,25 @@ def _workspace(nbytes: int, device, ws):
             raise ValueError(f"workspace too small: {nbytes} bytes needed")
         return ws
     return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def mem_timer_start(*kernels: str) -> None:
+    """Record HIP events around every launch of the named kernels (pkmem.h)."""
+    _check(load().mem_timer_start(",".join(kernels).encode()))
+
+
+def mem_timer_stop() -> None:
+    _check(load().mem_timer_stop())
+
+
+def mem_timer_read(cap: int = 1 << 16) -> list:
+    """[(kernel_position, ms)] of the launches recorded since the last read."""
+    ms = (ctypes.c_float * cap)()
+    which = (ctypes.c_int * cap)()
+    n = load().mem_timer_read(ms, which, cap)
+    if n < 0:
+        _check(n)
+    return [(int(which[i]), float(ms[i])) for i in range(min(n, cap))]
 
 
 def mem_search_workspace_size(T: int, H: int, S: int, k: int) -> int:

@@ -4,6 +4,8 @@
 #include <stdio.h>
 
 #include <string>
+#include <utility>
+#include <vector>
 
 #include "../../include/pkmem.h"
 #include "pk_internal.h"
@@ -145,9 +147,90 @@ int bag_backward_common(const char* fn, const void* dy, const void* values, pkme
   return PKMEM_OK;
 }
 
+// Benchmark timer state (host side, single-threaded use).
+struct TimedLaunch {
+  int kernel;  // position of the kernel's name in the timer's list
+  hipEvent_t start, stop;
+};
+struct TimerState {
+  std::vector<std::string> names;
+  bool on = false;
+  std::vector<TimedLaunch> events;
+};
+TimerState g_timer;
+
+int timer_slot(const char* name) {
+  for (size_t i = 0; i < g_timer.names.size(); ++i)
+    if (g_timer.names[i] == name) return (int)i;
+  return -1;
+}
+
 }  // namespace
 
+namespace pk {
+
+LaunchTimer::LaunchTimer(const char* name, hipStream_t st) : st_(st) {
+  if (!g_timer.on) return;
+  const int slot = timer_slot(name);
+  if (slot < 0) return;
+  hipEvent_t a, b;
+  if (hipEventCreate(&a) != hipSuccess) return;
+  if (hipEventCreate(&b) != hipSuccess) { hipEventDestroy(a); return; }
+  hipEventRecord(a, st_);
+  stop_ = b;
+  g_timer.events.push_back({slot, a, b});
+}
+
+LaunchTimer::~LaunchTimer() {
+  if (stop_) hipEventRecord(stop_, st_);
+}
+
+}  // namespace pk
+
 extern "C" {
+
+int mem_timer_start(const char* kernels) {
+  if (!kernels) return fail(PKMEM_ERR_INVALID, "mem_timer_start: null kernel list");
+  g_timer.names.clear();
+  std::string cur;
+  for (const char* c = kernels;; ++c) {
+    if (*c == ',' || *c == '\0') {
+      if (!cur.empty()) g_timer.names.push_back(cur);
+      cur.clear();
+      if (*c == '\0') break;
+    } else if (*c != ' ') {
+      cur.push_back(*c);
+    }
+  }
+  g_timer.on = !g_timer.names.empty();
+  return PKMEM_OK;
+}
+
+int mem_timer_stop(void) {
+  g_timer.on = false;
+  return PKMEM_OK;
+}
+
+int mem_timer_read(float* ms_out, int* kernel_out, int cap) {
+  int n = 0;
+  hipError_t err = hipSuccess;
+  for (auto& ev : g_timer.events) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(ev.stop);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev.start, ev.stop);
+    if (e != hipSuccess && err == hipSuccess) err = e;
+    if (n < cap) {
+      if (ms_out) ms_out[n] = ms;
+      if (kernel_out) kernel_out[n] = ev.kernel;
+    }
+    ++n;
+    hipEventDestroy(ev.start);
+    hipEventDestroy(ev.stop);
+  }
+  g_timer.events.clear();
+  if (err != hipSuccess) return hip_status(err, "mem_timer_read");
+  return n;
+}
 
 const char* mem_last_error(void) { return g_last_error.c_str(); }
 

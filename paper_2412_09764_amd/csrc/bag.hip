@@ -214,6 +214,7 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream
 hipError_t launch_softmax_backward(const float* w, const float* grad_w, int64_t rows, int k,
                                    float* grad_scores, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
+  LaunchTimer lt("softmax_backward", st);
   hipLaunchKernelGGL(k_softmax_bwd, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, st, w,
                      grad_w, rows, k, grad_scores);
   return hipGetLastError();
@@ -240,6 +241,7 @@ hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_
   if (T <= 0) return hipSuccess;
   const dim3 grid((unsigned)((T + 3) / 4)), block(256);
   const int C = D * (bf16 ? 2 : 4) / 16;
+  LaunchTimer lt("bag_forward", st);
 #define PK_FWD(CPL, CL)                                                                            \
   if (bf16)                                                                                        \
     hipLaunchKernelGGL((k_bag_fwd<uint16_t, CPL, CL, 4>), grid, block, 0, st,                      \
@@ -258,6 +260,7 @@ hipError_t launch_bag_backward_atomic(bool bf16, const void* dy, const void* val
   if (T <= 0) return hipSuccess;
   const dim3 grid((unsigned)((T + 3) / 4)), block(256);
   const int C = D * (bf16 ? 2 : 4) / 16;
+  LaunchTimer lt("bag_backward_atomic", st);
 #define PK_BWD(CPL, CL)                                                                         \
   if (bf16)                                                                                     \
     hipLaunchKernelGGL((k_bag_bwd_atomic<uint16_t, CPL, CL>), grid, block, 0, st,               \

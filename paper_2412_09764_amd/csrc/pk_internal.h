@@ -7,6 +7,21 @@
 
 namespace pk {
 
+// Scope guard for benchmark instrumentation: while a timer runs for `name`
+// (mem_timer_start), records a HIP event pair around the launches made in its
+// scope, on the launch stream.  Costs one string compare otherwise.
+class LaunchTimer {
+ public:
+  LaunchTimer(const char* name, hipStream_t st);
+  ~LaunchTimer();
+  LaunchTimer(const LaunchTimer&) = delete;
+  LaunchTimer& operator=(const LaunchTimer&) = delete;
+
+ private:
+  hipStream_t st_;
+  hipEvent_t stop_ = nullptr;
+};
+
 // Candidate slots kept per (token, head, half) between the filter pass and the
 // per-row sort of the search kernel.
 constexpr int CAND_CAP = 128;

@@ -382,8 +382,11 @@ static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, i
                                uint32_t* ovf, hipStream_t st) {
   const int64_t tiles = (T_ + SEARCH_TOK - 1) / SEARCH_TOK;
   const int64_t blocks = tiles * 2 * H;
-  hipLaunchKernelGGL((k_score_topk<T, NSTEP>), dim3((unsigned)blocks), dim3(256), 0, st,
-                     (const T*)q, (const T*)subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf);
+  {
+    LaunchTimer lt("score_topk", st);
+    hipLaunchKernelGGL((k_score_topk<T, NSTEP>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const T*)q, (const T*)subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds = (size_t)S * sizeof(float);
@@ -423,6 +426,7 @@ hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, in
   if (blocks > 8192) blocks = 8192;
   if (blocks < 1) blocks = 1;
   const dim3 g((unsigned)blocks), b(256);
+  LaunchTimer lt("cartesian", st);
   if (np <= 64) hipLaunchKernelGGL(k_cartesian<1>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
   else if (np <= 128) hipLaunchKernelGGL(k_cartesian<2>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
   else if (np <= 256) hipLaunchKernelGGL(k_cartesian<4>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);

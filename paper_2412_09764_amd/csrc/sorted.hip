@@ -345,40 +345,45 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
   if (num_rows_dev) *num_rows_dev = b.misc;
   hipError_t e = launch_fill_u32(b.misc, 0u, 1, st);
   if (e != hipSuccess || L == 0) return e;
+  const uint32_t* ks = nullptr;
+  const uint32_t* vs = nullptr;
 
   // 1. radix sort of (row, lookup) by row
-  int key_bits = 1;
-  while (key_bits < 32 && (int64_t(1) << key_bits) < N) ++key_bits;
-  const int64_t nblk = cdiv(L, SORT_TILE);
-  const void* kin = idx;
-  const uint32_t* vin = nullptr;
-  uint32_t *kout = b.keys_a, *vout = b.vals_a;
-  for (int shift = 0, pass = 0; shift < key_bits; shift += RADIX_BITS, ++pass) {
-    const int bits = (key_bits - shift) < RADIX_BITS ? (key_bits - shift) : RADIX_BITS;
-    if (pass == 0)
-      hipLaunchKernelGGL(k_radix_hist<true>, dim3((unsigned)nblk), dim3(256), 0, st, kin, L, shift, bits, nblk, b.hist);
-    else
-      hipLaunchKernelGGL(k_radix_hist<false>, dim3((unsigned)nblk), dim3(256), 0, st, kin, L, shift, bits, nblk, b.hist);
-    e = exclusive_scan(b.hist, (int64_t)RADIX * nblk, b.sums, st);
-    if (e != hipSuccess) return e;
-    if (pass == 0)
-      hipLaunchKernelGGL(k_radix_scatter<true>, dim3((unsigned)nblk), dim3(256), 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
-    else
-      hipLaunchKernelGGL(k_radix_scatter<false>, dim3((unsigned)nblk), dim3(256), 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
-    kin = kout;
-    vin = vout;
-    if (kout == b.keys_a) { kout = b.keys_b; vout = b.vals_b; }
-    else { kout = b.keys_a; vout = b.vals_a; }
-  }
-  const uint32_t* ks = reinterpret_cast<const uint32_t*>(kin);
-  const uint32_t* vs = vin;
+  {
+    LaunchTimer lt_sort("sort_by_row", st);
+    int key_bits = 1;
+    while (key_bits < 32 && (int64_t(1) << key_bits) < N) ++key_bits;
+    const int64_t nblk = cdiv(L, SORT_TILE);
+    const void* kin = idx;
+    const uint32_t* vin = nullptr;
+    uint32_t *kout = b.keys_a, *vout = b.vals_a;
+    for (int shift = 0, pass = 0; shift < key_bits; shift += RADIX_BITS, ++pass) {
+      const int bits = (key_bits - shift) < RADIX_BITS ? (key_bits - shift) : RADIX_BITS;
+      if (pass == 0)
+        hipLaunchKernelGGL(k_radix_hist<true>, dim3((unsigned)nblk), dim3(256), 0, st, kin, L, shift, bits, nblk, b.hist);
+      else
+        hipLaunchKernelGGL(k_radix_hist<false>, dim3((unsigned)nblk), dim3(256), 0, st, kin, L, shift, bits, nblk, b.hist);
+      e = exclusive_scan(b.hist, (int64_t)RADIX * nblk, b.sums, st);
+      if (e != hipSuccess) return e;
+      if (pass == 0)
+        hipLaunchKernelGGL(k_radix_scatter<true>, dim3((unsigned)nblk), dim3(256), 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+      else
+        hipLaunchKernelGGL(k_radix_scatter<false>, dim3((unsigned)nblk), dim3(256), 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+      kin = kout;
+      vin = vout;
+      if (kout == b.keys_a) { kout = b.keys_b; vout = b.vals_b; }
+      else { kout = b.keys_a; vout = b.vals_a; }
+    }
+    ks = reinterpret_cast<const uint32_t*>(kin);
+    vs = vin;
 
-  // 2. segments of equal rows
-  const unsigned lb = (unsigned)cdiv(L, 256);
-  hipLaunchKernelGGL(k_seg_flags, dim3(lb), dim3(256), 0, st, ks, L, b.hist);
-  e = exclusive_scan(b.hist, L, b.sums, st);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_seg_starts, dim3(lb), dim3(256), 0, st, ks, L, b.hist, b.seg, b.misc);
+    // 2. segments of equal rows
+    const unsigned lb = (unsigned)cdiv(L, 256);
+    hipLaunchKernelGGL(k_seg_flags, dim3(lb), dim3(256), 0, st, ks, L, b.hist);
+    e = exclusive_scan(b.hist, L, b.sums, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_seg_starts, dim3(lb), dim3(256), 0, st, ks, L, b.hist, b.seg, b.misc);
+  }
 
   // 3. one lane group per touched row
   const int C = D * (bf16 ? 2 : 4) / 16;
@@ -386,6 +391,7 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
   if (blocks > 16384) blocks = 16384;
   const dim3 grid((unsigned)blocks), block(256);
   const bool sparse = rows_out != nullptr;
+  LaunchTimer lt("bag_backward_rows", st);
 #define PK_ROWS(CPL, CL)                                                                          \
   if (bf16) {                                                                                     \
     if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, CPL, CL, true>), grid, block, 0, st,  \
