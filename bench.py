@@ -138,6 +138,9 @@ def main():
     ap.add_argument("--bwd-mode", default="auto", choices=["auto", "atomic", "sorted"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="before the steps, run one plain device copy of this many MiB "
+                         "(reference for scaling memory counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -182,6 +185,15 @@ def main():
     else:
         gv = torch.zeros((N, D), dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
+    if args.copy_calibration_mib > 0:
+        nfl = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(nfl, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"[bench] copy calibration: {args.copy_calibration_mib} MiB read + written")
     log("[bench] inputs resident; warming up")
 
     L = pk.load()

@@ -43,7 +43,35 @@ struct Row16<float> {
   }
 };
 
-__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+// The token's lookups are read 64 at a time, one per lane, with a single
+// coalesced load; lookup j of the chunk is then taken from lane j (readlane
+// into scalar registers when the whole wave works on one lookup, a lane
+// shuffle when lane groups work on different lookups).
+template <int G>
+struct LookupChunk {
+  uint32_t lo, hi;
+  float w;
+  __device__ __forceinline__ void load(const int64_t* ti, const float* tw, int c0, int nb, int lane) {
+    const int64_t r = lane < nb ? ti[c0 + lane] : 0;
+    lo = (uint32_t)r;
+    hi = (uint32_t)((uint64_t)r >> 32);
+    w = lane < nb ? tw[c0 + lane] : 0.f;
+  }
+  __device__ __forceinline__ void get(int j, int64_t& r, float& ww) const {
+    if constexpr (G == 1) {
+      const uint32_t a = __builtin_amdgcn_readlane(lo, j);
+      const uint32_t b = __builtin_amdgcn_readlane(hi, j);
+      r = (int64_t)(((uint64_t)b << 32) | a);
+      ww = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), j));
+    } else {
+      const uint32_t a = __shfl(lo, j, WAVE);
+      const uint32_t b = __shfl(hi, j, WAVE);
+      r = (int64_t)(((uint64_t)b << 32) | a);
+      ww = __shfl(w, j, WAVE);
+    }
+  }
+};
 
 // y[t] = sum_j w[t,j] V[idx[t,j]]; fp32 accumulation, one rounding at the end.
 template <typename V, int CPL, int CL, int U>
@@ -71,38 +99,51 @@ __global__ __launch_bounds__(256) void k_bag_fwd(const V* __restrict__ values, i
 
   const int64_t* ti = idx + t * bag;
   const float* tw = w + t * bag;
-  int j = grp;
-  for (; j + (U - 1) * G < bag; j += U * G) {
-    int64_t r[U];
-    float ww[U];
+  for (int c0 = 0; c0 < bag; c0 += WAVE) {
+    const int nb = (bag - c0) < WAVE ? (bag - c0) : WAVE;
+    LookupChunk<G> lk;
+    lk.load(ti, tw, c0, nb, lane);
+    // Blocks of U*G lookups, then a tail; every lane group runs the same trip
+    // counts (the shuffles in lk.get need the whole wave).
+    const int full = nb / (U * G);
+    for (int m = 0; m < full; ++m) {
+      const int j = m * U * G + grp;
+      int64_t r[U];
+      float ww[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) { r[u] = ti[j + u * G]; ww[u] = tw[j + u * G]; }
-    uint4 v[U][CPL];
+      for (int u = 0; u < U; ++u) lk.get(j + u * G, r[u], ww[u]);
+      uint4 v[U][CPL];
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+      for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int i = 0; i < CPL; ++i)
-        v[u][i] = ok[i] ? ld16(values + r[u] * D + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
+        for (int i = 0; i < CPL; ++i)
+          v[u][i] = ok[i] ? ld16_nt(values + r[u] * D + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+          float f[R::N];
+          R::unpack(v[u][i], f);
+#pragma unroll
+          for (int e = 0; e < R::N; ++e) acc[i][e] = fmaf(ww[u], f[e], acc[i][e]);
+        }
+    }
+    const int base = full * U * G;
+    const int tail = (nb - base + G - 1) / G;
+    for (int q = 0; q < tail; ++q) {
+      const int j = base + q * G + grp;
+      const bool live = j < nb;
+      int64_t r;
+      float ww;
+      lk.get(live ? j : base, r, ww);
 #pragma unroll
       for (int i = 0; i < CPL; ++i) {
+        if (!ok[i] || !live) continue;
         float f[R::N];
-        R::unpack(v[u][i], f);
+        R::unpack(ld16_nt(values + r * D + (size_t)(i * CL + cl) * R::N), f);
 #pragma unroll
-        for (int e = 0; e < R::N; ++e) acc[i][e] = fmaf(ww[u], f[e], acc[i][e]);
+        for (int e = 0; e < R::N; ++e) acc[i][e] = fmaf(ww, f[e], acc[i][e]);
       }
-  }
-  for (; j < bag; j += G) {
-    const int64_t r = ti[j];
-    const float ww = tw[j];
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      if (!ok[i]) continue;
-      float f[R::N];
-      R::unpack(ld16(values + r * D + (size_t)(i * CL + cl) * R::N), f);
-#pragma unroll
-      for (int e = 0; e < R::N; ++e) acc[i][e] = fmaf(ww, f[e], acc[i][e]);
     }
   }
   if (G > 1) {
@@ -188,16 +229,21 @@ __global__ __launch_bounds__(256) void k_bag_bwd_atomic(const V* __restrict__ dy
 }
 
 // grad_scores = w * (grad_w - sum_j w_j grad_w_j) per (token, head) row of k.
+// A row is handled by KG = k rounded up to a power of two lanes (coalesced).
+template <int KG>
 __global__ __launch_bounds__(256) void k_softmax_bwd(const float* __restrict__ w,
                                                      const float* __restrict__ gw, int64_t rows,
                                                      int k, float* __restrict__ gz) {
-  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (r >= rows) return;
-  const float* wr = w + r * k;
-  const float* gr = gw + r * k;
-  float inner = 0.f;
-  for (int j = 0; j < k; ++j) inner = fmaf(wr[j], gr[j], inner);
-  for (int j = 0; j < k; ++j) gz[r * k + j] = wr[j] * (gr[j] - inner);
+  constexpr int RPW = WAVE / KG;  // rows per wave
+  const int lane = threadIdx.x & 63;
+  const int64_t r = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW + lane / KG;
+  const int j = lane % KG;
+  const bool live = r < rows && j < k;
+  const size_t o = (size_t)(live ? r : 0) * k + j;
+  const float wv = live ? w[o] : 0.f;
+  const float gv = live ? gw[o] : 0.f;
+  const float inner = group_sum<KG>(wv * gv);
+  if (live) gz[o] = wv * (gv - inner);
 }
 
 __global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t value, int64_t count) {
@@ -215,8 +261,19 @@ hipError_t launch_softmax_backward(const float* w, const float* grad_w, int64_t 
                                    float* grad_scores, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   LaunchTimer lt("softmax_backward", st);
-  hipLaunchKernelGGL(k_softmax_bwd, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, st, w,
-                     grad_w, rows, k, grad_scores);
+  int kg = 1;
+  while (kg < k) kg <<= 1;
+  const int64_t rows_per_block = 4 * (WAVE / kg);
+  const dim3 grid((unsigned)((rows + rows_per_block - 1) / rows_per_block)), block(256);
+  switch (kg) {
+    case 1: hipLaunchKernelGGL(k_softmax_bwd<1>, grid, block, 0, st, w, grad_w, rows, k, grad_scores); break;
+    case 2: hipLaunchKernelGGL(k_softmax_bwd<2>, grid, block, 0, st, w, grad_w, rows, k, grad_scores); break;
+    case 4: hipLaunchKernelGGL(k_softmax_bwd<4>, grid, block, 0, st, w, grad_w, rows, k, grad_scores); break;
+    case 8: hipLaunchKernelGGL(k_softmax_bwd<8>, grid, block, 0, st, w, grad_w, rows, k, grad_scores); break;
+    case 16: hipLaunchKernelGGL(k_softmax_bwd<16>, grid, block, 0, st, w, grad_w, rows, k, grad_scores); break;
+    case 32: hipLaunchKernelGGL(k_softmax_bwd<32>, grid, block, 0, st, w, grad_w, rows, k, grad_scores); break;
+    default: hipLaunchKernelGGL(k_softmax_bwd<64>, grid, block, 0, st, w, grad_w, rows, k, grad_scores); break;
+  }
   return hipGetLastError();
 }
 
@@ -244,10 +301,11 @@ hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_
   LaunchTimer lt("bag_forward", st);
 #define PK_FWD(CPL, CL)                                                                            \
   if (bf16)                                                                                        \
-    hipLaunchKernelGGL((k_bag_fwd<uint16_t, CPL, CL, 4>), grid, block, 0, st,                      \
+    hipLaunchKernelGGL((k_bag_fwd<uint16_t, CPL, CL, PK_FWD_UNROLL>), grid, block, 0, st,          \
                        (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);                 \
   else                                                                                             \
-    hipLaunchKernelGGL((k_bag_fwd<float, CPL, CL, 4>), grid, block, 0, st, (const float*)values, D, \
+    hipLaunchKernelGGL((k_bag_fwd<float, CPL, CL, PK_FWD_UNROLL>), grid, block, 0, st,             \
+                       (const float*)values, D,                                                    \
                        idx, w, T, bag, (float*)y);
   PK_ROW_DISPATCH(C, PK_FWD);
 #undef PK_FWD

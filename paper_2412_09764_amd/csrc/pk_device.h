@@ -8,6 +8,36 @@ namespace pk {
 
 constexpr int WAVE = 64;
 
+// Tuning knobs (compile-time; the defaults are the measured best on MI355X).
+#ifndef PK_FWD_UNROLL
+#define PK_FWD_UNROLL 4  // lookups in flight per lane group in the gather
+#endif
+#ifndef PK_STREAM_NT
+#define PK_STREAM_NT 1   // non-temporal hints on value / gradient rows streamed once
+#endif
+
+// ------------------------------------------------------- 16-byte access ----
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+// Non-temporal 16-byte load / store: for data streamed once per pass.
+__device__ __forceinline__ uint4 ld16_nt(const void* p) {
+#if PK_STREAM_NT
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return uint4{v.x, v.y, v.z, v.w};
+#else
+  return ld16(p);
+#endif
+}
+__device__ __forceinline__ void st16_nt(void* p, uint4 v) {
+#if PK_STREAM_NT
+  const u32x4_t x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<u32x4_t*>(p));
+#else
+  *reinterpret_cast<uint4*>(p) = v;
+#endif
+}
+
 // ---------------------------------------------------------------- bf16 ----
 __device__ __forceinline__ float bf16_lo(uint32_t two) { return __uint_as_float(two << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t two) { return __uint_as_float(two & 0xFFFF0000u); }

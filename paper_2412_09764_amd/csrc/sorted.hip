@@ -215,92 +215,131 @@ __global__ __launch_bounds__(256) void k_seg_starts(const uint32_t* __restrict__
 }
 
 // ------------------------------------------------------- per-row backward ----
+// Quad layout: a row of D elements is D/4 quads of 4 consecutive elements; the
+// CL lanes of a group own quads q = m*CL + cl (m < NQ).  A bf16 quad is 8 bytes
+// and an fp32 quad 16 bytes, so every instruction of a group reads or writes
+// one contiguous span of the row, for the bf16 inputs and the fp32 gradient
+// alike (no partial cache lines).
 template <typename V>
-struct Row16s;
+struct Quad;
 template <>
-struct Row16s<uint16_t> {
-  static constexpr int N = 8;
-  __device__ static __forceinline__ void unpack(const uint4& v, float (&f)[8]) {
-    f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
-    f[4] = bf16_lo(v.z); f[5] = bf16_hi(v.z); f[6] = bf16_lo(v.w); f[7] = bf16_hi(v.w);
+struct Quad<uint16_t> {
+  __device__ static __forceinline__ uint2 load(const uint16_t* p) { return *reinterpret_cast<const uint2*>(p); }
+  __device__ static __forceinline__ uint2 load_nt(const uint16_t* p) {
+#if PK_STREAM_NT
+    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+    const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+    return uint2{v.x, v.y};
+#else
+    return load(p);
+#endif
   }
+  __device__ static __forceinline__ void unpack(const uint2& v, float (&f)[4]) {
+    f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
+  }
+  using raw = uint2;
+  __device__ static __forceinline__ raw zero() { return uint2{0, 0}; }
 };
 template <>
-struct Row16s<float> {
-  static constexpr int N = 4;
+struct Quad<float> {
+  __device__ static __forceinline__ uint4 load(const float* p) { return ld16(p); }
+  __device__ static __forceinline__ uint4 load_nt(const float* p) { return ld16_nt(p); }
   __device__ static __forceinline__ void unpack(const uint4& v, float (&f)[4]) {
     f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
     f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
   }
+  using raw = uint4;
+  __device__ static __forceinline__ raw zero() { return uint4{0, 0, 0, 0}; }
 };
 
-__device__ __forceinline__ uint4 ldg16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
-
-template <typename V, int CPL, int CL, bool SPARSE>
+// One lane group per touched row.  Value and gradient rows are streamed once
+// per step with non-temporal accesses, so they do not push the re-read dy rows
+// and metadata out of the caches.  The next segment's bounds are fetched one
+// iteration ahead, and the old gradient row is read into the accumulator
+// together with the value row, so a group waits for about two dependent memory
+// round trips per touched row.
+template <typename V, int NQ, int CL, bool SPARSE>
 __global__ __launch_bounds__(256) void k_bag_bwd_rows(
     const V* __restrict__ dy, const V* __restrict__ values, int D, const float* __restrict__ w,
     int bag, const uint32_t* __restrict__ rows_sorted, const uint32_t* __restrict__ lookups,
     const uint32_t* __restrict__ seg_start, const uint32_t* __restrict__ nseg,
     float* __restrict__ grad_values, int64_t* __restrict__ rows_out,
     float* __restrict__ grad_rows_out, float* __restrict__ grad_w) {
-  using R = Row16s<V>;
+  using Q = Quad<V>;
   constexpr int G = WAVE / CL;
   const int lane = threadIdx.x & 63;
   const int grp = lane / CL, cl = lane % CL;
-  const int C = D / R::N;
-  const uint32_t U = *nseg;
-  bool ok[CPL];
+  const int nquad = D / 4;
+  const int64_t U = *nseg;
+  const bool dense = !SPARSE && grad_values != nullptr;
+  bool ok[NQ];
 #pragma unroll
-  for (int i = 0; i < CPL; ++i) ok[i] = (i * CL + cl) < C;
+  for (int m = 0; m < NQ; ++m) ok[m] = (m * CL + cl) < nquad;
 
   const int64_t groups = (int64_t)gridDim.x * 4 * G;
-  for (int64_t u = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * G + grp; u < U; u += groups) {
-    const uint32_t s0 = seg_start[u], s1 = seg_start[u + 1];
-    const int64_t row = rows_sorted[s0];
-    float vr[CPL][R::N], acc[CPL][R::N];
+  int64_t u = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * G + grp;
+  uint32_t s0 = 0, s1 = 0;
+  int64_t row = 0;
+  if (u < U) {
+    s0 = seg_start[u];
+    s1 = seg_start[u + 1];
+    row = rows_sorted[s0];
+  }
+  while (u < U) {
+    typename Q::raw vraw[NQ];
+    float acc[NQ][4];
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      const uint4 v = ok[i] ? ldg16(values + row * D + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
-      R::unpack(v, vr[i]);
-#pragma unroll
-      for (int e = 0; e < R::N; ++e) acc[i][e] = 0.f;
+    for (int m = 0; m < NQ; ++m) {
+      const size_t e0 = (size_t)(m * CL + cl) * 4;
+      vraw[m] = ok[m] ? Q::load_nt(values + row * D + e0) : Q::zero();
+      const uint4 g = (ok[m] && dense) ? ld16_nt(grad_values + row * D + e0) : uint4{0, 0, 0, 0};
+      acc[m][0] = __uint_as_float(g.x); acc[m][1] = __uint_as_float(g.y);
+      acc[m][2] = __uint_as_float(g.z); acc[m][3] = __uint_as_float(g.w);
+    }
+    const int64_t un = u + groups;
+    uint32_t s0n = 0, s1n = 0;
+    if (un < U) {
+      s0n = seg_start[un];
+      s1n = seg_start[un + 1];
     }
     for (uint32_t s = s0; s < s1; ++s) {
       const uint32_t l = lookups[s];
       const int64_t t = l / (uint32_t)bag;
       const float ww = w[l];
+      typename Q::raw graw[NQ];
+#pragma unroll
+      for (int m = 0; m < NQ; ++m)
+        graw[m] = ok[m] ? Q::load(dy + t * D + (size_t)(m * CL + cl) * 4) : Q::zero();
       float part = 0.f;
 #pragma unroll
-      for (int i = 0; i < CPL; ++i) {
-        const uint4 v = ok[i] ? ldg16(dy + t * D + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
-        float g[R::N];
-        R::unpack(v, g);
+      for (int m = 0; m < NQ; ++m) {
+        float g[4], v[4];
+        Q::unpack(graw[m], g);
+        Q::unpack(vraw[m], v);
 #pragma unroll
-        for (int e = 0; e < R::N; ++e) {
-          acc[i][e] = fmaf(ww, g[e], acc[i][e]);
-          part = fmaf(g[e], vr[i][e], part);
+        for (int e = 0; e < 4; ++e) {
+          acc[m][e] = fmaf(ww, g[e], acc[m][e]);
+          part = fmaf(g[e], v[e], part);
         }
       }
       part = group_sum<CL>(part);
       if (cl == 0) grad_w[l] = part;
     }
-    if (!SPARSE && grad_values == nullptr) continue;
+    const int64_t rown = (un < U) ? (int64_t)rows_sorted[s0n] : 0;
+    if (SPARSE || dense) {
+      float* dst = SPARSE ? grad_rows_out + (size_t)u * D : grad_values + row * D;
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      if (!ok[i]) continue;
-      const size_t c0 = (size_t)(i * CL + cl) * R::N;
-      float* dst = SPARSE ? grad_rows_out + (size_t)u * D + c0 : grad_values + row * D + c0;
-#pragma unroll
-      for (int e0 = 0; e0 < R::N; e0 += 4) {
-        float4 o = make_float4(acc[i][e0], acc[i][e0 + 1], acc[i][e0 + 2], acc[i][e0 + 3]);
-        if (!SPARSE) {
-          const float4 old = *reinterpret_cast<const float4*>(dst + e0);
-          o.x += old.x; o.y += old.y; o.z += old.z; o.w += old.w;
-        }
-        *reinterpret_cast<float4*>(dst + e0) = o;
-      }
+      for (int m = 0; m < NQ; ++m)
+        if (ok[m])
+          st16_nt(dst + (size_t)(m * CL + cl) * 4,
+                  uint4{__float_as_uint(acc[m][0]), __float_as_uint(acc[m][1]),
+                        __float_as_uint(acc[m][2]), __float_as_uint(acc[m][3])});
     }
-    if (SPARSE && lane % CL == 0) rows_out[u] = row;
+    if (SPARSE && cl == 0) rows_out[u] = row;
+    u = un;
+    s0 = s0n;
+    s1 = s1n;
+    row = rown;
   }
 }
 
@@ -386,38 +425,38 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
   }
 
   // 3. one lane group per touched row
-  const int C = D * (bf16 ? 2 : 4) / 16;
+  const int nquad = D / 4;
   int64_t blocks = cdiv(L, 4);
   if (blocks > 16384) blocks = 16384;
   const dim3 grid((unsigned)blocks), block(256);
   const bool sparse = rows_out != nullptr;
   LaunchTimer lt("bag_backward_rows", st);
-#define PK_ROWS(CPL, CL)                                                                          \
+#define PK_ROWS(NQ, CL)                                                                           \
   if (bf16) {                                                                                     \
-    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, CPL, CL, true>), grid, block, 0, st,  \
+    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, NQ, CL, true>), grid, block, 0, st,   \
         (const uint16_t*)dy, (const uint16_t*)values, D, w, bag, ks, vs, b.seg, b.misc,            \
         grad_values, rows_out, grad_rows_out, grad_w);                                            \
-    else hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, CPL, CL, false>), grid, block, 0, st,       \
+    else hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, NQ, CL, false>), grid, block, 0, st,        \
         (const uint16_t*)dy, (const uint16_t*)values, D, w, bag, ks, vs, b.seg, b.misc,            \
         grad_values, rows_out, grad_rows_out, grad_w);                                            \
   } else {                                                                                        \
-    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<float, CPL, CL, true>), grid, block, 0, st,     \
+    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<float, NQ, CL, true>), grid, block, 0, st,      \
         (const float*)dy, (const float*)values, D, w, bag, ks, vs, b.seg, b.misc, grad_values,     \
         rows_out, grad_rows_out, grad_w);                                                         \
-    else hipLaunchKernelGGL((k_bag_bwd_rows<float, CPL, CL, false>), grid, block, 0, st,          \
+    else hipLaunchKernelGGL((k_bag_bwd_rows<float, NQ, CL, false>), grid, block, 0, st,           \
         (const float*)dy, (const float*)values, D, w, bag, ks, vs, b.seg, b.misc, grad_values,     \
         rows_out, grad_rows_out, grad_w);                                                         \
   }
-  if (C > 256) { PK_ROWS(8, 64); }
-  else if (C > 128) { PK_ROWS(4, 64); }
-  else if (C > 64) { PK_ROWS(2, 64); }
-  else if (C > 32) { PK_ROWS(1, 64); }
-  else if (C > 16) { PK_ROWS(1, 32); }
-  else if (C > 8) { PK_ROWS(1, 16); }
-  else if (C > 4) { PK_ROWS(1, 8); }
-  else if (C > 2) { PK_ROWS(1, 4); }
-  else if (C > 1) { PK_ROWS(1, 2); }
-  else { PK_ROWS(1, 1); }
+  if (nquad > 512) { PK_ROWS(16, 64); }
+  else if (nquad > 256) { PK_ROWS(8, 64); }
+  else if (nquad > 128) { PK_ROWS(4, 64); }
+  else if (nquad > 64) { PK_ROWS(2, 64); }
+  else if (nquad > 32) { PK_ROWS(1, 64); }
+  else if (nquad > 16) { PK_ROWS(1, 32); }
+  else if (nquad > 8) { PK_ROWS(1, 16); }
+  else if (nquad > 4) { PK_ROWS(1, 8); }
+  else if (nquad > 2) { PK_ROWS(1, 4); }
+  else { PK_ROWS(1, 2); }
 #undef PK_ROWS
   return hipGetLastError();
 }
