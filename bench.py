@@ -194,6 +194,20 @@ def main():
         torch.cuda.synchronize()
         del src, dst
         log(f"[bench] copy calibration: {args.copy_calibration_mib} MiB read + written")
+    # practical streaming peak of this machine: a plain 4 GiB device-to-device copy
+    src = torch.empty(1 << 30, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbps = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del src, dst
+    log(f"[bench] device copy: {copy_gbps:.0f} GB/s (read + write)")
     log("[bench] inputs resident; warming up")
 
     L = pk.load()
@@ -317,6 +331,7 @@ def main():
         "gather": bw("bag_forward"),
         "scatter": bw("bag_backward_rows") or bw("bag_backward_atomic"),
         "search": bw("score_topk"),
+        "stream_copy_GBps": round(copy_gbps, 1),
         "touched_rows": U,
         "max_row_multiplicity": max_mult,
     }

@@ -30,6 +30,8 @@ HIPCC_FLAGS = [
     "-Wno-unused-function",
     # no packed-fp32 instructions in generated code (v_pk_{add,mul,fma}_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in ordinary VGPRs: the scores feed VALU compares directly
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     f"-I{os.path.join(ROOT, 'include')}",
     f"-I{CSRC}",
 ]
@@ -65,7 +67,8 @@ def build(jobs: int = 8, verbose: bool = False) -> str:
         for f in futs:
             f.result()
     tmp = LIB + ".tmp"
-    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,--no-undefined", *objs, "-o", tmp],
+         verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -7,7 +7,7 @@
 #include <utility>
 #include <vector>
 
-#include "../../include/pkmem.h"
+#include "pkmem.h"
 #include "pk_internal.h"
 
 namespace {

@@ -13,7 +13,13 @@ constexpr int WAVE = 64;
 #define PK_FWD_UNROLL 4  // lookups in flight per lane group in the gather
 #endif
 #ifndef PK_STREAM_NT
-#define PK_STREAM_NT 1   // non-temporal hints on value / gradient rows streamed once
+#define PK_STREAM_NT 1   // non-temporal hints on value rows streamed once
+#endif
+#ifndef PK_GRAD_NT_LOAD
+#define PK_GRAD_NT_LOAD 1   // non-temporal hint on the gradient-row read
+#endif
+#ifndef PK_GRAD_NT_STORE
+#define PK_GRAD_NT_STORE 1  // non-temporal hint on the gradient-row write
 #endif
 
 // ------------------------------------------------------- 16-byte access ----
@@ -21,6 +27,24 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 // Non-temporal 16-byte load / store: for data streamed once per pass.
+template <bool NT>
+__device__ __forceinline__ uint4 ld16_hint(const void* p) {
+  if constexpr (NT) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return uint4{v.x, v.y, v.z, v.w};
+  } else {
+    return ld16(p);
+  }
+}
+template <bool NT>
+__device__ __forceinline__ void st16_hint(void* p, uint4 v) {
+  if constexpr (NT) {
+    const u32x4_t x = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(x, reinterpret_cast<u32x4_t*>(p));
+  } else {
+    *reinterpret_cast<uint4*>(p) = v;
+  }
+}
 __device__ __forceinline__ uint4 ld16_nt(const void* p) {
 #if PK_STREAM_NT
   const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
@@ -36,6 +60,12 @@ __device__ __forceinline__ void st16_nt(void* p, uint4 v) {
 #else
   *reinterpret_cast<uint4*>(p) = v;
 #endif
+}
+
+// Direct global -> LDS copy of 16 bytes per lane (gfx950): lane i's bytes land
+// at lds_base + 16 * i; lds_base must be the same for the whole wave.
+__device__ __forceinline__ void lds_dma16(const void* gptr, void* lds_base) {
+  __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
 }
 
 // ---------------------------------------------------------------- bf16 ----

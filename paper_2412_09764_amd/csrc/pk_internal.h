@@ -25,8 +25,9 @@ class LaunchTimer {
 // Candidate slots kept per (token, head, half) between the filter pass and the
 // per-row sort of the search kernel.
 constexpr int CAND_CAP = 128;
-// Tokens per workgroup of the scoring kernel (4 waves x 32 tokens).
-constexpr int SEARCH_TOK = 128;
+// Waves and tokens per workgroup of the scoring kernel (32 tokens per wave).
+constexpr int SEARCH_WAVES = 8;
+constexpr int SEARCH_TOK = 32 * SEARCH_WAVES;
 
 // Number of (i1, i2) rank pairs with (i1 + 1) * (i2 + 1) <= k: only these can
 // reach the top k of the k*k sums when both half lists are sorted.

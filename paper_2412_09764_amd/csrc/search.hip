@@ -31,7 +31,7 @@ namespace pk {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 
-constexpr int CHUNK_ROWS = 32;  // sub-keys per LDS chunk = one MFMA tile
+constexpr int CHUNK_ROWS = 64;  // sub-keys per LDS chunk = two MFMA tiles
 
 template <typename T>
 struct MfmaOp;
@@ -71,20 +71,24 @@ struct MfmaOp<float> {
 __device__ __forceinline__ int acc_row(int j, int kh) { return 8 * (j >> 2) + 4 * kh + (j & 3); }
 
 template <typename T, int NSTEP>
-__global__ __launch_bounds__(256) void k_score_topk(
+__global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
     const T* __restrict__ q, const T* __restrict__ subkeys, int64_t ntok, int H, int n, int S,
     int k, uint64_t* __restrict__ cand, int32_t* __restrict__ half_idx,
     float* __restrict__ half_score, uint32_t* __restrict__ ovf) {
   using M = MfmaOp<T>;
-  constexpr int DPAD = NSTEP * M::KSTEP;                   // padded half dim
-  constexpr int ROW_BYTES = DPAD * M::ESIZE + 16;          // +16 B: LDS bank skew
-  constexpr int CHUNK_BYTES = CHUNK_ROWS * ROW_BYTES;
-  constexpr int SEGS_PER_ROW = DPAD * M::ESIZE / 16;       // 16-byte segments per row
-  constexpr int SEGS = CHUNK_ROWS * SEGS_PER_ROW;
-  constexpr int SPT = (SEGS + 255) / 256;                  // segments per thread
-  constexpr int ELEMS_PER_SEG = 16 / M::ESIZE;
+  constexpr int DPAD = NSTEP * M::KSTEP;      // padded half dim
+  constexpr int RB = DPAD * M::ESIZE;         // bytes per sub-key row in LDS
+  constexpr int NCOL = RB / 16;               // 16-byte segments per row
+  constexpr int SWZ = (NCOL < 16 ? NCOL : 16) - 1;
+  constexpr int EPS = 16 / M::ESIZE;          // elements per segment
+  constexpr int CBYTES = CHUNK_ROWS * RB;
 
-  __shared__ __align__(16) unsigned char kbuf[2][CHUNK_BYTES];
+  // Sub-key chunks of 64 rows, double buffered.  Segment (row, col) of a chunk
+  // sits at row * RB + (col ^ (row & SWZ)) * 16: rows that the same fragment
+  // read touches land in different banks without padding, which keeps every
+  // wave's 1 KiB of a chunk contiguous for the direct global -> LDS loads.
+  __shared__ __align__(16) unsigned char kbuf0[CBYTES];
+  __shared__ __align__(16) unsigned char kbuf1[CBYTES];
   __shared__ int cnt[SEARCH_TOK];
 
   const int d = n >> 1;
@@ -111,70 +115,81 @@ __global__ __launch_bounds__(256) void k_score_topk(
     }
   }
 
-  uint4 pre[SPT];
-  auto load_chunk = [&](int c) {
-#pragma unroll
-    for (int i = 0; i < SPT; ++i) {
-      const int seg = tid + i * 256;
-      uint4 v = {0, 0, 0, 0};
-      if (seg < SEGS) {
-        const int r = seg / SEGS_PER_ROW, cs = seg % SEGS_PER_ROW;
-        const int row = c * CHUNK_ROWS + r;
-        const int e0 = cs * ELEMS_PER_SEG;
-        if (row < S && e0 < d) v = *reinterpret_cast<const uint4*>(kbase + (size_t)row * d + e0);
-      }
-      pre[i] = v;
+  // Chunk c into buffer b: 64*NCOL segments, 64 per wave instruction, each
+  // lane's 16 bytes going to LDS at base + 16*lane.  Rows past S and padded
+  // columns read a valid (finite) sub-key element instead: padded columns
+  // meet zero query entries and rows past S are masked out.
+  auto issue_chunk = [&](int c, unsigned char* buf) {
+    for (int i = wave; i < NCOL; i += SEARCH_WAVES) {
+      const int sidx = i * WAVE + lane;
+      const int r = sidx / NCOL, pc = sidx % NCOL;
+      const int lc = pc ^ (r & SWZ);
+      int row = c * CHUNK_ROWS + r;
+      row = row < S ? row : S - 1;
+      int e0 = lc * EPS;
+      e0 = e0 < d ? e0 : 0;
+      lds_dma16(kbase + (size_t)row * d + e0, &buf[i * WAVE * 16]);
     }
   };
-  auto store_chunk = [&](int b) {
+  // Both 32-row tiles of the chunk in buffer b, accumulators interleaved.
+  auto tile_pair = [&](const unsigned char* base, f32x16_t& a0, f32x16_t& a1) {
+    a0 = f32x16_t{};
+    a1 = f32x16_t{};
 #pragma unroll
-    for (int i = 0; i < SPT; ++i) {
-      const int seg = tid + i * 256;
-      if (seg < SEGS) {
-        const int r = seg / SEGS_PER_ROW, cs = seg % SEGS_PER_ROW;
-        *reinterpret_cast<uint4*>(&kbuf[b][r * ROW_BYTES + cs * 16]) = pre[i];
-      }
+    for (int s = 0; s < NSTEP; ++s) {
+      const int e = s * M::KSTEP + kh * M::LANE_K;  // first reduction element of the fragment
+      const int seg = (e * M::ESIZE) >> 4;
+      const int within = (e * M::ESIZE) & 15;
+      const int off = ((seg ^ (col & SWZ)) << 4) + within;
+      const auto fa = M::load(base + col * RB + off);
+      const auto fb = M::load(base + (32 + col) * RB + off);
+      a0 = M::mma(fa, bq[s], a0);
+      a1 = M::mma(fb, bq[s], a1);
     }
   };
-  auto tile_mma = [&](int b) {
-    f32x16_t acc = {};
-    const unsigned char* base = &kbuf[b][col * ROW_BYTES + kh * M::LANE_K * M::ESIZE];
-#pragma unroll
-    for (int s = 0; s < NSTEP; ++s) acc = M::mma(M::load(base + s * M::KSTEP * M::ESIZE), bq[s], acc);
-    return acc;
-  };
-
+  // One pass over all sub-keys; body(acc, c, half) sees each 32-row tile.
   const int nch = (S + CHUNK_ROWS - 1) / CHUNK_ROWS;
+  auto sweep = [&](auto&& body) {
+    // Unrolled by two so each step names its buffers statically; the LDS reads
+    // of one buffer then need not wait for the loads in flight into the other.
+    issue_chunk(0, kbuf0);
+    for (int c = 0; c < nch; c += 2) {
+      __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of chunk c have landed
+      __syncthreads();                // ... and every wave's; kbuf1 is free
+      if (c + 1 < nch) issue_chunk(c + 1, kbuf1);
+      f32x16_t a0, a1;
+      tile_pair(kbuf0, a0, a1);
+      body(a0, c, 0);
+      body(a1, c, 1);
+      if (c + 1 < nch) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (c + 2 < nch) issue_chunk(c + 2, kbuf0);
+        tile_pair(kbuf1, a0, a1);
+        body(a0, c + 1, 0);
+        body(a1, c + 1, 1);
+      }
+    }
+    __syncthreads();
+  };
+  const int nfull = S / CHUNK_ROWS;  // chunks with all 64 rows valid
 
-  // ---- pass 1: maxima of the 64 interleaved groups -------------------------
+  // ---- pass 1: maxima of the 64 interleaved groups (group = row mod 64) ----
   float mx[32];
 #pragma unroll
   for (int i = 0; i < 32; ++i) mx[i] = -INFINITY;
-
-  auto group_max = [&](const f32x16_t& acc, int c, int half) {
+  sweep([&](const f32x16_t& acc, int c, int half) {
+    if (c < nfull) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int row = c * CHUNK_ROWS + acc_row(j, kh);
-      const float v = row < S ? acc[j] : -INFINITY;
-      mx[half * 16 + j] = fmaxf(mx[half * 16 + j], v);
+      for (int j = 0; j < 16; ++j) mx[half * 16 + j] = fmaxf(mx[half * 16 + j], acc[j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int row = c * CHUNK_ROWS + half * 32 + acc_row(j, kh);
+        mx[half * 16 + j] = fmaxf(mx[half * 16 + j], row < S ? acc[j] : -INFINITY);
+      }
     }
-  };
-
-  load_chunk(0);
-  store_chunk(0);
-  __syncthreads();
-  for (int c = 0; c < nch; c += 2) {
-    if (c + 1 < nch) load_chunk(c + 1);
-    group_max(tile_mma(0), c, 0);
-    if (c + 1 < nch) store_chunk(1);
-    __syncthreads();
-    if (c + 1 < nch) {
-      if (c + 2 < nch) load_chunk(c + 2);
-      group_max(tile_mma(1), c + 1, 1);
-      if (c + 2 < nch) store_chunk(0);
-      __syncthreads();
-    }
-  }
+  });
 
   // Threshold = k-th largest of this token's 64 group maxima (32 in this lane,
   // 32 in lane ^ 32).  Sort both halves, form the bitonic half-cleaner of the
@@ -201,46 +216,39 @@ __global__ __launch_bounds__(256) void k_score_topk(
   }
 
   // ---- pass 2: collect candidates >= threshold ------------------------------
+  // A lane reserves slots for all its survivors of a tile with one LDS atomic;
+  // candidates are stored raw: (score bits << 32) | row.
   if (tid < SEARCH_TOK) cnt[tid] = 0;
+  __syncthreads();
   const size_t rid = ((size_t)(tok_ok ? tok : 0) * H + h) * 2 + p;
   uint64_t* my_cand = cand + rid * CAND_CAP;
   int* my_cnt = &cnt[wave * 32 + col];
-
-  auto collect = [&](const f32x16_t& acc, int c) {
+  sweep([&](const f32x16_t& acc, int c, int half) {
+    const int r0 = c * CHUNK_ROWS + half * 32;
     uint32_t m = 0;
+    if (c < nfull) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int row = c * CHUNK_ROWS + acc_row(j, kh);
-      if (row < S && acc[j] >= th) m |= 1u << j;
+      for (int j = 15; j >= 0; --j) m = (m << 1) | (acc[j] >= th ? 1u : 0u);
+    } else {
+#pragma unroll
+      for (int j = 15; j >= 0; --j) m = (m << 1) | ((acc[j] >= th && r0 + acc_row(j, kh) < S) ? 1u : 0u);
     }
     if (!tok_ok) m = 0;
     if (__ballot(m != 0) == 0) return;
+    int pos = 0;
+    if (m) pos = atomicAdd(my_cnt, __popc(m));
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       if (m & (1u << j)) {
-        const int pos = atomicAdd(my_cnt, 1);
-        if (pos < CAND_CAP) my_cand[pos] = make_key(acc[j], (uint32_t)(c * CHUNK_ROWS + acc_row(j, kh)));
+        if (pos < CAND_CAP)
+          my_cand[pos] = (uint64_t(__float_as_uint(acc[j])) << 32) | uint32_t(r0 + acc_row(j, kh));
+        ++pos;
       }
     }
-  };
-
-  load_chunk(0);
-  store_chunk(0);
-  __syncthreads();
-  for (int c = 0; c < nch; c += 2) {
-    if (c + 1 < nch) load_chunk(c + 1);
-    collect(tile_mma(0), c);
-    if (c + 1 < nch) store_chunk(1);
-    __syncthreads();
-    if (c + 1 < nch) {
-      if (c + 2 < nch) load_chunk(c + 2);
-      collect(tile_mma(1), c + 1);
-      if (c + 2 < nch) store_chunk(0);
-      __syncthreads();
-    }
-  }
+  });
 
   // ---- pass 3: sort each row's candidates, keep the first k ---------------
+  auto to_key = [](uint64_t raw) { return make_key(__uint_as_float(uint32_t(raw >> 32)), uint32_t(raw)); };
   for (int i = 0; i < 32; ++i) {
     const int64_t t = tile * SEARCH_TOK + wave * 32 + i;
     if (t >= ntok) break;
@@ -256,11 +264,11 @@ __global__ __launch_bounds__(256) void k_score_topk(
     const uint64_t* rc = cand + r * CAND_CAP;
     uint64_t key;
     if (c <= WAVE) {
-      uint64_t v[1] = {lane < c ? rc[lane] : 0ull};
+      uint64_t v[1] = {lane < c ? to_key(rc[lane]) : 0ull};
       wave_sort_desc<1>(v, lane);
       key = v[0];
     } else {
-      uint64_t v[2] = {rc[lane], lane + WAVE < c ? rc[lane + WAVE] : 0ull};
+      uint64_t v[2] = {to_key(rc[lane]), lane + WAVE < c ? to_key(rc[lane + WAVE]) : 0ull};
       wave_sort_desc<2>(v, lane);
       key = v[0];
     }
@@ -384,7 +392,7 @@ static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, i
   const int64_t blocks = tiles * 2 * H;
   {
     LaunchTimer lt("score_topk", st);
-    hipLaunchKernelGGL((k_score_topk<T, NSTEP>), dim3((unsigned)blocks), dim3(256), 0, st,
+    hipLaunchKernelGGL((k_score_topk<T, NSTEP>), dim3((unsigned)blocks), dim3(64 * SEARCH_WAVES), 0, st,
                        (const T*)q, (const T*)subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf);
   }
   hipError_t e = hipGetLastError();

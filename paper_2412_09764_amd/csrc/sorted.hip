@@ -292,7 +292,8 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
     for (int m = 0; m < NQ; ++m) {
       const size_t e0 = (size_t)(m * CL + cl) * 4;
       vraw[m] = ok[m] ? Q::load_nt(values + row * D + e0) : Q::zero();
-      const uint4 g = (ok[m] && dense) ? ld16_nt(grad_values + row * D + e0) : uint4{0, 0, 0, 0};
+      const uint4 g = (ok[m] && dense) ? ld16_hint<PK_GRAD_NT_LOAD>(grad_values + row * D + e0)
+                                       : uint4{0, 0, 0, 0};
       acc[m][0] = __uint_as_float(g.x); acc[m][1] = __uint_as_float(g.y);
       acc[m][2] = __uint_as_float(g.z); acc[m][3] = __uint_as_float(g.w);
     }
@@ -331,7 +332,7 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
 #pragma unroll
       for (int m = 0; m < NQ; ++m)
         if (ok[m])
-          st16_nt(dst + (size_t)(m * CL + cl) * 4,
+          st16_hint<PK_GRAD_NT_STORE>(dst + (size_t)(m * CL + cl) * 4,
                   uint4{__float_as_uint(acc[m][0]), __float_as_uint(acc[m][1]),
                         __float_as_uint(acc[m][2]), __float_as_uint(acc[m][3])});
     }
