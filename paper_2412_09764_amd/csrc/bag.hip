@@ -74,18 +74,30 @@ struct LookupChunk {
 };
 
 // y[t] = sum_j w[t,j] V[idx[t,j]]; fp32 accumulation, one rounding at the end.
-template <typename V, int CPL, int CL, int U>
+// The output rows are stored non-temporal: a trickle of ordinary stores in the
+// middle of the gather's random-read stream costs it about 12% on MI355X.
+// Lookups go in groups of U per lane group through a two-deep register ring:
+// the loads of group m+1 are in flight while group m is accumulated.  FULL
+// means every lane owns CPL whole chunks (C == CPL * CL), so no chunk needs a
+// per-lane predicate.
+// SPLIT > 1 (full rows of 64-lane groups only) spreads a token over SPLIT
+// waves, each owning CPL consecutive 1 KiB slabs of every row: more, smaller
+// waves in flight.
+template <typename V, int CPL, int CL, int U, bool FULL, int SPLIT>
 __global__ __launch_bounds__(256) void k_bag_fwd(const V* __restrict__ values, int D,
                                                  const int64_t* __restrict__ idx,
                                                  const float* __restrict__ w, int64_t T, int bag,
                                                  V* __restrict__ y) {
   using R = Row16<V>;
   constexpr int G = WAVE / CL;
+  static_assert(SPLIT == 1 || (FULL && CL == WAVE), "split waves need full 64-lane rows");
   const int lane = threadIdx.x & 63;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
   const int C = D / R::N;
-  const int grp = lane / CL, cl = lane % CL;
+  const int64_t nwaves = (int64_t)gridDim.x * 4;
+  for (int64_t gw = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); gw < T * SPLIT; gw += nwaves) {
+  const int64_t t = gw / SPLIT;
+  const int slab = (int)(gw % SPLIT);
+  const int grp = lane / CL, cl = lane % CL + slab * CPL * CL;
 
   float acc[CPL][R::N];
 #pragma unroll
@@ -95,7 +107,34 @@ __global__ __launch_bounds__(256) void k_bag_fwd(const V* __restrict__ values, i
 
   bool ok[CPL];
 #pragma unroll
-  for (int i = 0; i < CPL; ++i) ok[i] = (i * CL + cl) < C;
+  for (int i = 0; i < CPL; ++i) ok[i] = FULL || (i * CL + cl) < C;
+
+  struct Group {
+    uint4 v[U][CPL];
+    float ww[U];
+  };
+  auto issue = [&](Group& g, const LookupChunk<G>& lk, int j0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      int64_t r;
+      lk.get(j0 + u * G, r, g.ww[u]);
+      const V* row = values + r * D + (size_t)cl * R::N;
+#pragma unroll
+      for (int i = 0; i < CPL; ++i)
+        g.v[u][i] = ok[i] ? ld16_nt(row + (size_t)i * CL * R::N) : uint4{0, 0, 0, 0};
+    }
+  };
+  auto consume = [&](const Group& g) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+        float f[R::N];
+        R::unpack(g.v[u][i], f);
+#pragma unroll
+        for (int e = 0; e < R::N; ++e) acc[i][e] = fmaf(g.ww[u], f[e], acc[i][e]);
+      }
+  };
 
   const int64_t* ti = idx + t * bag;
   const float* tw = w + t * bag;
@@ -106,28 +145,26 @@ __global__ __launch_bounds__(256) void k_bag_fwd(const V* __restrict__ values, i
     // Blocks of U*G lookups, then a tail; every lane group runs the same trip
     // counts (the shuffles in lk.get need the whole wave).
     const int full = nb / (U * G);
-    for (int m = 0; m < full; ++m) {
-      const int j = m * U * G + grp;
-      int64_t r[U];
-      float ww[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) lk.get(j + u * G, r[u], ww[u]);
-      uint4 v[U][CPL];
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int i = 0; i < CPL; ++i)
-          v[u][i] = ok[i] ? ld16_nt(values + r[u] * D + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int i = 0; i < CPL; ++i) {
-          float f[R::N];
-          R::unpack(v[u][i], f);
-#pragma unroll
-          for (int e = 0; e < R::N; ++e) acc[i][e] = fmaf(ww[u], f[e], acc[i][e]);
+#if PK_FWD_RING
+    if (full > 0) {
+      Group ga, gb;
+      issue(ga, lk, grp);
+      for (int m = 0; m < full; m += 2) {
+        if (m + 1 < full) issue(gb, lk, (m + 1) * U * G + grp);
+        consume(ga);
+        if (m + 1 < full) {
+          if (m + 2 < full) issue(ga, lk, (m + 2) * U * G + grp);
+          consume(gb);
         }
+      }
     }
+#else
+    for (int m = 0; m < full; ++m) {
+      Group ga;
+      issue(ga, lk, m * U * G + grp);
+      consume(ga);
+    }
+#endif
     const int base = full * U * G;
     const int tail = (nb - base + G - 1) / G;
     for (int q = 0; q < tail; ++q) {
@@ -157,7 +194,8 @@ __global__ __launch_bounds__(256) void k_bag_fwd(const V* __restrict__ values, i
   if (grp == 0) {
 #pragma unroll
     for (int i = 0; i < CPL; ++i)
-      if (ok[i]) *reinterpret_cast<uint4*>(y + t * D + (size_t)(i * CL + cl) * R::N) = R::pack(acc[i]);
+      if (ok[i]) st16_nt(y + t * D + (size_t)(i * CL + cl) * R::N, R::pack(acc[i]));
+  }
   }
 }
 
@@ -293,20 +331,58 @@ hipError_t launch_softmax_backward(const float* w, const float* grad_w, int64_t 
     else { MACRO(1, 1); }                            \
   } while (0)
 
+// One wave per unit of work, or a persistent grid of PK_FWD_BLOCKS workgroups
+// striding over the units.
+static unsigned fwd_blocks(int64_t waves) {
+  int64_t b = (waves + 3) / 4;
+  if (PK_FWD_BLOCKS > 0 && b > PK_FWD_BLOCKS) b = PK_FWD_BLOCKS;
+  return (unsigned)b;
+}
+
 hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_t* idx,
                               const float* w, int64_t T, int bag, void* y, hipStream_t st) {
   if (T <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((T + 3) / 4)), block(256);
   const int C = D * (bf16 ? 2 : 4) / 16;
   LaunchTimer lt("bag_forward", st);
-#define PK_FWD(CPL, CL)                                                                            \
-  if (bf16)                                                                                        \
-    hipLaunchKernelGGL((k_bag_fwd<uint16_t, CPL, CL, PK_FWD_UNROLL>), grid, block, 0, st,          \
-                       (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);                 \
-  else                                                                                             \
-    hipLaunchKernelGGL((k_bag_fwd<float, CPL, CL, PK_FWD_UNROLL>), grid, block, 0, st,             \
-                       (const float*)values, D,                                                    \
-                       idx, w, T, bag, (float*)y);
+  // Full rows of 4 or 8 slabs are split over PK_FWD_SPLIT waves per token.
+  constexpr int SP = PK_FWD_SPLIT;
+  if (C == 256 && (4 % SP) == 0) {
+    const dim3 grid(fwd_blocks(T * SP)), block(256);
+    if (bf16)
+      hipLaunchKernelGGL((k_bag_fwd<uint16_t, 4 / SP, 64, PK_FWD_UNROLL, true, SP>), grid, block, 0,
+                         st, (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);
+    else
+      hipLaunchKernelGGL((k_bag_fwd<float, 4 / SP, 64, PK_FWD_UNROLL, true, SP>), grid, block, 0, st,
+                         (const float*)values, D, idx, w, T, bag, (float*)y);
+    return hipGetLastError();
+  }
+  if (C == 512 && (8 % SP) == 0) {
+    const dim3 grid(fwd_blocks(T * SP)), block(256);
+    if (bf16)
+      hipLaunchKernelGGL((k_bag_fwd<uint16_t, 8 / SP, 64, PK_FWD_UNROLL, true, SP>), grid, block, 0,
+                         st, (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);
+    else
+      hipLaunchKernelGGL((k_bag_fwd<float, 8 / SP, 64, PK_FWD_UNROLL, true, SP>), grid, block, 0, st,
+                         (const float*)values, D, idx, w, T, bag, (float*)y);
+    return hipGetLastError();
+  }
+  const dim3 grid(fwd_blocks(T)), block(256);
+#define PK_FWD(CPL, CL)                                                                              \
+  if (C == (CPL) * (CL)) {                                                                           \
+    if (bf16)                                                                                        \
+      hipLaunchKernelGGL((k_bag_fwd<uint16_t, CPL, CL, PK_FWD_UNROLL, true, 1>), grid, block, 0, st,  \
+                         (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);                 \
+    else                                                                                             \
+      hipLaunchKernelGGL((k_bag_fwd<float, CPL, CL, PK_FWD_UNROLL, true, 1>), grid, block, 0, st,     \
+                         (const float*)values, D, idx, w, T, bag, (float*)y);                       \
+  } else {                                                                                           \
+    if (bf16)                                                                                        \
+      hipLaunchKernelGGL((k_bag_fwd<uint16_t, CPL, CL, PK_FWD_UNROLL, false, 1>), grid, block, 0, st, \
+                         (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);                 \
+    else                                                                                             \
+      hipLaunchKernelGGL((k_bag_fwd<float, CPL, CL, PK_FWD_UNROLL, false, 1>), grid, block, 0, st,    \
+                         (const float*)values, D, idx, w, T, bag, (float*)y);                       \
+  }
   PK_ROW_DISPATCH(C, PK_FWD);
 #undef PK_FWD
   return hipGetLastError();

@@ -10,7 +10,16 @@ constexpr int WAVE = 64;
 
 // Tuning knobs (compile-time; the defaults are the measured best on MI355X).
 #ifndef PK_FWD_UNROLL
-#define PK_FWD_UNROLL 4  // lookups in flight per lane group in the gather
+#define PK_FWD_UNROLL 2  // lookups per group (two groups in flight) in the gather
+#endif
+#ifndef PK_FWD_RING
+#define PK_FWD_RING 1    // two-deep register ring of lookup groups in the gather
+#endif
+#ifndef PK_FWD_BLOCKS
+#define PK_FWD_BLOCKS 4096  // persistent grid of this many workgroups (0: one wave per token)
+#endif
+#ifndef PK_FWD_SPLIT
+#define PK_FWD_SPLIT 1   // waves per token in the gather for 4 KiB / 8 KiB rows
 #endif
 #ifndef PK_STREAM_NT
 #define PK_STREAM_NT 1   // non-temporal hints on value rows streamed once
