@@ -43,6 +43,9 @@ Function pins (tests under tests/test_oracle_*.py):
   bag_backward     torch autograd (fp64, CPU); central finite differences;
                    dense A.T @ dy; sum of score gradients is zero
   invert_index     multiset and ordering invariants
+  search_backward  central finite differences of the selected scores at a fixed
+                   selection; torch autograd (fp64); the bilinear identities
+                   sum(grad_q * q) = sum(grad_z * z) = sum(grad_K * K)
 """
 from __future__ import annotations
 
@@ -60,6 +63,7 @@ __all__ = [
     "bag_backward",
     "bag_backward_rows",
     "invert_index",
+    "search_backward",
 ]
 
 
@@ -279,3 +283,41 @@ def invert_index(idx: np.ndarray) -> dict:
         lookups.extend(groups[r])
         row_ptr[u + 1] = len(lookups)
     return dict(rows=rows, row_ptr=row_ptr, lookups=np.array(lookups, dtype=np.int64))
+
+
+def search_backward(q: np.ndarray, subkeys: np.ndarray, idx: np.ndarray,
+                    grad_z: np.ndarray, grad_subkeys_in=None) -> dict:
+    """Gradient of the selected scores with respect to queries and sub-keys.
+
+    The keys are trainable parameters (Sec. 3); the selection itself is
+    piecewise constant and passes no gradient.  With the composed index
+    i = i1 * S + i2 of Sec. 3.1.1, the selected score of rank j is
+      z[t,h,j] = q[t,h,:d] . K[h,0,i1] + q[t,h,d:] . K[h,1,i2]
+    so, given grad_z = dL/dz:
+      grad_q[t,h,:d]  = sum_j grad_z[t,h,j] K[h,0,i1_j]
+      grad_q[t,h,d:]  = sum_j grad_z[t,h,j] K[h,1,i2_j]
+      grad_K[h,0,i]  += sum over (t,j) with i1_j = i of grad_z[t,h,j] q[t,h,:d]
+      grad_K[h,1,i]  += sum over (t,j) with i2_j = i of grad_z[t,h,j] q[t,h,d:]
+    grad_K accumulates onto grad_subkeys_in (default zeros).
+    Returns grad_q [T,H,n] and grad_K [H,2,S,d].
+    """
+    q = _f64(q)
+    K = _f64(subkeys)
+    T, H, n = q.shape
+    d = n // 2
+    S = K.shape[2]
+    idx = np.asarray(idx)
+    gz = _f64(grad_z)
+    k = idx.shape[2]
+    grad_q = np.zeros((T, H, n))
+    grad_K = np.zeros(K.shape) if grad_subkeys_in is None else _f64(grad_subkeys_in).copy()
+    for t in range(T):
+        for h in range(H):
+            for j in range(k):
+                i1, i2 = divmod(int(idx[t, h, j]), S)
+                g = gz[t, h, j]
+                grad_q[t, h, :d] += g * K[h, 0, i1]
+                grad_q[t, h, d:] += g * K[h, 1, i2]
+                grad_K[h, 0, i1] += g * q[t, h, :d]
+                grad_K[h, 1, i2] += g * q[t, h, d:]
+    return dict(grad_q=grad_q, grad_K=grad_K)

@@ -20,6 +20,10 @@ What pins what:
   bag backward  - torch autograd of that embedding_bag and of softmax in
                   fp64; central finite differences; dense A.T @ dy;
                   the score gradients of one (token, head) sum to zero.
+  search bwd    - central finite differences of the selected scores at a
+                  fixed selection; torch autograd of the gathered scores;
+                  the bilinear identities sum(grad_q q) = sum(grad_z z) =
+                  sum(grad_K K); accumulation onto an existing key gradient.
 """
 from __future__ import annotations
 
@@ -218,3 +222,60 @@ def check_accumulate(bag_bwd_fn, rng):
     g0 = bag_bwd_fn(dy, V, idx, w, H, k)
     g1 = bag_bwd_fn(dy, V, idx, w, H, k, grad_values_in=base)
     np.testing.assert_allclose(g1["grad_values"], base + g0["grad_values"], rtol=1e-14, atol=1e-15)
+
+
+def selected_scores(q, K, idx):
+    """z[t,h,j] for a fixed selection (used only as the function that the
+    finite differences and autograd differentiate)."""
+    T, H, n = q.shape
+    d = n // 2
+    S = K.shape[2]
+    k = idx.shape[2]
+    z = np.zeros((T, H, k))
+    for t in range(T):
+        for h in range(H):
+            for j in range(k):
+                i1, i2 = divmod(int(idx[t, h, j]), S)
+                z[t, h, j] = q[t, h, :d] @ K[h, 0, i1] + q[t, h, d:] @ K[h, 1, i2]
+    return z
+
+
+def check_search_backward(search_fn, bwd_fn, rng, T=4, H=2, S=5, d=3, k=4, h=1e-6):
+    q = rng.standard_normal((T, H, 2 * d))
+    K = rng.standard_normal((H, 2, S, d))
+    idx = search_fn(q, K, k)["idx"]
+    gz = rng.standard_normal((T, H, k))
+    g = bwd_fn(q, K, idx, gz)
+    L = lambda qq, KK: float((selected_scores(qq, KK, idx) * gz).sum())  # noqa: E731
+    # central differences at the fixed selection (the score is bilinear, so
+    # the difference quotient is exact up to rounding)
+    for (t, hh, e) in [(0, 0, 0), (1, 1, 4), (3, 0, 2), (2, 1, 5)]:
+        qp = q.copy(); qp[t, hh, e] += h
+        qm = q.copy(); qm[t, hh, e] -= h
+        fd = (L(qp, K) - L(qm, K)) / (2 * h)
+        assert abs(fd - g["grad_q"][t, hh, e]) < 1e-7, (t, hh, e, fd, g["grad_q"][t, hh, e])
+    for (hh, p, i, e) in [(0, 0, int(idx[0, 0, 0]) // S, 1), (1, 1, int(idx[2, 1, 1]) % S, 2), (0, 1, 4, 0)]:
+        Kp = K.copy(); Kp[hh, p, i, e] += h
+        Km = K.copy(); Km[hh, p, i, e] -= h
+        fd = (L(q, Kp) - L(q, Km)) / (2 * h)
+        assert abs(fd - g["grad_K"][hh, p, i, e]) < 1e-7, (hh, p, i, e, fd, g["grad_K"][hh, p, i, e])
+    # torch autograd of the gathered scores
+    qt = torch.tensor(q, requires_grad=True)
+    Kt = torch.tensor(K, requires_grad=True)
+    it = torch.tensor(idx)
+    i1, i2 = it // S, it % S
+    hh_ = torch.arange(H).view(1, H, 1).expand_as(it)
+    z = (qt[..., :d].unsqueeze(2) * Kt[hh_, 0, i1]).sum(-1) + (qt[..., d:].unsqueeze(2) * Kt[hh_, 1, i2]).sum(-1)
+    (z * torch.tensor(gz)).sum().backward()
+    np.testing.assert_allclose(g["grad_q"], qt.grad.numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(g["grad_K"], Kt.grad.numpy(), rtol=1e-12, atol=1e-14)
+    # bilinearity: sum(grad_q . q) = sum(grad_z . z) = sum(grad_K . K)
+    zz = selected_scores(q, K, idx)
+    lhs = float((g["grad_q"] * q).sum())
+    mid = float((gz * zz).sum())
+    rhs = float((g["grad_K"] * K).sum())
+    assert abs(lhs - mid) < 1e-10 * max(1.0, abs(mid)) and abs(rhs - mid) < 1e-10 * max(1.0, abs(mid))
+    # accumulation onto an existing sub-key gradient
+    base = rng.standard_normal(K.shape)
+    g2 = bwd_fn(q, K, idx, gz, base)
+    np.testing.assert_allclose(g2["grad_K"], base + g["grad_K"], rtol=1e-14, atol=1e-15)

@@ -145,3 +145,36 @@ def test_catches_weighted_grad_w():
         out["grad_w"] = out["grad_w"] * np.asarray(w).reshape(out["grad_w"].shape)
         return out
     assert _bag_fails(bwd=bwd) > 0
+
+
+def _sbwd_fails(bwd):
+    try:
+        pins.check_search_backward(oracle.search, bwd, np.random.default_rng(61))
+    except (AssertionError, ValueError, IndexError):
+        return True
+    return False
+
+
+def test_real_search_backward_passes():
+    assert not _sbwd_fails(oracle.search_backward)
+
+
+def test_catches_search_backward_halves_swapped():
+    def bwd(q, K, idx, gz, base=None):
+        out = oracle.search_backward(q, K[:, ::-1], idx, gz, None if base is None else base[:, ::-1])
+        out["grad_K"] = out["grad_K"][:, ::-1]
+        return out
+    assert _sbwd_fails(bwd)
+
+
+def test_catches_search_backward_index_transposed():
+    def bwd(q, K, idx, gz, base=None):
+        S = K.shape[2]
+        return oracle.search_backward(q, K, (idx % S) * S + idx // S, gz, base)
+    assert _sbwd_fails(bwd)
+
+
+def test_catches_search_backward_key_grad_not_accumulated():
+    def bwd(q, K, idx, gz, base=None):
+        return oracle.search_backward(q, K, idx, gz, None)
+    assert _sbwd_fails(bwd)

@@ -59,3 +59,8 @@ def test_search_outputs_consistent():
                 assert out["score"][t, h, j] == out["half_score"][t, h, 0, a] + out["half_score"][t, h, 1, b]
     assert np.all(np.diff(out["score"], axis=-1) <= 0)
     np.testing.assert_allclose(out["w"].sum(-1), 1.0, atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_search_backward_pins(seed):
+    pins.check_search_backward(oracle.search, oracle.search_backward, np.random.default_rng(60 + seed))
