@@ -34,7 +34,7 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
 MFMA_F32_PEAK_TFLOPS = 157.3
 
 KERNELS = ["score_topk", "cartesian", "bag_forward", "sort_by_row", "bag_backward_rows",
-           "bag_backward_atomic", "softmax_backward"]
+           "bag_backward_atomic", "softmax_backward", "search_backward"]
 KERNEL_SOURCES = {
     "score_topk": ["search.hip", "pk_device.h"],
     "cartesian": ["search.hip", "pk_device.h"],
@@ -43,6 +43,7 @@ KERNEL_SOURCES = {
     "softmax_backward": ["bag.hip"],
     "sort_by_row": ["sorted.hip", "pk_device.h"],
     "bag_backward_rows": ["sorted.hip", "pk_device.h"],
+    "search_backward": ["search_bwd.hip", "pk_device.h"],
 }
 
 
@@ -272,6 +273,25 @@ def main():
         per_kernel.setdefault(KERNELS[pos], []).append(ms)
     kernel_ms = {kname: round(sum(v) / len(v), 4) for kname, v in per_kernel.items()}
 
+    # Search backward (gradients into queries and sub-keys): measured on its
+    # own, after the timed steps; not part of the step's throughput.
+    gq = torch.empty((T, H, wl.n), dtype=torch.float32, device=dev)
+    gK = torch.zeros((H, 2, wl.S, wl.d), dtype=torch.float32, device=dev)
+    def sbwd():
+        pk._check(L.mem_search_backward(q.data_ptr(), KDT, K.data_ptr(), KDT, T, H, wl.n, wl.S, k,
+                                        idx.data_ptr(), gz.data_ptr(), gq.data_ptr(),
+                                        gK.data_ptr(), None, 0, st))
+    sbwd()
+    torch.cuda.synchronize()
+    pk.mem_timer_start("search_backward")
+    for _ in range(args.steps):
+        sbwd()
+    torch.cuda.synchronize()
+    pk.mem_timer_stop()
+    sb = [ms for _, ms in pk.mem_timer_read()]
+    search_bwd_ms = sum(sb) / len(sb)
+    del gq, gK
+
     # touched rows of the last step's selection (outside the timed region)
     uniq, counts = torch.unique(idx.view(-1), return_counts=True)
     U = int(uniq.numel())
@@ -331,6 +351,7 @@ def main():
         "gather": bw("bag_forward"),
         "scatter": bw("bag_backward_rows") or bw("bag_backward_atomic"),
         "search": bw("score_topk"),
+        "search_backward_ms": round(search_bwd_ms, 4),
         "stream_copy_GBps": round(copy_gbps, 1),
         "touched_rows": U,
         "max_row_multiplicity": max_mult,

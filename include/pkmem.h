@@ -98,6 +98,31 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
                void* ws, size_t ws_bytes, pkmem_stream_t stream);
 
 /* ------------------------------------------------------------------------ *
+ * Search backward: gradient of the selected scores with respect to the
+ * queries and the sub-keys (the keys are trainable parameters, Sec. 3; the
+ * selection is piecewise constant and passes no gradient).  With
+ * i1 = idx / S, i2 = idx % S the score of rank j is
+ *   z[t,h,j] = q[t,h,0:d] . subkeys[h,0,i1] + q[t,h,d:n] . subkeys[h,1,i2].
+ *
+ *   q, subkeys, T, H, n, S, k   as for mem_search (same dtype rules and limits).
+ *   idx          [T, H, k] int64  mem_search's selection.
+ *   grad_scores  [T, H, k] fp32   dL/dz (mem_bag_backward's grad_scores).
+ * Outputs (each may be NULL to skip it):
+ *   grad_q        [T, H, n] fp32, written:
+ *                 grad_q[t,h,0:d] = sum_j gz[t,h,j] subkeys[h,0,i1_j], likewise half 1.
+ *   grad_subkeys  [H, 2, S, n/2] fp32, ACCUMULATED (+=):
+ *                 += sum over (t,j) with i1_j = i of gz[t,h,j] q[t,h,0:d], likewise half 1.
+ *                 Summed with fp32 atomics: not bitwise deterministic run to run.
+ * Needs no workspace (ws may be NULL, ws_bytes 0).
+ * ------------------------------------------------------------------------ */
+size_t mem_search_backward_workspace_size(int64_t T, int H, int S, int k);
+
+int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                        int64_t T, int H, int n, int S, int k, const int64_t* idx,
+                        const float* grad_scores, float* grad_q, float* grad_subkeys,
+                        void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
  * Weighted EmbeddingBag forward, sum mode (Sec. 3, Eq. (1) y = s V_I; Sec. 3.1.4).
  *
  *   values [N, D]   value table, dtype v_dt; D % 8 == 0.
@@ -150,6 +175,7 @@ int mem_bag_backward_sparse(const void* dy, const void* values, pkmem_dtype v_dt
  * makes the library record a HIP event pair on the launch stream around every
  * following launch of a listed kernel:
  *   "score_topk", "cartesian"              (mem_search)
+ *   "search_backward"                      (mem_search_backward)
  *   "bag_forward"                          (mem_bag_forward)
  *   "bag_backward_atomic", "sort_by_row",
  *   "bag_backward_rows", "softmax_backward" (mem_bag_backward[_sparse])

@@ -19,7 +19,8 @@ import os
 import torch  # noqa: F401  (first: the library binds to the HIP runtime torch loads)
 
 __all__ = [
-    "PkmemError", "load", "lib_path", "mem_search", "mem_bag_forward", "mem_bag_backward",
+    "PkmemError", "load", "lib_path", "mem_search", "mem_search_backward", "mem_bag_forward",
+    "mem_bag_backward",
     "mem_bag_backward_sparse", "mem_search_workspace_size", "mem_bag_backward_workspace_size",
     "BWD_MODES", "F32", "BF16", "mem_timer_start", "mem_timer_stop", "mem_timer_read",
 ]
@@ -54,6 +55,10 @@ def load() -> ctypes.CDLL:
     L.mem_search_workspace_size.restype = SZ
     L.mem_search.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, SZ, P]
     L.mem_search.restype = I32
+    L.mem_search_backward_workspace_size.argtypes = [I64, I32, I32, I32]
+    L.mem_search_backward_workspace_size.restype = SZ
+    L.mem_search_backward.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, SZ, P]
+    L.mem_search_backward.restype = I32
     L.mem_bag_forward.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P]
     L.mem_bag_forward.restype = I32
     L.mem_bag_backward_workspace_size.argtypes = [I64, I32, I32, I64, I32, I32]
@@ -173,6 +178,28 @@ def mem_search(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None, 
                         _ptr(idx_out), _ptr(w_out), _ptr(score_out), _ptr(half_idx_out),
                         _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
     return idx_out, w_out, score_out, half_idx_out
+
+
+def mem_search_backward(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tensor,
+                        grad_scores: torch.Tensor, *, grad_q=None, grad_subkeys=None,
+                        want_grad_q: bool = True, want_grad_subkeys: bool = True, stream=None):
+    """Gradients of the selected scores into q ([T,H,n], written) and the
+    sub-keys ([H,2,S,n/2], ACCUMULATED; a zero table is allocated if none is
+    given).  Returns (grad_q, grad_subkeys)."""
+    L = load()
+    _dev(q, subkeys, idx, grad_scores)
+    T, H, n = q.shape
+    S = subkeys.shape[2]
+    k = idx.shape[2]
+    if grad_q is None and want_grad_q:
+        grad_q = torch.empty((T, H, n), dtype=torch.float32, device=q.device)
+    if grad_subkeys is None and want_grad_subkeys:
+        grad_subkeys = torch.zeros(subkeys.shape, dtype=torch.float32, device=q.device)
+    _dev(grad_q, grad_subkeys)
+    _check(L.mem_search_backward(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
+                                 _ptr(idx), _ptr(grad_scores), _ptr(grad_q), _ptr(grad_subkeys),
+                                 None, 0, _stream(stream)))
+    return grad_q, grad_subkeys
 
 
 def mem_bag_forward(values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor, *, y_out=None,

@@ -59,6 +59,28 @@ SearchWs search_ws(void* base, int64_t T, int H, int k) {
   return w;
 }
 
+int check_search_shapes(const char* fn, const void* q, pkmem_dtype q_dt, const void* subkeys,
+                        pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k) {
+  if (!dtype_ok(q_dt) || !dtype_ok(k_dt)) return fail(PKMEM_ERR_INVALID, "%s: unknown dtype", fn);
+  if (q_dt != k_dt) return fail(PKMEM_ERR_UNSUPPORTED, "%s: queries and sub-keys must share a dtype", fn);
+  if (T < 0) return fail(PKMEM_ERR_INVALID, "%s: T must be >= 0", fn);
+  if (H < 1) return fail(PKMEM_ERR_INVALID, "%s: H must be >= 1", fn);
+  if (n < 2 || n % 2 != 0) return fail(PKMEM_ERR_INVALID, "%s: n must be even and >= 2 (got %d)", fn, n);
+  const int d = n / 2;
+  if (q_dt == PKMEM_BF16 && (d % 8 != 0 || d > PKMEM_DHALF_MAX))
+    return fail(PKMEM_ERR_UNSUPPORTED, "%s: bf16 needs n/2 a multiple of 8 and <= %d (got %d)", fn, PKMEM_DHALF_MAX, d);
+  if (q_dt == PKMEM_F32 && (d % 4 != 0 || d > 64))
+    return fail(PKMEM_ERR_UNSUPPORTED, "%s: fp32 needs n/2 a multiple of 4 and <= 64 (got %d)", fn, d);
+  if (S < 1) return fail(PKMEM_ERR_INVALID, "%s: S must be >= 1", fn);
+  if (S > PKMEM_SMAX) return fail(PKMEM_ERR_UNSUPPORTED, "%s: S > %d", fn, PKMEM_SMAX);
+  if (k < 1 || k > S) return fail(PKMEM_ERR_INVALID, "%s: need 1 <= k <= S (k=%d, S=%d)", fn, k, S);
+  if (k > PKMEM_KMAX) return fail(PKMEM_ERR_UNSUPPORTED, "%s: k > %d", fn, PKMEM_KMAX);
+  if ((T * H * 2) > (int64_t)0xFFFFFFFF) return fail(PKMEM_ERR_UNSUPPORTED, "%s: T*H*2 must be < 2^32", fn);
+  if (T > 0 && (!q || !subkeys)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (!aligned(q, 16) || !aligned(subkeys, 16)) return fail(PKMEM_ERR_INVALID, "%s: q and subkeys must be 16-byte aligned", fn);
+  return PKMEM_OK;
+}
+
 int check_bag_shapes(const char* fn, pkmem_dtype v_dt, int64_t N, int D, int64_t T, int bag) {
   if (!dtype_ok(v_dt)) return fail(PKMEM_ERR_INVALID, "%s: unknown value dtype %d", fn, (int)v_dt);
   if (N < 1) return fail(PKMEM_ERR_INVALID, "%s: N must be >= 1 (got %lld)", fn, (long long)N);
@@ -246,23 +268,9 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
                int H, int n, int S, int k, int64_t* idx_out, float* w_out, float* score_out,
                int32_t* half_idx_out, void* ws, size_t ws_bytes, pkmem_stream_t stream) {
   const char* fn = "mem_search";
-  if (!dtype_ok(q_dt) || !dtype_ok(k_dt)) return fail(PKMEM_ERR_INVALID, "%s: unknown dtype", fn);
-  if (q_dt != k_dt) return fail(PKMEM_ERR_UNSUPPORTED, "%s: queries and sub-keys must share a dtype", fn);
-  if (T < 0) return fail(PKMEM_ERR_INVALID, "%s: T must be >= 0", fn);
-  if (H < 1) return fail(PKMEM_ERR_INVALID, "%s: H must be >= 1", fn);
-  if (n < 2 || n % 2 != 0) return fail(PKMEM_ERR_INVALID, "%s: n must be even and >= 2 (got %d)", fn, n);
-  const int d = n / 2;
-  if (q_dt == PKMEM_BF16 && (d % 8 != 0 || d > PKMEM_DHALF_MAX))
-    return fail(PKMEM_ERR_UNSUPPORTED, "%s: bf16 needs n/2 a multiple of 8 and <= %d (got %d)", fn, PKMEM_DHALF_MAX, d);
-  if (q_dt == PKMEM_F32 && (d % 4 != 0 || d > 64))
-    return fail(PKMEM_ERR_UNSUPPORTED, "%s: fp32 needs n/2 a multiple of 4 and <= 64 (got %d)", fn, d);
-  if (S < 1) return fail(PKMEM_ERR_INVALID, "%s: S must be >= 1", fn);
-  if (S > PKMEM_SMAX) return fail(PKMEM_ERR_UNSUPPORTED, "%s: S > %d", fn, PKMEM_SMAX);
-  if (k < 1 || k > S) return fail(PKMEM_ERR_INVALID, "%s: need 1 <= k <= S (k=%d, S=%d)", fn, k, S);
-  if (k > PKMEM_KMAX) return fail(PKMEM_ERR_UNSUPPORTED, "%s: k > %d", fn, PKMEM_KMAX);
-  if ((T * H * 2) > (int64_t)0xFFFFFFFF) return fail(PKMEM_ERR_UNSUPPORTED, "%s: T*H*2 must be < 2^32", fn);
-  if (T > 0 && (!q || !subkeys || !idx_out || !w_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
-  if (!aligned(q, 16) || !aligned(subkeys, 16)) return fail(PKMEM_ERR_INVALID, "%s: q and subkeys must be 16-byte aligned", fn);
+  int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k);
+  if (rc) return rc;
+  if (T > 0 && (!idx_out || !w_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
   const SearchWs need = search_ws(nullptr, T, H, k);
   if (!ws || ws_bytes < need.bytes)
     return fail(PKMEM_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need.bytes, ws ? ws_bytes : (size_t)0);
@@ -277,6 +285,27 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
   e = pk::launch_cartesian(hidx, w.half_score, T, H, S, k, idx_out, w_out, score_out, st);
   if (e != hipSuccess) return hip_status(e, fn);
   return PKMEM_OK;
+}
+
+size_t mem_search_backward_workspace_size(int64_t T, int H, int S, int k) {
+  (void)T; (void)H; (void)S; (void)k;
+  return 0;
+}
+
+int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                        int64_t T, int H, int n, int S, int k, const int64_t* idx,
+                        const float* grad_scores, float* grad_q, float* grad_subkeys, void* ws,
+                        size_t ws_bytes, pkmem_stream_t stream) {
+  (void)ws; (void)ws_bytes;
+  const char* fn = "mem_search_backward";
+  int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k);
+  if (rc) return rc;
+  if (T > 0 && (!idx || !grad_scores)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (T == 0 || (!grad_q && !grad_subkeys)) return PKMEM_OK;
+  hipError_t e = pk::launch_search_backward(q_dt == PKMEM_BF16, q, subkeys, T, H, n, S, k, idx,
+                                            grad_scores, grad_q, grad_subkeys,
+                                            reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, fn);
 }
 
 int mem_bag_forward(const void* values, pkmem_dtype v_dt, int64_t N, int D, const int64_t* idx,

@@ -43,6 +43,11 @@ hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, in
                             int S, int k, int64_t* idx_out, float* w_out, float* score_out,
                             hipStream_t st);
 
+// ---- search backward (search_bwd.hip) --------------------------------------
+hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
+                                  int n, int S, int k, const int64_t* idx, const float* gz,
+                                  float* grad_q, float* grad_K, hipStream_t st);
+
 // ---- bag (bag.hip) ---------------------------------------------------------
 hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_t* idx,
                               const float* w, int64_t T, int bag, void* y, hipStream_t st);

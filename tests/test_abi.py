@@ -162,3 +162,28 @@ def test_sparse_backward_rejects(lib):
     rc = f(FAKE, FAKE, BF16, 4096, 64, FAKE, FAKE, 0, 2, 4, FAKE, FAKE, 32, ctypes.addressof(nrows),
            None, None, FAKE, BIG_WS, None)
     assert rc == OK and nrows.value == 0
+
+
+def sbwd(lib, q=FAKE, qdt=BF16, K=FAKE, kdt=BF16, T=8, H=2, n=64, S=16, k=4, idx=FAKE, gz=FAKE,
+         gq=FAKE, gk=FAKE):
+    return lib.mem_search_backward(q, qdt, K, kdt, T, H, n, S, k, idx, gz, gq, gk, None, 0, None)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(n=63), INVALID, "even"),
+    (dict(k=17), INVALID, "k <= S"),
+    (dict(S=9000), UNSUPPORTED, "S >"),
+    (dict(qdt=F32), UNSUPPORTED, "share a dtype"),
+    (dict(idx=0), INVALID, "null"),
+    (dict(gz=0), INVALID, "null"),
+    (dict(q=FAKE + 2), INVALID, "aligned"),
+])
+def test_search_backward_rejects(lib, kw, code, text):
+    assert sbwd(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def test_search_backward_noops(lib):
+    assert sbwd(lib, T=0) == OK
+    assert sbwd(lib, gq=None, gk=None) == OK          # nothing requested
+    assert lib.mem_search_backward_workspace_size(100, 4, 2048, 32) == 0
