@@ -21,6 +21,9 @@ constexpr int WAVE = 64;
 #ifndef PK_FWD_SPLIT
 #define PK_FWD_SPLIT 1   // waves per token in the gather for 4 KiB / 8 KiB rows
 #endif
+#ifndef PK_ROWS_BATCH
+#define PK_ROWS_BATCH 2  // adjacent touched rows per lane group per iteration (sorted backward)
+#endif
 #ifndef PK_STREAM_NT
 #define PK_STREAM_NT 1   // non-temporal hints on value rows streamed once
 #endif

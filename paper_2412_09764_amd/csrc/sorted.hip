@@ -254,11 +254,12 @@ struct Quad<float> {
 
 // One lane group per touched row.  Value and gradient rows are streamed once
 // per step with non-temporal accesses, so they do not push the re-read dy rows
-// and metadata out of the caches.  The next segment's bounds are fetched one
-// iteration ahead, and the old gradient row is read into the accumulator
-// together with the value row, so a group waits for about two dependent memory
-// round trips per touched row.
-template <typename V, int NQ, int CL, bool SPARSE>
+// and metadata out of the caches.  A lane group takes SB adjacent segments per
+// iteration (loads of all of them, then all of their gradient-row stores: one
+// longer read burst and one contiguous write burst), with the next batch's
+// bounds prefetched; the old gradient row is read into the accumulator
+// together with the value row.
+template <typename V, int NQ, int CL, bool SPARSE, int SB>
 __global__ __launch_bounds__(256) void k_bag_bwd_rows(
     const V* __restrict__ dy, const V* __restrict__ values, int D, const float* __restrict__ w,
     int bag, const uint32_t* __restrict__ rows_sorted, const uint32_t* __restrict__ lookups,
@@ -276,71 +277,96 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
 #pragma unroll
   for (int m = 0; m < NQ; ++m) ok[m] = (m * CL + cl) < nquad;
 
-  const int64_t groups = (int64_t)gridDim.x * 4 * G;
-  int64_t u = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * G + grp;
-  uint32_t s0 = 0, s1 = 0;
-  int64_t row = 0;
-  if (u < U) {
-    s0 = seg_start[u];
-    s1 = seg_start[u + 1];
-    row = rows_sorted[s0];
+  const int64_t step = (int64_t)gridDim.x * 4 * G * SB;
+  int64_t u0 = (((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * G + grp) * SB;
+  uint32_t s0[SB], s1[SB];
+  int64_t row[SB];
+#pragma unroll
+  for (int b = 0; b < SB; ++b) {
+    const bool live = u0 + b < U;
+    s0[b] = live ? seg_start[u0 + b] : 0;
+    s1[b] = live ? seg_start[u0 + b + 1] : 0;
+    row[b] = live ? (int64_t)rows_sorted[s0[b]] : 0;
   }
-  while (u < U) {
-    typename Q::raw vraw[NQ];
-    float acc[NQ][4];
+  while (u0 < U) {
+    typename Q::raw vraw[SB][NQ];
+    float acc[SB][NQ][4];
 #pragma unroll
-    for (int m = 0; m < NQ; ++m) {
-      const size_t e0 = (size_t)(m * CL + cl) * 4;
-      vraw[m] = ok[m] ? Q::load_nt(values + row * D + e0) : Q::zero();
-      const uint4 g = (ok[m] && dense) ? ld16_hint<PK_GRAD_NT_LOAD>(grad_values + row * D + e0)
-                                       : uint4{0, 0, 0, 0};
-      acc[m][0] = __uint_as_float(g.x); acc[m][1] = __uint_as_float(g.y);
-      acc[m][2] = __uint_as_float(g.z); acc[m][3] = __uint_as_float(g.w);
-    }
-    const int64_t un = u + groups;
-    uint32_t s0n = 0, s1n = 0;
-    if (un < U) {
-      s0n = seg_start[un];
-      s1n = seg_start[un + 1];
-    }
-    for (uint32_t s = s0; s < s1; ++s) {
-      const uint32_t l = lookups[s];
-      const int64_t t = l / (uint32_t)bag;
-      const float ww = w[l];
-      typename Q::raw graw[NQ];
-#pragma unroll
-      for (int m = 0; m < NQ; ++m)
-        graw[m] = ok[m] ? Q::load(dy + t * D + (size_t)(m * CL + cl) * 4) : Q::zero();
-      float part = 0.f;
+    for (int b = 0; b < SB; ++b) {
+      const bool live = u0 + b < U;
 #pragma unroll
       for (int m = 0; m < NQ; ++m) {
-        float g[4], v[4];
-        Q::unpack(graw[m], g);
-        Q::unpack(vraw[m], v);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[m][e] = fmaf(ww, g[e], acc[m][e]);
-          part = fmaf(g[e], v[e], part);
-        }
+        const size_t e0 = (size_t)(m * CL + cl) * 4;
+        vraw[b][m] = (ok[m] && live) ? Q::load_nt(values + row[b] * D + e0) : Q::zero();
+        const uint4 g = (ok[m] && dense && live)
+                            ? ld16_hint<PK_GRAD_NT_LOAD>(grad_values + row[b] * D + e0)
+                            : uint4{0, 0, 0, 0};
+        acc[b][m][0] = __uint_as_float(g.x); acc[b][m][1] = __uint_as_float(g.y);
+        acc[b][m][2] = __uint_as_float(g.z); acc[b][m][3] = __uint_as_float(g.w);
       }
-      part = group_sum<CL>(part);
-      if (cl == 0) grad_w[l] = part;
     }
-    const int64_t rown = (un < U) ? (int64_t)rows_sorted[s0n] : 0;
-    if (SPARSE || dense) {
-      float* dst = SPARSE ? grad_rows_out + (size_t)u * D : grad_values + row * D;
+    const int64_t un = u0 + step;
+    uint32_t s0n[SB], s1n[SB];
 #pragma unroll
-      for (int m = 0; m < NQ; ++m)
-        if (ok[m])
-          st16_hint<PK_GRAD_NT_STORE>(dst + (size_t)(m * CL + cl) * 4,
-                  uint4{__float_as_uint(acc[m][0]), __float_as_uint(acc[m][1]),
-                        __float_as_uint(acc[m][2]), __float_as_uint(acc[m][3])});
+    for (int b = 0; b < SB; ++b) {
+      const bool live = un + b < U;
+      s0n[b] = live ? seg_start[un + b] : 0;
+      s1n[b] = live ? seg_start[un + b + 1] : 0;
     }
-    if (SPARSE && cl == 0) rows_out[u] = row;
-    u = un;
-    s0 = s0n;
-    s1 = s1n;
-    row = rown;
+#pragma unroll
+    for (int b = 0; b < SB; ++b) {
+      for (uint32_t s = s0[b]; s < s1[b]; ++s) {
+        const uint32_t l = lookups[s];
+        const int64_t t = l / (uint32_t)bag;
+        const float ww = w[l];
+        typename Q::raw graw[NQ];
+#pragma unroll
+        for (int m = 0; m < NQ; ++m)
+          graw[m] = ok[m] ? Q::load(dy + t * D + (size_t)(m * CL + cl) * 4) : Q::zero();
+        float part = 0.f;
+#pragma unroll
+        for (int m = 0; m < NQ; ++m) {
+          float g[4], v[4];
+          Q::unpack(graw[m], g);
+          Q::unpack(vraw[b][m], v);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[b][m][e] = fmaf(ww, g[e], acc[b][m][e]);
+            part = fmaf(g[e], v[e], part);
+          }
+        }
+        part = group_sum<CL>(part);
+        if (cl == 0) grad_w[l] = part;
+      }
+    }
+    int64_t rown[SB];
+#pragma unroll
+    for (int b = 0; b < SB; ++b) rown[b] = (un + b < U) ? (int64_t)rows_sorted[s0n[b]] : 0;
+    if (SPARSE || dense) {
+#pragma unroll
+      for (int b = 0; b < SB; ++b) {
+        if (u0 + b >= U) continue;
+        float* dst = SPARSE ? grad_rows_out + (size_t)(u0 + b) * D : grad_values + row[b] * D;
+#pragma unroll
+        for (int m = 0; m < NQ; ++m)
+          if (ok[m])
+            st16_hint<PK_GRAD_NT_STORE>(dst + (size_t)(m * CL + cl) * 4,
+                                        uint4{__float_as_uint(acc[b][m][0]), __float_as_uint(acc[b][m][1]),
+                                              __float_as_uint(acc[b][m][2]), __float_as_uint(acc[b][m][3])});
+      }
+    }
+    if (SPARSE && cl == 0) {
+#pragma unroll
+      for (int b = 0; b < SB; ++b)
+        if (u0 + b < U) rows_out[u0 + b] = row[b];
+    }
+    u0 = un;
+#pragma unroll
+    for (int b = 0; b < SB; ++b) {
+      s0[b] = s0n[b];
+      s1[b] = s1n[b];
+      row[b] = rown[b];
+    }
   }
 }
 
@@ -427,24 +453,24 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
 
   // 3. one lane group per touched row
   const int nquad = D / 4;
-  int64_t blocks = cdiv(L, 4);
+  int64_t blocks = cdiv(L, 4 * PK_ROWS_BATCH);
   if (blocks > 16384) blocks = 16384;
   const dim3 grid((unsigned)blocks), block(256);
   const bool sparse = rows_out != nullptr;
   LaunchTimer lt("bag_backward_rows", st);
 #define PK_ROWS(NQ, CL)                                                                           \
   if (bf16) {                                                                                     \
-    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, NQ, CL, true>), grid, block, 0, st,   \
+    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, NQ, CL, true, PK_ROWS_BATCH>), grid, block, 0, st,   \
         (const uint16_t*)dy, (const uint16_t*)values, D, w, bag, ks, vs, b.seg, b.misc,            \
         grad_values, rows_out, grad_rows_out, grad_w);                                            \
-    else hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, NQ, CL, false>), grid, block, 0, st,        \
+    else hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, NQ, CL, false, PK_ROWS_BATCH>), grid, block, 0, st,        \
         (const uint16_t*)dy, (const uint16_t*)values, D, w, bag, ks, vs, b.seg, b.misc,            \
         grad_values, rows_out, grad_rows_out, grad_w);                                            \
   } else {                                                                                        \
-    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<float, NQ, CL, true>), grid, block, 0, st,      \
+    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<float, NQ, CL, true, PK_ROWS_BATCH>), grid, block, 0, st,      \
         (const float*)dy, (const float*)values, D, w, bag, ks, vs, b.seg, b.misc, grad_values,     \
         rows_out, grad_rows_out, grad_w);                                                         \
-    else hipLaunchKernelGGL((k_bag_bwd_rows<float, NQ, CL, false>), grid, block, 0, st,           \
+    else hipLaunchKernelGGL((k_bag_bwd_rows<float, NQ, CL, false, PK_ROWS_BATCH>), grid, block, 0, st,           \
         (const float*)dy, (const float*)values, D, w, bag, ks, vs, b.seg, b.misc, grad_values,     \
         rows_out, grad_rows_out, grad_w);                                                         \
   }
