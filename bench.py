@@ -277,10 +277,12 @@ def main():
     # own, after the timed steps; not part of the step's throughput.
     gq = torch.empty((T, H, wl.n), dtype=torch.float32, device=dev)
     gK = torch.zeros((H, 2, wl.S, wl.d), dtype=torch.float32, device=dev)
+    ws_sb = torch.empty(max(1, pk.load().mem_search_backward_workspace_size(T, H, wl.S, k)),
+                        dtype=torch.uint8, device=dev)
     def sbwd():
         pk._check(L.mem_search_backward(q.data_ptr(), KDT, K.data_ptr(), KDT, T, H, wl.n, wl.S, k,
                                         idx.data_ptr(), gz.data_ptr(), gq.data_ptr(),
-                                        gK.data_ptr(), None, 0, st))
+                                        gK.data_ptr(), ws_sb.data_ptr(), ws_sb.numel(), st))
     sbwd()
     torch.cuda.synchronize()
     pk.mem_timer_start("search_backward")
@@ -290,7 +292,7 @@ def main():
     pk.mem_timer_stop()
     sb = [ms for _, ms in pk.mem_timer_read()]
     search_bwd_ms = sum(sb) / len(sb)
-    del gq, gK
+    del gq, gK, ws_sb
 
     # touched rows of the last step's selection (outside the timed region)
     uniq, counts = torch.unique(idx.view(-1), return_counts=True)

@@ -105,15 +105,18 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
  *   z[t,h,j] = q[t,h,0:d] . subkeys[h,0,i1] + q[t,h,d:n] . subkeys[h,1,i2].
  *
  *   q, subkeys, T, H, n, S, k   as for mem_search (same dtype rules and limits).
- *   idx          [T, H, k] int64  mem_search's selection.
+ *   idx          [T, H, k] int64  mem_search's selection; lookups whose index lies
+ *                outside [0, S*S) contribute nothing (mem_search never writes one).
  *   grad_scores  [T, H, k] fp32   dL/dz (mem_bag_backward's grad_scores).
  * Outputs (each may be NULL to skip it):
  *   grad_q        [T, H, n] fp32, written:
  *                 grad_q[t,h,0:d] = sum_j gz[t,h,j] subkeys[h,0,i1_j], likewise half 1.
  *   grad_subkeys  [H, 2, S, n/2] fp32, ACCUMULATED (+=):
  *                 += sum over (t,j) with i1_j = i of gz[t,h,j] q[t,h,0:d], likewise half 1.
- *                 Summed with fp32 atomics: not bitwise deterministic run to run.
- * Needs no workspace (ws may be NULL, ws_bytes 0).
+ *                 Bitwise deterministic: the (lookup, half) pairs are sorted by sub-key
+ *                 and each sub-key row is summed by one wave in token order, no atomics.
+ *                 Requires 2*T*H*k < 2^32.
+ * Workspace: mem_search_backward_workspace_size(T, H, S, k) bytes, 256-byte aligned.
  * ------------------------------------------------------------------------ */
 size_t mem_search_backward_workspace_size(int64_t T, int H, int S, int k);
 

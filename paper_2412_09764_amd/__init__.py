@@ -182,7 +182,8 @@ def mem_search(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None, 
 
 def mem_search_backward(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tensor,
                         grad_scores: torch.Tensor, *, grad_q=None, grad_subkeys=None,
-                        want_grad_q: bool = True, want_grad_subkeys: bool = True, stream=None):
+                        want_grad_q: bool = True, want_grad_subkeys: bool = True, workspace=None,
+                        stream=None):
     """Gradients of the selected scores into q ([T,H,n], written) and the
     sub-keys ([H,2,S,n/2], ACCUMULATED; a zero table is allocated if none is
     given).  Returns (grad_q, grad_subkeys)."""
@@ -196,9 +197,11 @@ def mem_search_backward(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tenso
     if grad_subkeys is None and want_grad_subkeys:
         grad_subkeys = torch.zeros(subkeys.shape, dtype=torch.float32, device=q.device)
     _dev(grad_q, grad_subkeys)
+    nbytes = int(L.mem_search_backward_workspace_size(T, H, S, k))
+    ws = _workspace(nbytes, q.device, workspace)
     _check(L.mem_search_backward(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
                                  _ptr(idx), _ptr(grad_scores), _ptr(grad_q), _ptr(grad_subkeys),
-                                 None, 0, _stream(stream)))
+                                 _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
     return grad_q, grad_subkeys
 
 

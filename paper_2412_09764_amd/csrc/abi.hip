@@ -288,22 +288,32 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
 }
 
 size_t mem_search_backward_workspace_size(int64_t T, int H, int S, int k) {
-  (void)T; (void)H; (void)S; (void)k;
-  return 0;
+  (void)S;
+  if (T < 0 || H < 1 || k < 1) return 0;
+  return pk::search_backward_ws_bytes(T, H, k);
 }
 
 int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
                         int64_t T, int H, int n, int S, int k, const int64_t* idx,
                         const float* grad_scores, float* grad_q, float* grad_subkeys, void* ws,
                         size_t ws_bytes, pkmem_stream_t stream) {
-  (void)ws; (void)ws_bytes;
   const char* fn = "mem_search_backward";
   int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k);
   if (rc) return rc;
   if (T > 0 && (!idx || !grad_scores)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (2 * T * (int64_t)H * k >= (int64_t(1) << 32))
+    return fail(PKMEM_ERR_UNSUPPORTED, "%s: 2*T*H*k must be < 2^32", fn);
+  if (2 * (int64_t)H * S >= (int64_t(1) << 31))
+    return fail(PKMEM_ERR_UNSUPPORTED, "%s: 2*H*S must be < 2^31", fn);
+  if (!aligned(grad_subkeys, 16) || !aligned(grad_q, 4))
+    return fail(PKMEM_ERR_INVALID, "%s: grad_subkeys must be 16-byte and grad_q 4-byte aligned", fn);
+  const size_t need = mem_search_backward_workspace_size(T, H, S, k);
+  if (!ws || ws_bytes < need)
+    return fail(PKMEM_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : (size_t)0);
+  if (!aligned(ws, 256)) return fail(PKMEM_ERR_INVALID, "%s: workspace must be 256-byte aligned", fn);
   if (T == 0 || (!grad_q && !grad_subkeys)) return PKMEM_OK;
   hipError_t e = pk::launch_search_backward(q_dt == PKMEM_BF16, q, subkeys, T, H, n, S, k, idx,
-                                            grad_scores, grad_q, grad_subkeys,
+                                            grad_scores, grad_q, grad_subkeys, ws,
                                             reinterpret_cast<hipStream_t>(stream));
   return hip_status(e, fn);
 }

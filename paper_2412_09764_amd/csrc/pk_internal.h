@@ -44,9 +44,13 @@ hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, in
                             hipStream_t st);
 
 // ---- search backward (search_bwd.hip) --------------------------------------
+size_t search_backward_ws_bytes(int64_t T, int H, int k);
+hipError_t sort_u32_segments(const uint32_t* keys, int64_t L, int key_bits, void* ws,
+                             const uint32_t** ks, const uint32_t** vs, const uint32_t** seg,
+                             const uint32_t** nseg, hipStream_t st);
 hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
                                   int n, int S, int k, const int64_t* idx, const float* gz,
-                                  float* grad_q, float* grad_K, hipStream_t st);
+                                  float* grad_q, float* grad_K, void* ws, hipStream_t st);
 
 // ---- bag (bag.hip) ---------------------------------------------------------
 hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_t* idx,

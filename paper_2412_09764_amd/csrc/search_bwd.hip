@@ -6,51 +6,93 @@
 // so grad_q[:d] = sum_j gz_j K[h,0,i1_j] and grad_K[h,0,i] += sum_{j: i1_j = i}
 // gz_j q[:d] (same for half 1).
 //
-// One wave per (token, head).  The k lookups sit one per lane; per half, each
-// lane finds the leader of its sub-key group (lowest rank with the same
-// sub-key index) and the group's summed gradient, in rank order.  The wave then
-// visits the distinct sub-keys only: it reads each needed sub-key row once for
-// grad_q and adds g * q_half into the gradient row with lane-contiguous fp32
-// atomics (no return).  Blocks are laid out so that consecutive blocks (which
-// the dispatcher spreads over the XCDs) take different heads: each head's
-// gradient table is then touched from as few XCDs as possible.
+// grad_q: one wave per (token, head).  The k lookups sit one per lane; per
+// half, each lane finds the leader of its sub-key group (lowest rank with the
+// same sub-key index) and the group's summed gradient, in rank order; the wave
+// reads each distinct sub-key row once.
+//
+// grad_K: every sub-key row is hot (only S rows per head and half), and fp32
+// atomics, in global memory or in LDS, serialise on them.  Instead the same
+// wave emits one (head, half, sub-key) sort key per group leader, with the
+// group's gradient sum, and the 2*T*H*k (lookup, half) pairs are sorted by key
+// with the library's stable radix sort.  One wave per segment then sums
+// gsum * q over the segment's tokens (in token order; each token's query half
+// is read once) and adds the sum into the sub-key row with one plain
+// read-modify-write: no atomics, bitwise deterministic.
 #include "pk_device.h"
 #include "pk_internal.h"
 
 namespace pk {
 
+// Four consecutive elements of a query or sub-key half row: bf16 (8 bytes) or
+// fp32 (16 bytes).
 template <typename T>
-__device__ __forceinline__ float elem_f32(const T* p);
+struct QQuad;
 template <>
-__device__ __forceinline__ float elem_f32<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+struct QQuad<uint16_t> {
+  uint2 raw;
+  __device__ __forceinline__ void load(const uint16_t* p) { raw = *reinterpret_cast<const uint2*>(p); }
+  __device__ __forceinline__ void fma_into(float g, float* a) const {
+    a[0] = fmaf(g, __uint_as_float(raw.x << 16), a[0]);
+    a[1] = fmaf(g, __uint_as_float(raw.x & 0xffff0000u), a[1]);
+    a[2] = fmaf(g, __uint_as_float(raw.y << 16), a[2]);
+    a[3] = fmaf(g, __uint_as_float(raw.y & 0xffff0000u), a[3]);
+  }
+};
 template <>
-__device__ __forceinline__ float elem_f32<float>(const float* p) { return *p; }
+struct QQuad<float> {
+  float4 raw;
+  __device__ __forceinline__ void load(const float* p) { raw = *reinterpret_cast<const float4*>(p); }
+  __device__ __forceinline__ void fma_into(float g, float* a) const {
+    a[0] = fmaf(g, raw.x, a[0]);
+    a[1] = fmaf(g, raw.y, a[1]);
+    a[2] = fmaf(g, raw.z, a[2]);
+    a[3] = fmaf(g, raw.w, a[3]);
+  }
+};
 
-// NE = elements per lane per half = ceil(d / 64).
-template <typename T, int NE>
-__global__ __launch_bounds__(256) void k_search_bwd(const T* __restrict__ q,
-                                                    const T* __restrict__ subkeys, int64_t ntok,
-                                                    int H, int n, int S, int k,
-                                                    const int64_t* __restrict__ idx,
-                                                    const float* __restrict__ gz,
-                                                    float* __restrict__ grad_q,
-                                                    float* __restrict__ grad_K) {
+// Per (token, head) wave, per half: lane j holds rank j's sub-key; each lane
+// finds the leader of its sub-key group (lowest rank with the same sub-key)
+// and the group's gradient sum, in rank order.  Then
+//   * grad_q (if wanted): the distinct sub-key rows are read QU at a time (all
+//     loads in flight together), lane l owning elements 4l..4l+3;
+//   * sort input (if wanted): pair x = ((t*H + h)*k + j)*2 + half gets the key
+//     (h*2 + half)*S + sub-key and value gsum when rank j leads its group, and
+//     the key 2*H*S (a skipped segment) otherwise.  Lookups whose index lies
+//     outside [0, S*S) count as absent.
+#ifndef PK_SBWD_QU
+#define PK_SBWD_QU 8
+#endif
+template <typename T>
+__global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
+                                                      const T* __restrict__ subkeys, int64_t ntok,
+                                                      int H, int n, int S, int k,
+                                                      const int64_t* __restrict__ idx,
+                                                      const float* __restrict__ gz,
+                                                      float* __restrict__ grad_q,
+                                                      uint2* __restrict__ keys,
+                                                      float2* __restrict__ gvals) {
+  constexpr int QU = PK_SBWD_QU;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int h = (int)(blockIdx.x % (unsigned)H);
   const int64_t t = (int64_t)(blockIdx.x / (unsigned)H) * 4 + wave;
   if (t >= ntok) return;
   const int d = n >> 1;
+  const bool qlane = lane * 4 < d;
+  const int ql = qlane ? lane * 4 : 0;
   const size_t r = (size_t)t * H + h;
-  const int64_t ix = lane < k ? idx[r * k + lane] : 0;
-  const float g = lane < k ? gz[r * k + lane] : 0.f;
-  const T* qrow = q + r * n;
+  const int64_t ix = lane < k ? idx[r * k + lane] : -1;
+  const bool okl = ix >= 0 && ix < (int64_t)S * S;
+  const float g = okl ? gz[r * k + lane] : 0.f;
+  const uint32_t nbins = (uint32_t)(2 * H) * (uint32_t)S;
+  uint32_t key[2];
+  float gs[2];
 
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
-    const int mine = (int)(p == 0 ? ix / S : ix % S);
-    // group sum in rank order; leader = first rank of the group
+    const int mine = okl ? (int)(p == 0 ? ix / S : ix % S) : -1;
     float gsum = 0.f;
-    bool leader = lane < k;
+    bool leader = okl;
     for (int j = 0; j < k; ++j) {
       const int oi = __builtin_amdgcn_readlane(mine, j);
       const float og = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), j));
@@ -59,66 +101,144 @@ __global__ __launch_bounds__(256) void k_search_bwd(const T* __restrict__ q,
         if (j < lane) leader = false;
       }
     }
-    uint64_t lead = __ballot(leader);
-    float qh[NE], dq[NE];
-#pragma unroll
-    for (int c = 0; c < NE; ++c) {
-      const int e = lane + 64 * c;
-      qh[c] = e < d ? elem_f32<T>(qrow + (size_t)p * d + e) : 0.f;
-      dq[c] = 0.f;
-    }
-    const T* kh = subkeys + (size_t)(h * 2 + p) * S * d;
-    float* gkh = grad_K ? grad_K + (size_t)(h * 2 + p) * S * d : nullptr;
-    while (lead) {
-      const int L = __builtin_ctzll(lead);
-      lead &= lead - 1;
-      const int i = __builtin_amdgcn_readlane(mine, L);
-      const float gg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gsum), L));
-      const T* krow = kh + (size_t)i * d;
-#pragma unroll
-      for (int c = 0; c < NE; ++c) {
-        const int e = lane + 64 * c;
-        if (e < d) {
-          dq[c] = fmaf(gg, elem_f32<T>(krow + e), dq[c]);
-          if (gkh) unsafeAtomicAdd(gkh + (size_t)i * d + e, gg * qh[c]);
-        }
-      }
-    }
+    key[p] = leader ? (uint32_t)(h * 2 + p) * (uint32_t)S + (uint32_t)mine : nbins;
+    gs[p] = gsum;
     if (grad_q) {
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+      const T* kh = subkeys + (size_t)(h * 2 + p) * S * d + ql;
+      uint64_t m = __ballot(leader);
+      while (m) {
+        QQuad<T> kq[QU];
+        float gg[QU];
+        const int first = __builtin_ctzll(m);
 #pragma unroll
-      for (int c = 0; c < NE; ++c) {
-        const int e = lane + 64 * c;
-        if (e < d) grad_q[r * n + (size_t)p * d + e] = dq[c];
+        for (int j = 0; j < QU; ++j) {
+          const bool has = m != 0;
+          const int L = has ? __builtin_ctzll(m) : first;
+          m = has ? (m & (m - 1)) : m;
+          const int i = __builtin_amdgcn_readlane(mine, L);
+          const float gj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gsum), L));
+          gg[j] = has ? gj : 0.f;
+          kq[j].load(kh + (size_t)i * d);
+        }
+#pragma unroll
+        for (int j = 0; j < QU; ++j) kq[j].fma_into(gg[j], acc);
       }
+      if (qlane)
+        *reinterpret_cast<float4*>(grad_q + r * n + (size_t)p * d + ql) =
+            make_float4(acc[0], acc[1], acc[2], acc[3]);
     }
   }
+  if (keys && lane < k) {
+    keys[r * k + lane] = uint2{key[0], key[1]};
+    gvals[r * k + lane] = make_float2(gs[0], gs[1]);
+  }
+}
+
+// One wave per segment (grid-stride) of the sorted pairs; a segment is one
+// (head, half, sub-key) and holds at most one pair per token, in token order.
+// Lane l owns elements 4l..4l+3 of the d-element row (d <= 256).  The pairs
+// are taken 64 at a time and consumed in order, QU at a time, with their
+// query-quad loads issued together; the sum is added into the sub-key row with
+// one read-modify-write.
+template <typename T>
+__global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, int H, int n,
+                                                       int S, int k,
+                                                       const float* __restrict__ gvals,
+                                                       const uint32_t* __restrict__ ks,
+                                                       const uint32_t* __restrict__ vs,
+                                                       const uint32_t* __restrict__ seg,
+                                                       const uint32_t* __restrict__ nseg_p,
+                                                       float* __restrict__ grad_K) {
+  constexpr int QU = PK_SBWD_QU;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t nseg = *nseg_p;
+  const int d = n >> 1;
+  const bool qlane = lane * 4 < d;
+  const int ql = qlane ? lane * 4 : 0;
+  const uint32_t nbins = (uint32_t)(2 * H) * (uint32_t)S;
+  const uint32_t hk2 = 2u * (uint32_t)H * (uint32_t)k;  // pairs per token
+  for (uint32_t u = blockIdx.x * 4u + wave; u < nseg; u += gridDim.x * 4u) {
+    const uint32_t s0 = seg[u], s1 = seg[u + 1];
+    const uint32_t bin = ks[s0];
+    if (bin >= nbins) continue;  // non-leading ranks and absent lookups
+    const int hp = (int)(bin / (uint32_t)S);
+    const int h = hp >> 1, p = hp & 1;
+    const T* qh = q + (size_t)h * n + (size_t)p * d + ql;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (uint32_t b0 = s0; b0 < s1; b0 += 64) {
+      const uint32_t e = b0 + lane;
+      const bool ok = e < s1;
+      const uint32_t x = ok ? vs[e] : 0u;
+      const uint32_t t = x / hk2;
+      const float gx = ok ? gvals[x] : 0.f;
+      const uint32_t cnt = (s1 - b0) < 64u ? (s1 - b0) : 64u;
+      for (uint32_t j0 = 0; j0 < cnt; j0 += QU) {
+        QQuad<T> qq[QU];
+        float gg[QU];
+#pragma unroll
+        for (int j = 0; j < QU; ++j) {
+          const bool has = j0 + j < cnt;
+          const int L = has ? (int)(j0 + j) : (int)j0;
+          const uint32_t tj = (uint32_t)__builtin_amdgcn_readlane((int)t, L);
+          const float xj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), L));
+          gg[j] = has ? xj : 0.f;
+          qq[j].load(qh + (size_t)tj * H * n);
+        }
+#pragma unroll
+        for (int j = 0; j < QU; ++j) qq[j].fma_into(gg[j], acc);
+      }
+    }
+    if (qlane) {
+      float4* dst = reinterpret_cast<float4*>(grad_K + (size_t)bin * d + ql);
+      float4 o = *dst;
+      o.x += acc[0]; o.y += acc[1]; o.z += acc[2]; o.w += acc[3];
+      *dst = o;
+    }
+  }
+}
+
+size_t search_backward_ws_bytes(int64_t T, int H, int k) {
+  const int64_t np = 2 * T * H * k;
+  return 2 * (((size_t)np * 4 + 255) / 256 * 256) + sorted_workspace_bytes(np);
 }
 
 template <typename T>
 static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, int H, int n, int S,
                               int k, const int64_t* idx, const float* gz, float* grad_q,
-                              float* grad_K, hipStream_t st) {
-  const int d = n / 2;
-  const int64_t blocks = ((T_ + 3) / 4) * H;
-  const dim3 grid((unsigned)blocks), block(256);
+                              float* grad_K, void* ws, hipStream_t st) {
   LaunchTimer lt("search_backward", st);
-  const int ne = (d + 63) / 64;
-#define PK_SB(NE)                                                                            \
-  hipLaunchKernelGGL((k_search_bwd<T, NE>), grid, block, 0, st, (const T*)q, (const T*)subkeys, \
-                     T_, H, n, S, k, idx, gz, grad_q, grad_K)
-  if (ne <= 1) PK_SB(1);
-  else if (ne <= 2) PK_SB(2);
-  else PK_SB(4);
-#undef PK_SB
+  const int64_t np = 2 * T_ * H * k;
+  const size_t arr = ((size_t)np * 4 + 255) / 256 * 256;
+  uint32_t* keys = reinterpret_cast<uint32_t*>(ws);
+  float* gvals = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + arr);
+  void* sort_ws = reinterpret_cast<char*>(ws) + 2 * arr;
+  hipLaunchKernelGGL(k_search_bwd_q<T>, dim3((unsigned)(((T_ + 3) / 4) * H)), dim3(256), 0, st,
+                     (const T*)q, (const T*)subkeys, T_, H, n, S, k, idx, gz, grad_q,
+                     grad_K ? reinterpret_cast<uint2*>(keys) : nullptr,
+                     grad_K ? reinterpret_cast<float2*>(gvals) : nullptr);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !grad_K) return e;
+  const uint32_t nbins = (uint32_t)(2 * H) * (uint32_t)S;  // plus the skipped key nbins
+  int key_bits = 1;
+  while (key_bits < 32 && (uint64_t(1) << key_bits) <= nbins) ++key_bits;
+  const uint32_t *ks, *vs, *seg, *nseg;
+  e = sort_u32_segments(keys, np, key_bits, sort_ws, &ks, &vs, &seg, &nseg, st);
+  if (e != hipSuccess) return e;
+  int64_t maxseg = (int64_t)nbins + 1 < np ? (int64_t)nbins + 1 : np;
+  int64_t blocks = (maxseg + 3) / 4;
+  if (blocks > 16384) blocks = 16384;
+  hipLaunchKernelGGL(k_sbwd_segments<T>, dim3((unsigned)blocks), dim3(256), 0, st, (const T*)q, H, n,
+                     S, k, gvals, ks, vs, seg, nseg, grad_K);
   return hipGetLastError();
 }
 
 hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
                                   int n, int S, int k, const int64_t* idx, const float* gz,
-                                  float* grad_q, float* grad_K, hipStream_t st) {
+                                  float* grad_q, float* grad_K, void* ws, hipStream_t st) {
   if (T <= 0) return hipSuccess;
-  if (bf16) return launch_sbwd<uint16_t>(q, subkeys, T, H, n, S, k, idx, gz, grad_q, grad_K, st);
-  return launch_sbwd<float>(q, subkeys, T, H, n, S, k, idx, gz, grad_q, grad_K, st);
+  if (bf16) return launch_sbwd<uint16_t>(q, subkeys, T, H, n, S, k, idx, gz, grad_q, grad_K, ws, st);
+  return launch_sbwd<float>(q, subkeys, T, H, n, S, k, idx, gz, grad_q, grad_K, ws, st);
 }
 
 }  // namespace pk

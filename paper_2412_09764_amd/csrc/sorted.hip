@@ -116,15 +116,18 @@ static hipError_t exclusive_scan(uint32_t* data, int64_t n, uint32_t* sums, hipS
 }
 
 // ----------------------------------------------------------- radix sort ----
-// Keys of the first pass come straight from the int64 lookup rows, values are
-// the lookup ids themselves.
-template <bool FIRST>
+// KM selects where a pass takes its items: SRC_I64 and SRC_U32 are first
+// passes (keys from an int64 or u32 array, values = item positions), SRC_NEXT
+// a later pass (keys and values from the previous pass's output).
+constexpr int SRC_I64 = 0, SRC_U32 = 1, SRC_NEXT = 2;
+
+template <int KM>
 __device__ __forceinline__ uint32_t sort_key(const void* keys, int64_t i) {
-  if constexpr (FIRST) return (uint32_t)reinterpret_cast<const int64_t*>(keys)[i];
+  if constexpr (KM == SRC_I64) return (uint32_t)reinterpret_cast<const int64_t*>(keys)[i];
   else return reinterpret_cast<const uint32_t*>(keys)[i];
 }
 
-template <bool FIRST>
+template <int KM>
 __global__ __launch_bounds__(256) void k_radix_hist(const void* __restrict__ keys, int64_t L,
                                                     int shift, int bits, int64_t nblk,
                                                     uint32_t* __restrict__ hist) {
@@ -136,13 +139,13 @@ __global__ __launch_bounds__(256) void k_radix_hist(const void* __restrict__ key
 #pragma unroll 4
   for (int i = 0; i < SORT_ITEMS; ++i) {
     const int64_t pos = tile + i * 256 + threadIdx.x;
-    if (pos < L) atomicAdd(&h[(sort_key<FIRST>(keys, pos) >> shift) & mask], 1u);
+    if (pos < L) atomicAdd(&h[(sort_key<KM>(keys, pos) >> shift) & mask], 1u);
   }
   __syncthreads();
   hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
 }
 
-template <bool FIRST>
+template <int KM>
 __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ keys_in,
                                                        const uint32_t* __restrict__ vals_in,
                                                        int64_t L, int shift, int bits, int64_t nblk,
@@ -163,8 +166,8 @@ __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ 
     // Items are taken in position order: slot-major, then thread order.
     const int64_t pos = tile + i * 256 + tid;
     const bool valid = pos < L;
-    const uint32_t key = valid ? sort_key<FIRST>(keys_in, pos) : 0u;
-    const uint32_t val = valid ? (FIRST ? (uint32_t)pos : vals_in[pos]) : 0u;
+    const uint32_t key = valid ? sort_key<KM>(keys_in, pos) : 0u;
+    const uint32_t val = valid ? (KM != SRC_NEXT ? (uint32_t)pos : vals_in[pos]) : 0u;
     const uint32_t dig = (key >> shift) & mask;
     uint64_t peers = __ballot(valid);
     for (int b = 0; b < bits; ++b) {
@@ -401,6 +404,61 @@ size_t sorted_workspace_bytes(int64_t L) {
          align256(4 * (size_t)(cdiv(scan_n, SCAN_TILE) + 1)) + align256(4 * (size_t)(L + 1)) + 256;
 }
 
+// Stable LSD radix sort of L keys (< 2^key_bits, from an int64 or a u32 array)
+// with their positions as values, then the segment starts of equal keys:
+// seg[0..U] in b.seg, U in b.misc[0].  *ks / *vs receive the sorted arrays.
+static hipError_t sort_segments(const void* keys, bool key64, int64_t L, int key_bits,
+                                const SortedWs& b, const uint32_t** ks, const uint32_t** vs,
+                                hipStream_t st) {
+  hipError_t e = hipSuccess;
+  const int64_t nblk = cdiv(L, SORT_TILE);
+  const void* kin = keys;
+  const uint32_t* vin = nullptr;
+  uint32_t *kout = b.keys_a, *vout = b.vals_a;
+  for (int shift = 0, pass = 0; shift < key_bits; shift += RADIX_BITS, ++pass) {
+    const int bits = (key_bits - shift) < RADIX_BITS ? (key_bits - shift) : RADIX_BITS;
+    const dim3 g((unsigned)nblk), blk(256);
+    if (pass > 0)
+      hipLaunchKernelGGL(k_radix_hist<SRC_NEXT>, g, blk, 0, st, kin, L, shift, bits, nblk, b.hist);
+    else if (key64)
+      hipLaunchKernelGGL(k_radix_hist<SRC_I64>, g, blk, 0, st, kin, L, shift, bits, nblk, b.hist);
+    else
+      hipLaunchKernelGGL(k_radix_hist<SRC_U32>, g, blk, 0, st, kin, L, shift, bits, nblk, b.hist);
+    e = exclusive_scan(b.hist, (int64_t)RADIX * nblk, b.sums, st);
+    if (e != hipSuccess) return e;
+    if (pass > 0)
+      hipLaunchKernelGGL(k_radix_scatter<SRC_NEXT>, g, blk, 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+    else if (key64)
+      hipLaunchKernelGGL(k_radix_scatter<SRC_I64>, g, blk, 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+    else
+      hipLaunchKernelGGL(k_radix_scatter<SRC_U32>, g, blk, 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+    kin = kout;
+    vin = vout;
+    if (kout == b.keys_a) { kout = b.keys_b; vout = b.vals_b; }
+    else { kout = b.keys_a; vout = b.vals_a; }
+  }
+  *ks = reinterpret_cast<const uint32_t*>(kin);
+  *vs = vin;
+  const unsigned lb = (unsigned)cdiv(L, 256);
+  hipLaunchKernelGGL(k_seg_flags, dim3(lb), dim3(256), 0, st, *ks, L, b.hist);
+  e = exclusive_scan(b.hist, L, b.sums, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_seg_starts, dim3(lb), dim3(256), 0, st, *ks, L, b.hist, b.seg, b.misc);
+  return hipGetLastError();
+}
+
+// Sort of u32 keys for other kernels of the library (same workspace layout).
+hipError_t sort_u32_segments(const uint32_t* keys, int64_t L, int key_bits, void* ws,
+                             const uint32_t** ks, const uint32_t** vs, const uint32_t** seg,
+                             const uint32_t** nseg, hipStream_t st) {
+  SortedWs b = carve(ws, L);
+  *seg = b.seg;
+  *nseg = b.misc;
+  hipError_t e = launch_fill_u32(b.misc, 0u, 1, st);
+  if (e != hipSuccess || L == 0) return e;
+  return sort_segments(keys, false, L, key_bits, b, ks, vs, st);
+}
+
 hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* values, int64_t N,
                                       int D, const int64_t* idx, const float* w, int64_t T,
                                       int bag, float* grad_values, int64_t* rows_out,
@@ -414,41 +472,13 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
   const uint32_t* ks = nullptr;
   const uint32_t* vs = nullptr;
 
-  // 1. radix sort of (row, lookup) by row
+  // 1. radix sort of (row, lookup) by row; 2. segments of equal rows
   {
     LaunchTimer lt_sort("sort_by_row", st);
     int key_bits = 1;
     while (key_bits < 32 && (int64_t(1) << key_bits) < N) ++key_bits;
-    const int64_t nblk = cdiv(L, SORT_TILE);
-    const void* kin = idx;
-    const uint32_t* vin = nullptr;
-    uint32_t *kout = b.keys_a, *vout = b.vals_a;
-    for (int shift = 0, pass = 0; shift < key_bits; shift += RADIX_BITS, ++pass) {
-      const int bits = (key_bits - shift) < RADIX_BITS ? (key_bits - shift) : RADIX_BITS;
-      if (pass == 0)
-        hipLaunchKernelGGL(k_radix_hist<true>, dim3((unsigned)nblk), dim3(256), 0, st, kin, L, shift, bits, nblk, b.hist);
-      else
-        hipLaunchKernelGGL(k_radix_hist<false>, dim3((unsigned)nblk), dim3(256), 0, st, kin, L, shift, bits, nblk, b.hist);
-      e = exclusive_scan(b.hist, (int64_t)RADIX * nblk, b.sums, st);
-      if (e != hipSuccess) return e;
-      if (pass == 0)
-        hipLaunchKernelGGL(k_radix_scatter<true>, dim3((unsigned)nblk), dim3(256), 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
-      else
-        hipLaunchKernelGGL(k_radix_scatter<false>, dim3((unsigned)nblk), dim3(256), 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
-      kin = kout;
-      vin = vout;
-      if (kout == b.keys_a) { kout = b.keys_b; vout = b.vals_b; }
-      else { kout = b.keys_a; vout = b.vals_a; }
-    }
-    ks = reinterpret_cast<const uint32_t*>(kin);
-    vs = vin;
-
-    // 2. segments of equal rows
-    const unsigned lb = (unsigned)cdiv(L, 256);
-    hipLaunchKernelGGL(k_seg_flags, dim3(lb), dim3(256), 0, st, ks, L, b.hist);
-    e = exclusive_scan(b.hist, L, b.sums, st);
+    e = sort_segments(idx, true, L, key_bits, b, &ks, &vs, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_seg_starts, dim3(lb), dim3(256), 0, st, ks, L, b.hist, b.seg, b.misc);
   }
 
   // 3. one lane group per touched row

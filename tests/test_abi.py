@@ -165,8 +165,8 @@ def test_sparse_backward_rejects(lib):
 
 
 def sbwd(lib, q=FAKE, qdt=BF16, K=FAKE, kdt=BF16, T=8, H=2, n=64, S=16, k=4, idx=FAKE, gz=FAKE,
-         gq=FAKE, gk=FAKE):
-    return lib.mem_search_backward(q, qdt, K, kdt, T, H, n, S, k, idx, gz, gq, gk, None, 0, None)
+         gq=FAKE, gk=FAKE, ws=FAKE, ws_bytes=BIG_WS):
+    return lib.mem_search_backward(q, qdt, K, kdt, T, H, n, S, k, idx, gz, gq, gk, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,code,text", [
@@ -177,6 +177,12 @@ def sbwd(lib, q=FAKE, qdt=BF16, K=FAKE, kdt=BF16, T=8, H=2, n=64, S=16, k=4, idx
     (dict(idx=0), INVALID, "null"),
     (dict(gz=0), INVALID, "null"),
     (dict(q=FAKE + 2), INVALID, "aligned"),
+    (dict(ws=0), WORKSPACE, "workspace"),
+    (dict(ws_bytes=8), WORKSPACE, "workspace"),
+    (dict(ws=FAKE + 8), INVALID, "256-byte"),
+    (dict(T=1 << 26, H=4, k=16), UNSUPPORTED, "2^32"),
+    (dict(T=1, H=1 << 18, S=8192, k=1), UNSUPPORTED, "2^31"),
+    (dict(gk=FAKE + 4), INVALID, "16-byte"),
 ])
 def test_search_backward_rejects(lib, kw, code, text):
     assert sbwd(lib, **kw) == code
@@ -186,4 +192,4 @@ def test_search_backward_rejects(lib, kw, code, text):
 def test_search_backward_noops(lib):
     assert sbwd(lib, T=0) == OK
     assert sbwd(lib, gq=None, gk=None) == OK          # nothing requested
-    assert lib.mem_search_backward_workspace_size(100, 4, 2048, 32) == 0
+    assert lib.mem_search_backward_workspace_size(100, 4, 2048, 32) >= 100 * 4 * 2 * 32 * 8

@@ -20,6 +20,8 @@ CASES = [
     ("bf16_k64_d64", 256, 2, 128, 64, 70, torch.bfloat16),
     ("f32_d64_S200", 200, 2, 128, 20, 99, torch.float32),
     ("bf16_d8_ties", 50, 3, 16, 10, 77, torch.bfloat16),
+    ("bf16_S8192_d256", 8192, 1, 512, 16, 300, torch.bfloat16),
+    ("f32_S3000_d24_k64", 3000, 2, 48, 64, 45, torch.float32),
 ]
 
 
@@ -87,3 +89,29 @@ def test_search_backward_full_size_sampled(gpu_lib):
     others = torch.ones(T, dtype=torch.bool, device=dev)
     others[torch.from_numpy(keep).to(dev)] = False
     assert float(gq[others].abs().max()) == 0.0
+
+
+def test_search_backward_deterministic_and_skips_invalid_indices(gpu_lib):
+    """Two calls give bitwise-equal gradients (sorted, atomic-free sums), and a
+    lookup whose index lies outside [0, S*S) contributes nothing: the result
+    equals the oracle's with that lookup's gradient set to zero."""
+    S, H, n, k, T = 128, 2, 64, 16, 300
+    g = torch.Generator().manual_seed(41)
+    q = torch.randn((T, H, n), generator=g).to(torch.bfloat16)
+    K = (torch.randn((H, 2, S, n // 2), generator=g) / 8).to(torch.bfloat16)
+    gz = torch.randn((T, H, k), generator=g)
+    idx, _, _, _ = pk.mem_search(q.cuda(), K.cuda(), k)
+    bad = [(0, 0, 3), (5, 1, 0), (299, 1, 15)]
+    for (t, h, j), v in zip(bad, (-1, S * S, 1 << 40)):
+        idx[t, h, j] = v
+    runs = [pk.mem_search_backward(q.cuda(), K.cuda(), idx, gz.cuda()) for _ in range(2)]
+    torch.cuda.synchronize()
+    assert torch.equal(runs[0][0], runs[1][0]) and torch.equal(runs[0][1], runs[1][1])
+    idx_ref = idx.cpu().numpy().copy()
+    gz_ref = gz.double().numpy().copy()
+    for t, h, j in bad:
+        idx_ref[t, h, j] = 0
+        gz_ref[t, h, j] = 0.0
+    ref = oracle.search_backward(h64(q), h64(K), idx_ref, gz_ref)
+    assert normwise(h64(runs[0][0]), ref["grad_q"]) <= TOL_F32
+    assert normwise(h64(runs[0][1]), ref["grad_K"]) <= TOL_F32
