@@ -43,7 +43,7 @@ KERNEL_SOURCES = {
     "softmax_backward": ["bag.hip"],
     "sort_by_row": ["sorted.hip", "pk_device.h"],
     "bag_backward_rows": ["sorted.hip", "pk_device.h"],
-    "search_backward": ["search_bwd.hip", "pk_device.h"],
+    "search_backward": ["search_bwd.hip", "sorted.hip", "pk_device.h"],
 }
 
 
