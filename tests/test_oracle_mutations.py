@@ -178,3 +178,23 @@ def test_catches_search_backward_key_grad_not_accumulated():
     def bwd(q, K, idx, gz, base=None):
         return oracle.search_backward(q, K, idx, gz, None)
     assert _sbwd_fails(bwd)
+
+
+def test_catches_search_backward_repeated_subkey_counted_once():
+    # a sub-key chosen by several ranks of one (token, head) must receive every
+    # rank's gradient; this mutant keeps only the first rank of each sub-key
+    def bwd(q, K, idx, gz, base=None):
+        S = K.shape[2]
+        gz = np.array(gz, dtype=np.float64, copy=True)
+        idx = np.asarray(idx)
+        T, H, k = idx.shape
+        for t in range(T):
+            for h in range(H):
+                seen = set()
+                for j in range(k):
+                    i1 = int(idx[t, h, j]) // S
+                    if i1 in seen:
+                        gz[t, h, j] = 0.0
+                    seen.add(i1)
+        return oracle.search_backward(q, K, idx, gz, base)
+    assert _sbwd_fails(bwd)
