@@ -46,6 +46,10 @@ Function pins (tests under tests/test_oracle_*.py):
   search_backward  central finite differences of the selected scores at a fixed
                    selection; torch autograd (fp64); the bilinear identities
                    sum(grad_q * q) = sum(grad_z * z) = sum(grad_K * K)
+  silu, gated_output, gated_backward
+                   torch.nn.functional.silu and torch autograd (fp64, CPU);
+                   closed forms silu(0) = 0, silu(ln 3) = (3/4) ln 3,
+                   silu'(0) = 1/2; central finite differences; limits
 """
 from __future__ import annotations
 
@@ -64,6 +68,9 @@ __all__ = [
     "bag_backward_rows",
     "invert_index",
     "search_backward",
+    "silu",
+    "gated_output",
+    "gated_backward",
 ]
 
 
@@ -321,3 +328,35 @@ def search_backward(q: np.ndarray, subkeys: np.ndarray, idx: np.ndarray,
                 grad_K[h, 0, i1] += g * q[t, h, :d]
                 grad_K[h, 1, i2] += g * q[t, h, d:]
     return dict(grad_q=grad_q, grad_K=grad_K)
+
+
+def silu(x: np.ndarray) -> np.ndarray:
+    """silu(x) = x * sigmoid(x) (Sec. 3.1.4, Memory+), in fp64.  The sigmoid
+    is taken as 1 / (1 + exp(-x)) for x >= 0 and exp(x) / (1 + exp(x)) for
+    x < 0, so neither branch overflows."""
+    x = _f64(x)
+    e = np.exp(-np.abs(x))
+    sig = np.where(x >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
+    return x * sig
+
+
+def gated_output(y: np.ndarray, gate: np.ndarray) -> np.ndarray:
+    """Memory+ gating (Sec. 3.1.4): the memory output becomes
+    (y * silu(x^T W1))^T W2.  The two projections are plain matrix products
+    done by the caller; the part on the memory path is the element-wise
+    out = y * silu(gate) with gate = x^T W1, both [T, D]."""
+    return _f64(y) * silu(gate)
+
+
+def gated_backward(d_out: np.ndarray, y: np.ndarray, gate: np.ndarray) -> dict:
+    """Backward of out = y * silu(g), element-wise, given d_out = dL/dout:
+      dy = d_out * silu(g)
+      dg = d_out * y * silu'(g),  silu'(g) = sig(g) * (1 + g * (1 - sig(g)))
+    (the derivative of g * sig(g), using sig' = sig * (1 - sig)).  dy then
+    feeds the bag backward in place of the plain memory output's gradient."""
+    d = _f64(d_out)
+    yy = _f64(y)
+    g = _f64(gate)
+    e = np.exp(-np.abs(g))
+    sig = np.where(g >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
+    return dict(dy=d * (g * sig), dg=d * yy * (sig * (1.0 + g * (1.0 - sig))))

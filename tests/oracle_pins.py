@@ -279,3 +279,49 @@ def check_search_backward(search_fn, bwd_fn, rng, T=4, H=2, S=5, d=3, k=4, h=1e-
     base = rng.standard_normal(K.shape)
     g2 = bwd_fn(q, K, idx, gz, base)
     np.testing.assert_allclose(g2["grad_K"], base + g["grad_K"], rtol=1e-14, atol=1e-15)
+
+
+# ---------------------------------------------------------------- Memory+ ----
+def check_gated_output(gated_fn, silu_fn, rng, T=5, D=7):
+    """out = y * silu(g): torch's silu (fp64, CPU) as the library routine, and
+    closed forms at points where the sigmoid is rational."""
+    y = rng.standard_normal((T, D))
+    g = 3.0 * rng.standard_normal((T, D))
+    ref = torch.tensor(y) * torch.nn.functional.silu(torch.tensor(g))
+    np.testing.assert_allclose(gated_fn(y, g), ref.numpy(), rtol=1e-13, atol=1e-15)
+    # sigmoid(0) = 1/2, sigmoid(ln 3) = 3/4, sigmoid(-ln 3) = 1/4
+    pts = np.array([0.0, np.log(3.0), -np.log(3.0)])
+    np.testing.assert_allclose(silu_fn(pts), [0.0, 0.75 * np.log(3.0), -0.25 * np.log(3.0)],
+                               rtol=1e-15, atol=0.0)
+    # limits: silu(x) -> x for large x, -> 0 for very negative x
+    assert math.isclose(silu_fn(np.array([40.0]))[0], 40.0, rel_tol=1e-15)
+    assert abs(silu_fn(np.array([-40.0]))[0]) < 1e-15
+    assert np.isfinite(silu_fn(np.array([-1000.0, 1000.0]))).all()
+    # y = 1 everywhere returns silu(g) itself
+    np.testing.assert_allclose(gated_fn(np.ones_like(g), g), silu_fn(g), rtol=0, atol=0)
+
+
+def check_gated_backward(bwd_fn, rng, T=4, D=6, h=1e-6):
+    """dy, dg of out = y * silu(g): torch autograd (fp64), central differences,
+    closed form at g = 0 (silu(0) = 0, silu'(0) = 1/2)."""
+    y = rng.standard_normal((T, D))
+    g = 2.0 * rng.standard_normal((T, D))
+    d = rng.standard_normal((T, D))
+    out = bwd_fn(d, y, g)
+    yt = torch.tensor(y, requires_grad=True)
+    gt = torch.tensor(g, requires_grad=True)
+    (yt * torch.nn.functional.silu(gt) * torch.tensor(d)).sum().backward()
+    np.testing.assert_allclose(out["dy"], yt.grad.numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(out["dg"], gt.grad.numpy(), rtol=1e-12, atol=1e-14)
+    # central differences of L = sum(d * y * silu(g)) in g, with silu written out here
+    silu = lambda x: x / (1.0 + np.exp(-x))  # noqa: E731
+    for (t, e) in [(0, 0), (1, 3), (3, 5)]:
+        gp = g.copy(); gp[t, e] += h
+        gm = g.copy(); gm[t, e] -= h
+        fd = (float((d * y * silu(gp)).sum()) - float((d * y * silu(gm)).sum())) / (2 * h)
+        assert abs(fd - out["dg"][t, e]) < 1e-7, (t, e, fd, out["dg"][t, e])
+    z = bwd_fn(d, y, np.zeros_like(g))
+    np.testing.assert_allclose(z["dy"], 0.0, atol=0)
+    np.testing.assert_allclose(z["dg"], 0.5 * d * y, rtol=1e-15, atol=0)
+    zero = bwd_fn(np.zeros_like(d), y, g)
+    assert not zero["dy"].any() and not zero["dg"].any()

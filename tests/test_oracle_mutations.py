@@ -198,3 +198,52 @@ def test_catches_search_backward_repeated_subkey_counted_once():
                     seen.add(i1)
         return oracle.search_backward(q, K, idx, gz, base)
     assert _sbwd_fails(bwd)
+
+
+def _gating_fails(out_fn=None, bwd_fn=None):
+    fails = 0
+    try:
+        pins.check_gated_output(out_fn or oracle.gated_output, oracle.silu, np.random.default_rng(81))
+    except (AssertionError, ValueError):
+        fails += 1
+    try:
+        pins.check_gated_backward(bwd_fn or oracle.gated_backward, np.random.default_rng(82))
+    except (AssertionError, ValueError):
+        fails += 1
+    return fails
+
+
+def _sig(x):
+    return 1.0 / (1.0 + np.exp(-np.asarray(x, dtype=np.float64)))
+
+
+def test_real_gating_passes():
+    assert _gating_fails() == 0
+
+
+def test_catches_sigmoid_gate_instead_of_silu():
+    assert _gating_fails(out_fn=lambda y, g: np.asarray(y) * _sig(g)) > 0
+
+
+def test_catches_gate_derivative_missing_factor():
+    def bwd(d, y, g):
+        out = oracle.gated_backward(d, y, g)
+        out["dg"] = np.asarray(d) * np.asarray(y) * _sig(g)
+        return out
+    assert _gating_fails(bwd_fn=bwd) > 0
+
+
+def test_catches_ungated_value_gradient():
+    def bwd(d, y, g):
+        out = oracle.gated_backward(d, y, g)
+        out["dy"] = np.asarray(d, dtype=np.float64)
+        return out
+    assert _gating_fails(bwd_fn=bwd) > 0
+
+
+def test_catches_gate_gradient_with_silu_not_its_derivative():
+    def bwd(d, y, g):
+        out = oracle.gated_backward(d, y, g)
+        out["dg"] = np.asarray(d) * np.asarray(y) * oracle.silu(g)
+        return out
+    assert _gating_fails(bwd_fn=bwd) > 0
