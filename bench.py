@@ -87,11 +87,23 @@ def alg_cost(kernel: str, wl, U: int, esz: int):
     if kernel == "bag_backward_atomic":
         # per lookup: value row read, fp32 gradient row read + write, (idx, w, grad_w); dy per token
         return "hbm", L * D * (esz + 8) + T * D * esz + L * 16
+    if kernel == "bag_forward_gated":
+        # the gather, plus the gate read and the gated and un-gated output rows
+        return "hbm", L * D * esz + 3 * T * D * esz + L * 12
+    if kernel == "gate_backward":
+        # d_out, gate, un-gated bag read; dy (value dtype) and fp32 gate gradient written
+        return "hbm", T * D * (4 * esz + 4)
     if kernel == "score_topk":
         return "mfma", 2.0 * T * H * 2 * S * d
     if kernel == "sort_by_row":
         return "hbm", None
     return "hbm", None
+
+
+def hbm_rate(alg_bytes, ms):
+    ach = alg_bytes / (ms / 1e3) / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(ach / HBM_PEAK_GBPS, 4), "alg_bytes_per_launch": alg_bytes, "ms": round(ms, 4)}
 
 
 def run_cpu_baseline(wl, q, K, V, dy, budget_s: float):
@@ -294,6 +306,31 @@ def main():
     search_bwd_ms = sum(sb) / len(sb)
     del gq, gK, ws_sb
 
+    # Memory+ gating (the gated gather and the gate backward): measured on
+    # their own after the timed steps, on the last step's selection.
+    gate = dy.clone()                       # N(0,1) gate pre-activation, value dtype
+    g_out = torch.empty_like(dy)
+    g_y = torch.empty_like(dy)
+    g_dy = torch.empty_like(dy)
+    g_dg = torch.empty((T, D), dtype=torch.float32, device=dev)
+    idx2, w2 = idx.view(T, -1), w.view(T, -1)
+    def gated():
+        pk.mem_bag_forward_gated(V, idx2, w2, gate, out=g_out, y_out=g_y)
+    def gate_bwd():
+        pk.mem_gate_backward(dy, gate, g_y, dy_out=g_dy, grad_gate=g_dg)
+    gplus = {}
+    for name, fn in (("bag_forward", gated), ("gate_backward", gate_bwd)):
+        fn()
+        torch.cuda.synchronize()
+        pk.mem_timer_start(name)
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        pk.mem_timer_stop()
+        v = [ms for _, ms in pk.mem_timer_read()]
+        gplus[name] = sum(v) / len(v)
+    del gate, g_out, g_y, g_dy, g_dg
+
     # touched rows of the last step's selection (outside the timed region)
     uniq, counts = torch.unique(idx.view(-1), return_counts=True)
     U = int(uniq.numel())
@@ -354,6 +391,12 @@ def main():
         "scatter": bw("bag_backward_rows") or bw("bag_backward_atomic"),
         "search": bw("score_topk"),
         "search_backward_ms": round(search_bwd_ms, 4),
+        "memory_plus": {
+            "bag_forward_gated_ms": round(gplus["bag_forward"], 4),
+            "gate_backward_ms": round(gplus["gate_backward"], 4),
+            "gated_gather": hbm_rate(alg_cost("bag_forward_gated", wl, U, esz)[1], gplus["bag_forward"]),
+            "gate_backward": hbm_rate(alg_cost("gate_backward", wl, U, esz)[1], gplus["gate_backward"]),
+        },
         "stream_copy_GBps": round(copy_gbps, 1),
         "touched_rows": U,
         "max_row_multiplicity": max_mult,

@@ -139,6 +139,38 @@ int mem_bag_forward(const void* values, pkmem_dtype v_dt, int64_t N, int D,
                     void* y_out, pkmem_stream_t stream);
 
 /* ------------------------------------------------------------------------ *
+ * Memory+ gating (Sec. 3.1.4): the layer's output becomes
+ * (y * silu(x^T W1))^T W2 with silu(x) = x * sigmoid(x).  The projections
+ * x^T W1 and .^T W2 are plain matrix products done by the caller; the
+ * element-wise gate is fused into the bag:
+ *
+ *   values, N, D, idx, w, T, bag   as for mem_bag_forward.
+ *   gate   [T, D] dtype v_dt   the gate pre-activation x^T W1.
+ *   out    [T, D] dtype v_dt   written: bag(t) * silu(gate[t]) elementwise,
+ *                              from the fp32 accumulator, rounded once.
+ *   y_out  [T, D] dtype v_dt   written when non-NULL: the un-gated bag (what
+ *                              mem_gate_backward needs), rounded once.
+ * All buffers 16-byte aligned.
+ * ------------------------------------------------------------------------ */
+int mem_bag_forward_gated(const void* values, pkmem_dtype v_dt, int64_t N, int D,
+                          const int64_t* idx, const float* w, int64_t T, int bag,
+                          const void* gate, void* y_out, void* out, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * Backward of out = y * silu(g), element-wise over [T, D]:
+ *   d_out, gate, y   [T, D] dtype v_dt: dL/dout, the gate, the un-gated bag.
+ *   dy_out     [T, D] dtype v_dt, written: d_out * silu(g), rounded once; pass
+ *              it to mem_bag_backward as its dy.
+ *   grad_gate  [T, D] fp32, written: d_out * y * silu'(g),
+ *              silu'(g) = sigmoid(g) * (1 + g * (1 - sigmoid(g))).
+ * D % 8 == 0; all buffers 16-byte aligned.  (Not fused into the sorted value
+ * backward, which reads dy once per lookup: computing it there would read
+ * d_out and the gate once per lookup instead.)
+ * ------------------------------------------------------------------------ */
+int mem_gate_backward(const void* d_out, const void* gate, const void* y, pkmem_dtype v_dt,
+                      int64_t T, int D, void* dy_out, float* grad_gate, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
  * EmbeddingBag backward and softmax backward (Sec. 3.1.4; Eq. (1)).
  *
  *   dy     [T, D]      upstream gradient of y, dtype v_dt.
@@ -179,7 +211,8 @@ int mem_bag_backward_sparse(const void* dy, const void* values, pkmem_dtype v_dt
  * following launch of a listed kernel:
  *   "score_topk", "cartesian"              (mem_search)
  *   "search_backward"                      (mem_search_backward)
- *   "bag_forward"                          (mem_bag_forward)
+ *   "bag_forward"                          (mem_bag_forward, mem_bag_forward_gated)
+ *   "gate_backward"                        (mem_gate_backward)
  *   "bag_backward_atomic", "sort_by_row",
  *   "bag_backward_rows", "softmax_backward" (mem_bag_backward[_sparse])
  * ("sort_by_row" spans the whole radix sort and segment pass.)

@@ -20,6 +20,7 @@ import torch  # noqa: F401  (first: the library binds to the HIP runtime torch l
 
 __all__ = [
     "PkmemError", "load", "lib_path", "mem_search", "mem_search_backward", "mem_bag_forward",
+    "mem_bag_forward_gated", "mem_gate_backward",
     "mem_bag_backward",
     "mem_bag_backward_sparse", "mem_search_workspace_size", "mem_bag_backward_workspace_size",
     "BWD_MODES", "F32", "BF16", "mem_timer_start", "mem_timer_stop", "mem_timer_read",
@@ -61,6 +62,10 @@ def load() -> ctypes.CDLL:
     L.mem_search_backward.restype = I32
     L.mem_bag_forward.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P]
     L.mem_bag_forward.restype = I32
+    L.mem_bag_forward_gated.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P, P, P]
+    L.mem_bag_forward_gated.restype = I32
+    L.mem_gate_backward.argtypes = [P, P, P, I32, I64, I32, P, P, P]
+    L.mem_gate_backward.restype = I32
     L.mem_bag_backward_workspace_size.argtypes = [I64, I32, I32, I64, I32, I32]
     L.mem_bag_backward_workspace_size.restype = SZ
     L.mem_bag_backward.argtypes = [P, P, I32, I64, I32, P, P, I64, I32, I32, P, P, P, I32, P, SZ, P]
@@ -221,6 +226,48 @@ def mem_bag_forward(values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor, *,
     _check(L.mem_bag_forward(_ptr(values), _dt(values), N, D, _ptr(idx), _ptr(w), T, bag,
                              _ptr(y_out), _stream(stream)))
     return y_out
+
+
+def mem_bag_forward_gated(values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor,
+                          gate: torch.Tensor, *, want_y=True, out=None, y_out=None, stream=None):
+    """Memory+ epilogue: out = bag * silu(gate), gate [T, D] in the value dtype.
+    Returns (out, y) with y the un-gated bag (None unless want_y)."""
+    L = load()
+    _dev(values, idx, w, gate)
+    N, D = values.shape
+    T = idx.shape[0]
+    bag = idx.numel() // T if T else (idx[0].numel() if idx.dim() > 1 else 1)
+    if idx.dtype != torch.int64 or w.dtype != torch.float32:
+        raise TypeError("idx must be int64 and w float32")
+    if gate.dtype != values.dtype or tuple(gate.shape) != (T, D) or not gate.is_contiguous():
+        raise ValueError("gate must be a contiguous [T, D] tensor of the value dtype")
+    if out is None:
+        out = torch.empty((T, D), dtype=values.dtype, device=values.device)
+    if y_out is None and want_y:
+        y_out = torch.empty((T, D), dtype=values.dtype, device=values.device)
+    _dev(out, y_out)
+    _check(L.mem_bag_forward_gated(_ptr(values), _dt(values), N, D, _ptr(idx), _ptr(w), T, bag,
+                                   _ptr(gate), _ptr(y_out), _ptr(out), _stream(stream)))
+    return out, y_out
+
+
+def mem_gate_backward(d_out: torch.Tensor, gate: torch.Tensor, y: torch.Tensor, *, dy_out=None,
+                      grad_gate=None, stream=None):
+    """Backward of out = y * silu(gate): returns (dy [value dtype], grad_gate fp32)."""
+    L = load()
+    _dev(d_out, gate, y)
+    T, D = d_out.shape
+    for t_ in (gate, y):
+        if t_.dtype != d_out.dtype or tuple(t_.shape) != (T, D) or not t_.is_contiguous():
+            raise ValueError("gate and y must be contiguous [T, D] tensors of d_out's dtype")
+    if dy_out is None:
+        dy_out = torch.empty((T, D), dtype=d_out.dtype, device=d_out.device)
+    if grad_gate is None:
+        grad_gate = torch.empty((T, D), dtype=torch.float32, device=d_out.device)
+    _dev(dy_out, grad_gate)
+    _check(L.mem_gate_backward(_ptr(d_out), _ptr(gate), _ptr(y), _dt(d_out), T, D, _ptr(dy_out),
+                               _ptr(grad_gate), _stream(stream)))
+    return dy_out, grad_gate
 
 
 def mem_bag_backward(dy: torch.Tensor, values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor,

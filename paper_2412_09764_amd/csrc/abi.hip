@@ -326,8 +326,38 @@ int mem_bag_forward(const void* values, pkmem_dtype v_dt, int64_t N, int D, cons
   if (T > 0 && (!values || !idx || !w || !y_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
   if (!aligned(values, 16) || !aligned(y_out, 16)) return fail(PKMEM_ERR_INVALID, "%s: values and y_out must be 16-byte aligned", fn);
   if (T == 0) return PKMEM_OK;
-  hipError_t e = pk::launch_bag_forward(v_dt == PKMEM_BF16, values, D, idx, w, T, bag, y_out,
+  hipError_t e = pk::launch_bag_forward(v_dt == PKMEM_BF16, values, D, idx, w, T, bag, y_out, nullptr, nullptr,
                                         reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, fn);
+}
+
+int mem_bag_forward_gated(const void* values, pkmem_dtype v_dt, int64_t N, int D, const int64_t* idx,
+                          const float* w, int64_t T, int bag, const void* gate, void* y_out,
+                          void* out, pkmem_stream_t stream) {
+  const char* fn = "mem_bag_forward_gated";
+  int rc = check_bag_shapes(fn, v_dt, N, D, T, bag);
+  if (rc) return rc;
+  if (T > 0 && (!values || !idx || !w || !gate || !out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (!aligned(values, 16) || !aligned(gate, 16) || !aligned(out, 16) || !aligned(y_out, 16))
+    return fail(PKMEM_ERR_INVALID, "%s: values, gate, y_out and out must be 16-byte aligned", fn);
+  if (T == 0) return PKMEM_OK;
+  hipError_t e = pk::launch_bag_forward(v_dt == PKMEM_BF16, values, D, idx, w, T, bag, out, gate,
+                                        y_out, reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, fn);
+}
+
+int mem_gate_backward(const void* d_out, const void* gate, const void* y, pkmem_dtype v_dt, int64_t T,
+                      int D, void* dy_out, float* grad_gate, pkmem_stream_t stream) {
+  const char* fn = "mem_gate_backward";
+  if (!dtype_ok(v_dt)) return fail(PKMEM_ERR_INVALID, "%s: unknown dtype %d", fn, (int)v_dt);
+  if (T < 0) return fail(PKMEM_ERR_INVALID, "%s: T must be >= 0", fn);
+  if (D < 8 || D % 8 != 0) return fail(PKMEM_ERR_UNSUPPORTED, "%s: D must be a positive multiple of 8 (got %d)", fn, D);
+  if (T > 0 && (!d_out || !gate || !y || !dy_out || !grad_gate)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (!aligned(d_out, 16) || !aligned(gate, 16) || !aligned(y, 16) || !aligned(dy_out, 16) || !aligned(grad_gate, 16))
+    return fail(PKMEM_ERR_INVALID, "%s: every buffer must be 16-byte aligned", fn);
+  if (T == 0) return PKMEM_OK;
+  hipError_t e = pk::launch_gate_backward(v_dt == PKMEM_BF16, d_out, gate, y, T, D, dy_out, grad_gate,
+                                          reinterpret_cast<hipStream_t>(stream));
   return hip_status(e, fn);
 }
 

@@ -83,11 +83,15 @@ struct LookupChunk {
 // SPLIT > 1 (full rows of 64-lane groups only) spreads a token over SPLIT
 // waves, each owning CPL consecutive 1 KiB slabs of every row: more, smaller
 // waves in flight.
+// Memory+ epilogue (Sec. 3.1.4): with a gate [T, D] the kernel writes
+// y = bag * silu(gate) instead of the bag, and the un-gated bag to y_plain
+// when that is non-null; both from the fp32 accumulator, one rounding each.
 template <typename V, int CPL, int CL, int U, bool FULL, int SPLIT>
 __global__ __launch_bounds__(256) void k_bag_fwd(const V* __restrict__ values, int D,
                                                  const int64_t* __restrict__ idx,
                                                  const float* __restrict__ w, int64_t T, int bag,
-                                                 V* __restrict__ y) {
+                                                 V* __restrict__ y, const V* __restrict__ gate,
+                                                 V* __restrict__ y_plain) {
   using R = Row16<V>;
   constexpr int G = WAVE / CL;
   static_assert(SPLIT == 1 || (FULL && CL == WAVE), "split waves need full 64-lane rows");
@@ -192,10 +196,55 @@ __global__ __launch_bounds__(256) void k_bag_fwd(const V* __restrict__ values, i
         for (int e = 0; e < R::N; ++e) acc[i][e] += __shfl_xor(acc[i][e], m, WAVE);
   }
   if (grp == 0) {
+    if (gate) {  // uniform
 #pragma unroll
-    for (int i = 0; i < CPL; ++i)
-      if (ok[i]) st16_nt(y + t * D + (size_t)(i * CL + cl) * R::N, R::pack(acc[i]));
+      for (int i = 0; i < CPL; ++i) {
+        if (!ok[i]) continue;
+        const size_t off = t * D + (size_t)(i * CL + cl) * R::N;
+        float gv[R::N], o[R::N];
+        R::unpack(ld16(gate + off), gv);
+        if (y_plain) st16_nt(y_plain + off, R::pack(acc[i]));
+#pragma unroll
+        for (int e = 0; e < R::N; ++e) o[e] = acc[i][e] * silu_f32(gv[e]);
+        st16_nt(y + off, R::pack(o));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < CPL; ++i)
+        if (ok[i]) st16_nt(y + t * D + (size_t)(i * CL + cl) * R::N, R::pack(acc[i]));
+    }
   }
+  }
+}
+
+// Backward of the Memory+ epilogue, element-wise in 16-byte chunks:
+//   dy = d_out * silu(g)                      (value dtype: the bag backward's dy)
+//   grad_gate = d_out * y * silu'(g),  silu'(g) = sig(g) * (1 + g * (1 - sig(g)))
+// with y the un-gated bag.  Grid-stride over the T*D/N chunks.
+template <typename V>
+__global__ __launch_bounds__(256) void k_gate_bwd(const V* __restrict__ d_out,
+                                                  const V* __restrict__ gate,
+                                                  const V* __restrict__ yb, int64_t nchunks,
+                                                  V* __restrict__ dy, float* __restrict__ grad_gate) {
+  using R = Row16<V>;
+  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < nchunks;
+       c += (int64_t)gridDim.x * 256) {
+    float d[R::N], g[R::N], yy[R::N], o[R::N], dg[R::N];
+    R::unpack(ld16_nt(d_out + c * R::N), d);
+    R::unpack(ld16_nt(gate + c * R::N), g);
+    R::unpack(ld16_nt(yb + c * R::N), yy);
+#pragma unroll
+    for (int e = 0; e < R::N; ++e) {
+      const float sig = 1.f / (1.f + expf(-g[e]));
+      o[e] = d[e] * (g[e] * sig);
+      dg[e] = d[e] * yy[e] * (sig * (1.f + g[e] * (1.f - sig)));
+    }
+    st16_nt(dy + c * R::N, R::pack(o));
+#pragma unroll
+    for (int e = 0; e < R::N; e += 4)
+      st16_nt(grad_gate + c * R::N + e,
+              uint4{__float_as_uint(dg[e]), __float_as_uint(dg[e + 1]), __float_as_uint(dg[e + 2]),
+                    __float_as_uint(dg[e + 3])});
   }
 }
 
@@ -340,7 +389,8 @@ static unsigned fwd_blocks(int64_t waves) {
 }
 
 hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_t* idx,
-                              const float* w, int64_t T, int bag, void* y, hipStream_t st) {
+                              const float* w, int64_t T, int bag, void* y, const void* gate,
+                              void* y_plain, hipStream_t st) {
   if (T <= 0) return hipSuccess;
   const int C = D * (bf16 ? 2 : 4) / 16;
   LaunchTimer lt("bag_forward", st);
@@ -350,20 +400,20 @@ hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_
     const dim3 grid(fwd_blocks(T * SP)), block(256);
     if (bf16)
       hipLaunchKernelGGL((k_bag_fwd<uint16_t, 4 / SP, 64, PK_FWD_UNROLL, true, SP>), grid, block, 0,
-                         st, (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);
+                         st, (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y, (const uint16_t*)gate, (uint16_t*)y_plain);
     else
       hipLaunchKernelGGL((k_bag_fwd<float, 4 / SP, 64, PK_FWD_UNROLL, true, SP>), grid, block, 0, st,
-                         (const float*)values, D, idx, w, T, bag, (float*)y);
+                         (const float*)values, D, idx, w, T, bag, (float*)y, (const float*)gate, (float*)y_plain);
     return hipGetLastError();
   }
   if (C == 512 && (8 % SP) == 0) {
     const dim3 grid(fwd_blocks(T * SP)), block(256);
     if (bf16)
       hipLaunchKernelGGL((k_bag_fwd<uint16_t, 8 / SP, 64, PK_FWD_UNROLL, true, SP>), grid, block, 0,
-                         st, (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);
+                         st, (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y, (const uint16_t*)gate, (uint16_t*)y_plain);
     else
       hipLaunchKernelGGL((k_bag_fwd<float, 8 / SP, 64, PK_FWD_UNROLL, true, SP>), grid, block, 0, st,
-                         (const float*)values, D, idx, w, T, bag, (float*)y);
+                         (const float*)values, D, idx, w, T, bag, (float*)y, (const float*)gate, (float*)y_plain);
     return hipGetLastError();
   }
   const dim3 grid(fwd_blocks(T)), block(256);
@@ -371,20 +421,38 @@ hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_
   if (C == (CPL) * (CL)) {                                                                           \
     if (bf16)                                                                                        \
       hipLaunchKernelGGL((k_bag_fwd<uint16_t, CPL, CL, PK_FWD_UNROLL, true, 1>), grid, block, 0, st,  \
-                         (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);                 \
+                         (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y, (const uint16_t*)gate, (uint16_t*)y_plain);                 \
     else                                                                                             \
       hipLaunchKernelGGL((k_bag_fwd<float, CPL, CL, PK_FWD_UNROLL, true, 1>), grid, block, 0, st,     \
-                         (const float*)values, D, idx, w, T, bag, (float*)y);                       \
+                         (const float*)values, D, idx, w, T, bag, (float*)y, (const float*)gate, (float*)y_plain);                       \
   } else {                                                                                           \
     if (bf16)                                                                                        \
       hipLaunchKernelGGL((k_bag_fwd<uint16_t, CPL, CL, PK_FWD_UNROLL, false, 1>), grid, block, 0, st, \
-                         (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y);                 \
+                         (const uint16_t*)values, D, idx, w, T, bag, (uint16_t*)y, (const uint16_t*)gate, (uint16_t*)y_plain);                 \
     else                                                                                             \
       hipLaunchKernelGGL((k_bag_fwd<float, CPL, CL, PK_FWD_UNROLL, false, 1>), grid, block, 0, st,    \
-                         (const float*)values, D, idx, w, T, bag, (float*)y);                       \
+                         (const float*)values, D, idx, w, T, bag, (float*)y, (const float*)gate, (float*)y_plain);                       \
   }
   PK_ROW_DISPATCH(C, PK_FWD);
 #undef PK_FWD
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_backward(bool bf16, const void* d_out, const void* gate, const void* y,
+                                int64_t T, int D, void* dy, float* grad_gate, hipStream_t st) {
+  if (T <= 0) return hipSuccess;
+  const int64_t nchunks = T * D / (bf16 ? 8 : 4);
+  int64_t blocks = (nchunks + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  LaunchTimer lt("gate_backward", st);
+  if (bf16)
+    hipLaunchKernelGGL(k_gate_bwd<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const uint16_t*)d_out, (const uint16_t*)gate, (const uint16_t*)y, nchunks,
+                       (uint16_t*)dy, grad_gate);
+  else
+    hipLaunchKernelGGL(k_gate_bwd<float>, dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const float*)d_out, (const float*)gate, (const float*)y, nchunks, (float*)dy,
+                       grad_gate);
   return hipGetLastError();
 }
 

@@ -81,6 +81,10 @@ __device__ __forceinline__ void lds_dma16(const void* gptr, void* lds_base) {
 }
 
 // ---------------------------------------------------------------- bf16 ----
+// silu(x) = x * sigmoid(x) = x / (1 + exp(-x)) (Memory+ gate, Sec. 3.1.4);
+// for very negative x the denominator overflows to inf and the result is -0.
+__device__ __forceinline__ float silu_f32(float x) { return x / (1.f + expf(-x)); }
+
 __device__ __forceinline__ float bf16_lo(uint32_t two) { return __uint_as_float(two << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t two) { return __uint_as_float(two & 0xFFFF0000u); }
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }

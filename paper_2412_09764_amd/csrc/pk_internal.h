@@ -54,7 +54,10 @@ hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys,
 
 // ---- bag (bag.hip) ---------------------------------------------------------
 hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_t* idx,
-                              const float* w, int64_t T, int bag, void* y, hipStream_t st);
+                              const float* w, int64_t T, int bag, void* y, const void* gate,
+                              void* y_plain, hipStream_t st);
+hipError_t launch_gate_backward(bool bf16, const void* d_out, const void* gate, const void* y,
+                                int64_t T, int D, void* dy, float* grad_gate, hipStream_t st);
 hipError_t launch_bag_backward_atomic(bool bf16, const void* dy, const void* values, int D,
                                       const int64_t* idx, const float* w, int64_t T, int bag,
                                       float* grad_values, float* grad_w, hipStream_t st);

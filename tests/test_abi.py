@@ -193,3 +193,43 @@ def test_search_backward_noops(lib):
     assert sbwd(lib, T=0) == OK
     assert sbwd(lib, gq=None, gk=None) == OK          # nothing requested
     assert lib.mem_search_backward_workspace_size(100, 4, 2048, 32) >= 100 * 4 * 2 * 32 * 8
+
+
+def fwdg(lib, V=FAKE, vdt=BF16, N=4096, D=64, idx=FAKE, w=FAKE, T=4, bag=8, gate=FAKE, y=FAKE, out=FAKE):
+    return lib.mem_bag_forward_gated(V, vdt, N, D, idx, w, T, bag, gate, y, out, None)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(D=12), UNSUPPORTED, "multiple of 8"),
+    (dict(vdt=5), INVALID, "dtype"),
+    (dict(gate=0), INVALID, "null"),
+    (dict(out=0), INVALID, "null"),
+    (dict(gate=FAKE + 8), INVALID, "aligned"),
+    (dict(y=FAKE + 4), INVALID, "aligned"),
+    (dict(bag=0), INVALID, "bag"),
+])
+def test_bag_forward_gated_rejects(lib, kw, code, text):
+    assert fwdg(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def gbwd(lib, d=FAKE, g=FAKE, y=FAKE, vdt=BF16, T=4, D=64, dy=FAKE, gg=FAKE):
+    return lib.mem_gate_backward(d, g, y, vdt, T, D, dy, gg, None)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(D=12), UNSUPPORTED, "multiple of 8"),
+    (dict(vdt=9), INVALID, "dtype"),
+    (dict(T=-1), INVALID, "T must"),
+    (dict(y=0), INVALID, "null"),
+    (dict(gg=0), INVALID, "null"),
+    (dict(gg=FAKE + 4), INVALID, "aligned"),
+])
+def test_gate_backward_rejects(lib, kw, code, text):
+    assert gbwd(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def test_gating_empty_batch_is_a_noop(lib):
+    assert fwdg(lib, T=0) == OK
+    assert gbwd(lib, T=0) == OK
