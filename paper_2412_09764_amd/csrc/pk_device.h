@@ -121,9 +121,37 @@ __device__ __forceinline__ float key_score(uint64_t key) { return ordered_to_f32
 __device__ __forceinline__ uint32_t key_index(uint64_t key) { return ~uint32_t(key); }
 
 // ---------------------------------------------------------- shuffles ----
+// Value of lane (lane ^ MASK) for a constant MASK.  Distances 1 and 2 are DPP
+// quad permutations (a VALU operand modifier), 4, 8 and 16 are ds_swizzle in
+// bit-mask mode (xor within 32 lanes: no address operand, no LDS access);
+// only 32 takes a ds_bpermute.
+template <int MASK>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
+  static_assert(MASK > 0 && MASK < WAVE && (MASK & (MASK - 1)) == 0, "power-of-two lane distance");
+  if constexpr (MASK == 1) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+  } else if constexpr (MASK == 2) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+  } else if constexpr (MASK <= 16) {
+    return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (MASK << 10));  // and 0x1f, xor MASK
+  } else {
+    return __shfl_xor(v, MASK, WAVE);
+  }
+}
+// The same for a run-time distance that unrolling turns into a constant.
+__device__ __forceinline__ uint32_t xor_lane_rt(uint32_t v, int mask) {
+  switch (mask) {
+    case 1: return xor_lane<1>(v);
+    case 2: return xor_lane<2>(v);
+    case 4: return xor_lane<4>(v);
+    case 8: return xor_lane<8>(v);
+    case 16: return xor_lane<16>(v);
+    default: return __shfl_xor(v, mask, WAVE);
+  }
+}
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
-  uint32_t lo = __shfl_xor(uint32_t(v), mask, WAVE);
-  uint32_t hi = __shfl_xor(uint32_t(v >> 32), mask, WAVE);
+  const uint32_t lo = xor_lane_rt(uint32_t(v), mask);
+  const uint32_t hi = xor_lane_rt(uint32_t(v >> 32), mask);
   return (uint64_t(hi) << 32) | lo;
 }
 __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {

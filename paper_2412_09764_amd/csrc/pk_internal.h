@@ -26,7 +26,10 @@ class LaunchTimer {
 // per-row sort of the search kernel.
 constexpr int CAND_CAP = 128;
 // Waves and tokens per workgroup of the scoring kernel (32 tokens per wave).
-constexpr int SEARCH_WAVES = 8;
+#ifndef PK_SEARCH_WAVES
+#define PK_SEARCH_WAVES 8
+#endif
+constexpr int SEARCH_WAVES = PK_SEARCH_WAVES;
 constexpr int SEARCH_TOK = 32 * SEARCH_WAVES;
 
 // Number of (i1, i2) rank pairs with (i1 + 1) * (i2 + 1) <= k: only these can
