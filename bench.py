@@ -44,6 +44,8 @@ KERNEL_SOURCES = {
     "sort_by_row": ["sorted.hip", "pk_device.h"],
     "bag_backward_rows": ["sorted.hip", "pk_device.h"],
     "search_backward": ["search_bwd.hip", "sorted.hip", "pk_device.h"],
+    "bag_forward_gated": ["bag.hip", "pk_device.h"],
+    "gate_backward": ["bag.hip", "pk_device.h"],
 }
 
 
@@ -394,8 +396,10 @@ def main():
         "memory_plus": {
             "bag_forward_gated_ms": round(gplus["bag_forward"], 4),
             "gate_backward_ms": round(gplus["gate_backward"], 4),
-            "gated_gather": hbm_rate(alg_cost("bag_forward_gated", wl, U, esz)[1], gplus["bag_forward"]),
-            "gate_backward": hbm_rate(alg_cost("gate_backward", wl, U, esz)[1], gplus["gate_backward"]),
+            "gated_gather": dict(hbm_rate(alg_cost("bag_forward_gated", wl, U, esz)[1], gplus["bag_forward"]),
+                                 traffic=measured_traffic("bag_forward_gated", wl.name)),
+            "gate_backward": dict(hbm_rate(alg_cost("gate_backward", wl, U, esz)[1], gplus["gate_backward"]),
+                                  traffic=measured_traffic("gate_backward", wl.name)),
         },
         "stream_copy_GBps": round(copy_gbps, 1),
         "touched_rows": U,
