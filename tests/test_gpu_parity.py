@@ -54,6 +54,10 @@ SEARCH_CASES = [
     ("bf16_k64", 256, 2, 128, 64, 70, torch.bfloat16),
     ("f32_d64_S200", 200, 2, 128, 20, 99, torch.float32),
     ("bf16_S2048_d256", 2048, 4, 512, 32, 129, torch.bfloat16),
+    ("bf16_S8192_k64_max", 8192, 1, 512, 64, 40, torch.bfloat16),
+    ("bf16_S3000_d256_ragged_chunk", 3000, 2, 512, 32, 33, torch.bfloat16),
+    ("bf16_T1", 1024, 4, 512, 32, 1, torch.bfloat16),
+    ("f32_d4_k3", 90, 2, 8, 3, 47, torch.float32),
 ]
 
 
@@ -140,6 +144,8 @@ BAG_CASES = [
     ("bf16_D8", 50, 8, 33, 3, 3, torch.bfloat16),
     ("bf16_D4096", 700, 4096, 21, 2, 16, torch.bfloat16),
     ("f32_D2048", 900, 2048, 40, 2, 8, torch.float32),
+    ("bf16_T1_D2048", 1000, 2048, 1, 4, 32, torch.bfloat16),
+    ("f32_D8_k1", 64, 8, 17, 1, 1, torch.float32),
 ]
 
 
