@@ -262,6 +262,14 @@ struct Quad<float> {
 // longer read burst and one contiguous write burst), with the next batch's
 // bounds prefetched; the old gradient row is read into the accumulator
 // together with the value row.
+// Lookups of a segment taken together: more for narrow rows (fewer registers
+// per dy row), capped by the lane group's width.
+template <int NQ, int CL>
+struct RowsBatch {
+  static constexpr int raw = NQ >= 16 ? 1 : (NQ >= 8 ? 2 : (NQ >= 4 ? 4 : 8));
+  static constexpr int value = raw < CL ? raw : CL;
+};
+
 template <typename V, int NQ, int CL, bool SPARSE, int SB>
 __global__ __launch_bounds__(256) void k_bag_bwd_rows(
     const V* __restrict__ dy, const V* __restrict__ values, int D, const float* __restrict__ w,
@@ -271,6 +279,7 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
     float* __restrict__ grad_rows_out, float* __restrict__ grad_w) {
   using Q = Quad<V>;
   constexpr int G = WAVE / CL;
+  constexpr int PB = RowsBatch<NQ, CL>::value;
   const int lane = threadIdx.x & 63;
   const int grp = lane / CL, cl = lane % CL;
   const int nquad = D / 4;
@@ -318,28 +327,47 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
     }
 #pragma unroll
     for (int b = 0; b < SB; ++b) {
-      for (uint32_t s = s0[b]; s < s1[b]; ++s) {
-        const uint32_t l = lookups[s];
-        const int64_t t = l / (uint32_t)bag;
-        const float ww = w[l];
-        typename Q::raw graw[NQ];
+      // The segment's lookups PB at a time: the group's lanes read PB lookup
+      // ids and weights with one load each, then all PB dy rows are in flight
+      // before the first is accumulated (lookup order is kept).
+      for (uint32_t s = s0[b]; s < s1[b]; s += PB) {
+        const uint32_t nb = (s1[b] - s) < (uint32_t)PB ? (s1[b] - s) : (uint32_t)PB;
+        const uint32_t lid = (uint32_t)cl < nb ? lookups[s + cl] : 0u;
+        const float wl = (uint32_t)cl < nb ? w[lid] : 0.f;
+        typename Q::raw graw[PB][NQ];
+        uint32_t lp[PB];
 #pragma unroll
-        for (int m = 0; m < NQ; ++m)
-          graw[m] = ok[m] ? Q::load(dy + t * D + (size_t)(m * CL + cl) * 4) : Q::zero();
-        float part = 0.f;
+        for (int pp = 0; pp < PB; ++pp) {
+          lp[pp] = __shfl(lid, pp, CL);
+          const int64_t t = lp[pp] / (uint32_t)bag;
 #pragma unroll
-        for (int m = 0; m < NQ; ++m) {
-          float g[4], v[4];
-          Q::unpack(graw[m], g);
-          Q::unpack(vraw[b][m], v);
+          for (int m = 0; m < NQ; ++m)
+            graw[pp][m] = (ok[m] && (uint32_t)pp < nb) ? Q::load(dy + t * D + (size_t)(m * CL + cl) * 4)
+                                                       : Q::zero();
+        }
+        float part[PB];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            acc[b][m][e] = fmaf(ww, g[e], acc[b][m][e]);
-            part = fmaf(g[e], v[e], part);
+        for (int pp = 0; pp < PB; ++pp) {
+          const float ww = __shfl(wl, pp, CL);
+          part[pp] = 0.f;
+#pragma unroll
+          for (int m = 0; m < NQ; ++m) {
+            float g[4], v[4];
+            Q::unpack(graw[pp][m], g);
+            Q::unpack(vraw[b][m], v);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              acc[b][m][e] = fmaf(ww, g[e], acc[b][m][e]);
+              part[pp] = fmaf(g[e], v[e], part[pp]);
+            }
           }
         }
-        part = group_sum<CL>(part);
-        if (cl == 0) grad_w[l] = part;
+#pragma unroll
+        for (int pp = 0; pp < PB; ++pp) part[pp] = group_sum<CL>(part[pp]);
+        float mine = part[0];
+#pragma unroll
+        for (int pp = 1; pp < PB; ++pp) mine = (cl == pp) ? part[pp] : mine;
+        if ((uint32_t)cl < nb) grad_w[lid] = mine;
       }
     }
     int64_t rown[SB];
