@@ -14,8 +14,14 @@
 //     sub-keys (group = row mod 64).  The k-th largest of those 64 maxima is a
 //     threshold with at least k distinct scores at or above it.
 //   * Pass 2 recomputes the same tiles (bitwise identical) and appends every
-//     score >= threshold, as a 64-bit (score, index) key, to the row's candidate
-//     list (typically about 43 of 2048 at k = 32).
+//     score >= threshold, as a raw 64-bit (score, index) record, to the row's
+//     candidate list (typically about 43 of 2048 at k = 32).  Its cost is
+//     instruction issue, not MFMA: a wave issues one instruction per four
+//     cycles, so the collection is one compare and a predicated store per
+//     accumulator slot, with the lane's count in a register (the two lanes
+//     holding a token's rows own half of its CAND_CAP slots each; a count
+//     past capacity keeps writing the last slot and sends the row to the
+//     rescan) - no masks, atomics or capacity branches.
 //   * Pass 3 sorts each row's candidates with a wave bitonic sort and writes the
 //     first k.  A row with more than CAND_CAP candidates (heavy ties) is listed
 //     for k_topk_fallback, which rescans it exactly.
@@ -89,7 +95,7 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   // wave's 1 KiB of a chunk contiguous for the direct global -> LDS loads.
   __shared__ __align__(16) unsigned char kbuf0[CBYTES];
   __shared__ __align__(16) unsigned char kbuf1[CBYTES];
-  __shared__ int cnt[SEARCH_TOK];
+  __shared__ int cnt[2 * SEARCH_TOK];  // candidates per (token, lane half)
 
   const int d = n >> 1;
   const int HP = 2 * H;
@@ -216,66 +222,90 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   }
 
   // ---- pass 2: collect candidates >= threshold ------------------------------
-  // A lane reserves slots for all its survivors of a tile with one LDS atomic;
-  // candidates are stored raw: (score bits << 32) | row.
-  if (tid < SEARCH_TOK) cnt[tid] = 0;
-  __syncthreads();
+  constexpr int HALF_CAP = CAND_CAP / 2;
   const size_t rid = ((size_t)(tok_ok ? tok : 0) * H + h) * 2 + p;
-  uint64_t* my_cand = cand + rid * CAND_CAP;
-  int* my_cnt = &cnt[wave * 32 + col];
+  uint64_t* my_cand = cand + rid * CAND_CAP + kh * HALF_CAP;
+  uint32_t my_cnt = 0;
+  const float thl = tok_ok ? th : INFINITY;  // scores are finite
   sweep([&](const f32x16_t& acc, int c, int half) {
-    const int r0 = c * CHUNK_ROWS + half * 32;
-    uint32_t m = 0;
-    if (c < nfull) {
+    const uint32_t r0 = (uint32_t)(c * CHUNK_ROWS + half * 32 + 4 * kh);
+    if (c < nfull) {  // uniform
 #pragma unroll
-      for (int j = 15; j >= 0; --j) m = (m << 1) | (acc[j] >= th ? 1u : 0u);
+      for (int j = 0; j < 16; ++j) {
+        if (acc[j] >= thl) {
+          my_cand[my_cnt < (uint32_t)HALF_CAP ? my_cnt : (uint32_t)HALF_CAP - 1] =
+              (uint64_t(__float_as_uint(acc[j])) << 32) | (r0 + 8 * (j >> 2) + (j & 3));
+          ++my_cnt;
+        }
+      }
     } else {
 #pragma unroll
-      for (int j = 15; j >= 0; --j) m = (m << 1) | ((acc[j] >= th && r0 + acc_row(j, kh) < S) ? 1u : 0u);
-    }
-    if (!tok_ok) m = 0;
-    if (__ballot(m != 0) == 0) return;
-    int pos = 0;
-    if (m) pos = atomicAdd(my_cnt, __popc(m));
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      if (m & (1u << j)) {
-        if (pos < CAND_CAP)
-          my_cand[pos] = (uint64_t(__float_as_uint(acc[j])) << 32) | uint32_t(r0 + acc_row(j, kh));
-        ++pos;
+      for (int j = 0; j < 16; ++j) {
+        const uint32_t row = r0 + 8 * (j >> 2) + (j & 3);
+        if (acc[j] >= thl && row < (uint32_t)S) {
+          my_cand[my_cnt < (uint32_t)HALF_CAP ? my_cnt : (uint32_t)HALF_CAP - 1] = (uint64_t(__float_as_uint(acc[j])) << 32) | row;
+          ++my_cnt;
+        }
       }
     }
   });
+  cnt[wave * 64 + lane] = (int)my_cnt;
+  __syncthreads();
 
   // ---- pass 3: sort each row's candidates, keep the first k ---------------
+  // Row i's records sit in two runs: c0 at slot 0, c1 at slot HALF_CAP; lane
+  // l takes record l (and l + 64) of their concatenation.  The next row's
+  // records are loaded before the current row is sorted.
   auto to_key = [](uint64_t raw) { return make_key(__uint_as_float(uint32_t(raw >> 32)), uint32_t(raw)); };
-  for (int i = 0; i < 32; ++i) {
-    const int64_t t = tile * SEARCH_TOK + wave * 32 + i;
-    if (t >= ntok) break;
-    const int c = cnt[wave * 32 + i];
-    const size_t r = ((size_t)t * H + h) * 2 + p;
-    if (c > CAND_CAP) {
+  int nrow = 32;
+  if (tile * SEARCH_TOK + wave * 32 + 32 > ntok) {
+    const int64_t left = ntok - (tile * SEARCH_TOK + wave * 32);
+    nrow = left < 0 ? 0 : (int)left;
+  }
+  auto fetch = [&](int i, uint64_t (&v)[2], int& c0, int& c1) {
+    c0 = cnt[wave * 64 + i];
+    c1 = cnt[wave * 64 + 32 + i];
+    v[0] = v[1] = 0ull;
+    if (c0 > HALF_CAP || c1 > HALF_CAP) return;  // overflow: handled by the rescan
+    const size_t r = ((size_t)(tile * SEARCH_TOK + wave * 32 + i) * H + h) * 2 + p;
+    const uint64_t* rc = cand + r * CAND_CAP;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int x = lane + e * WAVE;
+      if (x < c0) v[e] = rc[x];
+      else if (x - c0 < c1) v[e] = rc[HALF_CAP + x - c0];
+    }
+  };
+  uint64_t cur[2], nxt[2] = {0ull, 0ull};
+  int c0 = 0, c1 = 0, n0 = 0, n1 = 0;
+  if (nrow > 0) fetch(0, cur, c0, c1);
+  for (int i = 0; i < nrow; ++i) {
+    if (i + 1 < nrow) fetch(i + 1, nxt, n0, n1);
+    const size_t r = ((size_t)(tile * SEARCH_TOK + wave * 32 + i) * H + h) * 2 + p;
+    const int c = c0 + c1;
+    if (c0 > HALF_CAP || c1 > HALF_CAP) {
       if (lane == 0) {
         const uint32_t slot = atomicAdd(&ovf[0], 1u);
         ovf[1 + slot] = (uint32_t)r;
       }
-      continue;
-    }
-    const uint64_t* rc = cand + r * CAND_CAP;
-    uint64_t key;
-    if (c <= WAVE) {
-      uint64_t v[1] = {lane < c ? to_key(rc[lane]) : 0ull};
-      wave_sort_desc<1>(v, lane);
-      key = v[0];
     } else {
-      uint64_t v[2] = {to_key(rc[lane]), lane + WAVE < c ? to_key(rc[lane + WAVE]) : 0ull};
-      wave_sort_desc<2>(v, lane);
-      key = v[0];
+      uint64_t key;
+      if (c <= WAVE) {
+        uint64_t v[1] = {lane < c ? to_key(cur[0]) : 0ull};
+        wave_sort_desc<1>(v, lane);
+        key = v[0];
+      } else {
+        uint64_t v[2] = {to_key(cur[0]), lane + WAVE < c ? to_key(cur[1]) : 0ull};
+        wave_sort_desc<2>(v, lane);
+        key = v[0];
+      }
+      if (lane < k) {
+        half_idx[r * k + lane] = (int32_t)key_index(key);
+        half_score[r * k + lane] = key_score(key);
+      }
     }
-    if (lane < k) {
-      half_idx[r * k + lane] = (int32_t)key_index(key);
-      half_score[r * k + lane] = key_score(key);
-    }
+    cur[0] = nxt[0]; cur[1] = nxt[1];
+    c0 = n0; c1 = n1;
   }
 }
 
