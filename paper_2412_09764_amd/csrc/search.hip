@@ -3,12 +3,12 @@
 //
 // Step 1, k_score_topk: for every (token, head, half) row, the top k of the S
 // half-key scores s[i] = q_half . K_half[i], ordered (score desc, index asc).
-//   * A workgroup owns 128 tokens of one (head, half); the (head, half) index is
-//     blockIdx % (2H), so with 2H = 8 each XCD streams only its own 1 MiB sub-key
-//     table and keeps it in its L2.
+//   * A workgroup owns SEARCH_TOK = 256 tokens (8 waves of 32) of one (head,
+//     half); the (head, half) index is blockIdx % (2H), so with 2H = 8 each XCD
+//     streams only its own 1 MiB sub-key table and keeps it in its L2.
 //   * Scores come from v_mfma_f32_32x32x16_bf16 (fp32 inputs: 32x32x2 f32) with
 //     sub-keys as the A operand (M = 32 sub-keys) and the wave's 32 queries as
-//     the register-resident B operand (N = 32 tokens); sub-key chunks of 32 rows
+//     the register-resident B operand (N = 32 tokens); sub-key chunks of 64 rows
 //     are staged through LDS, double buffered.  Scores never leave registers.
 //   * Pass 1 keeps, per token, the maximum of each of 64 interleaved groups of
 //     sub-keys (group = row mod 64).  The k-th largest of those 64 maxima is a
@@ -23,8 +23,8 @@
 //     past capacity keeps writing the last slot and sends the row to the
 //     rescan) - no masks, atomics or capacity branches.
 //   * Pass 3 sorts each row's candidates with a wave bitonic sort and writes the
-//     first k.  A row with more than CAND_CAP candidates (heavy ties) is listed
-//     for k_topk_fallback, which rescans it exactly.
+//     first k.  A row whose lane half overflowed its CAND_CAP / 2 slots (heavy
+//     ties) is listed for k_topk_fallback, which rescans it exactly.
 // Step 2, k_cartesian: per (token, head) the top k of the sums s1[a] + s2[b]
 //   over rank pairs with (a+1)(b+1) <= k (every other pair is beaten by at
 //   least k pairs), ordered (sum desc, composed index i1*S + i2 asc), then the

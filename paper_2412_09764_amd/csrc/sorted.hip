@@ -7,8 +7,9 @@
 //      digit-major histogram, and a stable scatter whose in-tile ranks come
 //      from wave ballots.  Keys are rows (< 2^26), values lookup ids.
 //   2. Segment heads (first lookup of each distinct row) -> seg_start[U + 1].
-//   3. One lane group per touched row: read the value row once, then for each
-//      contributing lookup (in lookup order) read dy[t], add w * dy into a
+//   3. One lane group per touched row (two adjacent rows per iteration): read
+//      the value row once, then take the contributing lookups in lookup order,
+//      a few at a time with their dy rows loaded together, add w * dy into a
 //      register accumulator and write grad_w = dy . V[row]; finally one
 //      read-modify-write of the fp32 gradient row (dense) or one write of the
 //      row's gradient (sparse).  Rows are visited in ascending order, so the
