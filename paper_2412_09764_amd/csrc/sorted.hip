@@ -331,10 +331,14 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
       // The segment's lookups PB at a time: the group's lanes read PB lookup
       // ids and weights with one load each, then all PB dy rows are in flight
       // before the first is accumulated (lookup order is kept).
+      // The next batch's lookup ids are loaded while this batch's dy rows are
+      // in flight, so a long segment costs one dependent round trip per batch.
+      uint32_t lid_next = (uint32_t)cl < s1[b] - s0[b] ? lookups[s0[b] + cl] : 0u;
       for (uint32_t s = s0[b]; s < s1[b]; s += PB) {
         const uint32_t nb = (s1[b] - s) < (uint32_t)PB ? (s1[b] - s) : (uint32_t)PB;
-        const uint32_t lid = (uint32_t)cl < nb ? lookups[s + cl] : 0u;
+        const uint32_t lid = lid_next;
         const float wl = (uint32_t)cl < nb ? w[lid] : 0.f;
+        lid_next = (uint32_t)cl + PB < s1[b] - s ? lookups[s + PB + cl] : 0u;
         typename Q::raw graw[PB][NQ];
         uint32_t lp[PB];
 #pragma unroll
