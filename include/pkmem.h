@@ -227,6 +227,20 @@ int mem_timer_start(const char* kernels);
 int mem_timer_stop(void);
 int mem_timer_read(float* ms_out, int* kernel_out, int cap);
 
+/* ------------------------------------------------------------------------ *
+ * Environment (read at every call):
+ *   PKMEM_DEBUG=1       before a kernel indexes with idx (mem_bag_forward[_gated],
+ *                       mem_bag_backward[_sparse], mem_search_backward) a device
+ *                       check that every index lies in [0, N) (or [0, S*S)); the
+ *                       call waits for it and returns PKMEM_ERR_INVALID if not.
+ *                       Off by default: indices from mem_search are in range by
+ *                       construction.  The check's flag is the only device
+ *                       memory the library allocates (4 bytes per device).
+ *   PKMEM_BWD_MODE=atomic|sorted
+ *                       what PKMEM_BWD_AUTO means, for mem_bag_backward and its
+ *                       workspace size.
+ * ------------------------------------------------------------------------ */
+
 /* Message for the last non-OK status returned to the calling thread. */
 const char* mem_last_error(void);
 

@@ -2,6 +2,8 @@
 // workspace carving, dispatch to the kernels.  Declared in include/pkmem.h.
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
 
 #include <string>
 #include <utility>
@@ -101,9 +103,44 @@ size_t bwd_ws_bytes(int64_t T, int H, int k, int mode) {
   return b;
 }
 
+// PKMEM_BWD_MODE=atomic|sorted in the environment overrides the library's
+// choice for PKMEM_BWD_AUTO (read at every call).
 int resolve_mode(int mode, int D) {
-  if (mode == PKMEM_BWD_AUTO) return D > 128 ? PKMEM_BWD_SORTED : PKMEM_BWD_ATOMIC;
-  return mode;
+  if (mode != PKMEM_BWD_AUTO) return mode;
+  const char* env = getenv("PKMEM_BWD_MODE");
+  if (env && strcmp(env, "atomic") == 0) return PKMEM_BWD_ATOMIC;
+  if (env && strcmp(env, "sorted") == 0) return PKMEM_BWD_SORTED;
+  return D > 128 ? PKMEM_BWD_SORTED : PKMEM_BWD_ATOMIC;
+}
+
+// PKMEM_DEBUG=1 in the environment (read at every call) checks on the device
+// that every index lies in [0, limit) before the kernels that use them run:
+// the call waits for the check and fails with PKMEM_ERR_INVALID otherwise.
+// The flag it needs is the only device memory the library allocates (4 bytes
+// per device, once, and only in debug mode).
+bool debug_checks() {
+  const char* env = getenv("PKMEM_DEBUG");
+  return env && env[0] && strcmp(env, "0") != 0;
+}
+
+int check_indices(const char* fn, const int64_t* idx, int64_t count, int64_t limit, hipStream_t st) {
+  if (!debug_checks() || count <= 0) return PKMEM_OK;
+  static uint32_t* flags[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, fn);
+  if (dev < 0 || dev >= 64) return fail(PKMEM_ERR_UNSUPPORTED, "%s: device %d", fn, dev);
+  if (!flags[dev]) {
+    e = hipMalloc(reinterpret_cast<void**>(&flags[dev]), sizeof(uint32_t));
+    if (e != hipSuccess) return hip_status(e, fn);
+  }
+  e = pk::launch_check_indices(idx, count, limit, flags[dev], st);
+  uint32_t bad = 0;
+  if (e == hipSuccess) e = hipMemcpyAsync(&bad, flags[dev], sizeof(bad), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_status(e, fn);
+  if (bad) return fail(PKMEM_ERR_INVALID, "%s: an index lies outside [0, %lld) (PKMEM_DEBUG)", fn, (long long)limit);
+  return PKMEM_OK;
 }
 
 int bag_backward_common(const char* fn, const void* dy, const void* values, pkmem_dtype v_dt,
@@ -139,6 +176,8 @@ int bag_backward_common(const char* fn, const void* dy, const void* values, pkme
   if (!aligned(ws, 256)) return fail(PKMEM_ERR_INVALID, "%s: workspace must be 256-byte aligned", fn);
   if (sparse) *num_rows_out = 0;
   if (T == 0) return PKMEM_OK;
+  rc = check_indices(fn, idx, L, N, st);
+  if (rc) return rc;
 
   char* p = reinterpret_cast<char*>(ws);
   float* gw = grad_w ? grad_w : reinterpret_cast<float*>(p);
@@ -312,6 +351,8 @@ int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pk
     return fail(PKMEM_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : (size_t)0);
   if (!aligned(ws, 256)) return fail(PKMEM_ERR_INVALID, "%s: workspace must be 256-byte aligned", fn);
   if (T == 0 || (!grad_q && !grad_subkeys)) return PKMEM_OK;
+  rc = check_indices(fn, idx, T * H * k, (int64_t)S * S, reinterpret_cast<hipStream_t>(stream));
+  if (rc) return rc;
   hipError_t e = pk::launch_search_backward(q_dt == PKMEM_BF16, q, subkeys, T, H, n, S, k, idx,
                                             grad_scores, grad_q, grad_subkeys, ws,
                                             reinterpret_cast<hipStream_t>(stream));
@@ -326,6 +367,8 @@ int mem_bag_forward(const void* values, pkmem_dtype v_dt, int64_t N, int D, cons
   if (T > 0 && (!values || !idx || !w || !y_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
   if (!aligned(values, 16) || !aligned(y_out, 16)) return fail(PKMEM_ERR_INVALID, "%s: values and y_out must be 16-byte aligned", fn);
   if (T == 0) return PKMEM_OK;
+  rc = check_indices(fn, idx, T * bag, N, reinterpret_cast<hipStream_t>(stream));
+  if (rc) return rc;
   hipError_t e = pk::launch_bag_forward(v_dt == PKMEM_BF16, values, D, idx, w, T, bag, y_out, nullptr, nullptr,
                                         reinterpret_cast<hipStream_t>(stream));
   return hip_status(e, fn);
@@ -341,6 +384,8 @@ int mem_bag_forward_gated(const void* values, pkmem_dtype v_dt, int64_t N, int D
   if (!aligned(values, 16) || !aligned(gate, 16) || !aligned(out, 16) || !aligned(y_out, 16))
     return fail(PKMEM_ERR_INVALID, "%s: values, gate, y_out and out must be 16-byte aligned", fn);
   if (T == 0) return PKMEM_OK;
+  rc = check_indices(fn, idx, T * bag, N, reinterpret_cast<hipStream_t>(stream));
+  if (rc) return rc;
   hipError_t e = pk::launch_bag_forward(v_dt == PKMEM_BF16, values, D, idx, w, T, bag, out, gate,
                                         y_out, reinterpret_cast<hipStream_t>(stream));
   return hip_status(e, fn);

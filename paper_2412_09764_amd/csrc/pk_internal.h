@@ -59,6 +59,8 @@ hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys,
 hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_t* idx,
                               const float* w, int64_t T, int bag, void* y, const void* gate,
                               void* y_plain, hipStream_t st);
+hipError_t launch_check_indices(const int64_t* idx, int64_t count, int64_t limit, uint32_t* bad,
+                                hipStream_t st);
 hipError_t launch_gate_backward(bool bf16, const void* d_out, const void* gate, const void* y,
                                 int64_t T, int D, void* dy, float* grad_gate, hipStream_t st);
 hipError_t launch_bag_backward_atomic(bool bf16, const void* dy, const void* values, int D,

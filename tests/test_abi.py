@@ -233,3 +233,16 @@ def test_gate_backward_rejects(lib, kw, code, text):
 def test_gating_empty_batch_is_a_noop(lib):
     assert fwdg(lib, T=0) == OK
     assert gbwd(lib, T=0) == OK
+
+
+def test_bwd_mode_environment_override(lib, monkeypatch):
+    args = (1000, 4, 32, 1 << 22, 2048, 0)
+    atomic = lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 2048, 1)
+    sorted_ = lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 2048, 2)
+    assert lib.mem_bag_backward_workspace_size(*args) == sorted_
+    monkeypatch.setenv("PKMEM_BWD_MODE", "atomic")
+    assert lib.mem_bag_backward_workspace_size(*args) == atomic
+    monkeypatch.setenv("PKMEM_BWD_MODE", "sorted")
+    assert lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 64, 0) == sorted_
+    # an explicit mode is never overridden
+    assert lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 2048, 1) == atomic
