@@ -48,9 +48,12 @@ hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, in
 
 // ---- search backward (search_bwd.hip) --------------------------------------
 size_t search_backward_ws_bytes(int64_t T, int H, int k);
-hipError_t sort_u32_segments(const uint32_t* keys, int64_t L, int key_bits, void* ws,
+void sort_u32_inputs(void* ws, int64_t Lmax, uint32_t** keys_in, uint32_t** vals_in);
+hipError_t sort_u32_segments(int64_t Lmax, const uint32_t* Ldev, int key_bits, void* ws,
                              const uint32_t** ks, const uint32_t** vs, const uint32_t** seg,
                              const uint32_t** nseg, hipStream_t st);
+size_t scan_scratch_u32(int64_t n);
+hipError_t scan_exclusive_u32(uint32_t* data, int64_t n, uint32_t* sums, hipStream_t st);
 hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
                                   int n, int S, int k, const int64_t* idx, const float* gz,
                                   float* grad_q, float* grad_K, void* ws, hipStream_t st);

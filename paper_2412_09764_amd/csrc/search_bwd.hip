@@ -14,11 +14,13 @@
 // grad_K: every sub-key row is hot (only S rows per head and half), and fp32
 // atomics, in global memory or in LDS, serialise on them.  Instead the same
 // wave emits one (head, half, sub-key) sort key per group leader, with the
-// group's gradient sum, and the 2*T*H*k (lookup, half) pairs are sorted by key
-// with the library's stable radix sort.  One wave per segment then sums
-// gsum * q over the segment's tokens (in token order; each token's query half
-// is read once) and adds the sum into the sub-key row with one plain
-// read-modify-write: no atomics, bitwise deterministic.
+// group's gradient sum, at the front of its (token, head, half) row of k
+// slots, and counts them; an exclusive scan of the counts places the leaders
+// contiguously (in slot order), and the library's stable radix sort orders
+// those pairs by key.  One wave per segment then sums gsum * q over the
+// segment's tokens (in token order; each token's query half is read once) and
+// adds the sum into the sub-key row with one plain read-modify-write: no
+// atomics, bitwise deterministic.
 #include "pk_device.h"
 #include "pk_internal.h"
 
@@ -56,10 +58,10 @@ struct QQuad<float> {
 // and the group's gradient sum, in rank order.  Then
 //   * grad_q (if wanted): the distinct sub-key rows are read QU at a time (all
 //     loads in flight together), lane l owning elements 4l..4l+3;
-//   * sort input (if wanted): pair x = ((t*H + h)*k + j)*2 + half gets the key
-//     (h*2 + half)*S + sub-key and value gsum when rank j leads its group, and
-//     the key 2*H*S (a skipped segment) otherwise.  Lookups whose index lies
-//     outside [0, S*S) count as absent.
+//   * sort input (if wanted): row rp = (t*H + h)*2 + half gets its leaders'
+//     keys (h*2 + half)*S + sub-key and group sums at slots rp*k + 0, 1, ...
+//     (in rank order of the leaders) and their number at counts[rp].  Lookups
+//     whose index lies outside [0, S*S) count as absent.
 #ifndef PK_SBWD_QU
 #define PK_SBWD_QU 8
 #endif
@@ -70,8 +72,9 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
                                                       const int64_t* __restrict__ idx,
                                                       const float* __restrict__ gz,
                                                       float* __restrict__ grad_q,
-                                                      uint2* __restrict__ keys,
-                                                      float2* __restrict__ gvals) {
+                                                      uint32_t* __restrict__ keys,
+                                                      float* __restrict__ gvals,
+                                                      uint32_t* __restrict__ counts) {
   constexpr int QU = PK_SBWD_QU;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int h = (int)(blockIdx.x % (unsigned)H);
@@ -84,9 +87,7 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
   const int64_t ix = lane < k ? idx[r * k + lane] : -1;
   const bool okl = ix >= 0 && ix < (int64_t)S * S;
   const float g = okl ? gz[r * k + lane] : 0.f;
-  const uint32_t nbins = (uint32_t)(2 * H) * (uint32_t)S;
-  uint32_t key[2];
-  float gs[2];
+  const uint64_t below = (1ull << lane) - 1ull;
 
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
@@ -101,8 +102,16 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
         if (j < lane) leader = false;
       }
     }
-    key[p] = leader ? (uint32_t)(h * 2 + p) * (uint32_t)S + (uint32_t)mine : nbins;
-    gs[p] = gsum;
+    if (keys) {
+      const uint64_t lm = __ballot(leader);
+      const size_t rp = r * 2 + p;
+      if (leader) {
+        const size_t x = rp * k + __popcll(lm & below);
+        keys[x] = (uint32_t)(h * 2 + p) * (uint32_t)S + (uint32_t)mine;
+        gvals[x] = gsum;
+      }
+      if (lane == 0) counts[rp] = (uint32_t)__popcll(lm);
+    }
     if (grad_q) {
       float acc[4] = {0.f, 0.f, 0.f, 0.f};
       const T* kh = subkeys + (size_t)(h * 2 + p) * S * d + ql;
@@ -129,9 +138,22 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
             make_float4(acc[0], acc[1], acc[2], acc[3]);
     }
   }
-  if (keys && lane < k) {
-    keys[r * k + lane] = uint2{key[0], key[1]};
-    gvals[r * k + lane] = make_float2(gs[0], gs[1]);
+}
+
+// The leaders of every row, packed: row rp's c = offs[rp+1] - offs[rp] keys
+// move from slots rp*k .. rp*k + c - 1 to offs[rp] ..; the value is the slot.
+__global__ __launch_bounds__(256) void k_sbwd_pack(const uint32_t* __restrict__ keys,
+                                                   const uint32_t* __restrict__ offs, int64_t rows,
+                                                   int k, uint32_t* __restrict__ keys_out,
+                                                   uint32_t* __restrict__ slot_out) {
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (x >= rows * k) return;
+  const int64_t rp = x / k;
+  const uint32_t j = (uint32_t)(x - rp * k);
+  const uint32_t o = offs[rp];
+  if (j < offs[rp + 1] - o) {
+    keys_out[o + j] = keys[x];
+    slot_out[o + j] = (uint32_t)x;
   }
 }
 
@@ -157,11 +179,11 @@ __global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, 
   const bool qlane = lane * 4 < d;
   const int ql = qlane ? lane * 4 : 0;
   const uint32_t nbins = (uint32_t)(2 * H) * (uint32_t)S;
-  const uint32_t hk2 = 2u * (uint32_t)H * (uint32_t)k;  // pairs per token
+  const uint32_t hk2 = 2u * (uint32_t)H * (uint32_t)k;  // slots per token
   for (uint32_t u = blockIdx.x * 4u + wave; u < nseg; u += gridDim.x * 4u) {
     const uint32_t s0 = seg[u], s1 = seg[u + 1];
     const uint32_t bin = ks[s0];
-    if (bin >= nbins) continue;  // non-leading ranks and absent lookups
+    if (bin >= nbins) continue;
     const int hp = (int)(bin / (uint32_t)S);
     const int h = hp >> 1, p = hp & 1;
     const T* qh = q + (size_t)h * n + (size_t)p * d + ql;
@@ -198,9 +220,15 @@ __global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, 
   }
 }
 
+// Workspace: keys and group sums per slot (2*T*H*k each), the row counts
+// (scanned in place into offsets, plus the total), the scan's partials, then
+// the sort of up to 2*T*H*k pairs.
+static size_t a256(size_t x) { return (x + 255) / 256 * 256; }
 size_t search_backward_ws_bytes(int64_t T, int H, int k) {
-  const int64_t np = 2 * T * H * k;
-  return 2 * (((size_t)np * 4 + 255) / 256 * 256) + sorted_workspace_bytes(np);
+  const int64_t rows = 2 * T * H;
+  const int64_t np = rows * k;
+  return 2 * a256((size_t)np * 4) + a256((size_t)(rows + 1) * 4) +
+         a256(scan_scratch_u32(rows + 1) * 4) + sorted_workspace_bytes(np);
 }
 
 template <typename T>
@@ -208,24 +236,42 @@ static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, in
                               int k, const int64_t* idx, const float* gz, float* grad_q,
                               float* grad_K, void* ws, hipStream_t st) {
   LaunchTimer lt("search_backward", st);
-  const int64_t np = 2 * T_ * H * k;
-  const size_t arr = ((size_t)np * 4 + 255) / 256 * 256;
-  uint32_t* keys = reinterpret_cast<uint32_t*>(ws);
-  float* gvals = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + arr);
-  void* sort_ws = reinterpret_cast<char*>(ws) + 2 * arr;
+  const int64_t rows = 2 * T_ * H;
+  const int64_t np = rows * k;
+  char* p = reinterpret_cast<char*>(ws);
+  uint32_t* keys = reinterpret_cast<uint32_t*>(p);
+  p += a256((size_t)np * 4);
+  float* gvals = reinterpret_cast<float*>(p);
+  p += a256((size_t)np * 4);
+  uint32_t* offs = reinterpret_cast<uint32_t*>(p);  // rows + 1
+  p += a256((size_t)(rows + 1) * 4);
+  uint32_t* sums = reinterpret_cast<uint32_t*>(p);
+  p += a256(scan_scratch_u32(rows + 1) * 4);
+  void* sort_ws = p;
+  hipError_t e = hipSuccess;
+  if (grad_K) e = launch_fill_u32(offs + rows, 0u, 1, st);  // the scan's last entry
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_search_bwd_q<T>, dim3((unsigned)(((T_ + 3) / 4) * H)), dim3(256), 0, st,
                      (const T*)q, (const T*)subkeys, T_, H, n, S, k, idx, gz, grad_q,
-                     grad_K ? reinterpret_cast<uint2*>(keys) : nullptr,
-                     grad_K ? reinterpret_cast<float2*>(gvals) : nullptr);
-  hipError_t e = hipGetLastError();
+                     grad_K ? keys : nullptr, grad_K ? gvals : nullptr, grad_K ? offs : nullptr);
+  e = hipGetLastError();
   if (e != hipSuccess || !grad_K) return e;
-  const uint32_t nbins = (uint32_t)(2 * H) * (uint32_t)S;  // plus the skipped key nbins
-  int key_bits = 1;
-  while (key_bits < 32 && (uint64_t(1) << key_bits) <= nbins) ++key_bits;
-  const uint32_t *ks, *vs, *seg, *nseg;
-  e = sort_u32_segments(keys, np, key_bits, sort_ws, &ks, &vs, &seg, &nseg, st);
+  // counts -> offsets; offs[rows] = number of leaders
+  e = scan_exclusive_u32(offs, rows + 1, sums, st);
   if (e != hipSuccess) return e;
-  int64_t maxseg = (int64_t)nbins + 1 < np ? (int64_t)nbins + 1 : np;
+  uint32_t *kin, *vin;
+  sort_u32_inputs(sort_ws, np, &kin, &vin);
+  hipLaunchKernelGGL(k_sbwd_pack, dim3((unsigned)((np + 255) / 256)), dim3(256), 0, st, keys, offs,
+                     rows, k, kin, vin);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const uint32_t nbins = (uint32_t)(2 * H) * (uint32_t)S;
+  int key_bits = 1;
+  while (key_bits < 32 && (uint64_t(1) << key_bits) < nbins) ++key_bits;
+  const uint32_t *ks, *vs, *seg, *nseg;
+  e = sort_u32_segments(np, offs + rows, key_bits, sort_ws, &ks, &vs, &seg, &nseg, st);
+  if (e != hipSuccess) return e;
+  int64_t maxseg = (int64_t)nbins < np ? (int64_t)nbins : np;
   int64_t blocks = (maxseg + 3) / 4;
   if (blocks > 16384) blocks = 16384;
   hipLaunchKernelGGL(k_sbwd_segments<T>, dim3((unsigned)blocks), dim3(256), 0, st, (const T*)q, H, n,

@@ -129,9 +129,15 @@ __device__ __forceinline__ uint32_t sort_key(const void* keys, int64_t i) {
 }
 
 template <int KM>
-__global__ __launch_bounds__(256) void k_radix_hist(const void* __restrict__ keys, int64_t L,
-                                                    int shift, int bits, int64_t nblk,
+__global__ __launch_bounds__(256) void k_radix_hist(const void* __restrict__ keys, int64_t Lmax,
+                                                    const uint32_t* __restrict__ Ldev, int shift,
+                                                    int bits, int64_t nblk,
                                                     uint32_t* __restrict__ hist) {
+  const int64_t L = (Ldev && (int64_t)*Ldev < Lmax) ? (int64_t)*Ldev : Lmax;
+  if ((int64_t)blockIdx.x * SORT_TILE >= L) {  // a tile past the count: empty
+    hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = 0u;
+    return;
+  }
   __shared__ uint32_t h[RADIX];
   h[threadIdx.x] = 0;
   __syncthreads();
@@ -149,10 +155,14 @@ __global__ __launch_bounds__(256) void k_radix_hist(const void* __restrict__ key
 template <int KM>
 __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ keys_in,
                                                        const uint32_t* __restrict__ vals_in,
-                                                       int64_t L, int shift, int bits, int64_t nblk,
+                                                       int64_t Lmax,
+                                                       const uint32_t* __restrict__ Ldev, int shift,
+                                                       int bits, int64_t nblk,
                                                        const uint32_t* __restrict__ offsets,
                                                        uint32_t* __restrict__ keys_out,
                                                        uint32_t* __restrict__ vals_out) {
+  const int64_t L = (Ldev && (int64_t)*Ldev < Lmax) ? (int64_t)*Ldev : Lmax;
+  if ((int64_t)blockIdx.x * SORT_TILE >= L) return;  // whole block: nothing to move
   __shared__ uint32_t run[RADIX];
   __shared__ uint32_t wcnt[4][RADIX];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -197,16 +207,20 @@ __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ 
 }
 
 // ------------------------------------------------------------- segments ----
-__global__ __launch_bounds__(256) void k_seg_flags(const uint32_t* __restrict__ keys, int64_t L,
+__global__ __launch_bounds__(256) void k_seg_flags(const uint32_t* __restrict__ keys, int64_t Lmax,
+                                                   const uint32_t* __restrict__ Ldev,
                                                    uint32_t* __restrict__ flags) {
+  const int64_t L = (Ldev && (int64_t)*Ldev < Lmax) ? (int64_t)*Ldev : Lmax;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < L) flags[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1u : 0u;
 }
 
-__global__ __launch_bounds__(256) void k_seg_starts(const uint32_t* __restrict__ keys, int64_t L,
+__global__ __launch_bounds__(256) void k_seg_starts(const uint32_t* __restrict__ keys, int64_t Lmax,
+                                                    const uint32_t* __restrict__ Ldev,
                                                     const uint32_t* __restrict__ excl,
                                                     uint32_t* __restrict__ seg_start,
                                                     uint32_t* __restrict__ nseg) {
+  const int64_t L = (Ldev && (int64_t)*Ldev < Lmax) ? (int64_t)*Ldev : Lmax;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= L) return;
   const bool head = (i == 0 || keys[i] != keys[i - 1]);
@@ -440,31 +454,34 @@ size_t sorted_workspace_bytes(int64_t L) {
 // Stable LSD radix sort of L keys (< 2^key_bits, from an int64 or a u32 array)
 // with their positions as values, then the segment starts of equal keys:
 // seg[0..U] in b.seg, U in b.misc[0].  *ks / *vs receive the sorted arrays.
+// L is the item count, or its upper bound when Ldev (device memory) holds the
+// count; vals_in, if given, are the first pass's values (else positions).
 static hipError_t sort_segments(const void* keys, bool key64, int64_t L, int key_bits,
                                 const SortedWs& b, const uint32_t** ks, const uint32_t** vs,
-                                hipStream_t st) {
+                                hipStream_t st, const uint32_t* vals_in = nullptr,
+                                const uint32_t* Ldev = nullptr) {
   hipError_t e = hipSuccess;
   const int64_t nblk = cdiv(L, SORT_TILE);
   const void* kin = keys;
-  const uint32_t* vin = nullptr;
+  const uint32_t* vin = vals_in;
   uint32_t *kout = b.keys_a, *vout = b.vals_a;
   for (int shift = 0, pass = 0; shift < key_bits; shift += RADIX_BITS, ++pass) {
     const int bits = (key_bits - shift) < RADIX_BITS ? (key_bits - shift) : RADIX_BITS;
     const dim3 g((unsigned)nblk), blk(256);
-    if (pass > 0)
-      hipLaunchKernelGGL(k_radix_hist<SRC_NEXT>, g, blk, 0, st, kin, L, shift, bits, nblk, b.hist);
+    if (pass > 0 || vals_in)
+      hipLaunchKernelGGL(k_radix_hist<SRC_NEXT>, g, blk, 0, st, kin, L, Ldev, shift, bits, nblk, b.hist);
     else if (key64)
-      hipLaunchKernelGGL(k_radix_hist<SRC_I64>, g, blk, 0, st, kin, L, shift, bits, nblk, b.hist);
+      hipLaunchKernelGGL(k_radix_hist<SRC_I64>, g, blk, 0, st, kin, L, Ldev, shift, bits, nblk, b.hist);
     else
-      hipLaunchKernelGGL(k_radix_hist<SRC_U32>, g, blk, 0, st, kin, L, shift, bits, nblk, b.hist);
+      hipLaunchKernelGGL(k_radix_hist<SRC_U32>, g, blk, 0, st, kin, L, Ldev, shift, bits, nblk, b.hist);
     e = exclusive_scan(b.hist, (int64_t)RADIX * nblk, b.sums, st);
     if (e != hipSuccess) return e;
-    if (pass > 0)
-      hipLaunchKernelGGL(k_radix_scatter<SRC_NEXT>, g, blk, 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+    if (pass > 0 || vals_in)
+      hipLaunchKernelGGL(k_radix_scatter<SRC_NEXT>, g, blk, 0, st, kin, vin, L, Ldev, shift, bits, nblk, b.hist, kout, vout);
     else if (key64)
-      hipLaunchKernelGGL(k_radix_scatter<SRC_I64>, g, blk, 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+      hipLaunchKernelGGL(k_radix_scatter<SRC_I64>, g, blk, 0, st, kin, vin, L, Ldev, shift, bits, nblk, b.hist, kout, vout);
     else
-      hipLaunchKernelGGL(k_radix_scatter<SRC_U32>, g, blk, 0, st, kin, vin, L, shift, bits, nblk, b.hist, kout, vout);
+      hipLaunchKernelGGL(k_radix_scatter<SRC_U32>, g, blk, 0, st, kin, vin, L, Ldev, shift, bits, nblk, b.hist, kout, vout);
     kin = kout;
     vin = vout;
     if (kout == b.keys_a) { kout = b.keys_b; vout = b.vals_b; }
@@ -473,23 +490,38 @@ static hipError_t sort_segments(const void* keys, bool key64, int64_t L, int key
   *ks = reinterpret_cast<const uint32_t*>(kin);
   *vs = vin;
   const unsigned lb = (unsigned)cdiv(L, 256);
-  hipLaunchKernelGGL(k_seg_flags, dim3(lb), dim3(256), 0, st, *ks, L, b.hist);
+  hipLaunchKernelGGL(k_seg_flags, dim3(lb), dim3(256), 0, st, *ks, L, Ldev, b.hist);
   e = exclusive_scan(b.hist, L, b.sums, st);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_seg_starts, dim3(lb), dim3(256), 0, st, *ks, L, b.hist, b.seg, b.misc);
+  hipLaunchKernelGGL(k_seg_starts, dim3(lb), dim3(256), 0, st, *ks, L, Ldev, b.hist, b.seg, b.misc);
   return hipGetLastError();
 }
 
-// Sort of u32 keys for other kernels of the library (same workspace layout).
-hipError_t sort_u32_segments(const uint32_t* keys, int64_t L, int key_bits, void* ws,
+// Sort of u32 keys with u32 values for other kernels of the library: up to
+// Lmax items, their count in device memory (*Ldev).  The input arrays must be
+// the ones sort_u32_inputs returns for this workspace (the first radix pass
+// reads them, the second overwrites them).
+void sort_u32_inputs(void* ws, int64_t Lmax, uint32_t** keys_in, uint32_t** vals_in) {
+  SortedWs b = carve(ws, Lmax);
+  *keys_in = b.keys_b;
+  *vals_in = b.vals_b;
+}
+
+hipError_t sort_u32_segments(int64_t Lmax, const uint32_t* Ldev, int key_bits, void* ws,
                              const uint32_t** ks, const uint32_t** vs, const uint32_t** seg,
                              const uint32_t** nseg, hipStream_t st) {
-  SortedWs b = carve(ws, L);
+  SortedWs b = carve(ws, Lmax);
   *seg = b.seg;
   *nseg = b.misc;
   hipError_t e = launch_fill_u32(b.misc, 0u, 1, st);
-  if (e != hipSuccess || L == 0) return e;
-  return sort_segments(keys, false, L, key_bits, b, ks, vs, st);
+  if (e != hipSuccess || Lmax == 0) return e;
+  return sort_segments(b.keys_b, false, Lmax, key_bits, b, ks, vs, st, b.vals_b, Ldev);
+}
+
+// Exclusive prefix sum of n u32 in place; sums needs scan_scratch_u32(n) entries.
+size_t scan_scratch_u32(int64_t n) { return (size_t)(cdiv(n, SCAN_TILE) + 1); }
+hipError_t scan_exclusive_u32(uint32_t* data, int64_t n, uint32_t* sums, hipStream_t st) {
+  return exclusive_scan(data, n, sums, st);
 }
 
 hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* values, int64_t N,
