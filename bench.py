@@ -88,8 +88,11 @@ def alg_cost(kernel: str, wl, U: int, esz: int):
         # selected value rows + output rows + (idx int64, w fp32) per lookup
         return "hbm", L * D * esz + T * D * esz + L * 12
     if kernel == "bag_backward_rows":
-        # per touched row: value row read, fp32 gradient row read + write, segment start;
+        # per touched row: value row read, segment start, and either the fp32 gradient
+        # row read + write (dense) or written once with its row id (sparse);
         # per token: dy row; per lookup: sorted row key, lookup id, w, grad_w
+        if wl.sparse_grad:
+            return "hbm", U * D * (esz + 4) + U * (4 + 8) + T * D * esz + L * 16
         return "hbm", U * D * (esz + 8) + U * 4 + T * D * esz + L * 16
     if kernel == "bag_backward_atomic":
         # per lookup: value row read, fp32 gradient row read + write, (idx, w, grad_w); dy per token
