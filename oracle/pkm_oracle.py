@@ -50,6 +50,24 @@ Function pins (tests under tests/test_oracle_*.py):
                    torch.nn.functional.silu and torch autograd (fp64, CPU);
                    closed forms silu(0) = 0, silu(ln 3) = (3/4) ln 3,
                    silu'(0) = 1/2; central finite differences; limits
+  query_layernorm  torch.nn.functional.layer_norm (fp64, CPU); closed form for
+                   [1, 2, 3, 4]; zero mean, mean square var / (var + eps);
+                   invariance to shift and (eps = 0) positive scale
+  round_bf16       torch's bf16 conversion of fp32 values; hand-worked ties
+  search_qnorm     eps = 0 on rows built with mean 0 and variance 4: equals
+                   the plain search (and brute force) on q / 2
+  search_backward_qnorm
+                   central finite differences in the raw queries at a fixed
+                   selection; torch autograd through layer_norm (fp64)
+
+Query normalisation (qk-normalisation, named in Sec. 3.1.4 as the remedy for
+unstable training of large memories, citing a LayerNorm of queries and keys).
+The paper gives no formula; reading: LayerNorm without affine parameters over
+each (token, head) query of n elements, biased variance, eps inside the
+square root; a query with zero variance and eps = 0 normalises to zeros.  The
+normalised query is stored in the query dtype (bf16 or fp32) before scoring,
+and that rounding passes gradients unchanged.  Sub-keys are parameters and are
+not normalised here.
 """
 from __future__ import annotations
 
@@ -71,6 +89,11 @@ __all__ = [
     "silu",
     "gated_output",
     "gated_backward",
+    "round_bf16",
+    "round_to",
+    "query_layernorm",
+    "search_qnorm",
+    "search_backward_qnorm",
 ]
 
 
@@ -360,3 +383,69 @@ def gated_backward(d_out: np.ndarray, y: np.ndarray, gate: np.ndarray) -> dict:
     e = np.exp(-np.abs(g))
     sig = np.where(g >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
     return dict(dy=d * (g * sig), dg=d * yy * (sig * (1.0 + g * (1.0 - sig))))
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Nearest value with an 8-bit significand (bfloat16's), ties to even,
+    from the exact fp64 value (no intermediate fp32 rounding).  Finite inputs
+    within bfloat16's normal range, or zero."""
+    x = _f64(x)
+    m, e = np.frexp(x)             # x = m * 2**e, 0.5 <= |m| < 1
+    m = np.rint(m * 256.0) / 256.0  # 8 significant bits; rint rounds half to even
+    return np.ldexp(m, e)
+
+
+def round_to(x: np.ndarray, dtype: str) -> np.ndarray:
+    """The value a kernel stores in `dtype`: "bf16", "fp32", or "fp64" (no rounding)."""
+    if dtype == "bf16":
+        return round_bf16(x)
+    if dtype == "fp32":
+        return _f64(np.asarray(x, dtype=np.float64).astype(np.float32))
+    if dtype == "fp64":
+        return _f64(x)
+    raise ValueError(dtype)
+
+
+def query_layernorm(q: np.ndarray, eps: float) -> dict:
+    """LayerNorm without affine parameters over the last axis (each (t, h)
+    query of n elements): mean, biased variance, rstd = 1 / sqrt(var + eps),
+    qhat = (q - mean) * rstd.  rstd is 0 where var + eps == 0."""
+    x = _f64(q)
+    mean = x.mean(axis=-1)
+    xc = x - mean[..., None]
+    var = (xc * xc).mean(axis=-1)
+    ve = var + float(eps)
+    rstd = np.where(ve > 0, 1.0 / np.sqrt(np.where(ve > 0, ve, 1.0)), 0.0)
+    return dict(qhat=xc * rstd[..., None], mean=mean, rstd=rstd, var=var)
+
+
+def search_qnorm(q: np.ndarray, subkeys: np.ndarray, k: int, eps: float,
+                 dtype: str = "fp64") -> dict:
+    """Product-key search of the normalised queries: qhat from
+    query_layernorm, rounded to the storage dtype, then `search`.  The result
+    also carries qhat (as scored), mean and rstd."""
+    ln = query_layernorm(q, eps)
+    qs = round_to(ln["qhat"], dtype)
+    out = search(qs, subkeys, k)
+    out.update(qhat=qs, mean=ln["mean"], rstd=ln["rstd"])
+    return out
+
+
+def search_backward_qnorm(q: np.ndarray, subkeys: np.ndarray, idx: np.ndarray,
+                          grad_z: np.ndarray, eps: float, dtype: str = "fp64",
+                          grad_subkeys_in=None) -> dict:
+    """Search backward through the query normalisation.  With g = dL/dqhat
+    from `search_backward` at the stored qhat (which also gives grad_K, built
+    from qhat as scored), the LayerNorm backward over each query is
+      grad_q = rstd * (g - mean(g) - xhat * mean(g * xhat)),
+    xhat = (q - mean) * rstd unrounded (the storage rounding passes the
+    gradient unchanged)."""
+    ln = query_layernorm(q, eps)
+    qs = round_to(ln["qhat"], dtype)
+    r = search_backward(qs, subkeys, idx, grad_z, grad_subkeys_in)
+    g = r["grad_q"]
+    xh = ln["qhat"]
+    gm = g.mean(axis=-1, keepdims=True)
+    gxm = (g * xh).mean(axis=-1, keepdims=True)
+    grad_q = ln["rstd"][..., None] * (g - gm - xh * gxm)
+    return dict(grad_q=grad_q, grad_K=r["grad_K"])

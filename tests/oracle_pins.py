@@ -24,6 +24,13 @@ What pins what:
                   fixed selection; torch autograd of the gathered scores;
                   the bilinear identities sum(grad_q q) = sum(grad_z z) =
                   sum(grad_K K); accumulation onto an existing key gradient.
+  query norm    - torch.nn.functional.layer_norm in fp64; the closed form
+                  for [1, 2, 3, 4]; zero mean, mean square var / (var + eps),
+                  shift and scale invariance; bf16 rounding against torch's
+                  conversion and hand-worked ties; with eps = 0, rows built to
+                  normalise exactly give the plain search (and brute force) of
+                  x / 2; the backward by central differences and torch
+                  autograd through layer_norm.
 """
 from __future__ import annotations
 
@@ -325,3 +332,148 @@ def check_gated_backward(bwd_fn, rng, T=4, D=6, h=1e-6):
     np.testing.assert_allclose(z["dg"], 0.5 * d * y, rtol=1e-15, atol=0)
     zero = bwd_fn(np.zeros_like(d), y, g)
     assert not zero["dy"].any() and not zero["dg"].any()
+
+
+# ---------------------------------------------------- query normalisation ----
+def check_query_layernorm(ln_fn, rng, T=5, H=3, n=12):
+    """LayerNorm without affine: torch.nn.functional.layer_norm (fp64, CPU) as
+    the library routine; the closed form for [1, 2, 3, 4]; zero mean and mean
+    square var / (var + eps); invariance to a shift, and (eps = 0) to a
+    positive scale; a constant query with eps = 0 gives zeros."""
+    q = 3.0 * rng.standard_normal((T, H, n)) + 1.5
+    for eps in (1e-5, 0.5):
+        out = ln_fn(q, eps)
+        ref = torch.nn.functional.layer_norm(torch.tensor(q), (n,), eps=eps)
+        np.testing.assert_allclose(out["qhat"], ref.numpy(), rtol=1e-13, atol=1e-14)
+        np.testing.assert_allclose(out["qhat"].mean(-1), 0.0, atol=1e-14)
+        var = ((q - q.mean(-1, keepdims=True)) ** 2).mean(-1)
+        np.testing.assert_allclose((out["qhat"] ** 2).mean(-1), var / (var + eps), rtol=1e-13)
+        np.testing.assert_allclose(out["qhat"], ln_fn(q + 7.25, eps)["qhat"], rtol=1e-11, atol=1e-12)
+    # mean 5/2, variance 5/4: (x - 5/2) / sqrt(5/4) = (2x - 5) / sqrt(5)
+    x = np.array([[[1.0, 2.0, 3.0, 4.0]]])
+    c = ln_fn(x, 0.0)
+    np.testing.assert_allclose(c["qhat"][0, 0], np.array([-3.0, -1.0, 1.0, 3.0]) / math.sqrt(5.0),
+                               rtol=1e-15, atol=0)
+    assert math.isclose(float(c["mean"][0, 0]), 2.5, rel_tol=0, abs_tol=0)
+    assert math.isclose(float(c["rstd"][0, 0]), 2.0 / math.sqrt(5.0), rel_tol=1e-15)
+    np.testing.assert_allclose(ln_fn(4.0 * q, 0.0)["qhat"], ln_fn(q, 0.0)["qhat"], rtol=1e-12, atol=1e-13)
+    z = ln_fn(np.full((1, 1, 6), 2.5), 0.0)
+    assert not z["qhat"].any() and float(z["rstd"][0, 0]) == 0.0
+
+
+def check_round_bf16(round_fn, rng):
+    """Against torch's bfloat16 conversion of fp32 values (for a value that is
+    exact in fp32 the single and the fp32-first roundings coincide), and hand
+    ties: 1 + 2^-8 lies halfway between 1 and 1 + 2^-7 and goes to the even 1;
+    1 + 3 * 2^-8 lies halfway between 1 + 2^-7 and 1 + 2^-6 and goes to 1 + 2^-6."""
+    x = (rng.standard_normal(4000) * np.exp2(rng.integers(-20, 20, 4000))).astype(np.float32)
+    ref = torch.tensor(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(round_fn(x.astype(np.float64)), ref)
+    ties = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, -(1 + 2.0 ** -8), 255.5, 0.0, 0.75])
+    np.testing.assert_array_equal(round_fn(ties), [1.0, 1 + 2.0 ** -6, -1.0, 256.0, 0.0, 0.75])
+
+
+def exact_norm_rows(rng, T, H, n, shift=True):
+    """Queries whose LayerNorm (eps = 0) is exact in binary arithmetic: each
+    (t, h) row is c + 2^m * x with x a permutation of 3n/16 entries of each of
+    +3 and -3 and 5n/16 of each of +1 and -1 (mean 0, variance 4), c an
+    integer and m in {-1, 0, 1, 2}; its normalised form is x / 2.  Returns
+    (q, x / 2).  n must be a multiple of 16."""
+    assert n % 16 == 0
+    a, b = 5 * n // 16, 3 * n // 16
+    base = np.array([3.0] * b + [-3.0] * b + [1.0] * a + [-1.0] * a)
+    xs = np.stack([rng.permutation(base) for _ in range(T * H)]).reshape(T, H, n)
+    c = rng.integers(-4, 5, size=(T, H, 1)).astype(np.float64) if shift else 0.0
+    m = np.exp2(rng.integers(-1, 3, size=(T, H, 1)).astype(np.float64)) if shift else 1.0
+    return c + m * xs, xs / 2.0
+
+
+def check_search_qnorm_exact(search_qnorm_fn, search_fn, brute_fn, rng, T=6, H=2, n=32, S=7, k=5):
+    """eps = 0 on exactly normalisable rows: the normalised search equals the
+    plain search, and brute force, on x / 2, ties included (integer sub-keys),
+    and reports mean c and rstd 1 / (2 * 2^m)."""
+    q, half = exact_norm_rows(rng, T, H, n)
+    K = rng.integers(-2, 3, size=(H, 2, S, n // 2)).astype(np.float64)
+    for dt in ("fp64", "bf16"):
+        out = search_qnorm_fn(q, K, k, 0.0, dt)
+        np.testing.assert_array_equal(out["qhat"], half)
+        ref = search_fn(half, K, k)
+        np.testing.assert_array_equal(out["idx"], ref["idx"])
+        np.testing.assert_array_equal(out["idx"], brute_fn(half, K, k)["idx"])
+        np.testing.assert_array_equal(out["score"], ref["score"])
+        np.testing.assert_allclose(out["w"], ref["w"], rtol=1e-15, atol=0)
+    np.testing.assert_allclose(out["mean"], q.mean(-1), rtol=0, atol=0)
+    spread = (q - q.mean(-1, keepdims=True))[..., :1] / (2.0 * half[..., :1])
+    np.testing.assert_allclose(out["rstd"], 1.0 / (2.0 * spread[..., 0]), rtol=1e-15)
+
+
+def check_search_backward_qnorm(search_qnorm_fn, bwd_fn, rng, T=3, H=2, S=5, d=4, k=3, h=1e-6):
+    """Gradient through the normalisation at a fixed selection: central
+    differences in the raw queries and sub-keys of L = sum(gz * z(LN(q))), and
+    torch autograd through layer_norm (fp64).  Storage rounding off (fp64)."""
+    n = 2 * d
+    q = 2.0 * rng.standard_normal((T, H, n)) + 0.7
+    K = rng.standard_normal((H, 2, S, d))
+    for eps in (1e-5, 0.25):
+        idx = search_qnorm_fn(q, K, k, eps, "fp64")["idx"]
+        gz = rng.standard_normal((T, H, k))
+        g = bwd_fn(q, K, idx, gz, eps, "fp64")
+
+        def L(qq, KK):
+            mu = qq.mean(-1, keepdims=True)
+            xc = qq - mu
+            qh = xc / np.sqrt((xc * xc).mean(-1, keepdims=True) + eps)
+            return float((selected_scores(qh, KK, idx) * gz).sum())
+
+        for (t, hh, e) in [(0, 0, 0), (1, 1, 5), (2, 0, 7), (0, 1, 3)]:
+            qp = q.copy(); qp[t, hh, e] += h
+            qm = q.copy(); qm[t, hh, e] -= h
+            fd = (L(qp, K) - L(qm, K)) / (2 * h)
+            assert abs(fd - g["grad_q"][t, hh, e]) < 2e-7, (eps, t, hh, e, fd, g["grad_q"][t, hh, e])
+        i1 = int(idx[0, 0, 0]) // S
+        Kp = K.copy(); Kp[0, 0, i1, 1] += h
+        Km = K.copy(); Km[0, 0, i1, 1] -= h
+        fd = (L(q, Kp) - L(q, Km)) / (2 * h)
+        assert abs(fd - g["grad_K"][0, 0, i1, 1]) < 2e-7
+        qt = torch.tensor(q, requires_grad=True)
+        Kt = torch.tensor(K, requires_grad=True)
+        qh = torch.nn.functional.layer_norm(qt, (n,), eps=eps)
+        it = torch.tensor(idx)
+        j1, j2 = it // S, it % S
+        hh_ = torch.arange(H).view(1, H, 1).expand_as(it)
+        z = (qh[..., :d].unsqueeze(2) * Kt[hh_, 0, j1]).sum(-1) + (qh[..., d:].unsqueeze(2) * Kt[hh_, 1, j2]).sum(-1)
+        (z * torch.tensor(gz)).sum().backward()
+        np.testing.assert_allclose(g["grad_q"], qt.grad.numpy(), rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(g["grad_K"], Kt.grad.numpy(), rtol=1e-10, atol=1e-12)
+        # a LayerNorm gradient is orthogonal to the constant direction
+        np.testing.assert_allclose(g["grad_q"].sum(-1), 0.0, atol=1e-10)
+    # bf16 storage: the scores (and so grad_K) use the rounded query, and the
+    # rounding passes the gradient unchanged into the LayerNorm backward
+    eps = 1e-5
+    idx = search_qnorm_fn(q, K, k, eps, "bf16")["idx"]
+    gz = rng.standard_normal((T, H, k))
+    g = bwd_fn(q, K, idx, gz, eps, "bf16")
+    qt = torch.tensor(q, requires_grad=True)
+    Kt = torch.tensor(K, requires_grad=True)
+    qh = torch.nn.functional.layer_norm(qt, (n,), eps=eps)
+    qs = qh + (qh.detach().float().to(torch.bfloat16).double() - qh.detach())
+    it = torch.tensor(idx)
+    j1, j2 = it // S, it % S
+    hh_ = torch.arange(H).view(1, H, 1).expand_as(it)
+    z = (qs[..., :d].unsqueeze(2) * Kt[hh_, 0, j1]).sum(-1) + (qs[..., d:].unsqueeze(2) * Kt[hh_, 1, j2]).sum(-1)
+    (z * torch.tensor(gz)).sum().backward()
+    np.testing.assert_allclose(g["grad_q"], qt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(g["grad_K"], Kt.grad.numpy(), rtol=1e-10, atol=1e-12)
+
+
+def check_search_qnorm_rounding(search_qnorm_fn, rng, T=4, H=2, n=48, S=6, k=3):
+    """The normalised queries as scored: torch's layer_norm (fp64) rounded by
+    torch to fp32, and to bf16 via fp32 (seeded random values, where the two
+    bf16 roundings coincide)."""
+    q = 1.7 * rng.standard_normal((T, H, n)) - 0.4
+    K = rng.standard_normal((H, 2, S, n // 2))
+    ref = torch.nn.functional.layer_norm(torch.tensor(q), (n,), eps=1e-5)
+    out = search_qnorm_fn(q, K, k, 1e-5, "fp32")
+    np.testing.assert_array_equal(out["qhat"], ref.float().double().numpy())
+    out = search_qnorm_fn(q, K, k, 1e-5, "bf16")
+    np.testing.assert_array_equal(out["qhat"], ref.float().to(torch.bfloat16).double().numpy())

@@ -247,3 +247,117 @@ def test_catches_gate_gradient_with_silu_not_its_derivative():
         out["dg"] = np.asarray(d) * np.asarray(y) * oracle.silu(g)
         return out
     assert _gating_fails(bwd_fn=bwd) > 0
+
+
+# ----------------------------------------------------- query normalisation ----
+def _qnorm_fails(ln=None, rnd=None, sq=None, bwd=None):
+    ln = ln or oracle.query_layernorm
+    rnd = rnd or oracle.round_bf16
+    sq = sq or oracle.search_qnorm
+    bwd = bwd or oracle.search_backward_qnorm
+    checks = [
+        lambda: pins.check_query_layernorm(ln, np.random.default_rng(101)),
+        lambda: pins.check_round_bf16(rnd, np.random.default_rng(102)),
+        lambda: pins.check_search_qnorm_exact(sq, oracle.search, oracle.brute_force_search,
+                                              np.random.default_rng(103)),
+        lambda: pins.check_search_qnorm_rounding(sq, np.random.default_rng(104)),
+        lambda: pins.check_search_backward_qnorm(sq, bwd, np.random.default_rng(105)),
+    ]
+    failures = 0
+    for c in checks:
+        try:
+            c()
+        except (AssertionError, ValueError, IndexError):
+            failures += 1
+    return failures
+
+
+def _ln(q, eps, ddof=0, eps_outside=False, halves=False):
+    x = np.asarray(q, dtype=np.float64)
+    if halves:
+        d = x.shape[-1] // 2
+        a, b = _ln(x[..., :d], eps), _ln(x[..., d:], eps)
+        return dict(qhat=np.concatenate([a["qhat"], b["qhat"]], -1), mean=a["mean"], rstd=a["rstd"])
+    mu = x.mean(-1)
+    xc = x - mu[..., None]
+    var = (xc * xc).sum(-1) / (x.shape[-1] - ddof)
+    rstd = 1.0 / (np.sqrt(var) + eps) if eps_outside else 1.0 / np.sqrt(var + eps)
+    return dict(qhat=xc * rstd[..., None], mean=mu, rstd=rstd)
+
+
+def _sq_with(ln):
+    def sq(q, K, k, eps, dtype="fp64"):
+        r = ln(q, eps)
+        qs = po.round_to(r["qhat"], dtype)
+        out = oracle.search(qs, K, k)
+        out.update(qhat=qs, mean=r["mean"], rstd=r["rstd"])
+        return out
+    return sq
+
+
+def test_real_qnorm_passes():
+    assert _qnorm_fails() == 0
+
+
+def test_catches_unbiased_variance():
+    ln = lambda q, eps: _ln(q, eps, ddof=1)  # noqa: E731
+    assert _qnorm_fails(ln=ln, sq=_sq_with(ln)) > 0
+
+
+def test_catches_eps_outside_the_root():
+    ln = lambda q, eps: _ln(q, eps, eps_outside=True)  # noqa: E731
+    assert _qnorm_fails(ln=ln, sq=_sq_with(ln)) > 0
+
+
+def test_catches_per_half_normalisation():
+    ln = lambda q, eps: _ln(q, eps, halves=True)  # noqa: E731
+    assert _qnorm_fails(ln=ln, sq=_sq_with(ln)) > 0
+
+
+def test_catches_bf16_truncation():
+    def trunc(x):
+        b = np.asarray(x, dtype=np.float64).astype(np.float32).view(np.uint32) & np.uint32(0xFFFF0000)
+        return b.view(np.float32).astype(np.float64)
+    assert _qnorm_fails(rnd=trunc) > 0
+
+
+def test_catches_unrounded_scoring():
+    def sq(q, K, k, eps, dtype="fp64"):
+        return oracle.search_qnorm(q, K, k, eps, "fp64")
+    assert _qnorm_fails(sq=sq) > 0
+
+
+def _bwd_variant(drop_mean=False, drop_proj=False, rounded_xhat=False, unrounded_dk=False):
+    def bwd(q, K, idx, gz, eps, dtype="fp64", base=None):
+        ln = oracle.query_layernorm(q, eps)
+        qs = po.round_to(ln["qhat"], dtype)
+        r = oracle.search_backward(ln["qhat"] if unrounded_dk else qs, K, idx, gz, base)
+        g = oracle.search_backward(qs, K, idx, gz)["grad_q"]
+        xh = qs if rounded_xhat else ln["qhat"]
+        out = g.copy()
+        if not drop_mean:
+            out -= g.mean(-1, keepdims=True)
+        if not drop_proj:
+            out -= xh * (g * xh).mean(-1, keepdims=True)
+        return dict(grad_q=ln["rstd"][..., None] * out, grad_K=r["grad_K"])
+    return bwd
+
+
+def test_qnorm_backward_variant_helper_is_faithful():
+    assert _qnorm_fails(bwd=_bwd_variant()) == 0
+
+
+def test_catches_qnorm_backward_without_mean_term():
+    assert _qnorm_fails(bwd=_bwd_variant(drop_mean=True)) > 0
+
+
+def test_catches_qnorm_backward_without_projection_term():
+    assert _qnorm_fails(bwd=_bwd_variant(drop_proj=True)) > 0
+
+
+def test_catches_qnorm_backward_with_rounded_xhat():
+    assert _qnorm_fails(bwd=_bwd_variant(rounded_xhat=True)) > 0
+
+
+def test_catches_qnorm_key_gradient_from_unrounded_query():
+    assert _qnorm_fails(bwd=_bwd_variant(unrounded_dk=True)) > 0
