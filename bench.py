@@ -46,6 +46,7 @@ KERNEL_SOURCES = {
     "search_backward": ["search_bwd.hip", "sorted.hip", "pk_device.h"],
     "bag_forward_gated": ["bag.hip", "pk_device.h"],
     "gate_backward": ["bag.hip", "pk_device.h"],
+    "qnorm": ["search.hip", "pk_device.h"],
 }
 
 
@@ -103,11 +104,18 @@ def alg_cost(kernel: str, wl, U: int, esz: int):
     if kernel == "gate_backward":
         # d_out, gate, un-gated bag read; dy (value dtype) and fp32 gate gradient written
         return "hbm", T * D * (4 * esz + 4)
+    if kernel == "qnorm":
+        # each query read once, its (mean, rstd) written
+        return "hbm", T * H * wl.n * esz_q(wl) + T * H * 8
     if kernel == "score_topk":
         return "mfma", 2.0 * T * H * 2 * S * d
     if kernel == "sort_by_row":
         return "hbm", None
     return "hbm", None
+
+
+def esz_q(wl):
+    return 2 if wl.key_dtype == "bf16" else 4
 
 
 def hbm_rate(alg_bytes, ms):
@@ -341,6 +349,41 @@ def main():
         gplus[name] = sum(v) / len(v)
     del gate, g_out, g_y, g_dy, g_dg
 
+    # Query normalisation fused into the search (and its backward), measured
+    # on its own after the timed steps on the same queries.
+    idx_qn, w_qn = torch.empty_like(idx), torch.empty_like(w)
+    def search_qn():
+        pk.mem_search_qnorm(q, K, k, 1e-5, idx_out=idx_qn, w_out=w_qn, want_score=False,
+                            workspace=ws_s)
+    search_qn()
+    torch.cuda.synchronize()
+    pk.mem_timer_start("qnorm", "score_topk", "cartesian")
+    for _ in range(args.steps):
+        search_qn()
+    torch.cuda.synchronize()
+    pk.mem_timer_stop()
+    qn = {}
+    for pos, ms in pk.mem_timer_read():
+        qn.setdefault(("qnorm", "score_topk", "cartesian")[pos], []).append(ms)
+    qn = {kn: sum(v) / len(v) for kn, v in qn.items()}
+    gq = torch.empty((T, H, wl.n), dtype=torch.float32, device=dev)
+    gK = torch.zeros((H, 2, wl.S, wl.d), dtype=torch.float32, device=dev)
+    ws_sb = torch.empty(max(1, pk.load().mem_search_backward_workspace_size(T, H, wl.S, k)),
+                        dtype=torch.uint8, device=dev)
+    def sbwd_qn():
+        pk.mem_search_backward_qnorm(q, K, idx_qn, gz, 1e-5, grad_q=gq, grad_subkeys=gK,
+                                     workspace=ws_sb)
+    sbwd_qn()
+    torch.cuda.synchronize()
+    pk.mem_timer_start("qnorm", "search_backward")
+    for _ in range(args.steps):
+        sbwd_qn()
+    torch.cuda.synchronize()
+    pk.mem_timer_stop()
+    sbq = [ms for _, ms in pk.mem_timer_read()]
+    search_bwd_qn_ms = sum(sbq) / args.steps
+    del gq, gK, ws_sb, idx_qn, w_qn
+
     # touched rows of the last step's selection (outside the timed region)
     uniq, counts = torch.unique(idx.view(-1), return_counts=True)
     U = int(uniq.numel())
@@ -408,6 +451,13 @@ def main():
                                  traffic=measured_traffic("bag_forward_gated", wl.name)),
             "gate_backward": dict(hbm_rate(alg_cost("gate_backward", wl, U, esz)[1], gplus["gate_backward"]),
                                   traffic=measured_traffic("gate_backward", wl.name)),
+        },
+        "query_norm": {
+            "qnorm_ms": round(qn["qnorm"], 4),
+            "score_topk_ms": round(qn["score_topk"], 4),
+            "cartesian_ms": round(qn["cartesian"], 4),
+            "search_backward_ms": round(search_bwd_qn_ms, 4),
+            "qnorm": hbm_rate(alg_cost("qnorm", wl, U, esz)[1], qn["qnorm"]),
         },
         "stream_copy_GBps": round(copy_gbps, 1),
         "touched_rows": U,

@@ -126,6 +126,47 @@ int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pk
                         void* ws, size_t ws_bytes, pkmem_stream_t stream);
 
 /* ------------------------------------------------------------------------ *
+ * Search with query normalisation (qk-normalisation, Sec. 3.1.4: used for
+ * large memories whose training is unstable), fused in front of the scoring.
+ * Each query row q[t,h,:] is replaced by LayerNorm without affine parameters,
+ *   qhat = (q - mean) * rstd,  rstd = 1 / sqrt(var + eps),
+ * mean and biased variance over the n elements in fp32 (rstd = 0 where
+ * var + eps == 0), qhat rounded to q_dt (nearest, ties to even) and then
+ * searched exactly as mem_search does.  The normalised queries are formed in
+ * registers by the scoring kernel; nothing of size [T, H, n] is written unless
+ * asked for.
+ *   eps          >= 0 and finite (LayerNorm's customary value is 1e-5).
+ *   qhat_out     [T, H, n] dtype q_dt, 16-byte aligned: the normalised queries
+ *                as scored; may be NULL.
+ *   stats_out    [T, H, 2] fp32: (mean, rstd) per query; may be NULL.
+ *   Everything else as for mem_search (same workspace size function).
+ * ------------------------------------------------------------------------ */
+int mem_search_qnorm(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                     int64_t T, int H, int n, int S, int k, float eps,
+                     int64_t* idx_out, float* w_out, float* score_out, int32_t* half_idx_out,
+                     void* qhat_out, float* stats_out,
+                     void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * Search backward through the query normalisation of mem_search_qnorm (same
+ * q, eps and selection).  The statistics are recomputed from q, bitwise as
+ * the forward computed them.  With g = dL/dqhat (mem_search_backward's
+ * grad_q formula at qhat):
+ *   grad_q        [T, H, n] fp32, written: rstd * (g - mean(g) - xhat * mean(g * xhat)),
+ *                 xhat = (q - mean) * rstd in fp32 (the rounding of qhat to q_dt
+ *                 passes the gradient unchanged);
+ *   grad_subkeys  [H, 2, S, n/2] fp32, ACCUMULATED: mem_search_backward's sum with
+ *                 qhat (as scored) in place of q; bitwise deterministic.
+ * Limits, workspace (mem_search_backward_workspace_size) and errors as for
+ * mem_search_backward; eps as for mem_search_qnorm.
+ * ------------------------------------------------------------------------ */
+int mem_search_backward_qnorm(const void* q, pkmem_dtype q_dt, const void* subkeys,
+                              pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k, float eps,
+                              const int64_t* idx, const float* grad_scores, float* grad_q,
+                              float* grad_subkeys, void* ws, size_t ws_bytes,
+                              pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
  * Weighted EmbeddingBag forward, sum mode (Sec. 3, Eq. (1) y = s V_I; Sec. 3.1.4).
  *
  *   values [N, D]   value table, dtype v_dt; D % 8 == 0.
@@ -209,8 +250,9 @@ int mem_bag_backward_sparse(const void* dy, const void* values, pkmem_dtype v_dt
  * mem_timer_start(kernels) takes a comma-separated list of kernel names and
  * makes the library record a HIP event pair on the launch stream around every
  * following launch of a listed kernel:
- *   "score_topk", "cartesian"              (mem_search)
- *   "search_backward"                      (mem_search_backward)
+ *   "score_topk", "cartesian"              (mem_search, mem_search_qnorm)
+ *   "qnorm"                                (mem_search_qnorm, mem_search_backward_qnorm)
+ *   "search_backward"                      (mem_search_backward[_qnorm])
  *   "bag_forward"                          (mem_bag_forward, mem_bag_forward_gated)
  *   "gate_backward"                        (mem_gate_backward)
  *   "bag_backward_atomic", "sort_by_row",

@@ -19,7 +19,8 @@ import os
 import torch  # noqa: F401  (first: the library binds to the HIP runtime torch loads)
 
 __all__ = [
-    "PkmemError", "load", "lib_path", "mem_search", "mem_search_backward", "mem_bag_forward",
+    "PkmemError", "load", "lib_path", "mem_search", "mem_search_backward", "mem_search_qnorm",
+    "mem_search_backward_qnorm", "mem_bag_forward",
     "mem_bag_forward_gated", "mem_gate_backward",
     "mem_bag_backward",
     "mem_bag_backward_sparse", "mem_search_workspace_size", "mem_bag_backward_workspace_size",
@@ -60,6 +61,13 @@ def load() -> ctypes.CDLL:
     L.mem_search_backward_workspace_size.restype = SZ
     L.mem_search_backward.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, SZ, P]
     L.mem_search_backward.restype = I32
+    F32 = ctypes.c_float
+    L.mem_search_qnorm.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, F32, P, P, P, P, P, P,
+                                   P, SZ, P]
+    L.mem_search_qnorm.restype = I32
+    L.mem_search_backward_qnorm.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, F32, P, P, P,
+                                            P, P, SZ, P]
+    L.mem_search_backward_qnorm.restype = I32
     L.mem_bag_forward.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P]
     L.mem_bag_forward.restype = I32
     L.mem_bag_forward_gated.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P, P, P]
@@ -163,6 +171,29 @@ def mem_search(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None, 
     Returns (idx int64 [T,H,k], w fp32 [T,H,k], score fp32 [T,H,k] or None,
     half_idx int32 [T,H,2,k] or None).
     """
+    return _search(q, subkeys, k, None, idx_out, w_out, score_out, half_idx_out, want_score,
+                   want_half, None, None, workspace, stream)[:4]
+
+
+def mem_search_qnorm(q: torch.Tensor, subkeys: torch.Tensor, k: int, eps: float = 1e-5, *,
+                     idx_out=None, w_out=None, score_out=None, half_idx_out=None,
+                     want_score: bool = True, want_half: bool = False, qhat_out=None,
+                     stats_out=None, want_qhat: bool = False, want_stats: bool = False,
+                     workspace=None, stream=None):
+    """mem_search of the LayerNorm-normalised queries (no affine, eps), the
+    normalisation fused into the scoring.  Returns (idx, w, score, half_idx,
+    qhat [T,H,n] in q's dtype or None, stats fp32 [T,H,2] (mean, rstd) or None)."""
+    T, H, n = q.shape
+    if qhat_out is None and want_qhat:
+        qhat_out = torch.empty((T, H, n), dtype=q.dtype, device=q.device)
+    if stats_out is None and want_stats:
+        stats_out = torch.empty((T, H, 2), dtype=torch.float32, device=q.device)
+    return _search(q, subkeys, k, float(eps), idx_out, w_out, score_out, half_idx_out, want_score,
+                   want_half, qhat_out, stats_out, workspace, stream)
+
+
+def _search(q, subkeys, k, eps, idx_out, w_out, score_out, half_idx_out, want_score, want_half,
+            qhat_out, stats_out, workspace, stream):
     L = load()
     _dev(q, subkeys)
     T, H, n = q.shape
@@ -179,10 +210,17 @@ def mem_search(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None, 
     _dev(idx_out, w_out, score_out, half_idx_out)
     nbytes = mem_search_workspace_size(T, H, S, k)
     ws = _workspace(nbytes, dev, workspace)
-    _check(L.mem_search(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
-                        _ptr(idx_out), _ptr(w_out), _ptr(score_out), _ptr(half_idx_out),
-                        _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
-    return idx_out, w_out, score_out, half_idx_out
+    if eps is None:
+        _check(L.mem_search(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
+                            _ptr(idx_out), _ptr(w_out), _ptr(score_out), _ptr(half_idx_out),
+                            _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+    else:
+        _dev(qhat_out, stats_out)
+        _check(L.mem_search_qnorm(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k, eps,
+                                  _ptr(idx_out), _ptr(w_out), _ptr(score_out), _ptr(half_idx_out),
+                                  _ptr(qhat_out), _ptr(stats_out), _ptr(ws),
+                                  ws.numel() * ws.element_size(), _stream(stream)))
+    return idx_out, w_out, score_out, half_idx_out, qhat_out, stats_out
 
 
 def mem_search_backward(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tensor,
@@ -192,6 +230,23 @@ def mem_search_backward(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tenso
     """Gradients of the selected scores into q ([T,H,n], written) and the
     sub-keys ([H,2,S,n/2], ACCUMULATED; a zero table is allocated if none is
     given).  Returns (grad_q, grad_subkeys)."""
+    return _search_backward(q, subkeys, idx, grad_scores, None, grad_q, grad_subkeys, want_grad_q,
+                            want_grad_subkeys, workspace, stream)
+
+
+def mem_search_backward_qnorm(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tensor,
+                              grad_scores: torch.Tensor, eps: float = 1e-5, *, grad_q=None,
+                              grad_subkeys=None, want_grad_q: bool = True,
+                              want_grad_subkeys: bool = True, workspace=None, stream=None):
+    """mem_search_backward through the query normalisation of
+    mem_search_qnorm (same q and eps): grad_q with respect to the raw
+    queries, grad_subkeys accumulated from the normalised ones."""
+    return _search_backward(q, subkeys, idx, grad_scores, float(eps), grad_q, grad_subkeys,
+                            want_grad_q, want_grad_subkeys, workspace, stream)
+
+
+def _search_backward(q, subkeys, idx, grad_scores, eps, grad_q, grad_subkeys, want_grad_q,
+                     want_grad_subkeys, workspace, stream):
     L = load()
     _dev(q, subkeys, idx, grad_scores)
     T, H, n = q.shape
@@ -204,9 +259,14 @@ def mem_search_backward(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tenso
     _dev(grad_q, grad_subkeys)
     nbytes = int(L.mem_search_backward_workspace_size(T, H, S, k))
     ws = _workspace(nbytes, q.device, workspace)
-    _check(L.mem_search_backward(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
-                                 _ptr(idx), _ptr(grad_scores), _ptr(grad_q), _ptr(grad_subkeys),
-                                 _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+    args = (_ptr(idx), _ptr(grad_scores), _ptr(grad_q), _ptr(grad_subkeys), _ptr(ws),
+            ws.numel() * ws.element_size(), _stream(stream))
+    if eps is None:
+        _check(L.mem_search_backward(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
+                                     *args))
+    else:
+        _check(L.mem_search_backward_qnorm(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n,
+                                           S, k, eps, *args))
     return grad_q, grad_subkeys
 
 

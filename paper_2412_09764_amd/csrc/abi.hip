@@ -41,6 +41,7 @@ struct SearchWs {
   int32_t* half_idx;
   float* half_score;
   uint32_t* ovf;
+  float2* qstats;  // per (token, head) query (mean, rstd) when normalising
   size_t bytes;
 };
 
@@ -57,6 +58,8 @@ SearchWs search_ws(void* base, int64_t T, int H, int k) {
   off += align256(rows * k * sizeof(float));
   w.ovf = reinterpret_cast<uint32_t*>(p + off);
   off += align256((rows + 1) * sizeof(uint32_t));
+  w.qstats = reinterpret_cast<float2*>(p + off);
+  off += align256((size_t)T * H * sizeof(float2));
   w.bytes = off;
   return w;
 }
@@ -303,13 +306,19 @@ size_t mem_search_workspace_size(int64_t T, int H, int S, int k) {
   return search_ws(nullptr, T, H, k).bytes;
 }
 
-int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt, int64_t T,
-               int H, int n, int S, int k, int64_t* idx_out, float* w_out, float* score_out,
-               int32_t* half_idx_out, void* ws, size_t ws_bytes, pkmem_stream_t stream) {
-  const char* fn = "mem_search";
+// The search, with the queries normalised (qnorm) or not.
+static int search_common(const char* fn, const void* q, pkmem_dtype q_dt, const void* subkeys,
+                         pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k, bool qnorm,
+                         float eps, int64_t* idx_out, float* w_out, float* score_out,
+                         int32_t* half_idx_out, void* qhat_out, float* stats_out, void* ws,
+                         size_t ws_bytes, pkmem_stream_t stream) {
   int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k);
   if (rc) return rc;
   if (T > 0 && (!idx_out || !w_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (qnorm && !(eps >= 0.f && eps <= 3.0e38f))
+    return fail(PKMEM_ERR_INVALID, "%s: eps must be finite and >= 0", fn);
+  if (!aligned(qhat_out, 16) || !aligned(stats_out, 8))
+    return fail(PKMEM_ERR_INVALID, "%s: qhat_out must be 16-byte and stats_out 8-byte aligned", fn);
   const SearchWs need = search_ws(nullptr, T, H, k);
   if (!ws || ws_bytes < need.bytes)
     return fail(PKMEM_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need.bytes, ws ? ws_bytes : (size_t)0);
@@ -317,29 +326,56 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
   if (T == 0) return PKMEM_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   SearchWs w = search_ws(ws, T, H, k);
+  const bool bf16 = q_dt == PKMEM_BF16;
+  float2* qstats = nullptr;
+  hipError_t e = hipSuccess;
+  if (qnorm) {
+    qstats = stats_out ? reinterpret_cast<float2*>(stats_out) : w.qstats;
+    e = pk::launch_qnorm(bf16, q, T * H, n, eps, qstats, qhat_out, st);
+    if (e != hipSuccess) return hip_status(e, fn);
+  }
   int32_t* hidx = half_idx_out ? half_idx_out : w.half_idx;
-  hipError_t e = pk::launch_search_half(q_dt == PKMEM_BF16, q, subkeys, T, H, n, S, k, w.cand, hidx,
-                                        w.half_score, w.ovf, st);
+  e = pk::launch_search_half(bf16, q, subkeys, T, H, n, S, k, qstats, w.cand, hidx, w.half_score,
+                             w.ovf, st);
   if (e != hipSuccess) return hip_status(e, fn);
   e = pk::launch_cartesian(hidx, w.half_score, T, H, S, k, idx_out, w_out, score_out, st);
   if (e != hipSuccess) return hip_status(e, fn);
   return PKMEM_OK;
 }
 
+int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt, int64_t T,
+               int H, int n, int S, int k, int64_t* idx_out, float* w_out, float* score_out,
+               int32_t* half_idx_out, void* ws, size_t ws_bytes, pkmem_stream_t stream) {
+  return search_common("mem_search", q, q_dt, subkeys, k_dt, T, H, n, S, k, false, 0.f, idx_out,
+                       w_out, score_out, half_idx_out, nullptr, nullptr, ws, ws_bytes, stream);
+}
+
+int mem_search_qnorm(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                     int64_t T, int H, int n, int S, int k, float eps, int64_t* idx_out,
+                     float* w_out, float* score_out, int32_t* half_idx_out, void* qhat_out,
+                     float* stats_out, void* ws, size_t ws_bytes, pkmem_stream_t stream) {
+  return search_common("mem_search_qnorm", q, q_dt, subkeys, k_dt, T, H, n, S, k, true, eps,
+                       idx_out, w_out, score_out, half_idx_out, qhat_out, stats_out, ws, ws_bytes,
+                       stream);
+}
+
 size_t mem_search_backward_workspace_size(int64_t T, int H, int S, int k) {
   (void)S;
   if (T < 0 || H < 1 || k < 1) return 0;
-  return pk::search_backward_ws_bytes(T, H, k);
+  // the sort and its inputs, then the queries' (mean, rstd) for the normalised variant
+  return pk::search_backward_ws_bytes(T, H, k) + align256((size_t)T * H * sizeof(float2));
 }
 
-int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
-                        int64_t T, int H, int n, int S, int k, const int64_t* idx,
-                        const float* grad_scores, float* grad_q, float* grad_subkeys, void* ws,
-                        size_t ws_bytes, pkmem_stream_t stream) {
-  const char* fn = "mem_search_backward";
+static int search_backward_common(const char* fn, const void* q, pkmem_dtype q_dt,
+                                  const void* subkeys, pkmem_dtype k_dt, int64_t T, int H, int n,
+                                  int S, int k, bool qnorm, float eps, const int64_t* idx,
+                                  const float* grad_scores, float* grad_q, float* grad_subkeys,
+                                  void* ws, size_t ws_bytes, pkmem_stream_t stream) {
   int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k);
   if (rc) return rc;
   if (T > 0 && (!idx || !grad_scores)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (qnorm && !(eps >= 0.f && eps <= 3.0e38f))
+    return fail(PKMEM_ERR_INVALID, "%s: eps must be finite and >= 0", fn);
   if (2 * T * (int64_t)H * k >= (int64_t(1) << 32))
     return fail(PKMEM_ERR_UNSUPPORTED, "%s: 2*T*H*k must be < 2^32", fn);
   if (2 * (int64_t)H * S >= (int64_t(1) << 31))
@@ -351,12 +387,39 @@ int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pk
     return fail(PKMEM_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : (size_t)0);
   if (!aligned(ws, 256)) return fail(PKMEM_ERR_INVALID, "%s: workspace must be 256-byte aligned", fn);
   if (T == 0 || (!grad_q && !grad_subkeys)) return PKMEM_OK;
-  rc = check_indices(fn, idx, T * H * k, (int64_t)S * S, reinterpret_cast<hipStream_t>(stream));
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  rc = check_indices(fn, idx, T * H * k, (int64_t)S * S, st);
   if (rc) return rc;
-  hipError_t e = pk::launch_search_backward(q_dt == PKMEM_BF16, q, subkeys, T, H, n, S, k, idx,
-                                            grad_scores, grad_q, grad_subkeys, ws,
-                                            reinterpret_cast<hipStream_t>(stream));
+  const bool bf16 = q_dt == PKMEM_BF16;
+  float2* qstats = nullptr;
+  if (qnorm) {
+    qstats = reinterpret_cast<float2*>(reinterpret_cast<char*>(ws) +
+                                       pk::search_backward_ws_bytes(T, H, k));
+    hipError_t e = pk::launch_qnorm(bf16, q, T * H, n, eps, qstats, nullptr, st);
+    if (e != hipSuccess) return hip_status(e, fn);
+  }
+  hipError_t e = pk::launch_search_backward(bf16, q, subkeys, T, H, n, S, k, idx, grad_scores,
+                                            qstats, grad_q, grad_subkeys, ws, st);
   return hip_status(e, fn);
+}
+
+int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                        int64_t T, int H, int n, int S, int k, const int64_t* idx,
+                        const float* grad_scores, float* grad_q, float* grad_subkeys, void* ws,
+                        size_t ws_bytes, pkmem_stream_t stream) {
+  return search_backward_common("mem_search_backward", q, q_dt, subkeys, k_dt, T, H, n, S, k,
+                                false, 0.f, idx, grad_scores, grad_q, grad_subkeys, ws, ws_bytes,
+                                stream);
+}
+
+int mem_search_backward_qnorm(const void* q, pkmem_dtype q_dt, const void* subkeys,
+                              pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k, float eps,
+                              const int64_t* idx, const float* grad_scores, float* grad_q,
+                              float* grad_subkeys, void* ws, size_t ws_bytes,
+                              pkmem_stream_t stream) {
+  return search_backward_common("mem_search_backward_qnorm", q, q_dt, subkeys, k_dt, T, H, n, S,
+                                k, true, eps, idx, grad_scores, grad_q, grad_subkeys, ws,
+                                ws_bytes, stream);
 }
 
 int mem_bag_forward(const void* values, pkmem_dtype v_dt, int64_t N, int D, const int64_t* idx,

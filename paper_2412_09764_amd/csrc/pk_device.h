@@ -99,6 +99,16 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
 }
 
+// Query normalisation (LayerNorm without affine): (x - mean) * rstd in fp32.
+// Every kernel that needs a normalised query element computes it with this
+// one expression, so the forward and the backward see the same bits.
+__device__ __forceinline__ float qn_apply(float x, float mean, float rstd) {
+  return (x - mean) * rstd;
+}
+__device__ __forceinline__ float round_bf16_f32(float v) {
+  return __uint_as_float(f32_to_bf16_bits(v) << 16);
+}
+
 // --------------------------------------------------- ordered 64-bit keys ----
 // A selection key orders (score descending, index ascending) as one unsigned
 // 64-bit integer, larger = better: the high word is the score mapped to an

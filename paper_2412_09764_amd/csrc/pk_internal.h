@@ -39,9 +39,16 @@ int cartesian_pairs(int k);
 // ---- search (search.hip) -------------------------------------------------
 // rows = T*H*2 (token, head, half) rows; cand = [rows, CAND_CAP] u64;
 // ovf = [1 + rows] u32 (count, then overflowed row ids).
+// qstats (nullable) = per (token, head) query (mean, rstd): the scoring then
+// normalises the queries as it loads them (see launch_qnorm).
 hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
-                              int n, int S, int k, uint64_t* cand, int32_t* half_idx,
-                              float* half_score, uint32_t* ovf, hipStream_t st);
+                              int n, int S, int k, const float2* qstats, uint64_t* cand,
+                              int32_t* half_idx, float* half_score, uint32_t* ovf,
+                              hipStream_t st);
+// LayerNorm statistics of rows = T*H queries of n elements into stats, and
+// (qhat non-null) the normalised queries in the query dtype.
+hipError_t launch_qnorm(bool bf16, const void* q, int64_t rows, int n, float eps, float2* stats,
+                        void* qhat, hipStream_t st);
 hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T, int H,
                             int S, int k, int64_t* idx_out, float* w_out, float* score_out,
                             hipStream_t st);
@@ -54,9 +61,13 @@ hipError_t sort_u32_segments(int64_t Lmax, const uint32_t* Ldev, int key_bits, v
                              const uint32_t** nseg, hipStream_t st);
 size_t scan_scratch_u32(int64_t n);
 hipError_t scan_exclusive_u32(uint32_t* data, int64_t n, uint32_t* sums, hipStream_t st);
+// qstats (nullable): the queries were normalised in the forward (their
+// (mean, rstd) from launch_qnorm); grad_q is then taken through the
+// normalisation and grad_K uses the normalised queries as scored.
 hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
                                   int n, int S, int k, const int64_t* idx, const float* gz,
-                                  float* grad_q, float* grad_K, void* ws, hipStream_t st);
+                                  const float2* qstats, float* grad_q, float* grad_K, void* ws,
+                                  hipStream_t st);
 
 // ---- bag (bag.hip) ---------------------------------------------------------
 hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_t* idx,

@@ -25,6 +25,11 @@
 //   * Pass 3 sorts each row's candidates with a wave bitonic sort and writes the
 //     first k.  A row whose lane half overflowed its CAND_CAP / 2 slots (heavy
 //     ties) is listed for k_topk_fallback, which rescans it exactly.
+//   * With query normalisation (qk-normalisation, Sec. 3.1.4) k_qnorm first
+//     computes each (token, head) query's mean and rstd = 1/sqrt(var + eps)
+//     (LayerNorm without affine, fp32, centred second pass); the scoring
+//     kernel normalises its query fragments as it loads them and rounds them
+//     to the query dtype, so the normalised queries never go through memory.
 // Step 2, k_cartesian: per (token, head) the top k of the sums s1[a] + s2[b]
 //   over rank pairs with (a+1)(b+1) <= k (every other pair is beaten by at
 //   least k pairs), ordered (sum desc, composed index i1*S + i2 asc), then the
@@ -56,6 +61,16 @@ struct MfmaOp<uint16_t> {  // bf16 storage
   }
   __device__ static __forceinline__ frag zero() { return __builtin_bit_cast(frag, uint4{0, 0, 0, 0}); }
   __device__ static __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
+  __device__ static __forceinline__ float stored(float v) { return round_bf16_f32(v); }
+  // Normalised fragment, rounded to bf16 (nearest, ties to even).
+  __device__ static __forceinline__ frag normalize(frag f, float mean, float rstd) {
+    uint4 u = __builtin_bit_cast(uint4, f);
+    u.x = pack_bf16x2(qn_apply(bf16_lo(u.x), mean, rstd), qn_apply(bf16_hi(u.x), mean, rstd));
+    u.y = pack_bf16x2(qn_apply(bf16_lo(u.y), mean, rstd), qn_apply(bf16_hi(u.y), mean, rstd));
+    u.z = pack_bf16x2(qn_apply(bf16_lo(u.z), mean, rstd), qn_apply(bf16_hi(u.z), mean, rstd));
+    u.w = pack_bf16x2(qn_apply(bf16_lo(u.w), mean, rstd), qn_apply(bf16_hi(u.w), mean, rstd));
+    return __builtin_bit_cast(frag, u);
+  }
 };
 
 template <>
@@ -70,7 +85,63 @@ struct MfmaOp<float> {
   __device__ static __forceinline__ frag load(const void* p) { return *reinterpret_cast<const float*>(p); }
   __device__ static __forceinline__ frag zero() { return 0.f; }
   __device__ static __forceinline__ float to_f32(float v) { return v; }
+  __device__ static __forceinline__ float stored(float v) { return v; }
+  __device__ static __forceinline__ frag normalize(frag f, float mean, float rstd) {
+    return qn_apply(f, mean, rstd);
+  }
 };
+
+// Per (token, head) query of n elements (n * esize <= 1 KiB): mean and
+// rstd = 1 / sqrt(var + eps) of LayerNorm without affine (biased variance,
+// fp32, centred second pass; rstd = 0 where var + eps == 0), one wave per
+// query, lane l holding the 16-byte chunk l.  qhat (optional) receives the
+// normalised query rounded to the query dtype, exactly as the scoring uses it.
+template <typename T>
+__global__ __launch_bounds__(256) void k_qnorm(const T* __restrict__ q, int64_t rows, int n,
+                                               float eps, float2* __restrict__ stats,
+                                               T* __restrict__ qhat) {
+  constexpr int EPL = 16 / (int)sizeof(T);
+  using M = MfmaOp<T>;
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;  // whole wave
+  const bool has = lane * EPL < n;
+  float x[EPL];
+  {
+    const uint4 raw = has ? ld16(q + r * n + lane * EPL) : uint4{0, 0, 0, 0};
+    const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) x[i] = M::to_f32(e[i]);
+  }
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) sum += x[i];
+  sum = group_sum<WAVE>(sum);
+  const float mean = sum / (float)n;
+  float sq = 0.f;
+  if (has) {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const float c = x[i] - mean;
+      sq = fmaf(c, c, sq);
+    }
+  }
+  sq = group_sum<WAVE>(sq);
+  const float ve = sq / (float)n + eps;
+  const float rstd = ve > 0.f ? 1.f / sqrtf(ve) : 0.f;
+  if (lane == 0) stats[r] = make_float2(mean, rstd);
+  if (qhat && has) {
+    uint4 o;
+    T* e = reinterpret_cast<T*>(&o);
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const float v = M::stored(qn_apply(x[i], mean, rstd));
+      if constexpr (sizeof(T) == 2) e[i] = (T)(__float_as_uint(v) >> 16);
+      else e[i] = v;
+    }
+    *reinterpret_cast<uint4*>(qhat + r * n + lane * EPL) = o;
+  }
+}
 
 // Row of the 32x32 MFMA result held in accumulator slot j of a lane whose
 // upper-half bit is kh (columns are lane & 31).
@@ -79,8 +150,8 @@ __device__ __forceinline__ int acc_row(int j, int kh) { return 8 * (j >> 2) + 4 
 template <typename T, int NSTEP>
 __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
     const T* __restrict__ q, const T* __restrict__ subkeys, int64_t ntok, int H, int n, int S,
-    int k, uint64_t* __restrict__ cand, int32_t* __restrict__ half_idx,
-    float* __restrict__ half_score, uint32_t* __restrict__ ovf) {
+    int k, const float2* __restrict__ qstats, uint64_t* __restrict__ cand,
+    int32_t* __restrict__ half_idx, float* __restrict__ half_score, uint32_t* __restrict__ ovf) {
   using M = MfmaOp<T>;
   constexpr int DPAD = NSTEP * M::KSTEP;      // padded half dim
   constexpr int RB = DPAD * M::ESIZE;         // bytes per sub-key row in LDS
@@ -110,14 +181,20 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   const T* kbase = subkeys + (size_t)hp * S * d;
 
   // Queries of this lane's token, as B fragments: lane supplies reduction
-  // elements [s*KSTEP + kh*LANE_K, +LANE_K) of column `col`.
+  // elements [s*KSTEP + kh*LANE_K, +LANE_K) of column `col`; normalised here
+  // when qstats holds the queries' (mean, rstd).
   typename M::frag bq[NSTEP];
   {
-    const T* qrow = q + ((size_t)(tok_ok ? tok : 0) * H + h) * n + (size_t)p * d;
+    const size_t qr = (size_t)(tok_ok ? tok : 0) * H + h;
+    const T* qrow = q + qr * n + (size_t)p * d;
+    const float2 qs = (qstats && tok_ok) ? qstats[qr] : make_float2(0.f, 1.f);
 #pragma unroll
     for (int s = 0; s < NSTEP; ++s) {
       const int e0 = s * M::KSTEP + kh * M::LANE_K;
-      bq[s] = (tok_ok && e0 + M::LANE_K <= d) ? M::load(qrow + e0) : M::zero();
+      const bool ld = tok_ok && e0 + M::LANE_K <= d;
+      typename M::frag f = ld ? M::load(qrow + e0) : M::zero();
+      if (qstats && ld) f = M::normalize(f, qs.x, qs.y);
+      bq[s] = f;
     }
   }
 
@@ -315,11 +392,14 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
 template <typename T>
 __global__ __launch_bounds__(256) void k_topk_fallback(const T* __restrict__ q,
                                                        const T* __restrict__ subkeys, int H, int n,
-                                                       int S, int k, const uint32_t* __restrict__ ovf,
+                                                       int S, int k,
+                                                       const float2* __restrict__ qstats,
+                                                       const uint32_t* __restrict__ ovf,
                                                        int32_t* __restrict__ half_idx,
                                                        float* __restrict__ half_score) {
   extern __shared__ float sc[];  // S scores
   __shared__ uint64_t red[4];
+  __shared__ float qv[256];      // the row's query half as scored (d <= 256)
   using M = MfmaOp<T>;
   const int d = n >> 1;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -331,9 +411,18 @@ __global__ __launch_bounds__(256) void k_topk_fallback(const T* __restrict__ q,
     const size_t t = (r >> 1) / (size_t)H;
     const T* qrow = q + (t * H + h) * (size_t)n + (size_t)p * d;
     const T* kb = subkeys + (size_t)(h * 2 + p) * S * d;
+    if (tid < d) {
+      float v = M::to_f32(qrow[tid]);
+      if (qstats) {
+        const float2 qs = qstats[t * H + h];
+        v = M::stored(qn_apply(v, qs.x, qs.y));
+      }
+      qv[tid] = v;
+    }
+    __syncthreads();
     for (int s = tid; s < S; s += 256) {
       float acc = 0.f;
-      for (int e = 0; e < d; ++e) acc = fmaf(M::to_f32(qrow[e]), M::to_f32(kb[(size_t)s * d + e]), acc);
+      for (int e = 0; e < d; ++e) acc = fmaf(qv[e], M::to_f32(kb[(size_t)s * d + e]), acc);
       sc[s] = acc;
     }
     __syncthreads();
@@ -416,43 +505,59 @@ int cartesian_pairs(int k) {
 
 template <typename T, int NSTEP>
 static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, int H, int n, int S,
-                               int k, uint64_t* cand, int32_t* half_idx, float* half_score,
-                               uint32_t* ovf, hipStream_t st) {
+                               int k, const float2* qstats, uint64_t* cand, int32_t* half_idx,
+                               float* half_score, uint32_t* ovf, hipStream_t st) {
   const int64_t tiles = (T_ + SEARCH_TOK - 1) / SEARCH_TOK;
   const int64_t blocks = tiles * 2 * H;
   {
     LaunchTimer lt("score_topk", st);
     hipLaunchKernelGGL((k_score_topk<T, NSTEP>), dim3((unsigned)blocks), dim3(64 * SEARCH_WAVES), 0, st,
-                       (const T*)q, (const T*)subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf);
+                       (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats, cand, half_idx,
+                       half_score, ovf);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds = (size_t)S * sizeof(float);
   hipLaunchKernelGGL((k_topk_fallback<T>), dim3(256), dim3(256), lds, st, (const T*)q,
-                     (const T*)subkeys, H, n, S, k, (const uint32_t*)ovf, half_idx, half_score);
+                     (const T*)subkeys, H, n, S, k, qstats, (const uint32_t*)ovf, half_idx, half_score);
+  return hipGetLastError();
+}
+
+hipError_t launch_qnorm(bool bf16, const void* q, int64_t rows, int n, float eps, float2* stats,
+                       void* qhat, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  LaunchTimer lt("qnorm", st);
+  const dim3 g((unsigned)((rows + 3) / 4)), b(256);
+  if (bf16)
+    hipLaunchKernelGGL(k_qnorm<uint16_t>, g, b, 0, st, (const uint16_t*)q, rows, n, eps, stats,
+                       (uint16_t*)qhat);
+  else
+    hipLaunchKernelGGL(k_qnorm<float>, g, b, 0, st, (const float*)q, rows, n, eps, stats,
+                       (float*)qhat);
   return hipGetLastError();
 }
 
 hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T_, int H,
-                              int n, int S, int k, uint64_t* cand, int32_t* half_idx,
-                              float* half_score, uint32_t* ovf, hipStream_t st) {
+                              int n, int S, int k, const float2* qstats, uint64_t* cand,
+                              int32_t* half_idx, float* half_score, uint32_t* ovf,
+                              hipStream_t st) {
   hipError_t e = launch_fill_u32(ovf, 0u, 1, st);
   if (e != hipSuccess) return e;
   const int d = n / 2;
   if (bf16) {
     const int steps = (d + 15) / 16;
-    if (steps <= 1) return launch_score<uint16_t, 1>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
-    if (steps <= 2) return launch_score<uint16_t, 2>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
-    if (steps <= 4) return launch_score<uint16_t, 4>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
-    if (steps <= 8) return launch_score<uint16_t, 8>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
-    return launch_score<uint16_t, 16>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+    if (steps <= 1) return launch_score<uint16_t, 1>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+    if (steps <= 2) return launch_score<uint16_t, 2>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+    if (steps <= 4) return launch_score<uint16_t, 4>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+    if (steps <= 8) return launch_score<uint16_t, 8>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+    return launch_score<uint16_t, 16>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
   }
   const int steps = (d + 1) / 2;
-  if (steps <= 2) return launch_score<float, 2>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
-  if (steps <= 4) return launch_score<float, 4>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
-  if (steps <= 8) return launch_score<float, 8>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
-  if (steps <= 16) return launch_score<float, 16>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
-  return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, cand, half_idx, half_score, ovf, st);
+  if (steps <= 2) return launch_score<float, 2>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+  if (steps <= 4) return launch_score<float, 4>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+  if (steps <= 8) return launch_score<float, 8>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+  if (steps <= 16) return launch_score<float, 16>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+  return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
 }
 
 hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T_, int H,

@@ -40,6 +40,19 @@ struct QQuad<uint16_t> {
     a[2] = fmaf(g, __uint_as_float(raw.y << 16), a[2]);
     a[3] = fmaf(g, __uint_as_float(raw.y & 0xffff0000u), a[3]);
   }
+  __device__ __forceinline__ void to_f32(float* v) const {
+    v[0] = __uint_as_float(raw.x << 16);
+    v[1] = __uint_as_float(raw.x & 0xffff0000u);
+    v[2] = __uint_as_float(raw.y << 16);
+    v[3] = __uint_as_float(raw.y & 0xffff0000u);
+  }
+  // The same with the normalised query as scored (rounded to bf16).
+  __device__ __forceinline__ void fma_into_norm(float g, float* a, float mean, float rstd) const {
+    float v[4];
+    to_f32(v);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = fmaf(g, round_bf16_f32(qn_apply(v[i], mean, rstd)), a[i]);
+  }
 };
 template <>
 struct QQuad<float> {
@@ -50,6 +63,15 @@ struct QQuad<float> {
     a[1] = fmaf(g, raw.y, a[1]);
     a[2] = fmaf(g, raw.z, a[2]);
     a[3] = fmaf(g, raw.w, a[3]);
+  }
+  __device__ __forceinline__ void to_f32(float* v) const {
+    v[0] = raw.x; v[1] = raw.y; v[2] = raw.z; v[3] = raw.w;
+  }
+  __device__ __forceinline__ void fma_into_norm(float g, float* a, float mean, float rstd) const {
+    a[0] = fmaf(g, qn_apply(raw.x, mean, rstd), a[0]);
+    a[1] = fmaf(g, qn_apply(raw.y, mean, rstd), a[1]);
+    a[2] = fmaf(g, qn_apply(raw.z, mean, rstd), a[2]);
+    a[3] = fmaf(g, qn_apply(raw.w, mean, rstd), a[3]);
   }
 };
 
@@ -62,6 +84,11 @@ struct QQuad<float> {
 //     keys (h*2 + half)*S + sub-key and group sums at slots rp*k + 0, 1, ...
 //     (in rank order of the leaders) and their number at counts[rp].  Lookups
 //     whose index lies outside [0, S*S) count as absent.
+// With qstats (the forward normalised the queries, LayerNorm without affine)
+// the two halves' gradients g with respect to the normalised query qhat stay
+// in registers and grad_q = rstd * (g - mean(g) - xhat * mean(g * xhat)) over
+// the query's n elements, xhat = (q - mean) * rstd in fp32 (the rounding of
+// qhat to the query dtype passes the gradient unchanged).
 #ifndef PK_SBWD_QU
 #define PK_SBWD_QU 8
 #endif
@@ -71,6 +98,7 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
                                                       int H, int n, int S, int k,
                                                       const int64_t* __restrict__ idx,
                                                       const float* __restrict__ gz,
+                                                      const float2* __restrict__ qstats,
                                                       float* __restrict__ grad_q,
                                                       uint32_t* __restrict__ keys,
                                                       float* __restrict__ gvals,
@@ -88,6 +116,7 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
   const bool okl = ix >= 0 && ix < (int64_t)S * S;
   const float g = okl ? gz[r * k + lane] : 0.f;
   const uint64_t below = (1ull << lane) - 1ull;
+  float gh[2][4];  // with qstats: both halves' gradients with respect to qhat
 
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
@@ -133,9 +162,44 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
 #pragma unroll
         for (int j = 0; j < QU; ++j) kq[j].fma_into(gg[j], acc);
       }
-      if (qlane)
+      if (qstats) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) gh[p][i] = qlane ? acc[i] : 0.f;
+      } else if (qlane) {
         *reinterpret_cast<float4*>(grad_q + r * n + (size_t)p * d + ql) =
             make_float4(acc[0], acc[1], acc[2], acc[3]);
+      }
+    }
+  }
+  if (qstats && grad_q) {
+    const float2 st = qstats[r];
+    float xh[2][4];
+    float sg = 0.f, sgx = 0.f;
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      QQuad<T> xq;
+      xq.load(q + r * n + (size_t)p * d + ql);
+      float v[4];
+      xq.to_f32(v);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        xh[p][i] = qlane ? qn_apply(v[i], st.x, st.y) : 0.f;
+        sg += gh[p][i];
+        sgx = fmaf(gh[p][i], xh[p][i], sgx);
+      }
+    }
+    sg = group_sum<WAVE>(sg);
+    sgx = group_sum<WAVE>(sgx);
+    const float mg = sg / (float)n, mgx = sgx / (float)n;
+    if (qlane) {
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        float o[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = st.y * (gh[p][i] - mg - xh[p][i] * mgx);
+        *reinterpret_cast<float4*>(grad_q + r * n + (size_t)p * d + ql) =
+            make_float4(o[0], o[1], o[2], o[3]);
+      }
     }
   }
 }
@@ -163,9 +227,10 @@ __global__ __launch_bounds__(256) void k_sbwd_pack(const uint32_t* __restrict__ 
 // are taken 64 at a time and consumed in order, QU at a time, with their
 // query-quad loads issued together; the sum is added into the sub-key row with
 // one read-modify-write.
-template <typename T>
+template <typename T, bool QN>
 __global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, int H, int n,
                                                        int S, int k,
+                                                       const float2* __restrict__ qstats,
                                                        const float* __restrict__ gvals,
                                                        const uint32_t* __restrict__ ks,
                                                        const uint32_t* __restrict__ vs,
@@ -194,10 +259,12 @@ __global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, 
       const uint32_t x = ok ? vs[e] : 0u;
       const uint32_t t = x / hk2;
       const float gx = ok ? gvals[x] : 0.f;
+      float2 st = make_float2(0.f, 1.f);
+      if constexpr (QN) st = qstats[(size_t)t * H + h];
       const uint32_t cnt = (s1 - b0) < 64u ? (s1 - b0) : 64u;
       for (uint32_t j0 = 0; j0 < cnt; j0 += QU) {
         QQuad<T> qq[QU];
-        float gg[QU];
+        float gg[QU], mj[QU], rj[QU];
 #pragma unroll
         for (int j = 0; j < QU; ++j) {
           const bool has = j0 + j < cnt;
@@ -205,10 +272,17 @@ __global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, 
           const uint32_t tj = (uint32_t)__builtin_amdgcn_readlane((int)t, L);
           const float xj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), L));
           gg[j] = has ? xj : 0.f;
+          if constexpr (QN) {
+            mj[j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.x), L));
+            rj[j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.y), L));
+          }
           qq[j].load(qh + (size_t)tj * H * n);
         }
 #pragma unroll
-        for (int j = 0; j < QU; ++j) qq[j].fma_into(gg[j], acc);
+        for (int j = 0; j < QU; ++j) {
+          if constexpr (QN) qq[j].fma_into_norm(gg[j], acc, mj[j], rj[j]);
+          else qq[j].fma_into(gg[j], acc);
+        }
       }
     }
     if (qlane) {
@@ -233,8 +307,8 @@ size_t search_backward_ws_bytes(int64_t T, int H, int k) {
 
 template <typename T>
 static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, int H, int n, int S,
-                              int k, const int64_t* idx, const float* gz, float* grad_q,
-                              float* grad_K, void* ws, hipStream_t st) {
+                              int k, const int64_t* idx, const float* gz, const float2* qstats,
+                              float* grad_q, float* grad_K, void* ws, hipStream_t st) {
   LaunchTimer lt("search_backward", st);
   const int64_t rows = 2 * T_ * H;
   const int64_t np = rows * k;
@@ -252,7 +326,7 @@ static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, in
   if (grad_K) e = launch_fill_u32(offs + rows, 0u, 1, st);  // the scan's last entry
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_search_bwd_q<T>, dim3((unsigned)(((T_ + 3) / 4) * H)), dim3(256), 0, st,
-                     (const T*)q, (const T*)subkeys, T_, H, n, S, k, idx, gz, grad_q,
+                     (const T*)q, (const T*)subkeys, T_, H, n, S, k, idx, gz, qstats, grad_q,
                      grad_K ? keys : nullptr, grad_K ? gvals : nullptr, grad_K ? offs : nullptr);
   e = hipGetLastError();
   if (e != hipSuccess || !grad_K) return e;
@@ -274,17 +348,23 @@ static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, in
   int64_t maxseg = (int64_t)nbins < np ? (int64_t)nbins : np;
   int64_t blocks = (maxseg + 3) / 4;
   if (blocks > 16384) blocks = 16384;
-  hipLaunchKernelGGL(k_sbwd_segments<T>, dim3((unsigned)blocks), dim3(256), 0, st, (const T*)q, H, n,
-                     S, k, gvals, ks, vs, seg, nseg, grad_K);
+  if (qstats)
+    hipLaunchKernelGGL((k_sbwd_segments<T, true>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const T*)q, H, n, S, k, qstats, gvals, ks, vs, seg, nseg, grad_K);
+  else
+    hipLaunchKernelGGL((k_sbwd_segments<T, false>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const T*)q, H, n, S, k, qstats, gvals, ks, vs, seg, nseg, grad_K);
   return hipGetLastError();
 }
 
 hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
                                   int n, int S, int k, const int64_t* idx, const float* gz,
-                                  float* grad_q, float* grad_K, void* ws, hipStream_t st) {
+                                  const float2* qstats, float* grad_q, float* grad_K, void* ws,
+                                  hipStream_t st) {
   if (T <= 0) return hipSuccess;
-  if (bf16) return launch_sbwd<uint16_t>(q, subkeys, T, H, n, S, k, idx, gz, grad_q, grad_K, ws, st);
-  return launch_sbwd<float>(q, subkeys, T, H, n, S, k, idx, gz, grad_q, grad_K, ws, st);
+  if (bf16)
+    return launch_sbwd<uint16_t>(q, subkeys, T, H, n, S, k, idx, gz, qstats, grad_q, grad_K, ws, st);
+  return launch_sbwd<float>(q, subkeys, T, H, n, S, k, idx, gz, qstats, grad_q, grad_K, ws, st);
 }
 
 }  // namespace pk

@@ -246,3 +246,42 @@ def test_bwd_mode_environment_override(lib, monkeypatch):
     assert lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 64, 0) == sorted_
     # an explicit mode is never overridden
     assert lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 2048, 1) == atomic
+
+
+def searchqn(lib, q=FAKE, qdt=BF16, K=FAKE, kdt=BF16, T=8, H=2, n=64, S=16, k=4, eps=1e-5,
+             idx=FAKE, w=FAKE, qhat=None, stats=None, ws=FAKE, ws_bytes=BIG_WS):
+    return lib.mem_search_qnorm(q, qdt, K, kdt, T, H, n, S, k, eps, idx, w, None, None, qhat, stats,
+                                ws, ws_bytes, None)
+
+
+def sbwdqn(lib, T=8, eps=1e-5, gq=FAKE, gk=FAKE, ws=FAKE, ws_bytes=BIG_WS, n=64):
+    return lib.mem_search_backward_qnorm(FAKE, BF16, FAKE, BF16, T, 2, n, 16, 4, eps, FAKE, FAKE, gq, gk,
+                                         ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(eps=-1e-3), INVALID, "eps"),
+    (dict(eps=float("nan")), INVALID, "eps"),
+    (dict(eps=float("inf")), INVALID, "eps"),
+    (dict(qhat=FAKE + 8), INVALID, "qhat_out"),
+    (dict(stats=FAKE + 4), INVALID, "stats_out"),
+    (dict(n=63), INVALID, "even"),
+    (dict(k=17), INVALID, "k <= S"),
+    (dict(idx=0), INVALID, "null"),
+    (dict(ws_bytes=16), WORKSPACE, "workspace"),
+])
+def test_search_qnorm_rejects(lib, kw, code, text):
+    assert searchqn(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def test_search_qnorm_noops_and_workspace(lib):
+    assert searchqn(lib, T=0) == OK
+    assert searchqn(lib, T=0, eps=0.0) == OK
+    assert sbwdqn(lib, T=0) == OK
+    assert sbwdqn(lib, gq=None, gk=None) == OK
+    assert sbwdqn(lib, eps=-1.0) == INVALID and "eps" in msg(lib)
+    assert sbwdqn(lib, n=63) == INVALID
+    # room for the per-query statistics on top of the plain search backward's needs
+    need = lib.mem_search_backward_workspace_size(8, 2, 16, 4)
+    assert sbwdqn(lib, ws_bytes=need - 1) == WORKSPACE
