@@ -457,7 +457,8 @@ def main():
             "score_topk_ms": round(qn["score_topk"], 4),
             "cartesian_ms": round(qn["cartesian"], 4),
             "search_backward_ms": round(search_bwd_qn_ms, 4),
-            "qnorm": hbm_rate(alg_cost("qnorm", wl, U, esz)[1], qn["qnorm"]),
+            "qnorm": dict(hbm_rate(alg_cost("qnorm", wl, U, esz)[1], qn["qnorm"]),
+                          traffic=measured_traffic("qnorm", wl.name)),
         },
         "stream_copy_GBps": round(copy_gbps, 1),
         "touched_rows": U,
