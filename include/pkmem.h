@@ -12,8 +12,9 @@
  *
  * Conventions for every entry point
  *   - Pointers are DEVICE pointers unless marked "host".  All device buffers are
- *     allocated and owned by the caller; the library never allocates or frees
- *     device memory and keeps no device state between calls.
+ *     allocated and owned by the caller; the library allocates no device memory
+ *     and keeps no device state between calls (one exception, off by default:
+ *     the 4-byte flag of the PKMEM_DEBUG index check, see Environment below).
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = null stream) and
  *     return once the work is enqueued.  mem_bag_backward_sparse is the only call
  *     that waits on the stream (it must report a row count to the host).
