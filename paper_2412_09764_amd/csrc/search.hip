@@ -202,7 +202,32 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   // lane's 16 bytes going to LDS at base + 16*lane.  Rows past S and padded
   // columns read a valid (finite) sub-key element instead: padded columns
   // meet zero query entries and rows past S are masked out.
+  // The lane's source element offsets within a chunk are the same for every
+  // chunk: computed once, so a chunk whose rows all exist costs one address
+  // add per load; the last, partial chunk clamps rows as it goes.
+  constexpr int NDMA = (NCOL + SEARCH_WAVES - 1) / SEARCH_WAVES;  // loads per wave, at most
+  uint32_t src_off[NDMA];  // element offset of the lane's segment in chunk 0
+#pragma unroll
+  for (int j = 0; j < NDMA; ++j) {
+    const int i = wave + j * SEARCH_WAVES;
+    const int sidx = i * WAVE + lane;
+    const int r = sidx / NCOL, pc = sidx % NCOL;
+    const int lc = pc ^ (r & SWZ);
+    int e0 = lc * EPS;
+    e0 = e0 < d ? e0 : 0;
+    src_off[j] = (uint32_t)(r * d + e0);
+  }
+  const int nfull_rows = S / CHUNK_ROWS;  // chunks whose 64 rows all exist
   auto issue_chunk = [&](int c, unsigned char* buf) {
+    if (c < nfull_rows) {
+      const T* cb = kbase + (size_t)c * CHUNK_ROWS * d;
+#pragma unroll
+      for (int j = 0; j < NDMA; ++j) {
+        const int i = wave + j * SEARCH_WAVES;
+        if (NCOL % SEARCH_WAVES == 0 || i < NCOL) lds_dma16(cb + src_off[j], &buf[i * WAVE * 16]);
+      }
+      return;
+    }
     for (int i = wave; i < NCOL; i += SEARCH_WAVES) {
       const int sidx = i * WAVE + lane;
       const int r = sidx / NCOL, pc = sidx % NCOL;
