@@ -34,9 +34,10 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
 MFMA_F32_PEAK_TFLOPS = 157.3
 
 KERNELS = ["score_topk", "cartesian", "bag_forward", "sort_by_row", "bag_backward_rows",
-           "bag_backward_atomic", "softmax_backward", "search_backward"]
+           "bag_backward_atomic", "softmax_backward", "search_backward", "topk_sort"]
 KERNEL_SOURCES = {
     "score_topk": ["search.hip", "pk_device.h"],
+    "topk_sort": ["search.hip", "pk_device.h"],
     "cartesian": ["search.hip", "pk_device.h"],
     "bag_forward": ["bag.hip", "pk_device.h"],
     "bag_backward_atomic": ["bag.hip", "pk_device.h"],
@@ -357,14 +358,14 @@ def main():
                             workspace=ws_s)
     search_qn()
     torch.cuda.synchronize()
-    pk.mem_timer_start("qnorm", "score_topk", "cartesian")
+    pk.mem_timer_start("qnorm", "score_topk", "cartesian", "topk_sort")
     for _ in range(args.steps):
         search_qn()
     torch.cuda.synchronize()
     pk.mem_timer_stop()
     qn = {}
     for pos, ms in pk.mem_timer_read():
-        qn.setdefault(("qnorm", "score_topk", "cartesian")[pos], []).append(ms)
+        qn.setdefault(("qnorm", "score_topk", "cartesian", "topk_sort")[pos], []).append(ms)
     qn = {kn: sum(v) / len(v) for kn, v in qn.items()}
     gq = torch.empty((T, H, wl.n), dtype=torch.float32, device=dev)
     gK = torch.zeros((H, 2, wl.S, wl.d), dtype=torch.float32, device=dev)
@@ -455,6 +456,7 @@ def main():
         "query_norm": {
             "qnorm_ms": round(qn["qnorm"], 4),
             "score_topk_ms": round(qn["score_topk"], 4),
+            "topk_sort_ms": round(qn["topk_sort"], 4),
             "cartesian_ms": round(qn["cartesian"], 4),
             "search_backward_ms": round(search_bwd_qn_ms, 4),
             "qnorm": dict(hbm_rate(alg_cost("qnorm", wl, U, esz)[1], qn["qnorm"]),

@@ -251,7 +251,7 @@ int mem_bag_backward_sparse(const void* dy, const void* values, pkmem_dtype v_dt
  * mem_timer_start(kernels) takes a comma-separated list of kernel names and
  * makes the library record a HIP event pair on the launch stream around every
  * following launch of a listed kernel:
- *   "score_topk", "cartesian"              (mem_search, mem_search_qnorm)
+ *   "score_topk", "topk_sort", "cartesian" (mem_search, mem_search_qnorm)
  *   "qnorm"                                (mem_search_qnorm, mem_search_backward_qnorm)
  *   "search_backward"                      (mem_search_backward[_qnorm])
  *   "bag_forward"                          (mem_bag_forward, mem_bag_forward_gated)

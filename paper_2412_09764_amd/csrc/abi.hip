@@ -38,6 +38,7 @@ inline bool dtype_ok(int t) { return t == PKMEM_F32 || t == PKMEM_BF16; }
 
 struct SearchWs {
   uint64_t* cand;
+  uint32_t* cnts;
   int32_t* half_idx;
   float* half_score;
   uint32_t* ovf;
@@ -52,6 +53,8 @@ SearchWs search_ws(void* base, int64_t T, int H, int k) {
   size_t off = 0;
   w.cand = reinterpret_cast<uint64_t*>(p + off);
   off += align256(rows * pk::CAND_CAP * sizeof(uint64_t));
+  w.cnts = reinterpret_cast<uint32_t*>(p + off);
+  off += align256(rows * 2 * sizeof(uint32_t));
   w.half_idx = reinterpret_cast<int32_t*>(p + off);
   off += align256(rows * k * sizeof(int32_t));
   w.half_score = reinterpret_cast<float*>(p + off);
@@ -335,8 +338,8 @@ static int search_common(const char* fn, const void* q, pkmem_dtype q_dt, const 
     if (e != hipSuccess) return hip_status(e, fn);
   }
   int32_t* hidx = half_idx_out ? half_idx_out : w.half_idx;
-  e = pk::launch_search_half(bf16, q, subkeys, T, H, n, S, k, qstats, w.cand, hidx, w.half_score,
-                             w.ovf, st);
+  e = pk::launch_search_half(bf16, q, subkeys, T, H, n, S, k, qstats, w.cand, w.cnts, hidx,
+                             w.half_score, w.ovf, st);
   if (e != hipSuccess) return hip_status(e, fn);
   e = pk::launch_cartesian(hidx, w.half_score, T, H, S, k, idx_out, w_out, score_out, st);
   if (e != hipSuccess) return hip_status(e, fn);

@@ -38,12 +38,13 @@ int cartesian_pairs(int k);
 
 // ---- search (search.hip) -------------------------------------------------
 // rows = T*H*2 (token, head, half) rows; cand = [rows, CAND_CAP] u64;
+// cnts = [rows, 2] u32 (candidates per run);
 // ovf = [1 + rows] u32 (count, then overflowed row ids).
 // qstats (nullable) = per (token, head) query (mean, rstd): the scoring then
 // normalises the queries as it loads them (see launch_qnorm).
 hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
                               int n, int S, int k, const float2* qstats, uint64_t* cand,
-                              int32_t* half_idx, float* half_score, uint32_t* ovf,
+                              uint32_t* cnts, int32_t* half_idx, float* half_score, uint32_t* ovf,
                               hipStream_t st);
 // LayerNorm statistics of rows = T*H queries of n elements into stats, and
 // (qhat non-null) the normalised queries in the query dtype.

@@ -21,10 +21,14 @@
 //     accumulator slot, with the lane's count in a register (the two lanes
 //     holding a token's rows own half of its CAND_CAP slots each; a count
 //     past capacity keeps writing the last slot and sends the row to the
-//     rescan) - no masks, atomics or capacity branches.
-//   * Pass 3 sorts each row's candidates with a wave bitonic sort and writes the
-//     first k.  A row whose lane half overflowed its CAND_CAP / 2 slots (heavy
-//     ties) is listed for k_topk_fallback, which rescans it exactly.
+//     rescan) - no masks, atomics or capacity branches; the two counts go to
+//     memory.
+//   * Pass 3, k_topk_sort, a kernel of its own (a sort needs few registers, so
+//     it runs at far higher occupancy than the scoring kernel, which is held
+//     to two waves per SIMD): per row a wave bitonic sort of the candidates,
+//     the first k written.  A row whose lane half overflowed its CAND_CAP / 2
+//     slots (heavy ties) is listed for k_topk_fallback, which rescans it
+//     exactly.
 //   * With query normalisation (qk-normalisation, Sec. 3.1.4) k_qnorm first
 //     computes each (token, head) query's mean and rstd = 1/sqrt(var + eps)
 //     (LayerNorm without affine, fp32, centred second pass); the scoring
@@ -151,7 +155,7 @@ template <typename T, int NSTEP>
 __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
     const T* __restrict__ q, const T* __restrict__ subkeys, int64_t ntok, int H, int n, int S,
     int k, const float2* __restrict__ qstats, uint64_t* __restrict__ cand,
-    int32_t* __restrict__ half_idx, float* __restrict__ half_score, uint32_t* __restrict__ ovf) {
+    uint32_t* __restrict__ cnts) {
   using M = MfmaOp<T>;
   constexpr int DPAD = NSTEP * M::KSTEP;      // padded half dim
   constexpr int RB = DPAD * M::ESIZE;         // bytes per sub-key row in LDS
@@ -166,7 +170,6 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   // wave's 1 KiB of a chunk contiguous for the direct global -> LDS loads.
   __shared__ __align__(16) unsigned char kbuf0[CBYTES];
   __shared__ __align__(16) unsigned char kbuf1[CBYTES];
-  __shared__ int cnt[2 * SEARCH_TOK];  // candidates per (token, lane half)
 
   const int d = n >> 1;
   const int HP = 2 * H;
@@ -351,63 +354,55 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
       }
     }
   });
-  cnt[wave * 64 + lane] = (int)my_cnt;
-  __syncthreads();
+  if (tok_ok) cnts[rid * 2 + kh] = my_cnt;
+}
 
-  // ---- pass 3: sort each row's candidates, keep the first k ---------------
-  // Row i's records sit in two runs: c0 at slot 0, c1 at slot HALF_CAP; lane
-  // l takes record l (and l + 64) of their concatenation.  The next row's
-  // records are loaded before the current row is sorted.
+// Pass 3 as a kernel of its own: one wave per (token, head, half) row at a
+// time.  The row's candidates sit in two runs (c0 records at slot 0, c1 at
+// slot CAND_CAP / 2); lane l takes record l (and l + 64) of their
+// concatenation; the wave sorts them as (score desc, index asc) keys and
+// writes the first k.  A row with an overflowed run goes to the rescan list.
+__global__ __launch_bounds__(256) void k_topk_sort(const uint64_t* __restrict__ cand,
+                                                   const uint32_t* __restrict__ cnts,
+                                                   int64_t rows, int k,
+                                                   int32_t* __restrict__ half_idx,
+                                                   float* __restrict__ half_score,
+                                                   uint32_t* __restrict__ ovf) {
+  constexpr uint32_t HALF_CAP = CAND_CAP / 2;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   auto to_key = [](uint64_t raw) { return make_key(__uint_as_float(uint32_t(raw >> 32)), uint32_t(raw)); };
-  int nrow = 32;
-  if (tile * SEARCH_TOK + wave * 32 + 32 > ntok) {
-    const int64_t left = ntok - (tile * SEARCH_TOK + wave * 32);
-    nrow = left < 0 ? 0 : (int)left;
-  }
-  auto fetch = [&](int i, uint64_t (&v)[2], int& c0, int& c1) {
-    c0 = cnt[wave * 64 + i];
-    c1 = cnt[wave * 64 + 32 + i];
-    v[0] = v[1] = 0ull;
-    if (c0 > HALF_CAP || c1 > HALF_CAP) return;  // overflow: handled by the rescan
-    const size_t r = ((size_t)(tile * SEARCH_TOK + wave * 32 + i) * H + h) * 2 + p;
-    const uint64_t* rc = cand + r * CAND_CAP;
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int x = lane + e * WAVE;
-      if (x < c0) v[e] = rc[x];
-      else if (x - c0 < c1) v[e] = rc[HALF_CAP + x - c0];
-    }
-  };
-  uint64_t cur[2], nxt[2] = {0ull, 0ull};
-  int c0 = 0, c1 = 0, n0 = 0, n1 = 0;
-  if (nrow > 0) fetch(0, cur, c0, c1);
-  for (int i = 0; i < nrow; ++i) {
-    if (i + 1 < nrow) fetch(i + 1, nxt, n0, n1);
-    const size_t r = ((size_t)(tile * SEARCH_TOK + wave * 32 + i) * H + h) * 2 + p;
-    const int c = c0 + c1;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < rows; r += (int64_t)gridDim.x * 4) {
+    const uint32_t c0 = cnts[r * 2], c1 = cnts[r * 2 + 1];
     if (c0 > HALF_CAP || c1 > HALF_CAP) {
       if (lane == 0) {
         const uint32_t slot = atomicAdd(&ovf[0], 1u);
         ovf[1 + slot] = (uint32_t)r;
       }
-    } else {
-      uint64_t key;
-      if (c <= WAVE) {
-        uint64_t v[1] = {lane < c ? to_key(cur[0]) : 0ull};
-        wave_sort_desc<1>(v, lane);
-        key = v[0];
-      } else {
-        uint64_t v[2] = {to_key(cur[0]), lane + WAVE < c ? to_key(cur[1]) : 0ull};
-        wave_sort_desc<2>(v, lane);
-        key = v[0];
-      }
-      if (lane < k) {
-        half_idx[r * k + lane] = (int32_t)key_index(key);
-        half_score[r * k + lane] = key_score(key);
-      }
+      continue;
     }
-    cur[0] = nxt[0]; cur[1] = nxt[1];
-    c0 = n0; c1 = n1;
+    const uint64_t* rc = cand + (size_t)r * CAND_CAP;
+    const uint32_t c = c0 + c1;
+    uint64_t raw[2] = {0ull, 0ull};
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const uint32_t x = (uint32_t)(lane + e * WAVE);
+      if (x < c0) raw[e] = rc[x];
+      else if (x - c0 < c1) raw[e] = rc[HALF_CAP + x - c0];
+    }
+    uint64_t key;
+    if (c <= (uint32_t)WAVE) {
+      uint64_t v[1] = {(uint32_t)lane < c ? to_key(raw[0]) : 0ull};
+      wave_sort_desc<1>(v, lane);
+      key = v[0];
+    } else {
+      uint64_t v[2] = {to_key(raw[0]), (uint32_t)lane + WAVE < c ? to_key(raw[1]) : 0ull};
+      wave_sort_desc<2>(v, lane);
+      key = v[0];
+    }
+    if (lane < k) {
+      half_idx[r * k + lane] = (int32_t)key_index(key);
+      half_score[r * k + lane] = key_score(key);
+    }
   }
 }
 
@@ -530,17 +525,27 @@ int cartesian_pairs(int k) {
 
 template <typename T, int NSTEP>
 static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, int H, int n, int S,
-                               int k, const float2* qstats, uint64_t* cand, int32_t* half_idx,
-                               float* half_score, uint32_t* ovf, hipStream_t st) {
+                               int k, const float2* qstats, uint64_t* cand, uint32_t* cnts,
+                               int32_t* half_idx, float* half_score, uint32_t* ovf,
+                               hipStream_t st) {
   const int64_t tiles = (T_ + SEARCH_TOK - 1) / SEARCH_TOK;
   const int64_t blocks = tiles * 2 * H;
   {
     LaunchTimer lt("score_topk", st);
     hipLaunchKernelGGL((k_score_topk<T, NSTEP>), dim3((unsigned)blocks), dim3(64 * SEARCH_WAVES), 0, st,
-                       (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats, cand, half_idx,
-                       half_score, ovf);
+                       (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats, cand, cnts);
   }
   hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  {
+    const int64_t rows = T_ * H * 2;
+    int64_t sb = (rows + 3) / 4;
+    if (sb > 16384) sb = 16384;
+    LaunchTimer lt("topk_sort", st);
+    hipLaunchKernelGGL(k_topk_sort, dim3((unsigned)sb), dim3(256), 0, st, (const uint64_t*)cand,
+                       (const uint32_t*)cnts, rows, k, half_idx, half_score, ovf);
+  }
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds = (size_t)S * sizeof(float);
   hipLaunchKernelGGL((k_topk_fallback<T>), dim3(256), dim3(256), lds, st, (const T*)q,
@@ -564,25 +569,25 @@ hipError_t launch_qnorm(bool bf16, const void* q, int64_t rows, int n, float eps
 
 hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T_, int H,
                               int n, int S, int k, const float2* qstats, uint64_t* cand,
-                              int32_t* half_idx, float* half_score, uint32_t* ovf,
+                              uint32_t* cnts, int32_t* half_idx, float* half_score, uint32_t* ovf,
                               hipStream_t st) {
   hipError_t e = launch_fill_u32(ovf, 0u, 1, st);
   if (e != hipSuccess) return e;
   const int d = n / 2;
   if (bf16) {
     const int steps = (d + 15) / 16;
-    if (steps <= 1) return launch_score<uint16_t, 1>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
-    if (steps <= 2) return launch_score<uint16_t, 2>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
-    if (steps <= 4) return launch_score<uint16_t, 4>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
-    if (steps <= 8) return launch_score<uint16_t, 8>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
-    return launch_score<uint16_t, 16>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+    if (steps <= 1) return launch_score<uint16_t, 1>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+    if (steps <= 2) return launch_score<uint16_t, 2>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+    if (steps <= 4) return launch_score<uint16_t, 4>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+    if (steps <= 8) return launch_score<uint16_t, 8>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+    return launch_score<uint16_t, 16>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
   }
   const int steps = (d + 1) / 2;
-  if (steps <= 2) return launch_score<float, 2>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
-  if (steps <= 4) return launch_score<float, 4>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
-  if (steps <= 8) return launch_score<float, 8>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
-  if (steps <= 16) return launch_score<float, 16>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
-  return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, qstats, cand, half_idx, half_score, ovf, st);
+  if (steps <= 2) return launch_score<float, 2>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+  if (steps <= 4) return launch_score<float, 4>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+  if (steps <= 8) return launch_score<float, 8>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+  if (steps <= 16) return launch_score<float, 16>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+  return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
 }
 
 hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T_, int H,
