@@ -59,6 +59,17 @@ Function pins (tests under tests/test_oracle_*.py):
   search_backward_qnorm
                    central finite differences in the raw queries at a fixed
                    selection; torch autograd through layer_norm (fp64)
+  search_extra     r = 0 gives `search`; every extra slot's score equals the
+                   brute-force full-key score of its index; an extra that
+                   repeats a selected index repeats its score; the weights
+                   are the closed-form softmax of the k + r scores
+
+Extra key-value pairs (Sec. 5.4, model ablations, names adding random
+key-value pairs beside the top-k during pre-training, without a formula).
+Reading: per (token, head) the caller draws r indices in [0, S*S) (the
+random numbers are inputs); each is scored like any full key, s1[i1] + s2[i2],
+and occupies its own slot after the k selected ones (a repeat of a selected
+index is a separate slot); the softmax runs over all k + r scores.
 
 Query normalisation (qk-normalisation, named in Sec. 3.1.4 as the remedy for
 unstable training of large memories, citing a LayerNorm of queries and keys).
@@ -94,6 +105,7 @@ __all__ = [
     "query_layernorm",
     "search_qnorm",
     "search_backward_qnorm",
+    "search_extra",
 ]
 
 
@@ -449,3 +461,37 @@ def search_backward_qnorm(q: np.ndarray, subkeys: np.ndarray, idx: np.ndarray,
     gxm = (g * xh).mean(axis=-1, keepdims=True)
     grad_q = ln["rstd"][..., None] * (g - gm - xh * gxm)
     return dict(grad_q=grad_q, grad_K=r["grad_K"])
+
+
+def search_extra(q: np.ndarray, subkeys: np.ndarray, k: int, extra_idx: np.ndarray) -> dict:
+    """The search of `search` plus r extra key-value pairs per (token, head).
+
+    extra_idx: [T, H, r] int, each in [0, S*S): composed indices chosen by the
+    caller.  Slot j < k is the j-th selected key (rank order), slot k + e the
+    e-th extra index, scored s1[i1] + s2[i2] with i1 = i // S, i2 = i % S.
+    Returns idx, score, w of shape [T, H, k + r] (softmax over all k + r
+    scores of a (token, head)); half_idx / half_score as in `search`.
+    """
+    q = _f64(q)
+    K = _f64(subkeys)
+    T, H, n = q.shape
+    d = n // 2
+    S = K.shape[2]
+    ex = np.asarray(extra_idx, dtype=np.int64)
+    r = ex.shape[2]
+    assert ex.shape[:2] == (T, H)
+    assert np.all((ex >= 0) & (ex < S * S))
+    base = search(q, K, k)
+    idx = np.zeros((T, H, k + r), dtype=np.int64)
+    score = np.zeros((T, H, k + r))
+    w = np.zeros((T, H, k + r))
+    for t in range(T):
+        for h in range(H):
+            idx[t, h, :k] = base["idx"][t, h]
+            score[t, h, :k] = base["score"][t, h]
+            for e in range(r):
+                i1, i2 = divmod(int(ex[t, h, e]), S)
+                idx[t, h, k + e] = ex[t, h, e]
+                score[t, h, k + e] = q[t, h, :d] @ K[h, 0, i1] + q[t, h, d:] @ K[h, 1, i2]
+            w[t, h] = softmax(score[t, h])
+    return dict(idx=idx, score=score, w=w, half_idx=base["half_idx"], half_score=base["half_score"])

@@ -31,6 +31,10 @@ What pins what:
                   normalise exactly give the plain search (and brute force) of
                   x / 2; the backward by central differences and torch
                   autograd through layer_norm.
+  extra pairs   - r = 0 gives the plain search; each extra slot's score is
+                  its key's brute-force full score (integer inputs, exact); a
+                  repeated selected index repeats its score; closed-form
+                  softmax over the k + r scores.
 """
 from __future__ import annotations
 
@@ -477,3 +481,34 @@ def check_search_qnorm_rounding(search_qnorm_fn, rng, T=4, H=2, n=48, S=6, k=3):
     np.testing.assert_array_equal(out["qhat"], ref.float().double().numpy())
     out = search_qnorm_fn(q, K, k, 1e-5, "bf16")
     np.testing.assert_array_equal(out["qhat"], ref.float().to(torch.bfloat16).double().numpy())
+
+
+# ------------------------------------------------------ extra key-value pairs ----
+def check_search_extra(extra_fn, search_fn, brute_fn, rng, T=5, H=2, S=6, d=3, k=4, r=3):
+    """Extra pairs: r = 0 is the plain search; every extra slot's score is the
+    full-key score of its index from the instantiated key set (brute force
+    over all S^2 keys, integer inputs: exact); a repeated selected index
+    repeats its score; the weights are exp(z) / sum exp(z) over the k + r
+    scores (closed form, written here without max subtraction)."""
+    q = rng.integers(-2, 3, size=(T, H, 2 * d)).astype(np.float64)
+    K = rng.integers(-2, 3, size=(H, 2, S, d)).astype(np.float64)
+    base = search_fn(q, K, k)
+    out0 = extra_fn(q, K, k, np.zeros((T, H, 0), dtype=np.int64))
+    np.testing.assert_array_equal(out0["idx"], base["idx"])
+    np.testing.assert_allclose(out0["w"], base["w"], rtol=1e-15, atol=0)
+    ex = rng.integers(0, S * S, size=(T, H, r))
+    ex[0, 0, 0] = base["idx"][0, 0, 2]          # repeat of a selected key
+    out = extra_fn(q, K, k, ex)
+    assert out["idx"].shape == (T, H, k + r)
+    np.testing.assert_array_equal(out["idx"][..., :k], base["idx"])
+    np.testing.assert_array_equal(out["idx"][..., k:], ex)
+    full = brute_fn(q, K, S * S)                # every key, rank order
+    for t in range(T):
+        for h in range(H):
+            score_of = dict(zip(full["idx"][t, h].tolist(), full["score"][t, h].tolist()))
+            for e in range(r):
+                assert out["score"][t, h, k + e] == score_of[int(ex[t, h, e])]
+    assert out["score"][0, 0, k] == out["score"][0, 0, 2]
+    z = out["score"]
+    np.testing.assert_allclose(out["w"], np.exp(z) / np.exp(z).sum(-1, keepdims=True), rtol=1e-12)
+    np.testing.assert_allclose(out["w"].sum(-1), 1.0, rtol=1e-14)

@@ -361,3 +361,53 @@ def test_catches_qnorm_backward_with_rounded_xhat():
 
 def test_catches_qnorm_key_gradient_from_unrounded_query():
     assert _qnorm_fails(bwd=_bwd_variant(unrounded_dk=True)) > 0
+
+
+# ------------------------------------------------------ extra key-value pairs ----
+def _extra_fails(fn):
+    failures = 0
+    for s in range(3):
+        try:
+            pins.check_search_extra(fn, oracle.search, oracle.brute_force_search,
+                                    np.random.default_rng(140 + s))
+        except (AssertionError, ValueError, IndexError, KeyError):
+            failures += 1
+    return failures
+
+
+def test_real_extra_passes():
+    assert _extra_fails(oracle.search_extra) == 0
+
+
+def test_catches_extra_halves_swapped():
+    def mutant(q, K, k, ex):
+        S = K.shape[2]
+        ex = np.asarray(ex)
+        return oracle.search_extra(q, K, k, (ex % S) * S + ex // S)
+    assert _extra_fails(mutant) > 0
+
+
+def test_catches_extras_left_out_of_the_softmax():
+    def mutant(q, K, k, ex):
+        out = oracle.search_extra(q, K, k, ex)
+        out["w"][..., :k] = oracle.search(q, K, k)["w"]
+        out["w"][..., k:] = 0.0
+        return out
+    assert _extra_fails(mutant) > 0
+
+
+def test_catches_extra_scored_with_one_half_only():
+    def mutant(q, K, k, ex):
+        out = oracle.search_extra(q, K, k, ex)
+        S = K.shape[2]
+        d = q.shape[2] // 2
+        T, H, r = np.asarray(ex).shape
+        for t in range(T):
+            for h in range(H):
+                for e in range(r):
+                    i1 = int(ex[t, h, e]) // S
+                    out["score"][t, h, k + e] = np.asarray(q, float)[t, h, :d] @ np.asarray(K, float)[h, 0, i1]
+                z = out["score"][t, h]
+                out["w"][t, h] = np.exp(z - z.max()) / np.exp(z - z.max()).sum()
+        return out
+    assert _extra_fails(mutant) > 0
