@@ -99,6 +99,29 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
                void* ws, size_t ws_bytes, pkmem_stream_t stream);
 
 /* ------------------------------------------------------------------------ *
+ * Search with extra key-value pairs beside the top-k (Sec. 5.4, model
+ * ablations: random key-value pairs added during pre-training).  For every
+ * (t, h) the caller supplies r composed indices (drawn as it likes, e.g.
+ * uniformly from [0, S*S)); each is scored like any full key,
+ *   z = q[t,h,0:d] . subkeys[h,0,i/S] + q[t,h,d:n] . subkeys[h,1,i%S],
+ * and occupies its own slot after the k selected ones (an index that is also
+ * selected appears twice); the softmax runs over all k + r scores.
+ *   r            0 <= r and k + r <= PKMEM_KMAX.
+ *   extra_idx    [T, H, r] int64 in [0, S*S) (not range-checked unless
+ *                PKMEM_DEBUG is set; an index outside is scored as index 0
+ *                and written out unchanged).
+ *   idx_out, w_out, score_out   [T, H, k + r]: slots 0..k-1 as mem_search's,
+ *                slots k..k+r-1 the extra pairs in the given order; w sums to
+ *                one over all k + r.  half_idx_out [T, H, 2, k] as mem_search's.
+ * The value bag and both backwards take these outputs as they are, with
+ * k + r in place of k.  Workspace: mem_search_workspace_size(T, H, S, k).
+ * ------------------------------------------------------------------------ */
+int mem_search_extra(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                     int64_t T, int H, int n, int S, int k, int r, const int64_t* extra_idx,
+                     int64_t* idx_out, float* w_out, float* score_out, int32_t* half_idx_out,
+                     void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
  * Search backward: gradient of the selected scores with respect to the
  * queries and the sub-keys (the keys are trainable parameters, Sec. 3; the
  * selection is piecewise constant and passes no gradient).  With
@@ -251,7 +274,8 @@ int mem_bag_backward_sparse(const void* dy, const void* values, pkmem_dtype v_dt
  * mem_timer_start(kernels) takes a comma-separated list of kernel names and
  * makes the library record a HIP event pair on the launch stream around every
  * following launch of a listed kernel:
- *   "score_topk", "topk_sort", "cartesian" (mem_search, mem_search_qnorm)
+ *   "score_topk", "topk_sort", "cartesian" (mem_search, mem_search_qnorm,
+ *                                           mem_search_extra)
  *   "qnorm"                                (mem_search_qnorm, mem_search_backward_qnorm)
  *   "search_backward"                      (mem_search_backward[_qnorm])
  *   "bag_forward"                          (mem_bag_forward, mem_bag_forward_gated)
@@ -273,7 +297,8 @@ int mem_timer_read(float* ms_out, int* kernel_out, int cap);
 /* ------------------------------------------------------------------------ *
  * Environment (read at every call):
  *   PKMEM_DEBUG=1       before a kernel indexes with idx (mem_bag_forward[_gated],
- *                       mem_bag_backward[_sparse], mem_search_backward) a device
+ *                       mem_bag_backward[_sparse], mem_search_backward[_qnorm],
+ *                       mem_search_extra's extra_idx) a device
  *                       check that every index lies in [0, N) (or [0, S*S)); the
  *                       call waits for it and returns PKMEM_ERR_INVALID if not.
  *                       Off by default: indices from mem_search are in range by

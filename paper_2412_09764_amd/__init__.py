@@ -20,7 +20,7 @@ import torch  # noqa: F401  (first: the library binds to the HIP runtime torch l
 
 __all__ = [
     "PkmemError", "load", "lib_path", "mem_search", "mem_search_backward", "mem_search_qnorm",
-    "mem_search_backward_qnorm", "mem_bag_forward",
+    "mem_search_backward_qnorm", "mem_search_extra", "mem_bag_forward",
     "mem_bag_forward_gated", "mem_gate_backward",
     "mem_bag_backward",
     "mem_bag_backward_sparse", "mem_search_workspace_size", "mem_bag_backward_workspace_size",
@@ -68,6 +68,9 @@ def load() -> ctypes.CDLL:
     L.mem_search_backward_qnorm.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, F32, P, P, P,
                                             P, P, SZ, P]
     L.mem_search_backward_qnorm.restype = I32
+    L.mem_search_extra.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, I32, P, P, P, P, P, P, SZ,
+                                   P]
+    L.mem_search_extra.restype = I32
     L.mem_bag_forward.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P]
     L.mem_bag_forward.restype = I32
     L.mem_bag_forward_gated.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P, P, P]
@@ -190,6 +193,39 @@ def mem_search_qnorm(q: torch.Tensor, subkeys: torch.Tensor, k: int, eps: float 
         stats_out = torch.empty((T, H, 2), dtype=torch.float32, device=q.device)
     return _search(q, subkeys, k, float(eps), idx_out, w_out, score_out, half_idx_out, want_score,
                    want_half, qhat_out, stats_out, workspace, stream)
+
+
+def mem_search_extra(q: torch.Tensor, subkeys: torch.Tensor, k: int, extra_idx: torch.Tensor, *,
+                     idx_out=None, w_out=None, score_out=None, half_idx_out=None,
+                     want_score: bool = True, want_half: bool = False, workspace=None,
+                     stream=None):
+    """mem_search plus r extra key-value pairs per (token, head): extra_idx
+    [T, H, r] int64 composed indices, scored as full keys, in slots k..k+r-1;
+    softmax over all k + r.  Returns (idx, w, score, half_idx) with k + r slots."""
+    L = load()
+    _dev(q, subkeys, extra_idx)
+    T, H, n = q.shape
+    S = subkeys.shape[2]
+    r = extra_idx.shape[2] if extra_idx.dim() == 3 else 0
+    if extra_idx.dtype != torch.int64:
+        raise ValueError("extra_idx must be int64")
+    dev = q.device
+    kk = k + r
+    if idx_out is None:
+        idx_out = torch.empty((T, H, kk), dtype=torch.int64, device=dev)
+    if w_out is None:
+        w_out = torch.empty((T, H, kk), dtype=torch.float32, device=dev)
+    if score_out is None and want_score:
+        score_out = torch.empty((T, H, kk), dtype=torch.float32, device=dev)
+    if half_idx_out is None and want_half:
+        half_idx_out = torch.empty((T, H, 2, k), dtype=torch.int32, device=dev)
+    _dev(idx_out, w_out, score_out, half_idx_out)
+    ws = _workspace(mem_search_workspace_size(T, H, S, k), dev, workspace)
+    _check(L.mem_search_extra(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k, r,
+                              _ptr(extra_idx), _ptr(idx_out), _ptr(w_out), _ptr(score_out),
+                              _ptr(half_idx_out), _ptr(ws), ws.numel() * ws.element_size(),
+                              _stream(stream)))
+    return idx_out, w_out, score_out, half_idx_out
 
 
 def _search(q, subkeys, k, eps, idx_out, w_out, score_out, half_idx_out, want_score, want_half,

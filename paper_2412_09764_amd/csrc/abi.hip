@@ -312,11 +312,15 @@ size_t mem_search_workspace_size(int64_t T, int H, int S, int k) {
 // The search, with the queries normalised (qnorm) or not.
 static int search_common(const char* fn, const void* q, pkmem_dtype q_dt, const void* subkeys,
                          pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k, bool qnorm,
-                         float eps, int64_t* idx_out, float* w_out, float* score_out,
-                         int32_t* half_idx_out, void* qhat_out, float* stats_out, void* ws,
-                         size_t ws_bytes, pkmem_stream_t stream) {
+                         float eps, int nex, const int64_t* ex_idx, int64_t* idx_out, float* w_out,
+                         float* score_out, int32_t* half_idx_out, void* qhat_out, float* stats_out,
+                         void* ws, size_t ws_bytes, pkmem_stream_t stream) {
   int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k);
   if (rc) return rc;
+  if (nex < 0) return fail(PKMEM_ERR_INVALID, "%s: r must be >= 0", fn);
+  if (k + nex > PKMEM_KMAX)
+    return fail(PKMEM_ERR_UNSUPPORTED, "%s: k + r must be <= %d (k=%d, r=%d)", fn, PKMEM_KMAX, k, nex);
+  if (T > 0 && nex > 0 && !ex_idx) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
   if (T > 0 && (!idx_out || !w_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
   if (qnorm && !(eps >= 0.f && eps <= 3.0e38f))
     return fail(PKMEM_ERR_INVALID, "%s: eps must be finite and >= 0", fn);
@@ -341,7 +345,12 @@ static int search_common(const char* fn, const void* q, pkmem_dtype q_dt, const 
   e = pk::launch_search_half(bf16, q, subkeys, T, H, n, S, k, qstats, w.cand, w.cnts, hidx,
                              w.half_score, w.ovf, st);
   if (e != hipSuccess) return hip_status(e, fn);
-  e = pk::launch_cartesian(hidx, w.half_score, T, H, S, k, idx_out, w_out, score_out, st);
+  if (nex > 0) {
+    rc = check_indices(fn, ex_idx, T * H * nex, (int64_t)S * S, st);
+    if (rc) return rc;
+  }
+  e = pk::launch_cartesian(hidx, w.half_score, T, H, S, k, bf16, q, subkeys, n, ex_idx, nex,
+                           idx_out, w_out, score_out, st);
   if (e != hipSuccess) return hip_status(e, fn);
   return PKMEM_OK;
 }
@@ -349,17 +358,27 @@ static int search_common(const char* fn, const void* q, pkmem_dtype q_dt, const 
 int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt, int64_t T,
                int H, int n, int S, int k, int64_t* idx_out, float* w_out, float* score_out,
                int32_t* half_idx_out, void* ws, size_t ws_bytes, pkmem_stream_t stream) {
-  return search_common("mem_search", q, q_dt, subkeys, k_dt, T, H, n, S, k, false, 0.f, idx_out,
-                       w_out, score_out, half_idx_out, nullptr, nullptr, ws, ws_bytes, stream);
+  return search_common("mem_search", q, q_dt, subkeys, k_dt, T, H, n, S, k, false, 0.f, 0, nullptr,
+                       idx_out, w_out, score_out, half_idx_out, nullptr, nullptr, ws, ws_bytes,
+                       stream);
 }
 
 int mem_search_qnorm(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
                      int64_t T, int H, int n, int S, int k, float eps, int64_t* idx_out,
                      float* w_out, float* score_out, int32_t* half_idx_out, void* qhat_out,
                      float* stats_out, void* ws, size_t ws_bytes, pkmem_stream_t stream) {
-  return search_common("mem_search_qnorm", q, q_dt, subkeys, k_dt, T, H, n, S, k, true, eps,
-                       idx_out, w_out, score_out, half_idx_out, qhat_out, stats_out, ws, ws_bytes,
-                       stream);
+  return search_common("mem_search_qnorm", q, q_dt, subkeys, k_dt, T, H, n, S, k, true, eps, 0,
+                       nullptr, idx_out, w_out, score_out, half_idx_out, qhat_out, stats_out, ws,
+                       ws_bytes, stream);
+}
+
+int mem_search_extra(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                     int64_t T, int H, int n, int S, int k, int r, const int64_t* extra_idx,
+                     int64_t* idx_out, float* w_out, float* score_out, int32_t* half_idx_out,
+                     void* ws, size_t ws_bytes, pkmem_stream_t stream) {
+  return search_common("mem_search_extra", q, q_dt, subkeys, k_dt, T, H, n, S, k, false, 0.f, r,
+                       extra_idx, idx_out, w_out, score_out, half_idx_out, nullptr, nullptr, ws,
+                       ws_bytes, stream);
 }
 
 size_t mem_search_backward_workspace_size(int64_t T, int H, int S, int k) {

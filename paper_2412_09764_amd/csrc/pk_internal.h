@@ -50,9 +50,13 @@ hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int
 // (qhat non-null) the normalised queries in the query dtype.
 hipError_t launch_qnorm(bool bf16, const void* q, int64_t rows, int n, float eps, float2* stats,
                         void* qhat, hipStream_t st);
+// nex extra key-value pairs per (token, head) (ex_idx [T,H,nex], scored from q
+// and the sub-keys) join the softmax after the k selected; outputs then have
+// k + nex slots per row.  nex = 0: q, subkeys and ex_idx are not read.
 hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T, int H,
-                            int S, int k, int64_t* idx_out, float* w_out, float* score_out,
-                            hipStream_t st);
+                            int S, int k, bool bf16, const void* q, const void* subkeys, int n,
+                            const int64_t* ex_idx, int nex, int64_t* idx_out, float* w_out,
+                            float* score_out, hipStream_t st);
 
 // ---- search backward (search_bwd.hip) --------------------------------------
 size_t search_backward_ws_bytes(int64_t T, int H, int k);

@@ -37,7 +37,8 @@
 // Step 2, k_cartesian: per (token, head) the top k of the sums s1[a] + s2[b]
 //   over rank pairs with (a+1)(b+1) <= k (every other pair is beaten by at
 //   least k pairs), ordered (sum desc, composed index i1*S + i2 asc), then the
-//   softmax over the k selected sums.
+//   softmax over the k selected sums (and over any extra key-value pairs the
+//   caller adds, scored in the same kernel).
 #include "pk_device.h"
 #include "pk_internal.h"
 
@@ -468,10 +469,19 @@ __global__ __launch_bounds__(256) void k_topk_fallback(const T* __restrict__ q,
   }
 }
 
-template <int E>
+// Extra key-value pairs (EXTRA): the row's nex caller-given composed indices
+// are scored like any full key, q1 . K1[i1] + q2 . K2[i2] (lane l holds
+// elements 4l..4l+3 of each half, fp32 products summed over the wave), and
+// occupy slots k .. k + nex - 1 after the selected ones; the softmax runs over
+// all k + nex.  An index outside [0, S*S) is read as 0 (no out-of-bounds
+// access) and written out as given.
+template <int E, typename T, bool EXTRA>
 __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ half_idx,
                                                    const float* __restrict__ half_score,
                                                    int64_t rows, int S, int k, int npairs,
+                                                   const T* __restrict__ q,
+                                                   const T* __restrict__ subkeys, int H, int n,
+                                                   const int64_t* __restrict__ ex_idx, int nex,
                                                    int64_t* __restrict__ idx_out,
                                                    float* __restrict__ w_out,
                                                    float* __restrict__ score_out) {
@@ -483,10 +493,82 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
   }
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < rows; r += (int64_t)gridDim.x * 4) {
-    const int32_t* i1 = half_idx + (size_t)r * 2 * k;
+  const int kk = EXTRA ? k + nex : k;  // slots per row
+  for (int64_t row = (int64_t)blockIdx.x * 4 + wave; row < rows; row += (int64_t)gridDim.x * 4) {
+    // extra pairs first: their loads overlap the candidate sort below
+    float ex_score = 0.f;
+    int64_t ex_given = 0;
+    if constexpr (EXTRA) {
+      const int h = (int)(row % H);
+      const int d = n >> 1;
+      const bool ql = lane * 4 < d;
+      const int qo = ql ? lane * 4 : 0;
+      float fa[4], fb[4];
+      {
+        QQuad<T> qa, qb;
+        qa.load(q + (size_t)row * n + qo);
+        qb.load(q + (size_t)row * n + d + qo);
+        qa.to_f32(fa);
+        qb.to_f32(fb);
+      }
+      const int64_t N = (int64_t)S * S;
+      ex_given = lane < nex ? ex_idx[(size_t)row * nex + lane] : 0;
+      const int64_t ex_safe = (ex_given >= 0 && ex_given < N) ? ex_given : 0;
+      const T* k1 = subkeys + (size_t)(h * 2) * S * d + qo;
+      const T* k2 = k1 + (size_t)S * d;
+      // eight extras at a time: their sub-key loads in flight together, then
+      // one transposed butterfly (4 + 2 + 1 + 3 exchanges) leaves extra j's
+      // sum in lanes 8j .. 8j + 7
+      for (int e0 = 0; e0 < nex; e0 += 8) {
+        QQuad<T> ka[8], kb[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int e = e0 + j < nex ? e0 + j : nex - 1;
+          const uint64_t ie = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)ex_safe, e) |
+                              ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(ex_safe >> 32), e) << 32);
+          const int i1 = (int)(ie / (uint64_t)S), i2 = (int)(ie % (uint64_t)S);
+          ka[j].load(k1 + (size_t)i1 * d);
+          kb[j].load(k2 + (size_t)i2 * d);
+        }
+        float p[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          float va[4], vb[4];
+          ka[j].to_f32(va);
+          kb[j].to_f32(vb);
+          float a = 0.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) a = fmaf(fa[i], va[i], a);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) a = fmaf(fb[i], vb[i], a);
+          p[j] = ql ? a : 0.f;
+        }
+        const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+        float p4[4], p2[2];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float send = b5 ? p[i] : p[i + 4];
+          p4[i] = (b5 ? p[i + 4] : p[i]) + __shfl_xor(send, 32, WAVE);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const float send = b4 ? p4[i] : p4[i + 2];
+          p2[i] = (b4 ? p4[i + 2] : p4[i]) + __shfl_xor(send, 16, WAVE);
+        }
+        float t1;
+        {
+          const float send = b3 ? p2[0] : p2[1];
+          t1 = (b3 ? p2[1] : p2[0]) + __shfl_xor(send, 8, WAVE);
+        }
+        t1 = group_sum<8>(t1);
+        const int src = (lane - e0) * 8;
+        const float got = __shfl(t1, src >= 0 && src < WAVE ? src : 0, WAVE);
+        if (lane >= e0 && lane < e0 + 8) ex_score = got;
+      }
+    }
+    const int32_t* i1 = half_idx + (size_t)row * 2 * k;
     const int32_t* i2 = i1 + k;
-    const float* s1 = half_score + (size_t)r * 2 * k;
+    const float* s1 = half_score + (size_t)row * 2 * k;
     const float* s2 = s1 + k;
     const float s1v = lane < k ? s1[lane] : 0.f;
     const float s2v = lane < k ? s2[lane] : 0.f;
@@ -503,14 +585,27 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
       v[e] = m < npairs ? make_key(sa + sb, (uint32_t)ia * (uint32_t)S + (uint32_t)ib) : 0ull;
     }
     wave_sort_desc<E>(v, lane);
-    const float z = key_score(v[0]);
-    const uint32_t ci = key_index(v[0]);
-    const float zmax = __shfl(z, 0, WAVE);
-    const float ex = lane < k ? expf(z - zmax) : 0.f;
+    float z = key_score(v[0]);
+    int64_t ci = (int64_t)key_index(v[0]);
+    float zmax;
+    if constexpr (EXTRA) {
+      const int src = lane >= k ? lane - k : 0;
+      const float zx = __shfl(ex_score, src, WAVE);
+      const int64_t ix = (int64_t)(((uint64_t)(uint32_t)__shfl((int)(ex_given >> 32), src, WAVE) << 32) |
+                                   (uint32_t)__shfl((int)(uint32_t)ex_given, src, WAVE));
+      if (lane >= k) { z = zx; ci = ix; }
+      float m = lane < kk ? z : -INFINITY;
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, WAVE));
+      zmax = m;
+    } else {
+      zmax = __shfl(z, 0, WAVE);
+    }
+    const float ex = lane < kk ? expf(z - zmax) : 0.f;
     const float sum = group_sum<WAVE>(ex);
-    if (lane < k) {
-      const size_t o = (size_t)r * k + lane;
-      idx_out[o] = (int64_t)ci;
+    if (lane < kk) {
+      const size_t o = (size_t)row * kk + lane;
+      idx_out[o] = ci;
       w_out[o] = ex / sum;
       if (score_out) score_out[o] = z;
     }
@@ -590,9 +685,29 @@ hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int
   return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
 }
 
+template <int E>
+static void cart_launch(dim3 g, dim3 b, hipStream_t st, const int32_t* half_idx,
+                        const float* half_score, int64_t rows, int S, int k, int np, bool bf16,
+                        const void* q, const void* subkeys, int H, int n, const int64_t* ex_idx,
+                        int nex, int64_t* idx_out, float* w_out, float* score_out) {
+  if (nex == 0)
+    hipLaunchKernelGGL((k_cartesian<E, uint16_t, false>), g, b, 0, st, half_idx, half_score, rows,
+                       S, k, np, (const uint16_t*)nullptr, (const uint16_t*)nullptr, H, n,
+                       (const int64_t*)nullptr, 0, idx_out, w_out, score_out);
+  else if (bf16)
+    hipLaunchKernelGGL((k_cartesian<E, uint16_t, true>), g, b, 0, st, half_idx, half_score, rows, S,
+                       k, np, (const uint16_t*)q, (const uint16_t*)subkeys, H, n, ex_idx, nex,
+                       idx_out, w_out, score_out);
+  else
+    hipLaunchKernelGGL((k_cartesian<E, float, true>), g, b, 0, st, half_idx, half_score, rows, S, k,
+                       np, (const float*)q, (const float*)subkeys, H, n, ex_idx, nex, idx_out,
+                       w_out, score_out);
+}
+
 hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T_, int H,
-                            int S, int k, int64_t* idx_out, float* w_out, float* score_out,
-                            hipStream_t st) {
+                            int S, int k, bool bf16, const void* q, const void* subkeys, int n,
+                            const int64_t* ex_idx, int nex, int64_t* idx_out, float* w_out,
+                            float* score_out, hipStream_t st) {
   const int64_t rows = T_ * H;
   const int np = cartesian_pairs(k);
   int64_t blocks = (rows + 3) / 4;
@@ -600,10 +715,10 @@ hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, in
   if (blocks < 1) blocks = 1;
   const dim3 g((unsigned)blocks), b(256);
   LaunchTimer lt("cartesian", st);
-  if (np <= 64) hipLaunchKernelGGL(k_cartesian<1>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
-  else if (np <= 128) hipLaunchKernelGGL(k_cartesian<2>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
-  else if (np <= 256) hipLaunchKernelGGL(k_cartesian<4>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
-  else hipLaunchKernelGGL(k_cartesian<8>, g, b, 0, st, half_idx, half_score, rows, S, k, np, idx_out, w_out, score_out);
+  if (np <= 64) cart_launch<1>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, idx_out, w_out, score_out);
+  else if (np <= 128) cart_launch<2>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, idx_out, w_out, score_out);
+  else if (np <= 256) cart_launch<4>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, idx_out, w_out, score_out);
+  else cart_launch<8>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, idx_out, w_out, score_out);
   return hipGetLastError();
 }
 

@@ -26,55 +26,6 @@
 
 namespace pk {
 
-// Four consecutive elements of a query or sub-key half row: bf16 (8 bytes) or
-// fp32 (16 bytes).
-template <typename T>
-struct QQuad;
-template <>
-struct QQuad<uint16_t> {
-  uint2 raw;
-  __device__ __forceinline__ void load(const uint16_t* p) { raw = *reinterpret_cast<const uint2*>(p); }
-  __device__ __forceinline__ void fma_into(float g, float* a) const {
-    a[0] = fmaf(g, __uint_as_float(raw.x << 16), a[0]);
-    a[1] = fmaf(g, __uint_as_float(raw.x & 0xffff0000u), a[1]);
-    a[2] = fmaf(g, __uint_as_float(raw.y << 16), a[2]);
-    a[3] = fmaf(g, __uint_as_float(raw.y & 0xffff0000u), a[3]);
-  }
-  __device__ __forceinline__ void to_f32(float* v) const {
-    v[0] = __uint_as_float(raw.x << 16);
-    v[1] = __uint_as_float(raw.x & 0xffff0000u);
-    v[2] = __uint_as_float(raw.y << 16);
-    v[3] = __uint_as_float(raw.y & 0xffff0000u);
-  }
-  // The same with the normalised query as scored (rounded to bf16).
-  __device__ __forceinline__ void fma_into_norm(float g, float* a, float mean, float rstd) const {
-    float v[4];
-    to_f32(v);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = fmaf(g, round_bf16_f32(qn_apply(v[i], mean, rstd)), a[i]);
-  }
-};
-template <>
-struct QQuad<float> {
-  float4 raw;
-  __device__ __forceinline__ void load(const float* p) { raw = *reinterpret_cast<const float4*>(p); }
-  __device__ __forceinline__ void fma_into(float g, float* a) const {
-    a[0] = fmaf(g, raw.x, a[0]);
-    a[1] = fmaf(g, raw.y, a[1]);
-    a[2] = fmaf(g, raw.z, a[2]);
-    a[3] = fmaf(g, raw.w, a[3]);
-  }
-  __device__ __forceinline__ void to_f32(float* v) const {
-    v[0] = raw.x; v[1] = raw.y; v[2] = raw.z; v[3] = raw.w;
-  }
-  __device__ __forceinline__ void fma_into_norm(float g, float* a, float mean, float rstd) const {
-    a[0] = fmaf(g, qn_apply(raw.x, mean, rstd), a[0]);
-    a[1] = fmaf(g, qn_apply(raw.y, mean, rstd), a[1]);
-    a[2] = fmaf(g, qn_apply(raw.z, mean, rstd), a[2]);
-    a[3] = fmaf(g, qn_apply(raw.w, mean, rstd), a[3]);
-  }
-};
-
 // Per (token, head) wave, per half: lane j holds rank j's sub-key; each lane
 // finds the leader of its sub-key group (lowest rank with the same sub-key)
 // and the group's gradient sum, in rank order.  Then

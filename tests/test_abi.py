@@ -285,3 +285,26 @@ def test_search_qnorm_noops_and_workspace(lib):
     # room for the per-query statistics on top of the plain search backward's needs
     need = lib.mem_search_backward_workspace_size(8, 2, 16, 4)
     assert sbwdqn(lib, ws_bytes=need - 1) == WORKSPACE
+
+
+def searchx(lib, T=8, k=4, r=3, ex=FAKE, S=16, ws_bytes=BIG_WS):
+    return lib.mem_search_extra(FAKE, BF16, FAKE, BF16, T, 2, 64, S, k, r, ex, FAKE, FAKE, None, None,
+                                FAKE, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(r=-1), INVALID, "r must"),
+    (dict(k=40, r=25, S=100), UNSUPPORTED, "k + r"),
+    (dict(ex=0), INVALID, "null"),
+    (dict(k=17), INVALID, "k <= S"),
+    (dict(ws_bytes=16), WORKSPACE, "workspace"),
+])
+def test_search_extra_rejects(lib, kw, code, text):
+    assert searchx(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def test_search_extra_noops(lib):
+    assert searchx(lib, T=0) == OK
+    assert searchx(lib, T=0, ex=0) == OK
+    assert searchx(lib, T=0, r=0, ex=0) == OK
