@@ -58,6 +58,10 @@ SEARCH_CASES = [
     ("bf16_S3000_d256_ragged_chunk", 3000, 2, 512, 32, 33, torch.bfloat16),
     ("bf16_T1", 1024, 4, 512, 32, 1, torch.bfloat16),
     ("f32_d4_k3", 90, 2, 8, 3, 47, torch.float32),
+    ("bf16_S1_k1", 1, 2, 16, 1, 70, torch.bfloat16),
+    ("f32_S1_d4", 1, 1, 8, 1, 5, torch.float32),
+    ("bf16_S2_k2_H8", 2, 8, 16, 2, 300, torch.bfloat16),
+    ("bf16_H16_S64", 64, 16, 32, 8, 40, torch.bfloat16),
 ]
 
 

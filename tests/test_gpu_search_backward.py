@@ -22,6 +22,9 @@ CASES = [
     ("bf16_d8_ties", 50, 3, 16, 10, 77, torch.bfloat16),
     ("bf16_S8192_d256", 8192, 1, 512, 16, 300, torch.bfloat16),
     ("f32_S3000_d24_k64", 3000, 2, 48, 64, 45, torch.float32),
+    ("bf16_S1_k1", 1, 2, 16, 1, 70, torch.bfloat16),
+    ("bf16_S2_k2_H8", 2, 8, 16, 2, 300, torch.bfloat16),
+    ("bf16_H16_S64", 64, 16, 32, 8, 40, torch.bfloat16),
 ]
 
 
