@@ -242,14 +242,18 @@ LaunchTimer::LaunchTimer(const char* name, hipStream_t st) : st_(st) {
   if (slot < 0) return;
   hipEvent_t a, b;
   if (hipEventCreate(&a) != hipSuccess) return;
-  if (hipEventCreate(&b) != hipSuccess) { hipEventDestroy(a); return; }
-  hipEventRecord(a, st_);
+  if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+  if (hipEventRecord(a, st_) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    (void)hipEventDestroy(b);
+    return;
+  }
   stop_ = b;
   g_timer.events.push_back({slot, a, b});
 }
 
 LaunchTimer::~LaunchTimer() {
-  if (stop_) hipEventRecord(stop_, st_);
+  if (stop_) (void)hipEventRecord(stop_, st_);
 }
 
 }  // namespace pk
@@ -291,8 +295,8 @@ int mem_timer_read(float* ms_out, int* kernel_out, int cap) {
       if (kernel_out) kernel_out[n] = ev.kernel;
     }
     ++n;
-    hipEventDestroy(ev.start);
-    hipEventDestroy(ev.stop);
+    (void)hipEventDestroy(ev.start);
+    (void)hipEventDestroy(ev.stop);
   }
   g_timer.events.clear();
   if (err != hipSuccess) return hip_status(err, "mem_timer_read");
