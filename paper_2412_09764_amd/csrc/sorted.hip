@@ -15,6 +15,11 @@
 //      row's gradient (sparse).  Rows are visited in ascending order, so the
 //      value and gradient tables are streamed nearly sequentially, and the
 //      result is bitwise deterministic.
+//   4. A row with more than LONG_SEG lookups would hold one lane group for
+//      its whole length: the per-row kernel lists it instead, and a second
+//      kernel gives each listed row a workgroup whose lane groups take
+//      contiguous runs of its lookups; their partial sums meet in LDS and are
+//      added in group order (still deterministic).
 #include "pk_device.h"
 #include "pk_internal.h"
 
@@ -25,6 +30,8 @@ constexpr int RADIX = 1 << RADIX_BITS;
 constexpr int SORT_ITEMS = 16;                 // keys per thread per tile
 constexpr int SORT_TILE = 256 * SORT_ITEMS;    // keys per workgroup tile
 constexpr int SCAN_ITEMS = 8;
+constexpr uint32_t LONG_SEG = 1024;  // lookups of a row beyond which it is split
+constexpr int LONG_WAVES = 8;        // waves of the workgroup that takes a long row
 constexpr int SCAN_TILE = 256 * SCAN_ITEMS;
 
 static inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -270,7 +277,10 @@ struct Quad<float> {
   __device__ static __forceinline__ raw zero() { return uint4{0, 0, 0, 0}; }
 };
 
-// One lane group per touched row.  Value and gradient rows are streamed once
+// One lane group per touched row.  A row with more than LONG_SEG lookups is
+// taken as empty here (its gradient row is written back unchanged, or as zero
+// in the sparse form) and summed afterwards by k_bag_bwd_long, in stream
+// order.  Value and gradient rows are streamed once
 // per step with non-temporal accesses, so they do not push the re-read dy rows
 // and metadata out of the caches.  A lane group takes SB adjacent segments per
 // iteration (loads of all of them, then all of their gradient-row stores: one
@@ -313,6 +323,7 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
     const bool live = u0 + b < U;
     s0[b] = live ? seg_start[u0 + b] : 0;
     s1[b] = live ? seg_start[u0 + b + 1] : 0;
+    if (s1[b] - s0[b] > LONG_SEG) s1[b] = s0[b];  // summed by k_bag_bwd_long
     row[b] = live ? (int64_t)rows_sorted[s0[b]] : 0;
   }
   while (u0 < U) {
@@ -339,6 +350,7 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
       const bool live = un + b < U;
       s0n[b] = live ? seg_start[un + b] : 0;
       s1n[b] = live ? seg_start[un + b + 1] : 0;
+      if (s1n[b] - s0n[b] > LONG_SEG) s1n[b] = s0n[b];
     }
 #pragma unroll
     for (int b = 0; b < SB; ++b) {
@@ -422,8 +434,9 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
 
 // -------------------------------------------------------------- launcher ----
 struct SortedWs {
-  uint32_t *keys_a, *vals_a, *keys_b, *vals_b, *hist, *sums, *seg, *misc;
+  uint32_t *keys_a, *vals_a, *keys_b, *vals_b, *hist, *sums, *seg, *misc, *long_list;
 };
+static int64_t max_long(int64_t L) { return L / LONG_SEG + 1; }
 
 static SortedWs carve(void* ws, int64_t L) {
   const int64_t nblk = cdiv(L, SORT_TILE);
@@ -439,7 +452,8 @@ static SortedWs carve(void* ws, int64_t L) {
   w.hist = take(4 * (size_t)scan_n);
   w.sums = take(4 * (size_t)(cdiv(scan_n, SCAN_TILE) + 1));
   w.seg = take(4 * (size_t)(L + 1));
-  w.misc = take(256);
+  w.misc = take(256);  // [0] segments, [1] long rows listed
+  w.long_list = take(4 * (size_t)max_long(L));
   return w;
 }
 
@@ -448,7 +462,8 @@ size_t sorted_workspace_bytes(int64_t L) {
   const int64_t hist_n = (int64_t)RADIX * nblk;
   const int64_t scan_n = (hist_n > L + 1 ? hist_n : L + 1);
   return 4 * align256(4 * (size_t)L) + align256(4 * (size_t)scan_n) +
-         align256(4 * (size_t)(cdiv(scan_n, SCAN_TILE) + 1)) + align256(4 * (size_t)(L + 1)) + 256;
+         align256(4 * (size_t)(cdiv(scan_n, SCAN_TILE) + 1)) + align256(4 * (size_t)(L + 1)) + 256 +
+         align256(4 * (size_t)max_long(L));
 }
 
 // Stable LSD radix sort of L keys (< 2^key_bits, from an int64 or a u32 array)
@@ -524,6 +539,123 @@ hipError_t scan_exclusive_u32(uint32_t* data, int64_t n, uint32_t* sums, hipStre
   return exclusive_scan(data, n, sums, st);
 }
 
+// Segments longer than LONG_SEG lookups, listed (in no particular order: each
+// is then summed on its own) for k_bag_bwd_long; k_bag_bwd_rows skips them.
+__global__ __launch_bounds__(256) void k_list_long(const uint32_t* __restrict__ seg_start,
+                                                   const uint32_t* __restrict__ nseg,
+                                                   uint32_t* __restrict__ long_list,
+                                                   uint32_t* __restrict__ long_cnt) {
+  const uint32_t U = *nseg;
+  for (uint32_t u = blockIdx.x * 256 + threadIdx.x; u < U; u += gridDim.x * 256)
+    if (seg_start[u + 1] - seg_start[u] > LONG_SEG) long_list[atomicAdd(long_cnt, 1u)] = u;
+}
+
+// Rows listed by k_list_long (more than LONG_SEG lookups), one workgroup
+// per row at a time: its ng lane groups (ng = LONG_WAVES * WAVE / CL, fewer
+// when the partial rows would not fit 64 KiB of LDS) take contiguous runs of
+// the row's lookups in lookup order, each writing grad_w and summing w * dy
+// into a partial row; the partials go to LDS and are added, in group order,
+// to the old gradient row (dense) or written as the row's gradient (sparse).
+template <typename V, int NQ, int CL, bool SPARSE>
+__global__ __launch_bounds__(64 * LONG_WAVES) void k_bag_bwd_long(
+    const V* __restrict__ dy, const V* __restrict__ values, int D, const float* __restrict__ w,
+    int bag, const uint32_t* __restrict__ rows_sorted, const uint32_t* __restrict__ lookups,
+    const uint32_t* __restrict__ seg_start, const uint32_t* __restrict__ long_list,
+    const uint32_t* __restrict__ long_cnt, float* __restrict__ grad_values,
+    int64_t* __restrict__ rows_out, float* __restrict__ grad_rows_out,
+    float* __restrict__ grad_w) {
+  using Q = Quad<V>;
+  constexpr int G = WAVE / CL;
+  constexpr int PB = RowsBatch<NQ, CL>::value;
+  extern __shared__ float part[];  // [ng][D]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = wave * G + lane / CL, cl = lane % CL;
+  const int nquad = D / 4;
+  int ng = LONG_WAVES * G;
+  if (ng > 16384 / D) ng = 16384 / D;  // 64 KiB of partial rows
+  const bool mine = grp < ng;
+  const bool dense = !SPARSE && grad_values != nullptr;
+  bool ok[NQ];
+#pragma unroll
+  for (int m = 0; m < NQ; ++m) ok[m] = mine && (m * CL + cl) < nquad;
+  const uint32_t nlong = *long_cnt;
+  for (uint32_t it = blockIdx.x; it < nlong; it += gridDim.x) {
+    const uint32_t u = long_list[it];
+    const uint32_t s0 = seg_start[u], s1 = seg_start[u + 1];
+    const int64_t row = (int64_t)rows_sorted[s0];
+    const uint32_t len = s1 - s0;
+    const uint32_t per = (len + (uint32_t)ng - 1) / (uint32_t)ng;
+    uint32_t a = mine ? (uint32_t)grp * per : len, z = mine ? (uint32_t)(grp + 1) * per : len;
+    a = (a < len ? a : len) + s0;
+    z = (z < len ? z : len) + s0;
+    typename Q::raw vraw[NQ];
+    float acc[NQ][4];
+#pragma unroll
+    for (int m = 0; m < NQ; ++m) {
+      vraw[m] = ok[m] ? Q::load(values + row * D + (size_t)(m * CL + cl) * 4) : Q::zero();
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[m][e] = 0.f;
+    }
+    for (uint32_t s = a; s < z; s += PB) {
+      const uint32_t nb = (z - s) < (uint32_t)PB ? (z - s) : (uint32_t)PB;
+      const uint32_t lid = (uint32_t)cl < nb ? lookups[s + cl] : 0u;
+      const float wl = (uint32_t)cl < nb ? w[lid] : 0.f;
+      typename Q::raw graw[PB][NQ];
+#pragma unroll
+      for (int pp = 0; pp < PB; ++pp) {
+        const uint32_t lp = __shfl(lid, pp, CL);
+        const int64_t t = lp / (uint32_t)bag;
+#pragma unroll
+        for (int m = 0; m < NQ; ++m)
+          graw[pp][m] = (ok[m] && (uint32_t)pp < nb) ? Q::load(dy + t * D + (size_t)(m * CL + cl) * 4)
+                                                     : Q::zero();
+      }
+      float part_w[PB];
+#pragma unroll
+      for (int pp = 0; pp < PB; ++pp) {
+        const float ww = __shfl(wl, pp, CL);
+        part_w[pp] = 0.f;
+#pragma unroll
+        for (int m = 0; m < NQ; ++m) {
+          float g[4], v[4];
+          Q::unpack(graw[pp][m], g);
+          Q::unpack(vraw[m], v);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[m][e] = fmaf(ww, g[e], acc[m][e]);
+            part_w[pp] = fmaf(g[e], v[e], part_w[pp]);
+          }
+        }
+      }
+#pragma unroll
+      for (int pp = 0; pp < PB; ++pp) part_w[pp] = group_sum<CL>(part_w[pp]);
+      float gwv = part_w[0];
+#pragma unroll
+      for (int pp = 1; pp < PB; ++pp) gwv = (cl == pp) ? part_w[pp] : gwv;
+      if ((uint32_t)cl < nb) grad_w[lid] = gwv;
+    }
+#pragma unroll
+    for (int m = 0; m < NQ; ++m)
+      if (ok[m]) {
+        float* d = part + (size_t)grp * D + (size_t)(m * CL + cl) * 4;
+        d[0] = acc[m][0]; d[1] = acc[m][1]; d[2] = acc[m][2]; d[3] = acc[m][3];
+      }
+    __syncthreads();
+    for (int qd = threadIdx.x; qd < nquad; qd += blockDim.x) {
+      float4 tot = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (dense) tot = *reinterpret_cast<const float4*>(grad_values + row * D + (size_t)qd * 4);
+      for (int gi = 0; gi < ng; ++gi) {
+        const float* sp = part + (size_t)gi * D + (size_t)qd * 4;
+        tot.x += sp[0]; tot.y += sp[1]; tot.z += sp[2]; tot.w += sp[3];
+      }
+      float* dst = SPARSE ? grad_rows_out + (size_t)u * D : grad_values + row * D;
+      if (SPARSE || dense) *reinterpret_cast<float4*>(dst + (size_t)qd * 4) = tot;
+    }
+    if (SPARSE && threadIdx.x == 0) rows_out[u] = row;
+    __syncthreads();  // the partial rows are reused for the next listed row
+  }
+}
+
 hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* values, int64_t N,
                                       int D, const int64_t* idx, const float* w, int64_t T,
                                       int bag, float* grad_values, int64_t* rows_out,
@@ -532,7 +664,7 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
   const int64_t L = T * bag;
   SortedWs b = carve(ws, L);
   if (num_rows_dev) *num_rows_dev = b.misc;
-  hipError_t e = launch_fill_u32(b.misc, 0u, 1, st);
+  hipError_t e = launch_fill_u32(b.misc, 0u, 2, st);
   if (e != hipSuccess || L == 0) return e;
   const uint32_t* ks = nullptr;
   const uint32_t* vs = nullptr;
@@ -552,22 +684,34 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
   if (blocks > 16384) blocks = 16384;
   const dim3 grid((unsigned)blocks), block(256);
   const bool sparse = rows_out != nullptr;
+  int64_t lblocks = max_long(L);
+  if (lblocks > 512) lblocks = 512;
+  const int ngrp_cap = 16384 / D;  // partial rows that fit 64 KiB
+  {
+    int64_t gb = cdiv(L, 256);
+    if (gb > 2048) gb = 2048;
+    hipLaunchKernelGGL(k_list_long, dim3((unsigned)gb), dim3(256), 0, st, b.seg, b.misc,
+                       b.long_list, b.misc + 1);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   LaunchTimer lt("bag_backward_rows", st);
+#define PK_ROWS_ONE(VT, NQ, CL, SP)                                                                \
+  {                                                                                                \
+    hipLaunchKernelGGL((k_bag_bwd_rows<VT, NQ, CL, SP, PK_ROWS_BATCH>), grid, block, 0, st,       \
+                       (const VT*)dy, (const VT*)values, D, w, bag, ks, vs, b.seg, b.misc,         \
+                       grad_values, rows_out, grad_rows_out, grad_w);                             \
+    const int ng = (LONG_WAVES * (WAVE / CL)) < ngrp_cap ? LONG_WAVES * (WAVE / CL) : ngrp_cap;    \
+    hipLaunchKernelGGL((k_bag_bwd_long<VT, NQ, CL, SP>), dim3((unsigned)lblocks),                  \
+                       dim3(64 * LONG_WAVES), (size_t)ng * D * sizeof(float), st, (const VT*)dy,   \
+                       (const VT*)values, D, w, bag, ks, vs, b.seg, b.long_list, b.misc + 1,       \
+                       grad_values, rows_out, grad_rows_out, grad_w);                             \
+  }
 #define PK_ROWS(NQ, CL)                                                                           \
   if (bf16) {                                                                                     \
-    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, NQ, CL, true, PK_ROWS_BATCH>), grid, block, 0, st,   \
-        (const uint16_t*)dy, (const uint16_t*)values, D, w, bag, ks, vs, b.seg, b.misc,            \
-        grad_values, rows_out, grad_rows_out, grad_w);                                            \
-    else hipLaunchKernelGGL((k_bag_bwd_rows<uint16_t, NQ, CL, false, PK_ROWS_BATCH>), grid, block, 0, st,        \
-        (const uint16_t*)dy, (const uint16_t*)values, D, w, bag, ks, vs, b.seg, b.misc,            \
-        grad_values, rows_out, grad_rows_out, grad_w);                                            \
+    if (sparse) PK_ROWS_ONE(uint16_t, NQ, CL, true) else PK_ROWS_ONE(uint16_t, NQ, CL, false)     \
   } else {                                                                                        \
-    if (sparse) hipLaunchKernelGGL((k_bag_bwd_rows<float, NQ, CL, true, PK_ROWS_BATCH>), grid, block, 0, st,      \
-        (const float*)dy, (const float*)values, D, w, bag, ks, vs, b.seg, b.misc, grad_values,     \
-        rows_out, grad_rows_out, grad_w);                                                         \
-    else hipLaunchKernelGGL((k_bag_bwd_rows<float, NQ, CL, false, PK_ROWS_BATCH>), grid, block, 0, st,           \
-        (const float*)dy, (const float*)values, D, w, bag, ks, vs, b.seg, b.misc, grad_values,     \
-        rows_out, grad_rows_out, grad_w);                                                         \
+    if (sparse) PK_ROWS_ONE(float, NQ, CL, true) else PK_ROWS_ONE(float, NQ, CL, false)           \
   }
   if (nquad > 512) { PK_ROWS(16, 64); }
   else if (nquad > 256) { PK_ROWS(8, 64); }
@@ -580,6 +724,7 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
   else if (nquad > 2) { PK_ROWS(1, 4); }
   else { PK_ROWS(1, 2); }
 #undef PK_ROWS
+#undef PK_ROWS_ONE
   return hipGetLastError();
 }
 
