@@ -59,10 +59,24 @@ Function pins (tests under tests/test_oracle_*.py):
   search_backward_qnorm
                    central finite differences in the raw queries at a fixed
                    selection; torch autograd through layer_norm (fp64)
+  search_sink, search_backward_sink
+                   zero sink key: logit 0, weights exp(z) / (1 + sum exp(z));
+                   a sink whose score dominates takes the whole weight; the
+                   other slots as `search_extra`; gradients by central
+                   differences and torch autograd (fp64)
   search_extra     r = 0 gives `search`; every extra slot's score equals the
                    brute-force full-key score of its index; an extra that
                    repeats a selected index repeats its score; the weights
                    are the closed-form softmax of the k + r scores
+
+Fixed ("sink") key-value pair (Sec. 5.4, model ablations, names one fixed
+key-value pair added to the selected ones as an anchor, without a formula).
+Reading: per head a key k_s[h] in R^n and a value row given by the caller (a
+row of the value table the caller adds, so the bag treats it as any other
+lookup); its score is the query's dot product with k_s[h], like any key's;
+it takes one more slot after the selected (and extra) ones and joins their
+softmax.  k_s = 0 gives the constant logit 0, the softmax with one added to
+its denominator.
 
 Extra key-value pairs (Sec. 5.4, model ablations, names adding random
 key-value pairs beside the top-k during pre-training, without a formula).
@@ -106,6 +120,8 @@ __all__ = [
     "search_qnorm",
     "search_backward_qnorm",
     "search_extra",
+    "search_sink",
+    "search_backward_sink",
 ]
 
 
@@ -495,3 +511,47 @@ def search_extra(q: np.ndarray, subkeys: np.ndarray, k: int, extra_idx: np.ndarr
                 score[t, h, k + e] = q[t, h, :d] @ K[h, 0, i1] + q[t, h, d:] @ K[h, 1, i2]
             w[t, h] = softmax(score[t, h])
     return dict(idx=idx, score=score, w=w, half_idx=base["half_idx"], half_score=base["half_score"])
+
+
+def search_sink(q: np.ndarray, subkeys: np.ndarray, k: int, extra_idx: np.ndarray,
+                sink_keys: np.ndarray, sink_row0: int) -> dict:
+    """`search_extra` plus one fixed key-value pair per head in the last slot:
+    score q[t,h] . sink_keys[h] (over all n elements), index sink_row0 + h
+    (the value-table row holding head h's sink value).  Softmax over all
+    k + r + 1 slots.  Returns idx, score, w of shape [T, H, k + r + 1]."""
+    q = _f64(q)
+    ks = _f64(sink_keys)
+    T, H, n = q.shape
+    assert ks.shape == (H, n)
+    base = search_extra(q, subkeys, k, extra_idx)
+    kk = base["idx"].shape[2] + 1
+    idx = np.zeros((T, H, kk), dtype=np.int64)
+    score = np.zeros((T, H, kk))
+    w = np.zeros((T, H, kk))
+    for t in range(T):
+        for h in range(H):
+            idx[t, h, :-1] = base["idx"][t, h]
+            score[t, h, :-1] = base["score"][t, h]
+            idx[t, h, -1] = sink_row0 + h
+            score[t, h, -1] = q[t, h] @ ks[h]
+            w[t, h] = softmax(score[t, h])
+    return dict(idx=idx, score=score, w=w, half_idx=base["half_idx"], half_score=base["half_score"])
+
+
+def search_backward_sink(q: np.ndarray, subkeys: np.ndarray, idx: np.ndarray, grad_z: np.ndarray,
+                         sink_keys: np.ndarray, grad_subkeys_in=None, grad_sink_in=None) -> dict:
+    """Gradients of the scores of `search_sink` (selection fixed): the first
+    k + r slots as `search_backward`, the last slot z = q . sink_keys[h]:
+      grad_q[t,h]      += grad_z[t,h,-1] * sink_keys[h]
+      grad_sink[h]     += sum_t grad_z[t,h,-1] * q[t,h]   (accumulated)."""
+    q = _f64(q)
+    ks = _f64(sink_keys)
+    gz = _f64(grad_z)
+    r = search_backward(q, subkeys, np.asarray(idx)[..., :-1], gz[..., :-1], grad_subkeys_in)
+    grad_q = r["grad_q"] + gz[..., -1:] * ks[None, :, :]
+    grad_sink = np.zeros(ks.shape) if grad_sink_in is None else _f64(grad_sink_in).copy()
+    T, H, _ = q.shape
+    for h in range(H):
+        for t in range(T):
+            grad_sink[h] += gz[t, h, -1] * q[t, h]
+    return dict(grad_q=grad_q, grad_K=r["grad_K"], grad_sink=grad_sink)

@@ -512,3 +512,74 @@ def check_search_extra(extra_fn, search_fn, brute_fn, rng, T=5, H=2, S=6, d=3, k
     z = out["score"]
     np.testing.assert_allclose(out["w"], np.exp(z) / np.exp(z).sum(-1, keepdims=True), rtol=1e-12)
     np.testing.assert_allclose(out["w"].sum(-1), 1.0, rtol=1e-14)
+
+
+# ------------------------------------------------------------ sink pair ----
+def check_search_sink(sink_fn, extra_fn, rng, T=4, H=2, S=6, d=3, k=3, r=2):
+    """Sink pair: with a zero key the sink's logit is 0 and the weights are
+    exp(z_j) / (1 + sum exp(z)) over the other slots (closed form); the other
+    slots are exactly `search_extra`'s; a sink key that scores far above every
+    key takes the whole weight; the sink slot carries row sink_row0 + h."""
+    n = 2 * d
+    q = rng.standard_normal((T, H, n))
+    K = rng.standard_normal((H, 2, S, d))
+    ex = rng.integers(0, S * S, size=(T, H, r))
+    base = extra_fn(q, K, k, ex)
+    out = sink_fn(q, K, k, ex, np.zeros((H, n)), 1000)
+    np.testing.assert_array_equal(out["idx"][..., :-1], base["idx"])
+    np.testing.assert_array_equal(out["idx"][..., -1], 1000 + np.arange(H)[None, :].repeat(T, 0))
+    np.testing.assert_allclose(out["score"][..., :-1], base["score"], rtol=0, atol=0)
+    assert not out["score"][..., -1].any()
+    e = np.exp(base["score"])
+    np.testing.assert_allclose(out["w"][..., :-1], e / (1.0 + e.sum(-1, keepdims=True)), rtol=1e-12)
+    np.testing.assert_allclose(out["w"][..., -1], 1.0 / (1.0 + e.sum(-1)), rtol=1e-12)
+    # a sink key equal to a real key (its two sub-keys concatenated), also
+    # passed as the last extra index: the two slots must score alike
+    ij = rng.integers(0, S, size=(H, 2))
+    ks_real = np.stack([np.concatenate([K[h, 0, ij[h, 0]], K[h, 1, ij[h, 1]]]) for h in range(H)])
+    ex2 = ex.copy()
+    ex2[..., -1] = (ij[:, 0] * S + ij[:, 1])[None, :]
+    same = sink_fn(q, K, k, ex2, ks_real, 0)
+    np.testing.assert_allclose(same["score"][..., -1], same["score"][..., -2], rtol=1e-12, atol=1e-12)
+    ks = np.stack([1e3 * q[:, h].sum(0) / np.linalg.norm(q[:, h].sum(0)) for h in range(H)])
+    hot = sink_fn(q, K, k, ex, ks, 7)
+    z = hot["score"]
+    dominant = (z[..., -1] > z[..., :-1].max(-1) + 60.0)
+    assert dominant.any()
+    np.testing.assert_allclose(hot["w"][..., -1][dominant], 1.0, rtol=1e-12)
+
+
+def check_search_backward_sink(sink_fn, bwd_fn, rng, T=3, H=2, S=5, d=2, k=2, r=1, h=1e-6):
+    """Sink gradients at a fixed selection: central differences in q and in the
+    sink keys of L = sum(gz * z), torch autograd (fp64), accumulation."""
+    n = 2 * d
+    q = rng.standard_normal((T, H, n))
+    K = rng.standard_normal((H, 2, S, d))
+    ks = rng.standard_normal((H, n))
+    ex = rng.integers(0, S * S, size=(T, H, r))
+    sel = sink_fn(q, K, k, ex, ks, S * S)
+    idx = sel["idx"]
+    gz = rng.standard_normal(idx.shape)
+    g = bwd_fn(q, K, idx, gz, ks)
+
+    def L(qq, kk):
+        z = selected_scores(qq, K, idx[..., :-1])
+        zs = np.einsum("thn,hn->th", qq, kk)
+        return float((z * gz[..., :-1]).sum() + (zs * gz[..., -1]).sum())
+
+    for (t, hh, e) in [(0, 0, 0), (2, 1, 3), (1, 0, 2)]:
+        qp = q.copy(); qp[t, hh, e] += h
+        qm = q.copy(); qm[t, hh, e] -= h
+        assert abs((L(qp, ks) - L(qm, ks)) / (2 * h) - g["grad_q"][t, hh, e]) < 1e-7
+    for (hh, e) in [(0, 1), (1, 3)]:
+        kp = ks.copy(); kp[hh, e] += h
+        km = ks.copy(); km[hh, e] -= h
+        assert abs((L(q, kp) - L(q, km)) / (2 * h) - g["grad_sink"][hh, e]) < 1e-7
+    qt = torch.tensor(q, requires_grad=True)
+    kt = torch.tensor(ks, requires_grad=True)
+    zs = (qt * kt[None]).sum(-1)
+    (zs * torch.tensor(gz[..., -1])).sum().backward()
+    np.testing.assert_allclose(g["grad_sink"], kt.grad.numpy(), rtol=1e-12, atol=1e-14)
+    base = rng.standard_normal(ks.shape)
+    g2 = bwd_fn(q, K, idx, gz, ks, None, base)
+    np.testing.assert_allclose(g2["grad_sink"], base + g["grad_sink"], rtol=1e-14, atol=1e-15)

@@ -411,3 +411,57 @@ def test_catches_extra_scored_with_one_half_only():
                 out["w"][t, h] = np.exp(z - z.max()) / np.exp(z - z.max()).sum()
         return out
     assert _extra_fails(mutant) > 0
+
+
+# ------------------------------------------------------------ sink pair ----
+def _sink_fails(fn=None, bwd=None):
+    failures = 0
+    for s in range(2):
+        try:
+            pins.check_search_sink(fn or oracle.search_sink, oracle.search_extra,
+                                   np.random.default_rng(180 + s))
+        except (AssertionError, ValueError, IndexError):
+            failures += 1
+        try:
+            pins.check_search_backward_sink(fn or oracle.search_sink, bwd or oracle.search_backward_sink,
+                                            np.random.default_rng(190 + s))
+        except (AssertionError, ValueError, IndexError):
+            failures += 1
+    return failures
+
+
+def test_real_sink_passes():
+    assert _sink_fails() == 0
+
+
+def test_catches_sink_outside_the_softmax():
+    def mutant(q, K, k, ex, ks, row0):
+        out = oracle.search_sink(q, K, k, ex, ks, row0)
+        base = oracle.search_extra(q, K, k, ex)
+        out["w"][..., :-1] = base["w"]
+        out["w"][..., -1] = 0.0
+        return out
+    assert _sink_fails(fn=mutant) > 0
+
+
+def test_catches_sink_scored_on_one_half():
+    def mutant(q, K, k, ex, ks, row0):
+        ks = np.asarray(ks, float).copy()
+        ks[:, ks.shape[1] // 2:] = 0.0
+        return oracle.search_sink(q, K, k, ex, ks, row0)
+    assert _sink_fails(fn=mutant) > 0
+
+
+def test_catches_sink_key_gradient_not_accumulated():
+    def bwd(q, K, idx, gz, ks, gK=None, gs=None):
+        return oracle.search_backward_sink(q, K, idx, gz, ks, gK, None)
+    assert _sink_fails(bwd=bwd) > 0
+
+
+def test_catches_sink_query_gradient_dropped():
+    def bwd(q, K, idx, gz, ks, gK=None, gs=None):
+        out = oracle.search_backward_sink(q, K, idx, gz, ks, gK, gs)
+        r = oracle.search_backward(q, K, np.asarray(idx)[..., :-1], np.asarray(gz)[..., :-1], gK)
+        out["grad_q"] = r["grad_q"]
+        return out
+    assert _sink_fails(bwd=bwd) > 0
