@@ -122,13 +122,40 @@ int mem_search_extra(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem
                      void* ws, size_t ws_bytes, pkmem_stream_t stream);
 
 /* ------------------------------------------------------------------------ *
+ * Search with a fixed ("sink") key-value pair (Sec. 5.4, model ablations: one
+ * fixed key-value pair added beside the selected ones).  mem_search_extra
+ * plus one more slot per (t, h): the key sink_keys[h, 0:n] is scored like any
+ * full key, z = q[t,h,:] . sink_keys[h,:] (a zero key gives the constant
+ * logit 0, one added to the softmax's denominator), and the slot's index is
+ * sink_row0 + h, a row of the value table that holds head h's sink value
+ * (the caller appends H such rows after the S*S key rows).
+ *   sink_keys    [H, n] dtype k_dt, 16-byte aligned (trainable or fixed).
+ *   sink_row0    >= S*S: the value-table row of head 0's sink value.
+ *   r, extra_idx as for mem_search_extra (r = 0: none); k + r + 1 <= PKMEM_KMAX.
+ *   idx_out, w_out, score_out   [T, H, k + r + 1]: slots 0..k+r-1 as
+ *                mem_search_extra's, slot k + r the sink's; the softmax runs
+ *                over all k + r + 1.  half_idx_out [T, H, 2, k] as mem_search's.
+ * The value bag and its backward take these outputs as they are, with
+ * k + r + 1 in place of k (the sink value's gradient lands in its row);
+ * the search backward is mem_search_backward_sink.
+ * Workspace: mem_search_workspace_size(T, H, S, k).
+ * ------------------------------------------------------------------------ */
+int mem_search_sink(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                    int64_t T, int H, int n, int S, int k, int r, const int64_t* extra_idx,
+                    const void* sink_keys, int64_t sink_row0,
+                    int64_t* idx_out, float* w_out, float* score_out, int32_t* half_idx_out,
+                    void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
  * Search backward: gradient of the selected scores with respect to the
  * queries and the sub-keys (the keys are trainable parameters, Sec. 3; the
  * selection is piecewise constant and passes no gradient).  With
  * i1 = idx / S, i2 = idx % S the score of rank j is
  *   z[t,h,j] = q[t,h,0:d] . subkeys[h,0,i1] + q[t,h,d:n] . subkeys[h,1,i2].
  *
- *   q, subkeys, T, H, n, S, k   as for mem_search (same dtype rules and limits).
+ *   q, subkeys, T, H, n, S  as for mem_search (same dtype rules and limits).
+ *   k            slots per row, 1 <= k <= PKMEM_KMAX (k + r after mem_search_extra,
+ *                which may exceed S).
  *   idx          [T, H, k] int64  mem_search's selection; lookups whose index lies
  *                outside [0, S*S) contribute nothing (mem_search never writes one).
  *   grad_scores  [T, H, k] fp32   dL/dz (mem_bag_backward's grad_scores).
@@ -148,6 +175,28 @@ int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pk
                         int64_t T, int H, int n, int S, int k, const int64_t* idx,
                         const float* grad_scores, float* grad_q, float* grad_subkeys,
                         void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * Search backward of mem_search_sink (same q, sub-keys, sink keys and
+ * selection).  k is the number of product-key slots per row (k + r of the
+ * forward); idx and grad_scores are [T, H, k + 1], slot k the sink's (its
+ * index is not read).  Slots 0..k-1 as mem_search_backward; the sink's score
+ * z = q . sink_keys[h] adds
+ *   grad_q[t,h,:]    += grad_scores[t,h,k] * sink_keys[h,:]   (grad_q written),
+ *   grad_sink[h,:]   += sum_t grad_scores[t,h,k] * q[t,h,:]   (ACCUMULATED),
+ * grad_sink [H, n] fp32, bitwise deterministic (per-chunk partial sums added
+ * in chunk order, no atomics); any of the three outputs may be NULL.
+ * Limits and errors as for mem_search_backward, with k + 1 <= PKMEM_KMAX.
+ * Workspace: mem_search_backward_sink_workspace_size(T, H, n, S, k) bytes,
+ * 256-byte aligned.
+ * ------------------------------------------------------------------------ */
+size_t mem_search_backward_sink_workspace_size(int64_t T, int H, int n, int S, int k);
+
+int mem_search_backward_sink(const void* q, pkmem_dtype q_dt, const void* subkeys,
+                             pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k,
+                             const int64_t* idx, const float* grad_scores, const void* sink_keys,
+                             float* grad_q, float* grad_subkeys, float* grad_sink,
+                             void* ws, size_t ws_bytes, pkmem_stream_t stream);
 
 /* ------------------------------------------------------------------------ *
  * Search with query normalisation (qk-normalisation, Sec. 3.1.4: used for
@@ -275,9 +324,9 @@ int mem_bag_backward_sparse(const void* dy, const void* values, pkmem_dtype v_dt
  * makes the library record a HIP event pair on the launch stream around every
  * following launch of a listed kernel:
  *   "score_topk", "topk_sort", "cartesian" (mem_search, mem_search_qnorm,
- *                                           mem_search_extra)
+ *                                           mem_search_extra, mem_search_sink)
  *   "qnorm"                                (mem_search_qnorm, mem_search_backward_qnorm)
- *   "search_backward"                      (mem_search_backward[_qnorm])
+ *   "search_backward"                      (mem_search_backward[_qnorm|_sink])
  *   "bag_forward"                          (mem_bag_forward, mem_bag_forward_gated)
  *   "gate_backward"                        (mem_gate_backward)
  *   "bag_backward_atomic", "sort_by_row",
@@ -297,8 +346,9 @@ int mem_timer_read(float* ms_out, int* kernel_out, int cap);
 /* ------------------------------------------------------------------------ *
  * Environment (read at every call):
  *   PKMEM_DEBUG=1       before a kernel indexes with idx (mem_bag_forward[_gated],
- *                       mem_bag_backward[_sparse], mem_search_backward[_qnorm],
- *                       mem_search_extra's extra_idx) a device
+ *                       mem_bag_backward[_sparse], mem_search_backward[_qnorm|_sink]
+ *                       (product-key slots), mem_search_extra's and
+ *                       mem_search_sink's extra_idx) a device
  *                       check that every index lies in [0, N) (or [0, S*S)); the
  *                       call waits for it and returns PKMEM_ERR_INVALID if not.
  *                       Off by default: indices from mem_search are in range by

@@ -20,7 +20,8 @@ import torch  # noqa: F401  (first: the library binds to the HIP runtime torch l
 
 __all__ = [
     "PkmemError", "load", "lib_path", "mem_search", "mem_search_backward", "mem_search_qnorm",
-    "mem_search_backward_qnorm", "mem_search_extra", "mem_bag_forward",
+    "mem_search_backward_qnorm", "mem_search_extra", "mem_search_sink",
+    "mem_search_backward_sink", "mem_bag_forward",
     "mem_bag_forward_gated", "mem_gate_backward",
     "mem_bag_backward",
     "mem_bag_backward_sparse", "mem_search_workspace_size", "mem_bag_backward_workspace_size",
@@ -71,6 +72,14 @@ def load() -> ctypes.CDLL:
     L.mem_search_extra.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, I32, P, P, P, P, P, P, SZ,
                                    P]
     L.mem_search_extra.restype = I32
+    L.mem_search_sink.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, I32, P, P, I64, P, P, P,
+                                  P, P, SZ, P]
+    L.mem_search_sink.restype = I32
+    L.mem_search_backward_sink_workspace_size.argtypes = [I64, I32, I32, I32, I32]
+    L.mem_search_backward_sink_workspace_size.restype = SZ
+    L.mem_search_backward_sink.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, P,
+                                           P, SZ, P]
+    L.mem_search_backward_sink.restype = I32
     L.mem_bag_forward.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P]
     L.mem_bag_forward.restype = I32
     L.mem_bag_forward_gated.argtypes = [P, I32, I64, I32, P, P, I64, I32, P, P, P, P]
@@ -202,15 +211,38 @@ def mem_search_extra(q: torch.Tensor, subkeys: torch.Tensor, k: int, extra_idx: 
     """mem_search plus r extra key-value pairs per (token, head): extra_idx
     [T, H, r] int64 composed indices, scored as full keys, in slots k..k+r-1;
     softmax over all k + r.  Returns (idx, w, score, half_idx) with k + r slots."""
+    return _search_extra(q, subkeys, k, extra_idx, None, 0, idx_out, w_out, score_out,
+                         half_idx_out, want_score, want_half, workspace, stream)
+
+
+def mem_search_sink(q: torch.Tensor, subkeys: torch.Tensor, k: int, sink_keys: torch.Tensor,
+                    sink_row0: int, extra_idx=None, *, idx_out=None, w_out=None, score_out=None,
+                    half_idx_out=None, want_score: bool = True, want_half: bool = False,
+                    workspace=None, stream=None):
+    """mem_search_extra (extra_idx [T, H, r] or None) plus one fixed key-value
+    pair per head in the last slot: key sink_keys [H, n] (subkeys' dtype),
+    scored q . sink_keys[h]; index sink_row0 + h (>= S*S, the value-table row of
+    head h's sink value).  Returns (idx, w, score, half_idx) with k + r + 1 slots."""
+    if extra_idx is None:
+        T, H, _ = q.shape
+        extra_idx = torch.empty((T, H, 0), dtype=torch.int64, device=q.device)
+    return _search_extra(q, subkeys, k, extra_idx, sink_keys, int(sink_row0), idx_out, w_out,
+                         score_out, half_idx_out, want_score, want_half, workspace, stream)
+
+
+def _search_extra(q, subkeys, k, extra_idx, sink_keys, sink_row0, idx_out, w_out, score_out,
+                  half_idx_out, want_score, want_half, workspace, stream):
     L = load()
-    _dev(q, subkeys, extra_idx)
+    _dev(q, subkeys, extra_idx, sink_keys)
     T, H, n = q.shape
     S = subkeys.shape[2]
     r = extra_idx.shape[2] if extra_idx.dim() == 3 else 0
     if extra_idx.dtype != torch.int64:
         raise ValueError("extra_idx must be int64")
+    if sink_keys is not None and (sink_keys.shape != (H, n) or sink_keys.dtype != subkeys.dtype):
+        raise ValueError("sink_keys must be [H, n] in the sub-keys' dtype")
     dev = q.device
-    kk = k + r
+    kk = k + r + (1 if sink_keys is not None else 0)
     if idx_out is None:
         idx_out = torch.empty((T, H, kk), dtype=torch.int64, device=dev)
     if w_out is None:
@@ -221,10 +253,14 @@ def mem_search_extra(q: torch.Tensor, subkeys: torch.Tensor, k: int, extra_idx: 
         half_idx_out = torch.empty((T, H, 2, k), dtype=torch.int32, device=dev)
     _dev(idx_out, w_out, score_out, half_idx_out)
     ws = _workspace(mem_search_workspace_size(T, H, S, k), dev, workspace)
-    _check(L.mem_search_extra(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k, r,
-                              _ptr(extra_idx), _ptr(idx_out), _ptr(w_out), _ptr(score_out),
-                              _ptr(half_idx_out), _ptr(ws), ws.numel() * ws.element_size(),
-                              _stream(stream)))
+    outs = (_ptr(idx_out), _ptr(w_out), _ptr(score_out), _ptr(half_idx_out), _ptr(ws),
+            ws.numel() * ws.element_size(), _stream(stream))
+    if sink_keys is None:
+        _check(L.mem_search_extra(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k, r,
+                                  _ptr(extra_idx), *outs))
+    else:
+        _check(L.mem_search_sink(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k, r,
+                                 _ptr(extra_idx), _ptr(sink_keys), sink_row0, *outs))
     return idx_out, w_out, score_out, half_idx_out
 
 
@@ -279,6 +315,36 @@ def mem_search_backward_qnorm(q: torch.Tensor, subkeys: torch.Tensor, idx: torch
     queries, grad_subkeys accumulated from the normalised ones."""
     return _search_backward(q, subkeys, idx, grad_scores, float(eps), grad_q, grad_subkeys,
                             want_grad_q, want_grad_subkeys, workspace, stream)
+
+
+def mem_search_backward_sink(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tensor,
+                             grad_scores: torch.Tensor, sink_keys: torch.Tensor, *, grad_q=None,
+                             grad_subkeys=None, grad_sink=None, want_grad_q: bool = True,
+                             want_grad_subkeys: bool = True, want_grad_sink: bool = True,
+                             workspace=None, stream=None):
+    """Search backward of mem_search_sink: idx and grad_scores [T, H, k + 1]
+    (last slot the sink's).  grad_q written; grad_subkeys and grad_sink
+    ([H, n] fp32) ACCUMULATED (zero tables allocated if none are given).
+    Returns (grad_q, grad_subkeys, grad_sink)."""
+    L = load()
+    _dev(q, subkeys, idx, grad_scores, sink_keys)
+    T, H, n = q.shape
+    S = subkeys.shape[2]
+    k = idx.shape[2] - 1
+    if grad_q is None and want_grad_q:
+        grad_q = torch.empty((T, H, n), dtype=torch.float32, device=q.device)
+    if grad_subkeys is None and want_grad_subkeys:
+        grad_subkeys = torch.zeros(subkeys.shape, dtype=torch.float32, device=q.device)
+    if grad_sink is None and want_grad_sink:
+        grad_sink = torch.zeros((H, n), dtype=torch.float32, device=q.device)
+    _dev(grad_q, grad_subkeys, grad_sink)
+    nbytes = int(L.mem_search_backward_sink_workspace_size(T, H, n, S, k))
+    ws = _workspace(nbytes, q.device, workspace)
+    _check(L.mem_search_backward_sink(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
+                                      _ptr(idx), _ptr(grad_scores), _ptr(sink_keys), _ptr(grad_q),
+                                      _ptr(grad_subkeys), _ptr(grad_sink), _ptr(ws),
+                                      ws.numel() * ws.element_size(), _stream(stream)))
+    return grad_q, grad_subkeys, grad_sink
 
 
 def _search_backward(q, subkeys, idx, grad_scores, eps, grad_q, grad_subkeys, want_grad_q,

@@ -67,8 +67,11 @@ SearchWs search_ws(void* base, int64_t T, int H, int k) {
   return w;
 }
 
+// k is the selection size (1 <= k <= min(S, KMAX)), or with slots the number
+// of product-key slots per row (1 <= k <= KMAX; extras may exceed S).
 int check_search_shapes(const char* fn, const void* q, pkmem_dtype q_dt, const void* subkeys,
-                        pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k) {
+                        pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k,
+                        bool slots = false) {
   if (!dtype_ok(q_dt) || !dtype_ok(k_dt)) return fail(PKMEM_ERR_INVALID, "%s: unknown dtype", fn);
   if (q_dt != k_dt) return fail(PKMEM_ERR_UNSUPPORTED, "%s: queries and sub-keys must share a dtype", fn);
   if (T < 0) return fail(PKMEM_ERR_INVALID, "%s: T must be >= 0", fn);
@@ -81,7 +84,7 @@ int check_search_shapes(const char* fn, const void* q, pkmem_dtype q_dt, const v
     return fail(PKMEM_ERR_UNSUPPORTED, "%s: fp32 needs n/2 a multiple of 4 and <= 64 (got %d)", fn, d);
   if (S < 1) return fail(PKMEM_ERR_INVALID, "%s: S must be >= 1", fn);
   if (S > PKMEM_SMAX) return fail(PKMEM_ERR_UNSUPPORTED, "%s: S > %d", fn, PKMEM_SMAX);
-  if (k < 1 || k > S) return fail(PKMEM_ERR_INVALID, "%s: need 1 <= k <= S (k=%d, S=%d)", fn, k, S);
+  if (k < 1 || (!slots && k > S)) return fail(PKMEM_ERR_INVALID, "%s: need 1 <= k <= S (k=%d, S=%d)", fn, k, S);
   if (k > PKMEM_KMAX) return fail(PKMEM_ERR_UNSUPPORTED, "%s: k > %d", fn, PKMEM_KMAX);
   if ((T * H * 2) > (int64_t)0xFFFFFFFF) return fail(PKMEM_ERR_UNSUPPORTED, "%s: T*H*2 must be < 2^32", fn);
   if (T > 0 && (!q || !subkeys)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
@@ -129,8 +132,8 @@ bool debug_checks() {
   return env && env[0] && strcmp(env, "0") != 0;
 }
 
-int check_indices(const char* fn, const int64_t* idx, int64_t count, int64_t limit, hipStream_t st) {
-  if (!debug_checks() || count <= 0) return PKMEM_OK;
+// The debug check's flag on the current device (allocated at first use).
+int debug_flag(const char* fn, uint32_t** flag) {
   static uint32_t* flags[64] = {};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -140,13 +143,39 @@ int check_indices(const char* fn, const int64_t* idx, int64_t count, int64_t lim
     e = hipMalloc(reinterpret_cast<void**>(&flags[dev]), sizeof(uint32_t));
     if (e != hipSuccess) return hip_status(e, fn);
   }
-  e = pk::launch_check_indices(idx, count, limit, flags[dev], st);
+  *flag = flags[dev];
+  return PKMEM_OK;
+}
+
+// Waits for the check launched (status e) and reads its flag.
+int debug_verdict(const char* fn, hipError_t e, uint32_t* flag, int64_t limit, hipStream_t st) {
   uint32_t bad = 0;
-  if (e == hipSuccess) e = hipMemcpyAsync(&bad, flags[dev], sizeof(bad), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipMemcpyAsync(&bad, flag, sizeof(bad), hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_status(e, fn);
   if (bad) return fail(PKMEM_ERR_INVALID, "%s: an index lies outside [0, %lld) (PKMEM_DEBUG)", fn, (long long)limit);
   return PKMEM_OK;
+}
+
+int check_indices(const char* fn, const int64_t* idx, int64_t count, int64_t limit, hipStream_t st) {
+  if (!debug_checks() || count <= 0) return PKMEM_OK;
+  uint32_t* flag = nullptr;
+  int rc = debug_flag(fn, &flag);
+  if (rc) return rc;
+  hipError_t e = pk::launch_check_indices(idx, count, limit, flag, st);
+  return debug_verdict(fn, e, flag, limit, st);
+}
+
+// check_indices over the first cols slots of each of rows rows, stride apart.
+int check_indices_strided(const char* fn, const int64_t* idx, int64_t rows, int cols, int stride,
+                          int64_t limit, hipStream_t st) {
+  if (cols == stride) return check_indices(fn, idx, rows * cols, limit, st);
+  if (!debug_checks() || rows <= 0) return PKMEM_OK;
+  uint32_t* flag = nullptr;
+  int rc = debug_flag(fn, &flag);
+  if (rc) return rc;
+  hipError_t e = pk::launch_check_indices_strided(idx, rows, cols, stride, limit, flag, st);
+  return debug_verdict(fn, e, flag, limit, st);
 }
 
 int bag_backward_common(const char* fn, const void* dy, const void* values, pkmem_dtype v_dt,
@@ -316,14 +345,23 @@ size_t mem_search_workspace_size(int64_t T, int H, int S, int k) {
 // The search, with the queries normalised (qnorm) or not.
 static int search_common(const char* fn, const void* q, pkmem_dtype q_dt, const void* subkeys,
                          pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k, bool qnorm,
-                         float eps, int nex, const int64_t* ex_idx, int64_t* idx_out, float* w_out,
-                         float* score_out, int32_t* half_idx_out, void* qhat_out, float* stats_out,
-                         void* ws, size_t ws_bytes, pkmem_stream_t stream) {
+                         float eps, int nex, const int64_t* ex_idx, bool has_sink,
+                         const void* sink, int64_t sink_row0, int64_t* idx_out, float* w_out, float* score_out,
+                         int32_t* half_idx_out, void* qhat_out, float* stats_out, void* ws,
+                         size_t ws_bytes, pkmem_stream_t stream) {
   int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k);
   if (rc) return rc;
   if (nex < 0) return fail(PKMEM_ERR_INVALID, "%s: r must be >= 0", fn);
-  if (k + nex > PKMEM_KMAX)
-    return fail(PKMEM_ERR_UNSUPPORTED, "%s: k + r must be <= %d (k=%d, r=%d)", fn, PKMEM_KMAX, k, nex);
+  if (k + nex + (has_sink ? 1 : 0) > PKMEM_KMAX)
+    return fail(PKMEM_ERR_UNSUPPORTED, "%s: k + r%s must be <= %d (k=%d, r=%d)", fn,
+                has_sink ? " + 1" : "", PKMEM_KMAX, k, nex);
+  if (has_sink) {
+    if (T > 0 && !sink) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+    if (!aligned(sink, 16)) return fail(PKMEM_ERR_INVALID, "%s: sink_keys must be 16-byte aligned", fn);
+    if (sink_row0 < (int64_t)S * S || sink_row0 > INT64_MAX - H)
+      return fail(PKMEM_ERR_INVALID, "%s: sink_row0 must be >= S*S = %lld (got %lld)", fn,
+                  (long long)S * S, (long long)sink_row0);
+  }
   if (T > 0 && nex > 0 && !ex_idx) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
   if (T > 0 && (!idx_out || !w_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
   if (qnorm && !(eps >= 0.f && eps <= 3.0e38f))
@@ -354,7 +392,7 @@ static int search_common(const char* fn, const void* q, pkmem_dtype q_dt, const 
     if (rc) return rc;
   }
   e = pk::launch_cartesian(hidx, w.half_score, T, H, S, k, bf16, q, subkeys, n, ex_idx, nex,
-                           idx_out, w_out, score_out, st);
+                           sink, sink_row0, idx_out, w_out, score_out, st);
   if (e != hipSuccess) return hip_status(e, fn);
   return PKMEM_OK;
 }
@@ -363,7 +401,7 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
                int H, int n, int S, int k, int64_t* idx_out, float* w_out, float* score_out,
                int32_t* half_idx_out, void* ws, size_t ws_bytes, pkmem_stream_t stream) {
   return search_common("mem_search", q, q_dt, subkeys, k_dt, T, H, n, S, k, false, 0.f, 0, nullptr,
-                       idx_out, w_out, score_out, half_idx_out, nullptr, nullptr, ws, ws_bytes,
+                       false, nullptr, 0, idx_out, w_out, score_out, half_idx_out, nullptr, nullptr, ws, ws_bytes,
                        stream);
 }
 
@@ -372,7 +410,7 @@ int mem_search_qnorm(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem
                      float* w_out, float* score_out, int32_t* half_idx_out, void* qhat_out,
                      float* stats_out, void* ws, size_t ws_bytes, pkmem_stream_t stream) {
   return search_common("mem_search_qnorm", q, q_dt, subkeys, k_dt, T, H, n, S, k, true, eps, 0,
-                       nullptr, idx_out, w_out, score_out, half_idx_out, qhat_out, stats_out, ws,
+                       nullptr, false, nullptr, 0, idx_out, w_out, score_out, half_idx_out, qhat_out, stats_out, ws,
                        ws_bytes, stream);
 }
 
@@ -381,8 +419,18 @@ int mem_search_extra(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem
                      int64_t* idx_out, float* w_out, float* score_out, int32_t* half_idx_out,
                      void* ws, size_t ws_bytes, pkmem_stream_t stream) {
   return search_common("mem_search_extra", q, q_dt, subkeys, k_dt, T, H, n, S, k, false, 0.f, r,
-                       extra_idx, idx_out, w_out, score_out, half_idx_out, nullptr, nullptr, ws,
-                       ws_bytes, stream);
+                       extra_idx, false, nullptr, 0, idx_out, w_out, score_out, half_idx_out, nullptr,
+                       nullptr, ws, ws_bytes, stream);
+}
+
+int mem_search_sink(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                    int64_t T, int H, int n, int S, int k, int r, const int64_t* extra_idx,
+                    const void* sink_keys, int64_t sink_row0, int64_t* idx_out, float* w_out,
+                    float* score_out, int32_t* half_idx_out, void* ws, size_t ws_bytes,
+                    pkmem_stream_t stream) {
+  return search_common("mem_search_sink", q, q_dt, subkeys, k_dt, T, H, n, S, k, false, 0.f, r,
+                       extra_idx, true, sink_keys, sink_row0, idx_out, w_out, score_out,
+                       half_idx_out, nullptr, nullptr, ws, ws_bytes, stream);
 }
 
 size_t mem_search_backward_workspace_size(int64_t T, int H, int S, int k) {
@@ -392,13 +440,31 @@ size_t mem_search_backward_workspace_size(int64_t T, int H, int S, int k) {
   return pk::search_backward_ws_bytes(T, H, k) + align256((size_t)T * H * sizeof(float2));
 }
 
+size_t mem_search_backward_sink_workspace_size(int64_t T, int H, int n, int S, int k) {
+  (void)S;
+  if (T < 0 || H < 1 || n < 2 || k < 1) return 0;
+  // the sort and its inputs, then the per-chunk partial sums of grad_sink
+  return pk::search_backward_ws_bytes(T, H, k) +
+         align256((size_t)pk::sink_chunks(T) * H * n * sizeof(float));
+}
+
+// k: product-key slots per row.  With a sink the rows of idx and grad_scores
+// hold k + 1 slots, the last the sink's.
 static int search_backward_common(const char* fn, const void* q, pkmem_dtype q_dt,
                                   const void* subkeys, pkmem_dtype k_dt, int64_t T, int H, int n,
                                   int S, int k, bool qnorm, float eps, const int64_t* idx,
-                                  const float* grad_scores, float* grad_q, float* grad_subkeys,
-                                  void* ws, size_t ws_bytes, pkmem_stream_t stream) {
-  int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k);
+                                  const float* grad_scores, bool has_sink, const void* sink,
+                                  float* grad_q, float* grad_subkeys, float* grad_sink, void* ws,
+                                  size_t ws_bytes, pkmem_stream_t stream) {
+  int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k, true);
   if (rc) return rc;
+  if (k > PKMEM_KMAX - (has_sink ? 1 : 0))
+    return fail(PKMEM_ERR_UNSUPPORTED, "%s: more than %d slots per row", fn, PKMEM_KMAX);
+  if (has_sink) {
+    if (T > 0 && (grad_q || grad_sink) && !sink) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+    if (!aligned(sink, 16) || !aligned(grad_sink, 4))
+      return fail(PKMEM_ERR_INVALID, "%s: sink_keys must be 16-byte and grad_sink 4-byte aligned", fn);
+  }
   if (T > 0 && (!idx || !grad_scores)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
   if (qnorm && !(eps >= 0.f && eps <= 3.0e38f))
     return fail(PKMEM_ERR_INVALID, "%s: eps must be finite and >= 0", fn);
@@ -408,13 +474,15 @@ static int search_backward_common(const char* fn, const void* q, pkmem_dtype q_d
     return fail(PKMEM_ERR_UNSUPPORTED, "%s: 2*H*S must be < 2^31", fn);
   if (!aligned(grad_subkeys, 16) || !aligned(grad_q, 4))
     return fail(PKMEM_ERR_INVALID, "%s: grad_subkeys must be 16-byte and grad_q 4-byte aligned", fn);
-  const size_t need = mem_search_backward_workspace_size(T, H, S, k);
+  const size_t need = has_sink ? mem_search_backward_sink_workspace_size(T, H, n, S, k)
+                               : mem_search_backward_workspace_size(T, H, S, k);
   if (!ws || ws_bytes < need)
     return fail(PKMEM_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws ? ws_bytes : (size_t)0);
   if (!aligned(ws, 256)) return fail(PKMEM_ERR_INVALID, "%s: workspace must be 256-byte aligned", fn);
-  if (T == 0 || (!grad_q && !grad_subkeys)) return PKMEM_OK;
+  if (T == 0 || (!grad_q && !grad_subkeys && !grad_sink)) return PKMEM_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  rc = check_indices(fn, idx, T * H * k, (int64_t)S * S, st);
+  const int kst = k + (has_sink ? 1 : 0);
+  rc = check_indices_strided(fn, idx, T * H, k, kst, (int64_t)S * S, st);
   if (rc) return rc;
   const bool bf16 = q_dt == PKMEM_BF16;
   float2* qstats = nullptr;
@@ -424,8 +492,13 @@ static int search_backward_common(const char* fn, const void* q, pkmem_dtype q_d
     hipError_t e = pk::launch_qnorm(bf16, q, T * H, n, eps, qstats, nullptr, st);
     if (e != hipSuccess) return hip_status(e, fn);
   }
-  hipError_t e = pk::launch_search_backward(bf16, q, subkeys, T, H, n, S, k, idx, grad_scores,
-                                            qstats, grad_q, grad_subkeys, ws, st);
+  float* sink_part = has_sink ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) +
+                                                        pk::search_backward_ws_bytes(T, H, k))
+                              : nullptr;
+  hipError_t e = pk::launch_search_backward(bf16, q, subkeys, T, H, n, S, k, kst, idx, grad_scores,
+                                            qstats, has_sink ? sink : nullptr, grad_q,
+                                            grad_subkeys, has_sink ? grad_sink : nullptr,
+                                            sink_part, ws, st);
   return hip_status(e, fn);
 }
 
@@ -434,8 +507,18 @@ int mem_search_backward(const void* q, pkmem_dtype q_dt, const void* subkeys, pk
                         const float* grad_scores, float* grad_q, float* grad_subkeys, void* ws,
                         size_t ws_bytes, pkmem_stream_t stream) {
   return search_backward_common("mem_search_backward", q, q_dt, subkeys, k_dt, T, H, n, S, k,
-                                false, 0.f, idx, grad_scores, grad_q, grad_subkeys, ws, ws_bytes,
-                                stream);
+                                false, 0.f, idx, grad_scores, false, nullptr, grad_q, grad_subkeys,
+                                nullptr, ws, ws_bytes, stream);
+}
+
+int mem_search_backward_sink(const void* q, pkmem_dtype q_dt, const void* subkeys,
+                             pkmem_dtype k_dt, int64_t T, int H, int n, int S, int k,
+                             const int64_t* idx, const float* grad_scores, const void* sink_keys,
+                             float* grad_q, float* grad_subkeys, float* grad_sink, void* ws,
+                             size_t ws_bytes, pkmem_stream_t stream) {
+  return search_backward_common("mem_search_backward_sink", q, q_dt, subkeys, k_dt, T, H, n, S, k,
+                                false, 0.f, idx, grad_scores, true, sink_keys, grad_q,
+                                grad_subkeys, grad_sink, ws, ws_bytes, stream);
 }
 
 int mem_search_backward_qnorm(const void* q, pkmem_dtype q_dt, const void* subkeys,
@@ -444,8 +527,8 @@ int mem_search_backward_qnorm(const void* q, pkmem_dtype q_dt, const void* subke
                               float* grad_subkeys, void* ws, size_t ws_bytes,
                               pkmem_stream_t stream) {
   return search_backward_common("mem_search_backward_qnorm", q, q_dt, subkeys, k_dt, T, H, n, S,
-                                k, true, eps, idx, grad_scores, grad_q, grad_subkeys, ws,
-                                ws_bytes, stream);
+                                k, true, eps, idx, grad_scores, false, nullptr, grad_q,
+                                grad_subkeys, nullptr, ws, ws_bytes, stream);
 }
 
 int mem_bag_forward(const void* values, pkmem_dtype v_dt, int64_t N, int D, const int64_t* idx,

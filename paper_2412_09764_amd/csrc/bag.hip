@@ -457,24 +457,32 @@ hipError_t launch_gate_backward(bool bf16, const void* d_out, const void* gate, 
 }
 
 // Debug check: *bad = 1 if any of the count indices lies outside [0, limit).
+// Element i of the rows * cols checked is idx[(i / cols) * stride + i % cols].
 __global__ __launch_bounds__(256) void k_check_indices(const int64_t* __restrict__ idx,
-                                                       int64_t count, int64_t limit,
-                                                       uint32_t* __restrict__ bad) {
+                                                       int64_t count, int cols, int stride,
+                                                       int64_t limit, uint32_t* __restrict__ bad) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count;
        i += (int64_t)gridDim.x * 256) {
-    const int64_t v = idx[i];
+    const int64_t v = idx[(i / cols) * stride + i % cols];
     if (v < 0 || v >= limit) *bad = 1u;
   }
 }
 
-hipError_t launch_check_indices(const int64_t* idx, int64_t count, int64_t limit, uint32_t* bad,
-                                hipStream_t st) {
+hipError_t launch_check_indices_strided(const int64_t* idx, int64_t rows, int cols, int stride,
+                                        int64_t limit, uint32_t* bad, hipStream_t st) {
   hipError_t e = launch_fill_u32(bad, 0u, 1, st);
+  const int64_t count = rows * cols;
   if (e != hipSuccess || count <= 0) return e;
   int64_t blocks = (count + 255) / 256;
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(k_check_indices, dim3((unsigned)blocks), dim3(256), 0, st, idx, count, limit, bad);
+  hipLaunchKernelGGL(k_check_indices, dim3((unsigned)blocks), dim3(256), 0, st, idx, count, cols,
+                     stride, limit, bad);
   return hipGetLastError();
+}
+
+hipError_t launch_check_indices(const int64_t* idx, int64_t count, int64_t limit, uint32_t* bad,
+                                hipStream_t st) {
+  return launch_check_indices_strided(idx, count, 1, 1, limit, bad, st);
 }
 
 hipError_t launch_bag_backward_atomic(bool bf16, const void* dy, const void* values, int D,

@@ -55,8 +55,9 @@ hipError_t launch_qnorm(bool bf16, const void* q, int64_t rows, int n, float eps
 // k + nex slots per row.  nex = 0: q, subkeys and ex_idx are not read.
 hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T, int H,
                             int S, int k, bool bf16, const void* q, const void* subkeys, int n,
-                            const int64_t* ex_idx, int nex, int64_t* idx_out, float* w_out,
-                            float* score_out, hipStream_t st);
+                            const int64_t* ex_idx, int nex, const void* sink,
+                            int64_t sink_row0, int64_t* idx_out, float* w_out, float* score_out,
+                            hipStream_t st);
 
 // ---- search backward (search_bwd.hip) --------------------------------------
 size_t search_backward_ws_bytes(int64_t T, int H, int k);
@@ -69,9 +70,14 @@ hipError_t scan_exclusive_u32(uint32_t* data, int64_t n, uint32_t* sums, hipStre
 // qstats (nullable): the queries were normalised in the forward (their
 // (mean, rstd) from launch_qnorm); grad_q is then taken through the
 // normalisation and grad_K uses the normalised queries as scored.
+// k product-key slots per row, rows kst apart in idx and gz; with a sink
+// (kst = k + 1) slot k is the sink's.  grad_sink needs sink_part of
+// sink_chunks(T) * H * n floats.
+int64_t sink_chunks(int64_t T);
 hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
-                                  int n, int S, int k, const int64_t* idx, const float* gz,
-                                  const float2* qstats, float* grad_q, float* grad_K, void* ws,
+                                  int n, int S, int k, int kst, const int64_t* idx, const float* gz,
+                                  const float2* qstats, const void* sink, float* grad_q,
+                                  float* grad_K, float* grad_sink, float* sink_part, void* ws,
                                   hipStream_t st);
 
 // ---- bag (bag.hip) ---------------------------------------------------------
@@ -80,6 +86,9 @@ hipError_t launch_bag_forward(bool bf16, const void* values, int D, const int64_
                               void* y_plain, hipStream_t st);
 hipError_t launch_check_indices(const int64_t* idx, int64_t count, int64_t limit, uint32_t* bad,
                                 hipStream_t st);
+// The first cols of every row of a [rows, stride] array.
+hipError_t launch_check_indices_strided(const int64_t* idx, int64_t rows, int cols, int stride,
+                                        int64_t limit, uint32_t* bad, hipStream_t st);
 hipError_t launch_gate_backward(bool bf16, const void* d_out, const void* gate, const void* y,
                                 int64_t T, int D, void* dy, float* grad_gate, hipStream_t st);
 hipError_t launch_bag_backward_atomic(bool bf16, const void* dy, const void* values, int D,

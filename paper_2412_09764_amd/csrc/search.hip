@@ -474,7 +474,9 @@ __global__ __launch_bounds__(256) void k_topk_fallback(const T* __restrict__ q,
 // elements 4l..4l+3 of each half, fp32 products summed over the wave), and
 // occupy slots k .. k + nex - 1 after the selected ones; the softmax runs over
 // all k + nex.  An index outside [0, S*S) is read as 0 (no out-of-bounds
-// access) and written out as given.
+// access) and written out as given.  With a sink (a fixed key-value pair per
+// head), one more slot follows: the key sink[h*n .. h*n + n - 1] is scored the
+// same way and the slot's index is sink_row0 + h.
 template <int E, typename T, bool EXTRA>
 __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ half_idx,
                                                    const float* __restrict__ half_score,
@@ -482,6 +484,7 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
                                                    const T* __restrict__ q,
                                                    const T* __restrict__ subkeys, int H, int n,
                                                    const int64_t* __restrict__ ex_idx, int nex,
+                                                   const T* __restrict__ sink, int64_t sink_row0,
                                                    int64_t* __restrict__ idx_out,
                                                    float* __restrict__ w_out,
                                                    float* __restrict__ score_out) {
@@ -493,7 +496,8 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
   }
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int kk = EXTRA ? k + nex : k;  // slots per row
+  const int nsc = EXTRA ? nex + (sink ? 1 : 0) : 0;  // full keys scored per row
+  const int kk = k + nsc;                             // slots per row
   for (int64_t row = (int64_t)blockIdx.x * 4 + wave; row < rows; row += (int64_t)gridDim.x * 4) {
     // extra pairs first: their loads overlap the candidate sort below
     float ex_score = 0.f;
@@ -512,23 +516,29 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
         qb.to_f32(fb);
       }
       const int64_t N = (int64_t)S * S;
-      ex_given = lane < nex ? ex_idx[(size_t)row * nex + lane] : 0;
+      ex_given = lane < nex ? ex_idx[(size_t)row * nex + lane] : (lane == nex ? sink_row0 + h : 0);
       const int64_t ex_safe = (ex_given >= 0 && ex_given < N) ? ex_given : 0;
       const T* k1 = subkeys + (size_t)(h * 2) * S * d + qo;
       const T* k2 = k1 + (size_t)S * d;
+      const T* ks1 = sink ? sink + (size_t)h * n + qo : k1;
       // eight extras at a time: their sub-key loads in flight together, then
       // one transposed butterfly (4 + 2 + 1 + 3 exchanges) leaves extra j's
       // sum in lanes 8j .. 8j + 7
-      for (int e0 = 0; e0 < nex; e0 += 8) {
+      for (int e0 = 0; e0 < nsc; e0 += 8) {
         QQuad<T> ka[8], kb[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const int e = e0 + j < nex ? e0 + j : nex - 1;
-          const uint64_t ie = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)ex_safe, e) |
-                              ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(ex_safe >> 32), e) << 32);
-          const int i1 = (int)(ie / (uint64_t)S), i2 = (int)(ie % (uint64_t)S);
-          ka[j].load(k1 + (size_t)i1 * d);
-          kb[j].load(k2 + (size_t)i2 * d);
+          const int e = e0 + j < nsc ? e0 + j : nsc - 1;
+          if (e < nex) {
+            const uint64_t ie = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)ex_safe, e) |
+                                ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(ex_safe >> 32), e) << 32);
+            const int i1 = (int)(ie / (uint64_t)S), i2 = (int)(ie % (uint64_t)S);
+            ka[j].load(k1 + (size_t)i1 * d);
+            kb[j].load(k2 + (size_t)i2 * d);
+          } else {  // the sink's key: both halves of one n-element row
+            ka[j].load(ks1);
+            kb[j].load(ks1 + d);
+          }
         }
         float p[8];
 #pragma unroll
@@ -689,25 +699,28 @@ template <int E>
 static void cart_launch(dim3 g, dim3 b, hipStream_t st, const int32_t* half_idx,
                         const float* half_score, int64_t rows, int S, int k, int np, bool bf16,
                         const void* q, const void* subkeys, int H, int n, const int64_t* ex_idx,
-                        int nex, int64_t* idx_out, float* w_out, float* score_out) {
-  if (nex == 0)
+                        int nex, const void* sink, int64_t sink_row0, int64_t* idx_out,
+                        float* w_out, float* score_out) {
+  if (nex == 0 && !sink)
     hipLaunchKernelGGL((k_cartesian<E, uint16_t, false>), g, b, 0, st, half_idx, half_score, rows,
                        S, k, np, (const uint16_t*)nullptr, (const uint16_t*)nullptr, H, n,
-                       (const int64_t*)nullptr, 0, idx_out, w_out, score_out);
+                       (const int64_t*)nullptr, 0, (const uint16_t*)nullptr, (int64_t)0, idx_out,
+                       w_out, score_out);
   else if (bf16)
     hipLaunchKernelGGL((k_cartesian<E, uint16_t, true>), g, b, 0, st, half_idx, half_score, rows, S,
                        k, np, (const uint16_t*)q, (const uint16_t*)subkeys, H, n, ex_idx, nex,
-                       idx_out, w_out, score_out);
+                       (const uint16_t*)sink, sink_row0, idx_out, w_out, score_out);
   else
     hipLaunchKernelGGL((k_cartesian<E, float, true>), g, b, 0, st, half_idx, half_score, rows, S, k,
-                       np, (const float*)q, (const float*)subkeys, H, n, ex_idx, nex, idx_out,
-                       w_out, score_out);
+                       np, (const float*)q, (const float*)subkeys, H, n, ex_idx, nex,
+                       (const float*)sink, sink_row0, idx_out, w_out, score_out);
 }
 
 hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T_, int H,
                             int S, int k, bool bf16, const void* q, const void* subkeys, int n,
-                            const int64_t* ex_idx, int nex, int64_t* idx_out, float* w_out,
-                            float* score_out, hipStream_t st) {
+                            const int64_t* ex_idx, int nex, const void* sink,
+                            int64_t sink_row0, int64_t* idx_out, float* w_out, float* score_out,
+                            hipStream_t st) {
   const int64_t rows = T_ * H;
   const int np = cartesian_pairs(k);
   int64_t blocks = (rows + 3) / 4;
@@ -715,10 +728,10 @@ hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, in
   if (blocks < 1) blocks = 1;
   const dim3 g((unsigned)blocks), b(256);
   LaunchTimer lt("cartesian", st);
-  if (np <= 64) cart_launch<1>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, idx_out, w_out, score_out);
-  else if (np <= 128) cart_launch<2>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, idx_out, w_out, score_out);
-  else if (np <= 256) cart_launch<4>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, idx_out, w_out, score_out);
-  else cart_launch<8>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, idx_out, w_out, score_out);
+  if (np <= 64) cart_launch<1>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink, sink_row0, idx_out, w_out, score_out);
+  else if (np <= 128) cart_launch<2>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink, sink_row0, idx_out, w_out, score_out);
+  else if (np <= 256) cart_launch<4>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink, sink_row0, idx_out, w_out, score_out);
+  else cart_launch<8>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink, sink_row0, idx_out, w_out, score_out);
   return hipGetLastError();
 }
 

@@ -35,6 +35,9 @@ namespace pk {
 //     keys (h*2 + half)*S + sub-key and group sums at slots rp*k + 0, 1, ...
 //     (in rank order of the leaders) and their number at counts[rp].  Lookups
 //     whose index lies outside [0, S*S) count as absent.
+// idx and gz rows are kst >= k slots apart; with a sink (a fixed key-value
+// pair per head scored as q . sink[h]) slot k of each row is the sink's and
+// grad_q gains gz[sink slot] * sink[h] (its index is never read).
 // With qstats (the forward normalised the queries, LayerNorm without affine)
 // the two halves' gradients g with respect to the normalised query qhat stay
 // in registers and grad_q = rstd * (g - mean(g) - xhat * mean(g * xhat)) over
@@ -46,9 +49,10 @@ namespace pk {
 template <typename T>
 __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
                                                       const T* __restrict__ subkeys, int64_t ntok,
-                                                      int H, int n, int S, int k,
+                                                      int H, int n, int S, int k, int kst,
                                                       const int64_t* __restrict__ idx,
                                                       const float* __restrict__ gz,
+                                                      const T* __restrict__ sink,
                                                       const float2* __restrict__ qstats,
                                                       float* __restrict__ grad_q,
                                                       uint32_t* __restrict__ keys,
@@ -63,9 +67,10 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
   const bool qlane = lane * 4 < d;
   const int ql = qlane ? lane * 4 : 0;
   const size_t r = (size_t)t * H + h;
-  const int64_t ix = lane < k ? idx[r * k + lane] : -1;
+  const int64_t ix = lane < k ? idx[r * kst + lane] : -1;
   const bool okl = ix >= 0 && ix < (int64_t)S * S;
-  const float g = okl ? gz[r * k + lane] : 0.f;
+  const float g = okl ? gz[r * kst + lane] : 0.f;
+  const float gsink = sink ? gz[r * kst + k] : 0.f;
   const uint64_t below = (1ull << lane) - 1ull;
   float gh[2][4];  // with qstats: both halves' gradients with respect to qhat
 
@@ -112,6 +117,11 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
         }
 #pragma unroll
         for (int j = 0; j < QU; ++j) kq[j].fma_into(gg[j], acc);
+      }
+      if (sink) {
+        QQuad<T> sq;
+        sq.load(sink + (size_t)h * n + (size_t)p * d + ql);
+        sq.fma_into(gsink, acc);
       }
       if (qstats) {
 #pragma unroll
@@ -245,6 +255,70 @@ __global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, 
   }
 }
 
+// grad_sink[h] += sum_t gz[t,h,sink slot] q[t,h], in two deterministic
+// passes.  k_sink_partial: one workgroup per (chunk of SINK_TCH tokens, head);
+// wave w takes the chunk's tokens w, w + 4, ... in order (SINK_U loads in
+// flight), lane l owns elements 4l..4l+3 of each half; the four waves' sums
+// are added in wave order into the chunk's partial row.  k_sink_reduce adds
+// the partial rows in chunk order into grad_sink.
+constexpr int SINK_TCH = 256;
+constexpr int SINK_U = 8;
+constexpr int SINK_NMAX = 512;  // n = 2d, d <= 256
+int64_t sink_chunks(int64_t T) { return (T + SINK_TCH - 1) / SINK_TCH; }
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_sink_partial(const T* __restrict__ q, int64_t ntok, int H,
+                                                      int n, int kst, int k,
+                                                      const float* __restrict__ gz,
+                                                      float* __restrict__ part) {
+  __shared__ float red[4][SINK_NMAX];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = (int)(blockIdx.x % (unsigned)H);
+  const int64_t c = blockIdx.x / (unsigned)H;
+  const int d = n >> 1;
+  const bool qlane = lane * 4 < d;
+  const int ql = qlane ? lane * 4 : 0;
+  const int64_t t0 = c * SINK_TCH;
+  const int64_t t1 = t0 + SINK_TCH < ntok ? t0 + SINK_TCH : ntok;
+  float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  for (int64_t tb = t0 + wave; tb < t1; tb += 4 * SINK_U) {
+    QQuad<T> qa[SINK_U], qb[SINK_U];
+    float g[SINK_U];
+#pragma unroll
+    for (int j = 0; j < SINK_U; ++j) {
+      const int64_t t = tb + 4 * j;
+      const bool has = t < t1;
+      const size_t r = (size_t)(has ? t : tb) * H + h;
+      g[j] = has ? gz[r * kst + k] : 0.f;
+      qa[j].load(q + r * n + ql);
+      qb[j].load(q + r * n + d + ql);
+    }
+#pragma unroll
+    for (int j = 0; j < SINK_U; ++j) {
+      qa[j].fma_into(g[j], acc[0]);
+      qb[j].fma_into(g[j], acc[1]);
+    }
+  }
+  if (qlane) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wave][p * d + ql + i] = acc[p][i];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < n; e += 256)
+    part[((size_t)c * H + h) * n + e] = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
+}
+
+__global__ __launch_bounds__(256) void k_sink_reduce(const float* __restrict__ part, int64_t nch,
+                                                     int Hn, float* __restrict__ grad_sink) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= Hn) return;
+  float s = 0.f;
+  for (int64_t c = 0; c < nch; ++c) s += part[(size_t)c * Hn + e];
+  grad_sink[e] += s;
+}
+
 // Workspace: keys and group sums per slot (2*T*H*k each), the row counts
 // (scanned in place into offsets, plus the total), the scan's partials, then
 // the sort of up to 2*T*H*k pairs.
@@ -258,9 +332,24 @@ size_t search_backward_ws_bytes(int64_t T, int H, int k) {
 
 template <typename T>
 static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, int H, int n, int S,
-                              int k, const int64_t* idx, const float* gz, const float2* qstats,
-                              float* grad_q, float* grad_K, void* ws, hipStream_t st) {
+                              int k, int kst, const int64_t* idx, const float* gz,
+                              const float2* qstats, const void* sink, float* grad_q, float* grad_K,
+                              float* grad_sink, float* sink_part, void* ws, hipStream_t st) {
   LaunchTimer lt("search_backward", st);
+  hipError_t e = hipSuccess;
+  if (grad_sink) {
+    const int64_t nch = sink_chunks(T_);
+    hipLaunchKernelGGL(k_sink_partial<T>, dim3((unsigned)(nch * H)), dim3(256), 0, st, (const T*)q,
+                       T_, H, n, kst, k, gz, sink_part);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int Hn = H * n;
+    hipLaunchKernelGGL(k_sink_reduce, dim3((unsigned)((Hn + 255) / 256)), dim3(256), 0, st,
+                       (const float*)sink_part, nch, Hn, grad_sink);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (!grad_q && !grad_K) return hipSuccess;
   const int64_t rows = 2 * T_ * H;
   const int64_t np = rows * k;
   char* p = reinterpret_cast<char*>(ws);
@@ -273,11 +362,11 @@ static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, in
   uint32_t* sums = reinterpret_cast<uint32_t*>(p);
   p += a256(scan_scratch_u32(rows + 1) * 4);
   void* sort_ws = p;
-  hipError_t e = hipSuccess;
   if (grad_K) e = launch_fill_u32(offs + rows, 0u, 1, st);  // the scan's last entry
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_search_bwd_q<T>, dim3((unsigned)(((T_ + 3) / 4) * H)), dim3(256), 0, st,
-                     (const T*)q, (const T*)subkeys, T_, H, n, S, k, idx, gz, qstats, grad_q,
+                     (const T*)q, (const T*)subkeys, T_, H, n, S, k, kst, idx, gz,
+                     grad_q ? (const T*)sink : nullptr, qstats, grad_q,
                      grad_K ? keys : nullptr, grad_K ? gvals : nullptr, grad_K ? offs : nullptr);
   e = hipGetLastError();
   if (e != hipSuccess || !grad_K) return e;
@@ -309,13 +398,16 @@ static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, in
 }
 
 hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
-                                  int n, int S, int k, const int64_t* idx, const float* gz,
-                                  const float2* qstats, float* grad_q, float* grad_K, void* ws,
+                                  int n, int S, int k, int kst, const int64_t* idx, const float* gz,
+                                  const float2* qstats, const void* sink, float* grad_q,
+                                  float* grad_K, float* grad_sink, float* sink_part, void* ws,
                                   hipStream_t st) {
   if (T <= 0) return hipSuccess;
   if (bf16)
-    return launch_sbwd<uint16_t>(q, subkeys, T, H, n, S, k, idx, gz, qstats, grad_q, grad_K, ws, st);
-  return launch_sbwd<float>(q, subkeys, T, H, n, S, k, idx, gz, qstats, grad_q, grad_K, ws, st);
+    return launch_sbwd<uint16_t>(q, subkeys, T, H, n, S, k, kst, idx, gz, qstats, sink, grad_q,
+                                 grad_K, grad_sink, sink_part, ws, st);
+  return launch_sbwd<float>(q, subkeys, T, H, n, S, k, kst, idx, gz, qstats, sink, grad_q, grad_K,
+                            grad_sink, sink_part, ws, st);
 }
 
 }  // namespace pk

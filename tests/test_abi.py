@@ -171,7 +171,8 @@ def sbwd(lib, q=FAKE, qdt=BF16, K=FAKE, kdt=BF16, T=8, H=2, n=64, S=16, k=4, idx
 
 @pytest.mark.parametrize("kw,code,text", [
     (dict(n=63), INVALID, "even"),
-    (dict(k=17), INVALID, "k <= S"),
+    (dict(k=0), INVALID, "k <= S"),
+    (dict(k=65), UNSUPPORTED, "k > 64"),
     (dict(S=9000), UNSUPPORTED, "S >"),
     (dict(qdt=F32), UNSUPPORTED, "share a dtype"),
     (dict(idx=0), INVALID, "null"),
@@ -192,6 +193,8 @@ def test_search_backward_rejects(lib, kw, code, text):
 def test_search_backward_noops(lib):
     assert sbwd(lib, T=0) == OK
     assert sbwd(lib, gq=None, gk=None) == OK          # nothing requested
+    # k counts slots (k + r after extra pairs) and may exceed S
+    assert sbwd(lib, T=0, k=17) == OK
     assert lib.mem_search_backward_workspace_size(100, 4, 2048, 32) >= 100 * 4 * 2 * 32 * 8
 
 
@@ -308,3 +311,69 @@ def test_search_extra_noops(lib):
     assert searchx(lib, T=0) == OK
     assert searchx(lib, T=0, ex=0) == OK
     assert searchx(lib, T=0, r=0, ex=0) == OK
+
+
+def searchs(lib, T=8, k=4, r=3, ex=FAKE, S=16, sink=FAKE, row0=256, ws_bytes=BIG_WS, idx=FAKE):
+    return lib.mem_search_sink(FAKE, BF16, FAKE, BF16, T, 2, 64, S, k, r, ex, sink, row0, idx, FAKE,
+                               None, None, FAKE, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(r=-1), INVALID, "r must"),
+    (dict(k=40, r=24, S=100), UNSUPPORTED, "k + r + 1"),
+    (dict(ex=0), INVALID, "null"),
+    (dict(sink=0), INVALID, "null"),
+    (dict(sink=FAKE + 8), INVALID, "sink_keys"),
+    (dict(row0=255), INVALID, "sink_row0"),
+    (dict(row0=-1), INVALID, "sink_row0"),
+    (dict(row0=(1 << 63) - 1), INVALID, "sink_row0"),
+    (dict(idx=0), INVALID, "null"),
+    (dict(k=17), INVALID, "k <= S"),
+    (dict(ws_bytes=16), WORKSPACE, "workspace"),
+])
+def test_search_sink_rejects(lib, kw, code, text):
+    assert searchs(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def test_search_sink_noops(lib):
+    assert searchs(lib, T=0) == OK
+    assert searchs(lib, T=0, sink=0, ex=0) == OK
+    assert searchs(lib, T=0, r=0, ex=0) == OK
+    assert searchs(lib, T=0, k=40, r=23, S=100, row0=10000) == OK   # 64 slots
+    assert searchs(lib, T=0, k=40, r=24, S=100, row0=10000) == UNSUPPORTED
+
+
+def sbwds(lib, T=8, H=2, n=64, S=16, k=4, sink=FAKE, gq=FAKE, gk=FAKE, gs=FAKE, ws=FAKE,
+          ws_bytes=BIG_WS):
+    return lib.mem_search_backward_sink(FAKE, BF16, FAKE, BF16, T, H, n, S, k, FAKE, FAKE, sink, gq,
+                                        gk, gs, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(k=64), UNSUPPORTED, "slots"),
+    (dict(k=0), INVALID, "k <= S"),
+    (dict(sink=0), INVALID, "null"),
+    (dict(sink=FAKE + 8), INVALID, "sink_keys"),
+    (dict(gs=FAKE + 2), INVALID, "grad_sink"),
+    (dict(ws_bytes=16), WORKSPACE, "workspace"),
+    (dict(n=63), INVALID, "even"),
+])
+def test_search_backward_sink_rejects(lib, kw, code, text):
+    assert sbwds(lib, **kw) == code
+    assert text in msg(lib)
+
+
+def test_search_backward_sink_noops_and_workspace(lib):
+    assert sbwds(lib, T=0) == OK
+    assert sbwds(lib, gq=None, gk=None, gs=None) == OK
+    assert sbwds(lib, T=0, gq=None, gs=None, sink=0) == OK   # only grad_subkeys: the sink is not read
+    assert sbwds(lib, k=63, T=0) == OK
+    # the plain search backward's needs plus the partial sums of grad_sink (one
+    # row of n floats per head and chunk of 256 tokens)
+    T, H, n, S, k = 1000, 4, 512, 2048, 33
+    need = lib.mem_search_backward_sink_workspace_size(T, H, n, S, k)
+    plain = lib.mem_search_backward_workspace_size(T, H, S, k) - ((T * H * 8 + 255) // 256) * 256
+    assert need >= plain + 4 * H * n * 4
+    assert sbwds(lib, T=T, H=H, n=n, S=S, k=k, ws_bytes=need - 1) == WORKSPACE
+    assert lib.mem_search_backward_sink_workspace_size(-1, 4, 64, 16, 4) == 0
