@@ -385,6 +385,50 @@ def main():
     search_bwd_qn_ms = sum(sbq) / args.steps
     del gq, gK, ws_sb, idx_qn, w_qn
 
+    # Extra key-value pairs (16 per token and head) and the fixed sink pair,
+    # each scored inside the cartesian kernel, and the sink's search backward
+    # (its grad_q term and the deterministic grad_sink sum): measured on their
+    # own after the timed steps on the same queries.
+    def kernel_avg(fn, names):
+        fn()
+        torch.cuda.synchronize()
+        pk.mem_timer_start(*names)
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        pk.mem_timer_stop()
+        acc = {}
+        for pos, ms in pk.mem_timer_read():
+            acc[names[pos]] = acc.get(names[pos], 0.0) + ms
+        return {kn: v / args.steps for kn, v in acc.items()}
+
+    r_ex = 16
+    ex_idx = torch.randint(0, N, (T, H, r_ex), generator=torch.Generator().manual_seed(11),
+                           dtype=torch.int64).to(dev)
+    sink_keys = (torch.randn((H, wl.n), generator=torch.Generator().manual_seed(12)) / 16).to(q.dtype).to(dev)
+    idx_x = torch.empty((T, H, k + r_ex), dtype=torch.int64, device=dev)
+    w_x = torch.empty((T, H, k + r_ex), dtype=torch.float32, device=dev)
+    extra_ms = kernel_avg(lambda: pk.mem_search_extra(q, K, k, ex_idx, idx_out=idx_x, w_out=w_x,
+                                                      want_score=False, workspace=ws_s),
+                          ("cartesian",))
+    del idx_x, w_x, ex_idx
+    idx_sk = torch.empty((T, H, k + 1), dtype=torch.int64, device=dev)
+    w_sk = torch.empty((T, H, k + 1), dtype=torch.float32, device=dev)
+    sink_ms = kernel_avg(lambda: pk.mem_search_sink(q, K, k, sink_keys, N, idx_out=idx_sk,
+                                                    w_out=w_sk, want_score=False, workspace=ws_s),
+                         ("cartesian",))
+    gz_sk = (torch.randn((T, H, k + 1), generator=torch.Generator().manual_seed(13)) * 0.01).to(dev)
+    gq = torch.empty((T, H, wl.n), dtype=torch.float32, device=dev)
+    gK = torch.zeros((H, 2, wl.S, wl.d), dtype=torch.float32, device=dev)
+    gS = torch.zeros((H, wl.n), dtype=torch.float32, device=dev)
+    ws_sk = torch.empty(max(1, pk.load().mem_search_backward_sink_workspace_size(T, H, wl.n, wl.S, k)),
+                        dtype=torch.uint8, device=dev)
+    sink_bwd_ms = kernel_avg(lambda: pk.mem_search_backward_sink(q, K, idx_sk, gz_sk, sink_keys,
+                                                                 grad_q=gq, grad_subkeys=gK,
+                                                                 grad_sink=gS, workspace=ws_sk),
+                             ("search_backward",))
+    del idx_sk, w_sk, gz_sk, gq, gK, gS, ws_sk, sink_keys
+
     # touched rows of the last step's selection (outside the timed region)
     uniq, counts = torch.unique(idx.view(-1), return_counts=True)
     U = int(uniq.numel())
@@ -462,6 +506,9 @@ def main():
             "qnorm": dict(hbm_rate(alg_cost("qnorm", wl, U, esz)[1], qn["qnorm"]),
                           traffic=measured_traffic("qnorm", wl.name)),
         },
+        "extra_pairs": {"r": r_ex, "cartesian_ms": round(extra_ms["cartesian"], 4)},
+        "sink_pair": {"cartesian_ms": round(sink_ms["cartesian"], 4),
+                      "search_backward_ms": round(sink_bwd_ms["search_backward"], 4)},
         "stream_copy_GBps": round(copy_gbps, 1),
         "touched_rows": U,
         "max_row_multiplicity": max_mult,
