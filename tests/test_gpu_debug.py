@@ -53,6 +53,35 @@ def test_debug_checks_reject_out_of_range_indices(gpu_lib, monkeypatch):
     torch.cuda.synchronize()
 
 
+def test_debug_checks_with_a_sink_slot(gpu_lib, monkeypatch):
+    """The sink's slot (index >= S*S by construction) passes the check of the
+    sink search backward, which covers the product-key slots only; a bad
+    product-key index or a bad extra index is rejected."""
+    T, S, H, n, k = 20, 16, 2, 32, 4
+    q = normal_tensor((T, H, n), 116, torch.bfloat16).cuda()
+    K = normal_tensor((H, 2, S, n // 2), 117, torch.bfloat16).cuda()
+    ks = normal_tensor((H, n), 118, torch.bfloat16).cuda()
+    idx, w, _, _ = pk.mem_search_sink(q, K, k, ks, S * S)
+    gz = torch.ones((T, H, k + 1), device="cuda")
+    ref = pk.mem_search_backward_sink(q, K, idx, gz, ks)
+    monkeypatch.setenv("PKMEM_DEBUG", "1")
+    got = pk.mem_search_backward_sink(q, K, idx, gz, ks)
+    for a, b in zip(ref, got):
+        assert torch.equal(a, b)
+    bad = idx.clone()
+    bad[5, 1, k - 1] = -3
+    with pytest.raises(pk.PkmemError) as e:
+        pk.mem_search_backward_sink(q, K, bad, gz, ks)
+    assert e.value.code == INVALID
+    ex = torch.zeros((T, H, 2), dtype=torch.int64, device="cuda")
+    ex[7, 0, 1] = S * S
+    with pytest.raises(pk.PkmemError) as e:
+        pk.mem_search_sink(q, K, k, ks, S * S, ex)
+    assert e.value.code == INVALID
+    monkeypatch.delenv("PKMEM_DEBUG")
+    torch.cuda.synchronize()
+
+
 def test_search_is_deterministic_run_to_run(gpu_lib):
     q = normal_tensor((700, 4, 512), 114, torch.bfloat16).cuda()
     K = normal_tensor((4, 2, 2048, 256), 115, torch.bfloat16, std=1 / 256).cuda()
