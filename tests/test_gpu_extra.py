@@ -141,3 +141,23 @@ def test_search_extra_full_size_sampled(gpu_lib):
     assert ok.mean() > 0.9
     assert normwise(h64(score[st])[..., wl.k:], ref["score"][..., wl.k:]) <= TOL_F32
     assert normwise(h64(w[st])[ok], ref["w"][ok]) <= TOL_F32
+
+
+def test_extra_slots_beyond_S_through_search_backward(gpu_lib):
+    """k + r may exceed S (S = 6, k = 6, r = 5: 11 slots, every extra a repeat
+    of some selected key): the search backward takes all 11 slots."""
+    S, H, n, k, r, T = 6, 2, 16, 6, 5, 90
+    dt = torch.bfloat16
+    q = int_tensor((T, H, n), 75, dt)
+    K = int_tensor((H, 2, S, n // 2), 76, dt)
+    ex = extra_indices(T, H, r, S, 77)
+    gz = torch.randn((T, H, k + r), generator=torch.Generator().manual_seed(78))
+    idx, w, score, _ = pk.mem_search_extra(q.cuda(), K.cuda(), k, ex.cuda())
+    gq, gK = pk.mem_search_backward(q.cuda(), K.cuda(), idx, gz.cuda())
+    torch.cuda.synchronize()
+    ref = oracle.search_extra(h64(q), h64(K), k, ex.numpy())
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    np.testing.assert_array_equal(h64(score), ref["score"])
+    s = oracle.search_backward(h64(q), h64(K), ref["idx"], h64(gz))
+    assert normwise(h64(gq), s["grad_q"]) <= TOL_F32
+    assert normwise(h64(gK), s["grad_K"]) <= TOL_F32
