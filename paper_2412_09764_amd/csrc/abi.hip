@@ -46,23 +46,23 @@ struct SearchWs {
   size_t bytes;
 };
 
+// The search workspace carved from base (only its size when base is null).
 SearchWs search_ws(void* base, int64_t T, int H, int k) {
   const size_t rows = (size_t)T * H * 2;
   char* p = reinterpret_cast<char*>(base);
-  SearchWs w;
   size_t off = 0;
-  w.cand = reinterpret_cast<uint64_t*>(p + off);
-  off += align256(rows * pk::CAND_CAP * sizeof(uint64_t));
-  w.cnts = reinterpret_cast<uint32_t*>(p + off);
-  off += align256(rows * 2 * sizeof(uint32_t));
-  w.half_idx = reinterpret_cast<int32_t*>(p + off);
-  off += align256(rows * k * sizeof(int32_t));
-  w.half_score = reinterpret_cast<float*>(p + off);
-  off += align256(rows * k * sizeof(float));
-  w.ovf = reinterpret_cast<uint32_t*>(p + off);
-  off += align256((rows + 1) * sizeof(uint32_t));
-  w.qstats = reinterpret_cast<float2*>(p + off);
-  off += align256((size_t)T * H * sizeof(float2));
+  auto take = [&](size_t bytes) -> char* {
+    char* at = p ? p + off : nullptr;
+    off += align256(bytes);
+    return at;
+  };
+  SearchWs w;
+  w.cand = reinterpret_cast<uint64_t*>(take(rows * pk::CAND_CAP * sizeof(uint64_t)));
+  w.cnts = reinterpret_cast<uint32_t*>(take(rows * 2 * sizeof(uint32_t)));
+  w.half_idx = reinterpret_cast<int32_t*>(take(rows * k * sizeof(int32_t)));
+  w.half_score = reinterpret_cast<float*>(take(rows * k * sizeof(float)));
+  w.ovf = reinterpret_cast<uint32_t*>(take((rows + 1) * sizeof(uint32_t)));
+  w.qstats = reinterpret_cast<float2*>(take((size_t)T * H * sizeof(float2)));
   w.bytes = off;
   return w;
 }
