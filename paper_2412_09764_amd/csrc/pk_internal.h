@@ -74,6 +74,12 @@ hipError_t scan_exclusive_u32(uint32_t* data, int64_t n, uint32_t* sums, hipStre
 // (kst = k + 1) slot k is the sink's.  grad_sink needs sink_part of
 // sink_chunks(T) * H * n floats.
 int64_t sink_chunks(int64_t T);
+// Appends to long_list (in no particular order) every segment u < *nseg with
+// seg_start[u+1] - seg_start[u] > thresh, counting them in *long_cnt, which
+// must be zero on entry.  max_seg bounds *nseg (sizes the grid).
+hipError_t launch_list_long(const uint32_t* seg_start, const uint32_t* nseg, int64_t max_seg,
+                            uint32_t thresh, uint32_t* long_list, uint32_t* long_cnt,
+                            hipStream_t st);
 hipError_t launch_search_backward(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
                                   int n, int S, int k, int kst, const int64_t* idx, const float* gz,
                                   const float2* qstats, const void* sink, float* grad_q,

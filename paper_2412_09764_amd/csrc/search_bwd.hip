@@ -20,7 +20,9 @@
 // those pairs by key.  One wave per segment then sums gsum * q over the
 // segment's tokens (in token order; each token's query half is read once) and
 // adds the sum into the sub-key row with one plain read-modify-write: no
-// atomics, bitwise deterministic.
+// atomics, bitwise deterministic.  A segment longer than 2048 pairs (a
+// sub-key that thousands of tokens chose) goes to a workgroup of 16 waves
+// instead, whose contiguous runs are added in run order.
 #include "pk_device.h"
 #include "pk_internal.h"
 
@@ -182,12 +184,61 @@ __global__ __launch_bounds__(256) void k_sbwd_pack(const uint32_t* __restrict__ 
   }
 }
 
+// Adds gsum * (query half as scored) of the sorted pairs [a, z) of one
+// (head h, half) segment into acc, in pair order: the pairs are taken 64 at a
+// time and consumed QU at a time, with their query-quad loads issued
+// together; lane l owns elements 4l..4l+3 of the half (qh points at them).
+template <typename T, bool QN>
+__device__ __forceinline__ void sbwd_sum_run(const T* qh, int H, int n, int h, uint32_t hk2,
+                                             const float2* __restrict__ qstats,
+                                             const float* __restrict__ gvals,
+                                             const uint32_t* __restrict__ vs, uint32_t a,
+                                             uint32_t z, int lane, float* acc) {
+  constexpr int QU = PK_SBWD_QU;
+  for (uint32_t b0 = a; b0 < z; b0 += 64) {
+    const uint32_t e = b0 + lane;
+    const bool ok = e < z;
+    const uint32_t x = ok ? vs[e] : 0u;
+    const uint32_t t = x / hk2;
+    const float gx = ok ? gvals[x] : 0.f;
+    float2 st = make_float2(0.f, 1.f);
+    if constexpr (QN) st = qstats[(size_t)t * H + h];
+    const uint32_t cnt = (z - b0) < 64u ? (z - b0) : 64u;
+    for (uint32_t j0 = 0; j0 < cnt; j0 += QU) {
+      QQuad<T> qq[QU];
+      float gg[QU], mj[QU], rj[QU];
+#pragma unroll
+      for (int j = 0; j < QU; ++j) {
+        const bool has = j0 + j < cnt;
+        const int L = has ? (int)(j0 + j) : (int)j0;
+        const uint32_t tj = (uint32_t)__builtin_amdgcn_readlane((int)t, L);
+        const float xj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), L));
+        gg[j] = has ? xj : 0.f;
+        if constexpr (QN) {
+          mj[j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.x), L));
+          rj[j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.y), L));
+        }
+        qq[j].load(qh + (size_t)tj * H * n);
+      }
+#pragma unroll
+      for (int j = 0; j < QU; ++j) {
+        if constexpr (QN) qq[j].fma_into_norm(gg[j], acc, mj[j], rj[j]);
+        else qq[j].fma_into(gg[j], acc);
+      }
+    }
+  }
+}
+
+// A segment of more than SBWD_LONG pairs (a sub-key chosen by that many
+// tokens) is summed by k_sbwd_long instead of one wave.
+constexpr uint32_t SBWD_LONG = 2048;
+constexpr int SBWD_LWAVES = 16;
+static int64_t sbwd_max_long(int64_t np) { return np / SBWD_LONG + 1; }
+
 // One wave per segment (grid-stride) of the sorted pairs; a segment is one
 // (head, half, sub-key) and holds at most one pair per token, in token order.
-// Lane l owns elements 4l..4l+3 of the d-element row (d <= 256).  The pairs
-// are taken 64 at a time and consumed in order, QU at a time, with their
-// query-quad loads issued together; the sum is added into the sub-key row with
-// one read-modify-write.
+// Lane l owns elements 4l..4l+3 of the d-element row (d <= 256).  The sum is
+// added into the sub-key row with one read-modify-write.
 template <typename T, bool QN>
 __global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, int H, int n,
                                                        int S, int k,
@@ -198,7 +249,6 @@ __global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, 
                                                        const uint32_t* __restrict__ seg,
                                                        const uint32_t* __restrict__ nseg_p,
                                                        float* __restrict__ grad_K) {
-  constexpr int QU = PK_SBWD_QU;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t nseg = *nseg_p;
   const int d = n >> 1;
@@ -209,49 +259,67 @@ __global__ __launch_bounds__(256) void k_sbwd_segments(const T* __restrict__ q, 
   for (uint32_t u = blockIdx.x * 4u + wave; u < nseg; u += gridDim.x * 4u) {
     const uint32_t s0 = seg[u], s1 = seg[u + 1];
     const uint32_t bin = ks[s0];
-    if (bin >= nbins) continue;
+    if (bin >= nbins || s1 - s0 > SBWD_LONG) continue;
     const int hp = (int)(bin / (uint32_t)S);
     const int h = hp >> 1, p = hp & 1;
     const T* qh = q + (size_t)h * n + (size_t)p * d + ql;
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (uint32_t b0 = s0; b0 < s1; b0 += 64) {
-      const uint32_t e = b0 + lane;
-      const bool ok = e < s1;
-      const uint32_t x = ok ? vs[e] : 0u;
-      const uint32_t t = x / hk2;
-      const float gx = ok ? gvals[x] : 0.f;
-      float2 st = make_float2(0.f, 1.f);
-      if constexpr (QN) st = qstats[(size_t)t * H + h];
-      const uint32_t cnt = (s1 - b0) < 64u ? (s1 - b0) : 64u;
-      for (uint32_t j0 = 0; j0 < cnt; j0 += QU) {
-        QQuad<T> qq[QU];
-        float gg[QU], mj[QU], rj[QU];
-#pragma unroll
-        for (int j = 0; j < QU; ++j) {
-          const bool has = j0 + j < cnt;
-          const int L = has ? (int)(j0 + j) : (int)j0;
-          const uint32_t tj = (uint32_t)__builtin_amdgcn_readlane((int)t, L);
-          const float xj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), L));
-          gg[j] = has ? xj : 0.f;
-          if constexpr (QN) {
-            mj[j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.x), L));
-            rj[j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.y), L));
-          }
-          qq[j].load(qh + (size_t)tj * H * n);
-        }
-#pragma unroll
-        for (int j = 0; j < QU; ++j) {
-          if constexpr (QN) qq[j].fma_into_norm(gg[j], acc, mj[j], rj[j]);
-          else qq[j].fma_into(gg[j], acc);
-        }
-      }
-    }
+    sbwd_sum_run<T, QN>(qh, H, n, h, hk2, qstats, gvals, vs, s0, s1, lane, acc);
     if (qlane) {
       float4* dst = reinterpret_cast<float4*>(grad_K + (size_t)bin * d + ql);
       float4 o = *dst;
       o.x += acc[0]; o.y += acc[1]; o.z += acc[2]; o.w += acc[3];
       *dst = o;
     }
+  }
+}
+
+// The segments listed in long_list, one workgroup of SBWD_LWAVES waves per
+// segment at a time: wave w sums the w-th contiguous run of the segment's
+// pairs (in pair order) into a partial row; the partial rows meet in LDS and
+// are added, in wave order, to the sub-key row with one read-modify-write.
+template <typename T, bool QN>
+__global__ __launch_bounds__(64 * SBWD_LWAVES) void k_sbwd_long(
+    const T* __restrict__ q, int H, int n, int S, int k, const float2* __restrict__ qstats,
+    const float* __restrict__ gvals, const uint32_t* __restrict__ ks,
+    const uint32_t* __restrict__ vs, const uint32_t* __restrict__ seg,
+    const uint32_t* __restrict__ long_list, const uint32_t* __restrict__ long_cnt,
+    float* __restrict__ grad_K) {
+  __shared__ float part[SBWD_LWAVES][256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int d = n >> 1;
+  const bool qlane = lane * 4 < d;
+  const int ql = qlane ? lane * 4 : 0;
+  const uint32_t nbins = (uint32_t)(2 * H) * (uint32_t)S;
+  const uint32_t hk2 = 2u * (uint32_t)H * (uint32_t)k;
+  const uint32_t nlong = *long_cnt;
+  for (uint32_t it = blockIdx.x; it < nlong; it += gridDim.x) {
+    const uint32_t u = long_list[it];
+    const uint32_t s0 = seg[u], s1 = seg[u + 1];
+    const uint32_t bin = ks[s0];
+    if (bin >= nbins) continue;  // the same for every wave of the workgroup
+    const int hp = (int)(bin / (uint32_t)S);
+    const int h = hp >> 1, p = hp & 1;
+    const T* qh = q + (size_t)h * n + (size_t)p * d + ql;
+    const uint32_t len = s1 - s0;
+    const uint32_t per = (len + SBWD_LWAVES - 1) / SBWD_LWAVES;
+    uint32_t a = (uint32_t)wave * per, z = a + per;
+    a = s0 + (a < len ? a : len);
+    z = s0 + (z < len ? z : len);
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    sbwd_sum_run<T, QN>(qh, H, n, h, hk2, qstats, gvals, vs, a, z, lane, acc);
+    if (qlane) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) part[wave][ql + i] = acc[i];
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < d; e += 64 * SBWD_LWAVES) {
+      float sum = grad_K[(size_t)bin * d + e];
+#pragma unroll
+      for (int w = 0; w < SBWD_LWAVES; ++w) sum += part[w][e];
+      grad_K[(size_t)bin * d + e] = sum;
+    }
+    __syncthreads();
   }
 }
 
@@ -320,14 +388,16 @@ __global__ __launch_bounds__(256) void k_sink_reduce(const float* __restrict__ p
 }
 
 // Workspace: keys and group sums per slot (2*T*H*k each), the row counts
-// (scanned in place into offsets, plus the total), the scan's partials, then
-// the sort of up to 2*T*H*k pairs.
+// (scanned in place into offsets, plus the total, plus the count of long
+// segments), the scan's partials, the list of long segments, then the sort of
+// up to 2*T*H*k pairs.
 static size_t a256(size_t x) { return (x + 255) / 256 * 256; }
 size_t search_backward_ws_bytes(int64_t T, int H, int k) {
   const int64_t rows = 2 * T * H;
   const int64_t np = rows * k;
-  return 2 * a256((size_t)np * 4) + a256((size_t)(rows + 1) * 4) +
-         a256(scan_scratch_u32(rows + 1) * 4) + sorted_workspace_bytes(np);
+  return 2 * a256((size_t)np * 4) + a256((size_t)(rows + 2) * 4) +
+         a256(scan_scratch_u32(rows + 1) * 4) + a256((size_t)sbwd_max_long(np) * 4) +
+         sorted_workspace_bytes(np);
 }
 
 template <typename T>
@@ -357,12 +427,15 @@ static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, in
   p += a256((size_t)np * 4);
   float* gvals = reinterpret_cast<float*>(p);
   p += a256((size_t)np * 4);
-  uint32_t* offs = reinterpret_cast<uint32_t*>(p);  // rows + 1
-  p += a256((size_t)(rows + 1) * 4);
+  uint32_t* offs = reinterpret_cast<uint32_t*>(p);  // rows + 1, then the long count
+  p += a256((size_t)(rows + 2) * 4);
   uint32_t* sums = reinterpret_cast<uint32_t*>(p);
   p += a256(scan_scratch_u32(rows + 1) * 4);
+  uint32_t* long_list = reinterpret_cast<uint32_t*>(p);
+  p += a256((size_t)sbwd_max_long(np) * 4);
   void* sort_ws = p;
-  if (grad_K) e = launch_fill_u32(offs + rows, 0u, 1, st);  // the scan's last entry
+  // the scan's last entry and the count of long segments
+  if (grad_K) e = launch_fill_u32(offs + rows, 0u, 2, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_search_bwd_q<T>, dim3((unsigned)(((T_ + 3) / 4) * H)), dim3(256), 0, st,
                      (const T*)q, (const T*)subkeys, T_, H, n, S, k, kst, idx, gz,
@@ -386,14 +459,26 @@ static hipError_t launch_sbwd(const void* q, const void* subkeys, int64_t T_, in
   e = sort_u32_segments(np, offs + rows, key_bits, sort_ws, &ks, &vs, &seg, &nseg, st);
   if (e != hipSuccess) return e;
   int64_t maxseg = (int64_t)nbins < np ? (int64_t)nbins : np;
+  uint32_t* long_cnt = offs + rows + 1;
+  e = launch_list_long(seg, nseg, maxseg, SBWD_LONG, long_list, long_cnt, st);
+  if (e != hipSuccess) return e;
   int64_t blocks = (maxseg + 3) / 4;
   if (blocks > 16384) blocks = 16384;
-  if (qstats)
+  int64_t lblocks = sbwd_max_long(np) < maxseg ? sbwd_max_long(np) : maxseg;
+  if (lblocks > 256) lblocks = 256;
+  if (qstats) {
     hipLaunchKernelGGL((k_sbwd_segments<T, true>), dim3((unsigned)blocks), dim3(256), 0, st,
                        (const T*)q, H, n, S, k, qstats, gvals, ks, vs, seg, nseg, grad_K);
-  else
+    hipLaunchKernelGGL((k_sbwd_long<T, true>), dim3((unsigned)lblocks), dim3(64 * SBWD_LWAVES), 0,
+                       st, (const T*)q, H, n, S, k, qstats, gvals, ks, vs, seg,
+                       (const uint32_t*)long_list, (const uint32_t*)long_cnt, grad_K);
+  } else {
     hipLaunchKernelGGL((k_sbwd_segments<T, false>), dim3((unsigned)blocks), dim3(256), 0, st,
                        (const T*)q, H, n, S, k, qstats, gvals, ks, vs, seg, nseg, grad_K);
+    hipLaunchKernelGGL((k_sbwd_long<T, false>), dim3((unsigned)lblocks), dim3(64 * SBWD_LWAVES),
+                       0, st, (const T*)q, H, n, S, k, qstats, gvals, ks, vs, seg,
+                       (const uint32_t*)long_list, (const uint32_t*)long_cnt, grad_K);
+  }
   return hipGetLastError();
 }
 

@@ -543,11 +543,23 @@ hipError_t scan_exclusive_u32(uint32_t* data, int64_t n, uint32_t* sums, hipStre
 // is then summed on its own) for k_bag_bwd_long; k_bag_bwd_rows skips them.
 __global__ __launch_bounds__(256) void k_list_long(const uint32_t* __restrict__ seg_start,
                                                    const uint32_t* __restrict__ nseg,
+                                                   uint32_t thresh,
                                                    uint32_t* __restrict__ long_list,
                                                    uint32_t* __restrict__ long_cnt) {
   const uint32_t U = *nseg;
   for (uint32_t u = blockIdx.x * 256 + threadIdx.x; u < U; u += gridDim.x * 256)
-    if (seg_start[u + 1] - seg_start[u] > LONG_SEG) long_list[atomicAdd(long_cnt, 1u)] = u;
+    if (seg_start[u + 1] - seg_start[u] > thresh) long_list[atomicAdd(long_cnt, 1u)] = u;
+}
+
+hipError_t launch_list_long(const uint32_t* seg_start, const uint32_t* nseg, int64_t max_seg,
+                            uint32_t thresh, uint32_t* long_list, uint32_t* long_cnt,
+                            hipStream_t st) {
+  int64_t gb = cdiv(max_seg, 256);
+  if (gb > 2048) gb = 2048;
+  if (gb < 1) gb = 1;
+  hipLaunchKernelGGL(k_list_long, dim3((unsigned)gb), dim3(256), 0, st, seg_start, nseg, thresh,
+                     long_list, long_cnt);
+  return hipGetLastError();
 }
 
 // Rows listed by k_list_long (more than LONG_SEG lookups), one workgroup
@@ -687,14 +699,8 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
   int64_t lblocks = max_long(L);
   if (lblocks > 512) lblocks = 512;
   const int ngrp_cap = 16384 / D;  // partial rows that fit 64 KiB
-  {
-    int64_t gb = cdiv(L, 256);
-    if (gb > 2048) gb = 2048;
-    hipLaunchKernelGGL(k_list_long, dim3((unsigned)gb), dim3(256), 0, st, b.seg, b.misc,
-                       b.long_list, b.misc + 1);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
+  e = launch_list_long(b.seg, b.misc, L, (uint32_t)LONG_SEG, b.long_list, b.misc + 1, st);
+  if (e != hipSuccess) return e;
   LaunchTimer lt("bag_backward_rows", st);
 #define PK_ROWS_ONE(VT, NQ, CL, SP)                                                                \
   {                                                                                                \

@@ -118,3 +118,37 @@ def test_search_backward_deterministic_and_skips_invalid_indices(gpu_lib):
     ref = oracle.search_backward(h64(q), h64(K), idx_ref, gz_ref)
     assert normwise(h64(runs[0][0]), ref["grad_q"]) <= TOL_F32
     assert normwise(h64(runs[0][1]), ref["grad_K"]) <= TOL_F32
+
+
+@pytest.mark.parametrize("qnorm", [False, True], ids=["plain", "qnorm"])
+def test_search_backward_long_segments(gpu_lib, qnorm):
+    """Sub-keys chosen by thousands of tokens: 3000 of the 3500 tokens select
+    the same 8 composed indices (2 x 4 sub-keys per head), so their sub-key
+    segments hold more than 2048 pairs and are summed by a workgroup each; the
+    other tokens' indices are uniform (short segments).  Against the oracle,
+    and bitwise repeatable."""
+    S, H, n, k, T, hot = 64, 2, 64, 8, 3500, 3000
+    q = int_tensor((T, H, n), 131, torch.bfloat16)
+    K = int_tensor((H, 2, S, n // 2), 132, torch.bfloat16)
+    g = torch.Generator().manual_seed(133)
+    j = torch.arange(k)
+    idx = torch.randint(0, S * S, (T, H, k), generator=g)
+    idx[:hot] = ((j // 4) * S + (j % 4)).view(1, 1, k)
+    idx = idx[torch.randperm(T, generator=g)].contiguous()  # hot tokens spread over the batch
+    gz = torch.randn((T, H, k), generator=g)
+    args = (q.cuda(), K.cuda(), idx.cuda(), gz.cuda())
+    if qnorm:
+        a = pk.mem_search_backward_qnorm(*args, 1e-5)
+        b = pk.mem_search_backward_qnorm(*args, 1e-5)
+        ref = oracle.search_backward_qnorm(h64(q), h64(K), idx.numpy(), h64(gz), 1e-5, "bf16")
+    else:
+        a = pk.mem_search_backward(*args)
+        b = pk.mem_search_backward(*args)
+        ref = oracle.search_backward(h64(q), h64(K), idx.numpy(), h64(gz))
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    assert normwise(h64(a[0]), ref["grad_q"]) <= TOL_F32
+    assert normwise(h64(a[1]), ref["grad_K"]) <= TOL_F32
+    # the hot sub-key rows themselves (the long segments)
+    for p, rows in ((0, [0, 1]), (1, [0, 1, 2, 3])):
+        assert normwise(h64(a[1])[:, p, rows], ref["grad_K"][:, p, rows]) <= TOL_F32
