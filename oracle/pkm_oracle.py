@@ -22,7 +22,7 @@ Paper: "Memory Layers at Scale" (arXiv 2412.09764).
                                backward propagates several output gradients
                                into the same value-gradient row.
 
-Readings where the paper is silent (each is also listed in the design doc):
+Readings where the paper is silent:
   * heads: H independent (query, sub-key pair) per token, one shared value
     table, per-head top-k and softmax, one bag of H*k rows summed;
   * composed index i = i1 * S + i2, with q1 = q[:n/2] scored against

@@ -148,7 +148,7 @@ int debug_flag(const char* fn, uint32_t** flag) {
 }
 
 // Waits for the check launched (status e) and reads its flag.
-int debug_verdict(const char* fn, hipError_t e, uint32_t* flag, int64_t limit, hipStream_t st) {
+int debug_outcome(const char* fn, hipError_t e, uint32_t* flag, int64_t limit, hipStream_t st) {
   uint32_t bad = 0;
   if (e == hipSuccess) e = hipMemcpyAsync(&bad, flag, sizeof(bad), hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
@@ -163,7 +163,7 @@ int check_indices(const char* fn, const int64_t* idx, int64_t count, int64_t lim
   int rc = debug_flag(fn, &flag);
   if (rc) return rc;
   hipError_t e = pk::launch_check_indices(idx, count, limit, flag, st);
-  return debug_verdict(fn, e, flag, limit, st);
+  return debug_outcome(fn, e, flag, limit, st);
 }
 
 // check_indices over the first cols slots of each of rows rows, stride apart.
@@ -175,7 +175,7 @@ int check_indices_strided(const char* fn, const int64_t* idx, int64_t rows, int 
   int rc = debug_flag(fn, &flag);
   if (rc) return rc;
   hipError_t e = pk::launch_check_indices_strided(idx, rows, cols, stride, limit, flag, st);
-  return debug_verdict(fn, e, flag, limit, st);
+  return debug_outcome(fn, e, flag, limit, st);
 }
 
 int bag_backward_common(const char* fn, const void* dy, const void* values, pkmem_dtype v_dt,
