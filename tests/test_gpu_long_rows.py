@@ -87,3 +87,21 @@ def test_segments_at_the_split_threshold(gpu_lib):
     assert normwise(h64(gv), ref["grad_values"]) <= TOL_F32
     assert normwise(h64(gw), ref["grad_w"]) <= TOL_F32
     assert np.abs(h64(gz) - ref["grad_z"]).max() <= TOL_F32 * np.abs(h64(w) * ref["grad_w"]).max()
+
+
+@pytest.mark.parametrize("mode", ["sorted", "atomic"])
+def test_backward_without_value_gradient(gpu_lib, mode):
+    """grad_values not requested (NULL): grad_w and grad_scores are bitwise
+    those of the full call (including rows long enough for the split path),
+    and match the oracle."""
+    N, D, T, H, k = 3000, 512, 900, 4, 8
+    V, idx, w, dy = skewed_inputs(N, D, T, H, k, torch.bfloat16, 141, 3, 0.6)
+    args = (dy.cuda(), V.cuda(), idx.cuda(), w.cuda())
+    _, gw_full, gz_full = pk.mem_bag_backward(*args, mode=mode)
+    gv_none, gw, gz = pk.mem_bag_backward(*args, want_grad_values=False, mode=mode)
+    torch.cuda.synchronize()
+    assert gv_none is None
+    assert torch.equal(gw, gw_full) and torch.equal(gz, gz_full)
+    ref = oracle.bag_backward(h64(dy), h64(V), idx.numpy(), h64(w), H, k)
+    assert normwise(h64(gw), ref["grad_w"]) <= TOL_F32
+    assert normwise(h64(gz), ref["grad_z"]) <= TOL_F32
