@@ -583,3 +583,35 @@ def check_search_backward_sink(sink_fn, bwd_fn, rng, T=3, H=2, S=5, d=2, k=2, r=
     base = rng.standard_normal(ks.shape)
     g2 = bwd_fn(q, K, idx, gz, ks, None, base)
     np.testing.assert_allclose(g2["grad_sink"], base + g["grad_sink"], rtol=1e-14, atol=1e-15)
+
+
+# ------------------------------------------------- rows form, inversion ----
+def check_rows_form(dense_fn, rows_fn, rng):
+    """The touched-rows form of the value gradient: ascending distinct rows,
+    each equal to the dense gradient's row exactly (same sums in the same
+    order); every untouched dense row is zero."""
+    V, idx, z, w, dy = random_bag_case(rng)
+    T, H, k = idx.shape
+    dense = dense_fn(dy, V, idx, w, H, k)["grad_values"]
+    rows = rows_fn(dy, V, idx, w, H, k)
+    assert list(rows["rows"]) == sorted(set(idx.ravel().tolist()))
+    np.testing.assert_array_equal(dense[rows["rows"]], rows["grad_rows"])
+    untouched = np.setdiff1d(np.arange(V.shape[0]), rows["rows"])
+    assert np.all(dense[untouched] == 0)
+
+
+def check_invert_index(inv_fn, rng):
+    """CSR inversion of lookup -> row: offsets end at L, rows strictly
+    ascending, every segment non-empty with ascending lookup ids that map back
+    to its row, and the (row, lookup) pairs are exactly the input's."""
+    idx = rng.integers(0, 20, size=300)
+    inv = inv_fn(idx)
+    assert inv["row_ptr"][0] == 0 and inv["row_ptr"][-1] == idx.size
+    assert np.all(np.diff(inv["rows"]) > 0)
+    pairs = []
+    for u, r in enumerate(inv["rows"]):
+        seg = inv["lookups"][inv["row_ptr"][u]:inv["row_ptr"][u + 1]]
+        assert len(seg) > 0 and np.all(np.diff(seg) > 0)
+        assert np.all(idx[seg] == r)
+        pairs += [(int(r), int(l)) for l in seg]
+    assert sorted(pairs) == sorted((int(r), l) for l, r in enumerate(idx))

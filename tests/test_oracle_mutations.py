@@ -465,3 +465,69 @@ def test_catches_sink_query_gradient_dropped():
         out["grad_q"] = r["grad_q"]
         return out
     assert _sink_fails(bwd=bwd) > 0
+
+
+# ------------------------------------------------- rows form, inversion ----
+def _rows_fails(rows_fn):
+    fails = 0
+    for s in range(2):
+        try:
+            pins.check_rows_form(oracle.bag_backward, rows_fn, np.random.default_rng(200 + s))
+        except AssertionError:
+            fails += 1
+    return fails
+
+
+def _inv_fails(inv_fn):
+    fails = 0
+    for s in range(2):
+        try:
+            pins.check_invert_index(inv_fn, np.random.default_rng(210 + s))
+        except (AssertionError, IndexError):
+            fails += 1
+    return fails
+
+
+def test_real_rows_form_and_inversion_pass():
+    assert _rows_fails(oracle.bag_backward_rows) == 0
+    assert _inv_fails(oracle.invert_index) == 0
+
+
+def test_catches_rows_descending():
+    def mutant(dy, V, idx, w, H, k):
+        r = oracle.bag_backward_rows(dy, V, idx, w, H, k)
+        return dict(r, rows=r["rows"][::-1], grad_rows=r["grad_rows"][::-1])
+    assert _rows_fails(mutant) > 0
+
+
+def test_catches_rows_overwrite_on_repeats():
+    def mutant(dy, V, idx, w, H, k):
+        r = oracle.bag_backward_rows(dy, V, idx, w, H, k)
+        T = dy.shape[0]
+        flat, wf = np.asarray(idx).reshape(T, -1), np.asarray(w, float).reshape(T, -1)
+        g = r["grad_rows"].copy()
+        for u, row in enumerate(r["rows"]):   # keep only the last lookup's term
+            t, j = [(t, j) for t in range(T) for j in range(flat.shape[1]) if flat[t, j] == row][-1]
+            g[u] = wf[t, j] * np.asarray(dy, float)[t]
+        return dict(r, grad_rows=g)
+    assert _rows_fails(mutant) > 0
+
+
+def test_catches_inversion_lookups_reversed_within_a_row():
+    def mutant(idx):
+        inv = oracle.invert_index(idx)
+        lk = inv["lookups"].copy()
+        for u in range(len(inv["rows"])):
+            a, b = inv["row_ptr"][u], inv["row_ptr"][u + 1]
+            lk[a:b] = lk[a:b][::-1]
+        return dict(inv, lookups=lk)
+    assert _inv_fails(mutant) > 0
+
+
+def test_catches_inversion_offsets_shifted():
+    def mutant(idx):
+        inv = oracle.invert_index(idx)
+        rp = inv["row_ptr"].copy()
+        rp[1:-1] += 1
+        return dict(inv, row_ptr=rp)
+    assert _inv_fails(mutant) > 0
