@@ -159,6 +159,14 @@ __global__ __launch_bounds__(256) void k_radix_hist(const void* __restrict__ key
   hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
 }
 
+// Stable scatter of one radix pass.  Wave w of the workgroup ranks the w-th
+// quarter of the tile (positions in order: 16 rounds of 64), each key's rank
+// within its digit coming from ballots and the wave's own digit counters in
+// LDS (a wave's LDS accesses stay in program order, so no barrier is needed
+// between rounds).  One block scan then gives each digit's start in the tile
+// and each wave's start within the digit; the tile is written to LDS in
+// sorted order and from there to its digits' runs, consecutive threads
+// writing consecutive addresses.  Keys of equal digit keep their order.
 template <int KM>
 __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ keys_in,
                                                        const uint32_t* __restrict__ vals_in,
@@ -168,10 +176,17 @@ __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ 
                                                        const uint32_t* __restrict__ offsets,
                                                        uint32_t* __restrict__ keys_out,
                                                        uint32_t* __restrict__ vals_out) {
+  constexpr int PER_WAVE = SORT_TILE / 4;  // contiguous keys ranked by one wave
+  constexpr int ROUNDS = PER_WAVE / WAVE;
   const int64_t L = (Ldev && (int64_t)*Ldev < Lmax) ? (int64_t)*Ldev : Lmax;
-  if ((int64_t)blockIdx.x * SORT_TILE >= L) return;  // whole block: nothing to move
-  __shared__ uint32_t run[RADIX];
-  __shared__ uint32_t wcnt[4][RADIX];
+  const int64_t tile = (int64_t)blockIdx.x * SORT_TILE;
+  if (tile >= L) return;  // whole block: nothing to move
+  __shared__ uint32_t run[RADIX];      // global start of each digit's run for this tile
+  __shared__ uint32_t tstart[RADIX];   // start of each digit within the tile
+  __shared__ uint32_t wcnt[4][RADIX];  // per-wave digit counts, then per-wave starts
+  __shared__ uint32_t wsum[4];
+  __shared__ uint32_t skey[SORT_TILE];
+  __shared__ uint32_t sval[SORT_TILE];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   run[tid] = offsets[(int64_t)tid * nblk + blockIdx.x];
 #pragma unroll
@@ -179,37 +194,55 @@ __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ 
   __syncthreads();
   const uint32_t mask = (1u << bits) - 1u;
   const uint64_t below = (1ull << lane) - 1ull;
-  const int64_t tile = (int64_t)blockIdx.x * SORT_TILE;
-  for (int i = 0; i < SORT_ITEMS; ++i) {
-    // Items are taken in position order: slot-major, then thread order.
-    const int64_t pos = tile + i * 256 + tid;
+  const int64_t wbase = tile + (int64_t)wave * PER_WAVE;
+  uint32_t key[ROUNDS], val[ROUNDS], rk[ROUNDS];
+#pragma unroll
+  for (int i = 0; i < ROUNDS; ++i) {
+    const int64_t pos = wbase + i * WAVE + lane;
     const bool valid = pos < L;
-    const uint32_t key = valid ? sort_key<KM>(keys_in, pos) : 0u;
-    const uint32_t val = valid ? (KM != SRC_NEXT ? (uint32_t)pos : vals_in[pos]) : 0u;
-    const uint32_t dig = (key >> shift) & mask;
+    key[i] = valid ? sort_key<KM>(keys_in, pos) : 0u;
+    val[i] = valid ? (KM != SRC_NEXT ? (uint32_t)pos : vals_in[pos]) : 0u;
+    const uint32_t dig = (key[i] >> shift) & mask;
     uint64_t peers = __ballot(valid);
     for (int b = 0; b < bits; ++b) {
       const bool bit = (dig >> b) & 1u;
       const uint64_t set = __ballot(bit);
       peers &= bit ? set : ~set;
     }
-    const uint32_t rank = (uint32_t)__popcll(peers & below);
-    const uint32_t total = (uint32_t)__popcll(peers);
-    const bool leader = valid && rank == 0;
-    if (leader) wcnt[wave][dig] = total;
-    __syncthreads();
-    if (valid) {
-      uint32_t dst = run[dig] + rank;
-      for (int w = 0; w < wave; ++w) dst += wcnt[w][dig];
-      keys_out[dst] = key;
-      vals_out[dst] = val;
+    const uint32_t r = (uint32_t)__popcll(peers & below);
+    rk[i] = wcnt[wave][dig] + r;  // keys of this digit in the wave's earlier rounds, then lanes
+    if (valid && r == 0) wcnt[wave][dig] += (uint32_t)__popcll(peers);
+  }
+  __syncthreads();
+  {  // thread tid = digit: the tile's digit starts and each wave's start within it
+    const uint32_t c0 = wcnt[0][tid], c1 = wcnt[1][tid], c2 = wcnt[2][tid], c3 = wcnt[3][tid];
+    uint32_t total;
+    const uint32_t st = block_exclusive_scan(c0 + c1 + c2 + c3, wsum, total);
+    tstart[tid] = st;
+    wcnt[0][tid] = st;
+    wcnt[1][tid] = st + c0;
+    wcnt[2][tid] = st + c0 + c1;
+    wcnt[3][tid] = st + c0 + c1 + c2;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < ROUNDS; ++i) {
+    const int64_t pos = wbase + i * WAVE + lane;
+    if (pos < L) {
+      const uint32_t p = wcnt[wave][(key[i] >> shift) & mask] + rk[i];
+      skey[p] = key[i];
+      sval[p] = val[i];
     }
-    __syncthreads();
-    if (leader) {
-      atomicAdd(&run[dig], total);
-      wcnt[wave][dig] = 0;
-    }
-    __syncthreads();
+  }
+  __syncthreads();
+  const int64_t left = L - tile;
+  const int n = left < SORT_TILE ? (int)left : SORT_TILE;
+  for (int e = tid; e < n; e += 256) {
+    const uint32_t kk = skey[e];
+    const uint32_t dig = (kk >> shift) & mask;
+    const uint32_t dst = run[dig] + (uint32_t)e - tstart[dig];
+    keys_out[dst] = kk;
+    vals_out[dst] = sval[e];
   }
 }
 
