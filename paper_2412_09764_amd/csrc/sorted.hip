@@ -123,6 +123,35 @@ static hipError_t exclusive_scan(uint32_t* data, int64_t n, uint32_t* sums, hipS
   return hipGetLastError();
 }
 
+// Per digit d (one workgroup each) of a radix pass: exclusive scan, in place,
+// of the tile counts hist[d*nblk .. (d+1)*nblk) (digit-major), and the digit's
+// total in totals[d]; the scatter adds the digits' bases (a scan of totals).
+__global__ __launch_bounds__(256) void k_scan_digits(uint32_t* __restrict__ hist, int64_t nblk,
+                                                     uint32_t* __restrict__ totals) {
+  __shared__ uint32_t wsum[4];
+  uint32_t* h = hist + (int64_t)blockIdx.x * nblk;
+  uint32_t carry = 0;
+  for (int64_t base = 0; base < nblk; base += SCAN_TILE) {
+    const int64_t i0 = base + (int64_t)threadIdx.x * SCAN_ITEMS;
+    uint32_t v[SCAN_ITEMS];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j) {
+      v[j] = (i0 + j < nblk) ? h[i0 + j] : 0u;
+      sum += v[j];
+    }
+    uint32_t total;
+    uint32_t run = carry + block_exclusive_scan(sum, wsum, total);
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j) {
+      if (i0 + j < nblk) h[i0 + j] = run;
+      run += v[j];
+    }
+    carry += total;
+  }
+  if (threadIdx.x == 0) totals[blockIdx.x] = carry;
+}
+
 // ----------------------------------------------------------- radix sort ----
 // KM selects where a pass takes its items: SRC_I64 and SRC_U32 are first
 // passes (keys from an int64 or u32 array, values = item positions), SRC_NEXT
@@ -174,6 +203,7 @@ __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ 
                                                        const uint32_t* __restrict__ Ldev, int shift,
                                                        int bits, int64_t nblk,
                                                        const uint32_t* __restrict__ offsets,
+                                                       const uint32_t* __restrict__ totals,
                                                        uint32_t* __restrict__ keys_out,
                                                        uint32_t* __restrict__ vals_out) {
   constexpr int PER_WAVE = SORT_TILE / 4;  // contiguous keys ranked by one wave
@@ -188,7 +218,11 @@ __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ 
   __shared__ uint32_t skey[SORT_TILE];
   __shared__ uint32_t sval[SORT_TILE];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  run[tid] = offsets[(int64_t)tid * nblk + blockIdx.x];
+  {  // thread tid = digit: where the digit starts overall, plus this tile's offset in it
+    uint32_t all;
+    const uint32_t dbase = block_exclusive_scan(totals[tid], wsum, all);
+    run[tid] = dbase + offsets[(int64_t)tid * nblk + blockIdx.x];
+  }
 #pragma unroll
   for (int w = 0; w < 4; ++w) wcnt[w][tid] = 0;
   __syncthreads();
@@ -467,7 +501,7 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
 
 // -------------------------------------------------------------- launcher ----
 struct SortedWs {
-  uint32_t *keys_a, *vals_a, *keys_b, *vals_b, *hist, *sums, *seg, *misc, *long_list;
+  uint32_t *keys_a, *vals_a, *keys_b, *vals_b, *hist, *sums, *seg, *misc, *long_list, *totals;
 };
 static int64_t max_long(int64_t L) { return L / LONG_SEG + 1; }
 
@@ -487,6 +521,7 @@ static SortedWs carve(void* ws, int64_t L) {
   w.seg = take(4 * (size_t)(L + 1));
   w.misc = take(256);  // [0] segments, [1] long rows listed
   w.long_list = take(4 * (size_t)max_long(L));
+  w.totals = take(4 * (size_t)RADIX);  // a radix pass's count per digit
   return w;
 }
 
@@ -496,7 +531,7 @@ size_t sorted_workspace_bytes(int64_t L) {
   const int64_t scan_n = (hist_n > L + 1 ? hist_n : L + 1);
   return 4 * align256(4 * (size_t)L) + align256(4 * (size_t)scan_n) +
          align256(4 * (size_t)(cdiv(scan_n, SCAN_TILE) + 1)) + align256(4 * (size_t)(L + 1)) + 256 +
-         align256(4 * (size_t)max_long(L));
+         align256(4 * (size_t)max_long(L)) + align256(4 * (size_t)RADIX);
 }
 
 // Stable LSD radix sort of L keys (< 2^key_bits, from an int64 or a u32 array)
@@ -522,14 +557,13 @@ static hipError_t sort_segments(const void* keys, bool key64, int64_t L, int key
       hipLaunchKernelGGL(k_radix_hist<SRC_I64>, g, blk, 0, st, kin, L, Ldev, shift, bits, nblk, b.hist);
     else
       hipLaunchKernelGGL(k_radix_hist<SRC_U32>, g, blk, 0, st, kin, L, Ldev, shift, bits, nblk, b.hist);
-    e = exclusive_scan(b.hist, (int64_t)RADIX * nblk, b.sums, st);
-    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_scan_digits, dim3(RADIX), blk, 0, st, b.hist, nblk, b.totals);
     if (pass > 0 || vals_in)
-      hipLaunchKernelGGL(k_radix_scatter<SRC_NEXT>, g, blk, 0, st, kin, vin, L, Ldev, shift, bits, nblk, b.hist, kout, vout);
+      hipLaunchKernelGGL(k_radix_scatter<SRC_NEXT>, g, blk, 0, st, kin, vin, L, Ldev, shift, bits, nblk, b.hist, b.totals, kout, vout);
     else if (key64)
-      hipLaunchKernelGGL(k_radix_scatter<SRC_I64>, g, blk, 0, st, kin, vin, L, Ldev, shift, bits, nblk, b.hist, kout, vout);
+      hipLaunchKernelGGL(k_radix_scatter<SRC_I64>, g, blk, 0, st, kin, vin, L, Ldev, shift, bits, nblk, b.hist, b.totals, kout, vout);
     else
-      hipLaunchKernelGGL(k_radix_scatter<SRC_U32>, g, blk, 0, st, kin, vin, L, Ldev, shift, bits, nblk, b.hist, kout, vout);
+      hipLaunchKernelGGL(k_radix_scatter<SRC_U32>, g, blk, 0, st, kin, vin, L, Ldev, shift, bits, nblk, b.hist, b.totals, kout, vout);
     kin = kout;
     vin = vout;
     if (kout == b.keys_a) { kout = b.keys_b; vout = b.vals_b; }
