@@ -281,30 +281,69 @@ __global__ __launch_bounds__(256) void k_radix_scatter(const void* __restrict__ 
 }
 
 // ------------------------------------------------------------- segments ----
-__global__ __launch_bounds__(256) void k_seg_flags(const uint32_t* __restrict__ keys, int64_t Lmax,
+// Segment heads of the sorted keys (i == 0 or keys[i] != keys[i-1]), counted
+// per scan tile (thread: SCAN_ITEMS consecutive keys); k_scan_top then turns
+// the counts into each tile's first segment number.
+__global__ __launch_bounds__(256) void k_seg_count(const uint32_t* __restrict__ keys, int64_t Lmax,
                                                    const uint32_t* __restrict__ Ldev,
-                                                   uint32_t* __restrict__ flags) {
+                                                   uint32_t* __restrict__ sums) {
+  __shared__ uint32_t wsum[4];
   const int64_t L = (Ldev && (int64_t)*Ldev < Lmax) ? (int64_t)*Ldev : Lmax;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < L) flags[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1u : 0u;
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
+  uint32_t prev = (base > 0 && base <= L) ? keys[base - 1] : 0u;
+  uint32_t s = 0;
+#pragma unroll
+  for (int i = 0; i < SCAN_ITEMS; ++i) {
+    const int64_t x = base + i;
+    if (x < L) {
+      const uint32_t kx = keys[x];
+      s += (x == 0 || kx != prev) ? 1u : 0u;
+      prev = kx;
+    }
+  }
+  uint32_t total;
+  block_exclusive_scan(s, wsum, total);
+  if (threadIdx.x == 0) sums[blockIdx.x] = total;
 }
 
-__global__ __launch_bounds__(256) void k_seg_starts(const uint32_t* __restrict__ keys, int64_t Lmax,
-                                                    const uint32_t* __restrict__ Ldev,
-                                                    const uint32_t* __restrict__ excl,
-                                                    uint32_t* __restrict__ seg_start,
-                                                    uint32_t* __restrict__ nseg) {
+// Each head i, with u = the number of heads before it, writes seg_start[u] = i;
+// the last item writes seg_start[U] = L and U (the number of segments).
+__global__ __launch_bounds__(256) void k_seg_place(const uint32_t* __restrict__ keys, int64_t Lmax,
+                                                   const uint32_t* __restrict__ Ldev,
+                                                   const uint32_t* __restrict__ sums,
+                                                   uint32_t* __restrict__ seg_start,
+                                                   uint32_t* __restrict__ nseg) {
+  __shared__ uint32_t wsum[4];
   const int64_t L = (Ldev && (int64_t)*Ldev < Lmax) ? (int64_t)*Ldev : Lmax;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= L) return;
-  const bool head = (i == 0 || keys[i] != keys[i - 1]);
-  if (head) seg_start[excl[i]] = (uint32_t)i;
-  if (i == L - 1) {
-    const uint32_t U = excl[i] + (head ? 1u : 0u);
-    seg_start[U] = (uint32_t)L;
-    *nseg = U;
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
+  uint32_t prev = (base > 0 && base <= L) ? keys[base - 1] : 0u;
+  bool head[SCAN_ITEMS];
+  uint32_t s = 0;
+#pragma unroll
+  for (int i = 0; i < SCAN_ITEMS; ++i) {
+    const int64_t x = base + i;
+    head[i] = false;
+    if (x < L) {
+      const uint32_t kx = keys[x];
+      head[i] = (x == 0 || kx != prev);
+      prev = kx;
+    }
+    s += head[i] ? 1u : 0u;
+  }
+  uint32_t total;
+  uint32_t run = sums[blockIdx.x] + block_exclusive_scan(s, wsum, total);
+#pragma unroll
+  for (int i = 0; i < SCAN_ITEMS; ++i) {
+    const int64_t x = base + i;
+    if (head[i]) seg_start[run] = (uint32_t)x;
+    run += head[i] ? 1u : 0u;
+    if (x == L - 1) {
+      seg_start[run] = (uint32_t)L;
+      *nseg = run;
+    }
   }
 }
+
 
 // ------------------------------------------------------- per-row backward ----
 // Quad layout: a row of D elements is D/4 quads of 4 consecutive elements; the
@@ -571,11 +610,11 @@ static hipError_t sort_segments(const void* keys, bool key64, int64_t L, int key
   }
   *ks = reinterpret_cast<const uint32_t*>(kin);
   *vs = vin;
-  const unsigned lb = (unsigned)cdiv(L, 256);
-  hipLaunchKernelGGL(k_seg_flags, dim3(lb), dim3(256), 0, st, *ks, L, Ldev, b.hist);
-  e = exclusive_scan(b.hist, L, b.sums, st);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_seg_starts, dim3(lb), dim3(256), 0, st, *ks, L, Ldev, b.hist, b.seg, b.misc);
+  const int64_t nb = cdiv(L, SCAN_TILE);
+  hipLaunchKernelGGL(k_seg_count, dim3((unsigned)nb), dim3(256), 0, st, *ks, L, Ldev, b.sums);
+  hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(256), 0, st, b.sums, nb);
+  hipLaunchKernelGGL(k_seg_place, dim3((unsigned)nb), dim3(256), 0, st, *ks, L, Ldev, b.sums, b.seg,
+                     b.misc);
   return hipGetLastError();
 }
 
