@@ -169,6 +169,14 @@ __device__ __forceinline__ uint32_t f32_to_ordered(float f) {
   if (u == 0x80000000u) u = 0u;
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
+// The smallest float above a finite x (-0 counts as +0): for finite z,
+// z >= next_up(x) exactly when z > x.
+__device__ __forceinline__ float next_up(float x) {
+  uint32_t u = __float_as_uint(x);
+  if (u == 0x80000000u) u = 0u;
+  u = (u & 0x80000000u) ? u - 1u : u + 1u;
+  return __uint_as_float(u);
+}
 __device__ __forceinline__ float ordered_to_f32(uint32_t o) {
   uint32_t u = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
   return __uint_as_float(u);

@@ -22,13 +22,15 @@
 //     holding a token's rows own half of its CAND_CAP slots each; a count
 //     past capacity keeps writing the last slot and sends the row to the
 //     rescan) - no masks, atomics or capacity branches; the two counts go to
-//     memory.
+//     memory.  A lane holding 2k records takes only scores above the
+//     threshold from then on (lower indices win ties), so rows of tied
+//     scores fit their slots.
 //   * Pass 3, k_topk_sort, a kernel of its own (a sort needs few registers, so
 //     it runs at far higher occupancy than the scoring kernel, which is held
 //     to two waves per SIMD): per row a wave bitonic sort of the candidates,
 //     the first k written.  A row whose lane half overflowed its CAND_CAP / 2
-//     slots (heavy ties) is listed for k_topk_fallback, which rescans it
-//     exactly.
+//     slots (more than that many scores above the threshold) is listed for
+//     k_topk_fallback, which rescans it exactly.
 //   * With query normalisation (qk-normalisation, Sec. 3.1.4) k_qnorm first
 //     computes each (token, head) query's mean and rstd = 1/sqrt(var + eps)
 //     (LayerNorm without affine, fp32, centred second pass); the scoring
@@ -328,17 +330,25 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   }
 
   // ---- pass 2: collect candidates >= threshold ------------------------------
+  // A lane meets its rows in increasing index order.  Once it holds 2k
+  // records it takes only scores above the threshold: of those 2k either k
+  // equal the threshold, and a later equal one has a higher index than all
+  // of them (ties go to the lower index), or k exceed it, and then no score
+  // equal to the threshold is among the k selected.  Heavily tied rows (equal
+  // sub-keys) thus stay within their slots; the test runs once per tile.
   constexpr int HALF_CAP = CAND_CAP / 2;
   const size_t rid = ((size_t)(tok_ok ? tok : 0) * H + h) * 2 + p;
   uint64_t* my_cand = cand + rid * CAND_CAP + kh * HALF_CAP;
   uint32_t my_cnt = 0;
   const float thl = tok_ok ? th : INFINITY;  // scores are finite
+  const float strict = next_up(thl);
+  float bound = thl;
   sweep([&](const f32x16_t& acc, int c, int half) {
     const uint32_t r0 = (uint32_t)(c * CHUNK_ROWS + half * 32 + 4 * kh);
     if (c < nfull) {  // uniform
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        if (acc[j] >= thl) {
+        if (acc[j] >= bound) {
           my_cand[my_cnt < (uint32_t)HALF_CAP ? my_cnt : (uint32_t)HALF_CAP - 1] =
               (uint64_t(__float_as_uint(acc[j])) << 32) | (r0 + 8 * (j >> 2) + (j & 3));
           ++my_cnt;
@@ -348,12 +358,13 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const uint32_t row = r0 + 8 * (j >> 2) + (j & 3);
-        if (acc[j] >= thl && row < (uint32_t)S) {
+        if (acc[j] >= bound && row < (uint32_t)S) {
           my_cand[my_cnt < (uint32_t)HALF_CAP ? my_cnt : (uint32_t)HALF_CAP - 1] = (uint64_t(__float_as_uint(acc[j])) << 32) | row;
           ++my_cnt;
         }
       }
     }
+    bound = my_cnt >= 2u * (uint32_t)k ? strict : bound;
   });
   if (tok_ok) cnts[rid * 2 + kh] = my_cnt;
 }

@@ -80,9 +80,9 @@ def test_search_integer_inputs_exact(gpu_lib, case):
     assert normwise(h64(w), ref["w"]) <= TOL_F32
 
 
-def test_search_all_ties_use_the_exact_fallback(gpu_lib):
-    # every score equal: each row's candidate list overflows; the result is the
-    # k lowest composed indices
+def test_search_all_ties(gpu_lib):
+    # every score equal: each lane keeps only its first k records at the
+    # threshold; the result is the k lowest composed indices
     T, H, S, n, k = 70, 2, 300, 32, 16
     q = torch.ones((T, H, n), dtype=torch.bfloat16).cuda()
     K = torch.ones((H, 2, S, n // 2), dtype=torch.bfloat16).cuda()
@@ -272,3 +272,61 @@ def test_full_path_tiny_workload(gpu_lib):
     assert normwise(h64(gv), b["grad_values"]) <= TOL_F32
     assert normwise(h64(gw), b["grad_w"]) <= TOL_F32
     assert normwise(h64(gz), b["grad_z"]) <= TOL_F32
+
+
+def test_search_equal_subkeys_at_scale(gpu_lib):
+    """All sub-keys equal (e.g. a constant initialisation), 2048 tokens at
+    S = 2048, n = 512: every score of a query ties; the k lowest composed
+    indices with equal weights."""
+    T, H, S, n, k = 2048, 4, 2048, 512, 32
+    q = normal_tensor((T, H, n), 151, torch.bfloat16).cuda()
+    K = torch.full((H, 2, S, n // 2), 0.0625, dtype=torch.bfloat16, device="cuda")
+    idx, w, score, hidx = gpu_lib.mem_search(q, K, k, want_half=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(hidx.cpu().numpy(), np.broadcast_to(np.arange(k), (T, H, 2, k)))
+    np.testing.assert_array_equal(idx.cpu().numpy(), np.broadcast_to(np.arange(k), (T, H, k)))
+    np.testing.assert_allclose(w.cpu().numpy(), 1.0 / k, rtol=1e-6)
+
+
+@pytest.mark.parametrize("rep", [7, 40, 300])
+def test_search_repeated_subkeys_integer(gpu_lib, rep):
+    """Sub-keys repeated in blocks of `rep` equal rows (integer values): ties at
+    every level, broken by the lower index; exact against the oracle."""
+    T, H, S, n, k = 300, 2, 900, 64, 32
+    q = int_tensor((T, H, n), 152, torch.bfloat16)
+    base = int_tensor((H, 2, S // rep + 1, n // 2), 153, torch.bfloat16)
+    K = base[:, :, torch.arange(S) // rep].contiguous()
+    idx, w, score, hidx = gpu_lib.mem_search(q.cuda(), K.cuda(), k, want_half=True)
+    torch.cuda.synchronize()
+    ref = oracle.search(h64(q), h64(K), k)
+    np.testing.assert_array_equal(hidx.cpu().numpy(), ref["half_idx"])
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    np.testing.assert_array_equal(h64(score), ref["score"])
+    assert normwise(h64(w), ref["w"]) <= TOL_F32
+
+
+def test_search_overflow_goes_to_the_exact_rescan(gpu_lib):
+    """More than 64 distinct scores above the threshold in one lane's rows:
+    the 64 rows of group 0 (row = 0 mod 64, all held by one lane) score far
+    above every other row, so the threshold (the k-th largest group maximum)
+    falls among the small scores and that lane's records exceed its slots; the
+    row is rescanned exactly.  fp32 keys make every score distinct."""
+    T, H, S, n, k = 40, 1, 4096, 8, 32
+    d = n // 2
+    q = torch.zeros((T, H, n), dtype=torch.float32)
+    q[:, :, 0] = 1.0
+    q[:, :, d] = 1.0
+    rows = torch.arange(S, dtype=torch.float32)
+    K = torch.zeros((H, 2, S, d), dtype=torch.float32)
+    K[:, 0, :, 0] = torch.where(rows % 64 == 0, 1000.0 + rows / 64, (rows % 64) + rows / 65536)
+    K[:, 1, :, 0] = -rows / 4096
+    q = q + 0.0
+    idx, w, score, hidx = gpu_lib.mem_search(q.cuda(), K.cuda(), k, want_half=True)
+    torch.cuda.synchronize()
+    ref = oracle.search(h64(q), h64(K), k)
+    np.testing.assert_array_equal(hidx.cpu().numpy(), ref["half_idx"])
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    assert normwise(h64(score), ref["score"]) <= TOL_F32
+    # half 0's selection is group 0's rows, the largest first
+    np.testing.assert_array_equal(hidx[:, :, 0].cpu().numpy(),
+                                  np.broadcast_to(np.arange(63, 63 - k, -1) * 64, (T, H, k)))
