@@ -70,3 +70,46 @@ def test_random_shape_full_path(gpu_lib, seed):
     s = oracle.search_backward(h64(q), h64(K), ref["idx"], b["grad_z"])
     assert normwise(h64(gq), s["grad_q"]) <= TOL_F32
     assert normwise(h64(gK), s["grad_K"]) <= TOL_F32
+
+
+@pytest.mark.parametrize("seed", list(range(2000, 2012)))
+def test_random_shape_extra_and_sink(gpu_lib, seed):
+    """Extra pairs (r random, possibly 0) and the sink pair over random shapes:
+    search exact, then the bag over k + r + 1 slots (the sink values in rows
+    S*S .. S*S + H - 1) and the sink search backward, against the oracle."""
+    c = random_shape(seed)
+    S, H, n, T, D, dt = c["S"], c["H"], c["n"], c["T"], c["D"], c["dt"]
+    rng = np.random.default_rng(seed)
+    k = min(c["k"], 48)
+    r = int(rng.integers(0, 64 - k))  # k + r + 1 <= 64
+    T = max(1, min(T, 12000 // (H * (k + r + 1))))
+    print(f"[random sink] seed {seed}: S={S} H={H} n={n} k={k} r={r} T={T} D={D} {dt}", flush=True)
+    N = S * S + H
+    q = int_tensor((T, H, n), seed + 1, dt)
+    K = int_tensor((H, 2, S, n // 2), seed + 2, dt)
+    ks = int_tensor((H, n), seed + 4, dt, -1, 1)
+    g = torch.Generator().manual_seed(seed + 3)
+    ex = torch.randint(0, S * S, (T, H, r), generator=g, dtype=torch.int64)
+    V = (torch.randn((N, D), generator=g) * 0.02).to(dt)
+    dy = torch.randn((T, D), generator=g).to(dt)
+    idx, w, score, _ = pk.mem_search_sink(q.cuda(), K.cuda(), k, ks.cuda(), S * S, ex.cuda())
+    torch.cuda.synchronize()
+    ref = oracle.search_sink(h64(q), h64(K), k, ex.numpy(), h64(ks), S * S)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    np.testing.assert_array_equal(h64(score), ref["score"])
+    assert normwise(h64(w), ref["w"]) <= TOL_F32
+    kk = k + r + 1
+    gv, gw, gz = pk.mem_bag_backward(dy.cuda(), V.cuda(), idx, w, mode="sorted")
+    gq, gK, gs = pk.mem_search_backward_sink(q.cuda(), K.cuda(), idx, gz, ks.cuda())
+    torch.cuda.synchronize()
+    b = oracle.bag_backward(h64(dy), h64(V), ref["idx"], ref["w"], H, kk)
+    assert normwise(h64(gv), b["grad_values"]) <= TOL_F32
+    assert normwise(h64(gz), b["grad_z"]) <= TOL_F32
+    s = oracle.search_backward_sink(h64(q), h64(K), ref["idx"], b["grad_z"], h64(ks))
+    assert normwise(h64(gq), s["grad_q"]) <= TOL_F32
+    assert normwise(h64(gK), s["grad_K"]) <= TOL_F32
+    # the sink's weight can be negligible (peaked softmax over integer scores):
+    # its score gradient then underflows in fp32, so the error is measured
+    # against one token's contribution to a key gradient as well
+    scale = max(np.abs(s["grad_sink"]).max(), np.abs(b["grad_z"]).max() * np.abs(h64(q)).max())
+    assert np.abs(h64(gs) - s["grad_sink"]).max() <= TOL_F32 * scale
