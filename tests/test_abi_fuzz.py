@@ -54,6 +54,11 @@ def test_search_family(lib, seed):
                                        _ptr(rng), ws, None) in CODES
         assert lib.mem_search_backward_qnorm(*args, 1e-5, _ptr(rng), _ptr(rng), _ptr(rng),
                                              _ptr(rng), _ptr(rng), ws, None) in CODES
+        row0 = int(rng.choice([-1, 0, max(a["S"], 0) ** 2, 1 << 40, (1 << 63) - 1]))
+        assert lib.mem_search_sink(*args, _sz(rng, -1, 40), _ptr(rng), _ptr(rng), row0, *outs,
+                                   _ptr(rng), ws, None) in CODES
+        assert lib.mem_search_backward_sink(*args, _ptr(rng), _ptr(rng), _ptr(rng), _ptr(rng),
+                                            _ptr(rng), _ptr(rng), _ptr(rng), ws, None) in CODES
 
 
 @pytest.mark.parametrize("seed", range(4))
@@ -88,5 +93,6 @@ def test_workspace_queries_never_fail(lib):
         T, H, S, k = _sz(rng, -5, 10 ** 6), _sz(rng, -2, 64), _sz(rng, -2, 9000), _sz(rng, -2, 70)
         assert lib.mem_search_workspace_size(T, H, S, k) >= 0
         assert lib.mem_search_backward_workspace_size(T, H, S, k) >= 0
+        assert lib.mem_search_backward_sink_workspace_size(T, H, _sz(rng, -2, 600), S, k) >= 0
         assert lib.mem_bag_backward_workspace_size(T, H, k, _sz(rng, -1, 10 ** 7),
                                                    _sz(rng, -8, 5000), int(rng.choice([0, 1, 2, 9]))) >= 0
