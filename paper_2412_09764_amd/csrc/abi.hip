@@ -43,6 +43,7 @@ struct SearchWs {
   float* half_score;
   uint32_t* ovf;
   float2* qstats;  // per (token, head) query (mean, rstd) when normalising
+  float* sink_part;  // per (token, head) the two halves' parts of the sink's score
   size_t bytes;
 };
 
@@ -63,6 +64,7 @@ SearchWs search_ws(void* base, int64_t T, int H, int k) {
   w.half_score = reinterpret_cast<float*>(take(rows * k * sizeof(float)));
   w.ovf = reinterpret_cast<uint32_t*>(take((rows + 1) * sizeof(uint32_t)));
   w.qstats = reinterpret_cast<float2*>(take((size_t)T * H * sizeof(float2)));
+  w.sink_part = reinterpret_cast<float*>(take((size_t)T * H * 2 * sizeof(float)));
   w.bytes = off;
   return w;
 }
@@ -384,15 +386,16 @@ static int search_common(const char* fn, const void* q, pkmem_dtype q_dt, const 
     if (e != hipSuccess) return hip_status(e, fn);
   }
   int32_t* hidx = half_idx_out ? half_idx_out : w.half_idx;
-  e = pk::launch_search_half(bf16, q, subkeys, T, H, n, S, k, qstats, w.cand, w.cnts, hidx,
-                             w.half_score, w.ovf, st);
+  e = pk::launch_search_half(bf16, q, subkeys, T, H, n, S, k, qstats, has_sink ? sink : nullptr,
+                             w.sink_part, w.cand, w.cnts, hidx, w.half_score, w.ovf, st);
   if (e != hipSuccess) return hip_status(e, fn);
   if (nex > 0) {
     rc = check_indices(fn, ex_idx, T * H * nex, (int64_t)S * S, st);
     if (rc) return rc;
   }
   e = pk::launch_cartesian(hidx, w.half_score, T, H, S, k, bf16, q, subkeys, n, ex_idx, nex,
-                           sink, sink_row0, idx_out, w_out, score_out, st);
+                           has_sink ? w.sink_part : nullptr, sink_row0, idx_out, w_out, score_out,
+                           st);
   if (e != hipSuccess) return hip_status(e, fn);
   return PKMEM_OK;
 }

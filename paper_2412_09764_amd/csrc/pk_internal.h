@@ -42,9 +42,12 @@ int cartesian_pairs(int k);
 // ovf = [1 + rows] u32 (count, then overflowed row ids).
 // qstats (nullable) = per (token, head) query (mean, rstd): the scoring then
 // normalises the queries as it loads them (see launch_qnorm).
+// With sink (a [H, n] key per head, the sub-keys' dtype), sink_part [T*H, 2]
+// receives each half's part of q . sink[h].
 hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
-                              int n, int S, int k, const float2* qstats, uint64_t* cand,
-                              uint32_t* cnts, int32_t* half_idx, float* half_score, uint32_t* ovf,
+                              int n, int S, int k, const float2* qstats, const void* sink,
+                              float* sink_part, uint64_t* cand, uint32_t* cnts,
+                              int32_t* half_idx, float* half_score, uint32_t* ovf,
                               hipStream_t st);
 // LayerNorm statistics of rows = T*H queries of n elements into stats, and
 // (qhat non-null) the normalised queries in the query dtype.
@@ -55,7 +58,7 @@ hipError_t launch_qnorm(bool bf16, const void* q, int64_t rows, int n, float eps
 // k + nex slots per row.  nex = 0: q, subkeys and ex_idx are not read.
 hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T, int H,
                             int S, int k, bool bf16, const void* q, const void* subkeys, int n,
-                            const int64_t* ex_idx, int nex, const void* sink,
+                            const int64_t* ex_idx, int nex, const float* sink_part,
                             int64_t sink_row0, int64_t* idx_out, float* w_out, float* score_out,
                             hipStream_t st);
 

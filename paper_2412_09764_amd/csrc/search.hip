@@ -70,6 +70,19 @@ struct MfmaOp<uint16_t> {  // bf16 storage
   __device__ static __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
   __device__ static __forceinline__ float stored(float v) { return round_bf16_f32(v); }
   // Normalised fragment, rounded to bf16 (nearest, ties to even).
+  // sum over the fragment's 8 elements of f[i] * s[i] (s: 8 bf16, 16-byte aligned)
+  __device__ static __forceinline__ float dot(frag f, const uint16_t* s) {
+    const uint4 u = __builtin_bit_cast(uint4, f);
+    const uint4 v = *reinterpret_cast<const uint4*>(s);
+    float a = bf16_lo(u.x) * bf16_lo(v.x);
+    a = fmaf(bf16_hi(u.x), bf16_hi(v.x), a);
+    a = fmaf(bf16_lo(u.y), bf16_lo(v.y), a);
+    a = fmaf(bf16_hi(u.y), bf16_hi(v.y), a);
+    a = fmaf(bf16_lo(u.z), bf16_lo(v.z), a);
+    a = fmaf(bf16_hi(u.z), bf16_hi(v.z), a);
+    a = fmaf(bf16_lo(u.w), bf16_lo(v.w), a);
+    return fmaf(bf16_hi(u.w), bf16_hi(v.w), a);
+  }
   __device__ static __forceinline__ frag normalize(frag f, float mean, float rstd) {
     uint4 u = __builtin_bit_cast(uint4, f);
     u.x = pack_bf16x2(qn_apply(bf16_lo(u.x), mean, rstd), qn_apply(bf16_hi(u.x), mean, rstd));
@@ -157,8 +170,8 @@ __device__ __forceinline__ int acc_row(int j, int kh) { return 8 * (j >> 2) + 4 
 template <typename T, int NSTEP>
 __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
     const T* __restrict__ q, const T* __restrict__ subkeys, int64_t ntok, int H, int n, int S,
-    int k, const float2* __restrict__ qstats, uint64_t* __restrict__ cand,
-    uint32_t* __restrict__ cnts) {
+    int k, const float2* __restrict__ qstats, const T* __restrict__ sink,
+    float* __restrict__ sink_part, uint64_t* __restrict__ cand, uint32_t* __restrict__ cnts) {
   using M = MfmaOp<T>;
   constexpr int DPAD = NSTEP * M::KSTEP;      // padded half dim
   constexpr int RB = DPAD * M::ESIZE;         // bytes per sub-key row in LDS
@@ -202,6 +215,26 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
       if (qstats && ld) f = M::normalize(f, qs.x, qs.y);
       bq[s] = f;
     }
+  }
+  // With a sink (a fixed key per head scored like any full key): this half's
+  // part of q . sink[h], from the fragments already in registers; the token's
+  // two lanes add their parts, and k_cartesian adds the two halves.
+  if (sink) {
+    const T* srow = sink + (size_t)h * n + (size_t)p * d;
+    float part = 0.f;
+    if constexpr (M::LANE_K > 1) {  // bf16: the fragments in registers
+#pragma unroll
+      for (int s = 0; s < NSTEP; ++s) {
+        const int e0 = s * M::KSTEP + kh * M::LANE_K;
+        if (e0 + M::LANE_K <= d) part += M::dot(bq[s], srow + e0);
+      }
+    } else {  // fp32: one element per fragment, read again (cached) to spare registers
+      const T* qrow = q + ((size_t)(tok_ok ? tok : 0) * H + h) * n + (size_t)p * d;
+#pragma unroll 8
+      for (int e = kh; e < d; e += 2) part = fmaf(M::to_f32(qrow[e]), M::to_f32(srow[e]), part);
+    }
+    part += __shfl_xor(part, 32, WAVE);
+    if (kh == 0 && tok_ok) sink_part[((size_t)tok * H + h) * 2 + p] = part;
   }
 
   // Chunk c into buffer b: 64*NCOL segments, 64 per wave instruction, each
@@ -486,8 +519,9 @@ __global__ __launch_bounds__(256) void k_topk_fallback(const T* __restrict__ q,
 // occupy slots k .. k + nex - 1 after the selected ones; the softmax runs over
 // all k + nex.  An index outside [0, S*S) is read as 0 (no out-of-bounds
 // access) and written out as given.  With a sink (a fixed key-value pair per
-// head), one more slot follows: the key sink[h*n .. h*n + n - 1] is scored the
-// same way and the slot's index is sink_row0 + h.
+// head), one more slot follows: its score is the sum of the two halves' parts
+// of q . sink[h] that the scoring kernel left in sink_part, and its index is
+// sink_row0 + h.
 template <int E, typename T, bool EXTRA>
 __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ half_idx,
                                                    const float* __restrict__ half_score,
@@ -495,7 +529,8 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
                                                    const T* __restrict__ q,
                                                    const T* __restrict__ subkeys, int H, int n,
                                                    const int64_t* __restrict__ ex_idx, int nex,
-                                                   const T* __restrict__ sink, int64_t sink_row0,
+                                                   const float* __restrict__ sink_part,
+                                                   int64_t sink_row0,
                                                    int64_t* __restrict__ idx_out,
                                                    float* __restrict__ w_out,
                                                    float* __restrict__ score_out) {
@@ -507,7 +542,7 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
   }
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nsc = EXTRA ? nex + (sink ? 1 : 0) : 0;  // full keys scored per row
+  const int nsc = EXTRA ? nex + (sink_part ? 1 : 0) : 0;  // full keys scored per row
   const int kk = k + nsc;                             // slots per row
   for (int64_t row = (int64_t)blockIdx.x * 4 + wave; row < rows; row += (int64_t)gridDim.x * 4) {
     // extra pairs first: their loads overlap the candidate sort below
@@ -515,77 +550,74 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
     int64_t ex_given = 0;
     if constexpr (EXTRA) {
       const int h = (int)(row % H);
-      const int d = n >> 1;
-      const bool ql = lane * 4 < d;
-      const int qo = ql ? lane * 4 : 0;
-      float fa[4], fb[4];
-      {
-        QQuad<T> qa, qb;
-        qa.load(q + (size_t)row * n + qo);
-        qb.load(q + (size_t)row * n + d + qo);
-        qa.to_f32(fa);
-        qb.to_f32(fb);
-      }
       const int64_t N = (int64_t)S * S;
       ex_given = lane < nex ? ex_idx[(size_t)row * nex + lane] : (lane == nex ? sink_row0 + h : 0);
-      const int64_t ex_safe = (ex_given >= 0 && ex_given < N) ? ex_given : 0;
-      const T* k1 = subkeys + (size_t)(h * 2) * S * d + qo;
-      const T* k2 = k1 + (size_t)S * d;
-      const T* ks1 = sink ? sink + (size_t)h * n + qo : k1;
-      // eight extras at a time: their sub-key loads in flight together, then
-      // one transposed butterfly (4 + 2 + 1 + 3 exchanges) leaves extra j's
-      // sum in lanes 8j .. 8j + 7
-      for (int e0 = 0; e0 < nsc; e0 += 8) {
-        QQuad<T> ka[8], kb[8];
+      if (nex > 0) {
+        const int d = n >> 1;
+        const bool ql = lane * 4 < d;
+        const int qo = ql ? lane * 4 : 0;
+        float fa[4], fb[4];
+        {
+          QQuad<T> qa, qb;
+          qa.load(q + (size_t)row * n + qo);
+          qb.load(q + (size_t)row * n + d + qo);
+          qa.to_f32(fa);
+          qb.to_f32(fb);
+        }
+        const int64_t ex_safe = (ex_given >= 0 && ex_given < N) ? ex_given : 0;
+        const T* k1 = subkeys + (size_t)(h * 2) * S * d + qo;
+        const T* k2 = k1 + (size_t)S * d;
+        // eight extras at a time: their sub-key loads in flight together, then
+        // one transposed butterfly (4 + 2 + 1 + 3 exchanges) leaves extra j's
+        // sum in lanes 8j .. 8j + 7
+        for (int e0 = 0; e0 < nex; e0 += 8) {
+          QQuad<T> ka[8], kb[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int e = e0 + j < nsc ? e0 + j : nsc - 1;
-          if (e < nex) {
+          for (int j = 0; j < 8; ++j) {
+            const int e = e0 + j < nex ? e0 + j : nex - 1;
             const uint64_t ie = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)ex_safe, e) |
                                 ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(ex_safe >> 32), e) << 32);
             const int i1 = (int)(ie / (uint64_t)S), i2 = (int)(ie % (uint64_t)S);
             ka[j].load(k1 + (size_t)i1 * d);
             kb[j].load(k2 + (size_t)i2 * d);
-          } else {  // the sink's key: both halves of one n-element row
-            ka[j].load(ks1);
-            kb[j].load(ks1 + d);
           }
-        }
-        float p[8];
+          float p[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          float va[4], vb[4];
-          ka[j].to_f32(va);
-          kb[j].to_f32(vb);
-          float a = 0.f;
+          for (int j = 0; j < 8; ++j) {
+            float va[4], vb[4];
+            ka[j].to_f32(va);
+            kb[j].to_f32(vb);
+            float a = 0.f;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) a = fmaf(fa[i], va[i], a);
+            for (int i = 0; i < 4; ++i) a = fmaf(fa[i], va[i], a);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) a = fmaf(fb[i], vb[i], a);
-          p[j] = ql ? a : 0.f;
-        }
-        const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
-        float p4[4], p2[2];
+            for (int i = 0; i < 4; ++i) a = fmaf(fb[i], vb[i], a);
+            p[j] = ql ? a : 0.f;
+          }
+          const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+          float p4[4], p2[2];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float send = b5 ? p[i] : p[i + 4];
-          p4[i] = (b5 ? p[i + 4] : p[i]) + __shfl_xor(send, 32, WAVE);
-        }
+          for (int i = 0; i < 4; ++i) {
+            const float send = b5 ? p[i] : p[i + 4];
+            p4[i] = (b5 ? p[i + 4] : p[i]) + __shfl_xor(send, 32, WAVE);
+          }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const float send = b4 ? p4[i] : p4[i + 2];
-          p2[i] = (b4 ? p4[i + 2] : p4[i]) + __shfl_xor(send, 16, WAVE);
+          for (int i = 0; i < 2; ++i) {
+            const float send = b4 ? p4[i] : p4[i + 2];
+            p2[i] = (b4 ? p4[i + 2] : p4[i]) + __shfl_xor(send, 16, WAVE);
+          }
+          float t1;
+          {
+            const float send = b3 ? p2[0] : p2[1];
+            t1 = (b3 ? p2[1] : p2[0]) + __shfl_xor(send, 8, WAVE);
+          }
+          t1 = group_sum<8>(t1);
+          const int src = (lane - e0) * 8;
+          const float got = __shfl(t1, src >= 0 && src < WAVE ? src : 0, WAVE);
+          if (lane >= e0 && lane < e0 + 8) ex_score = got;
         }
-        float t1;
-        {
-          const float send = b3 ? p2[0] : p2[1];
-          t1 = (b3 ? p2[1] : p2[0]) + __shfl_xor(send, 8, WAVE);
-        }
-        t1 = group_sum<8>(t1);
-        const int src = (lane - e0) * 8;
-        const float got = __shfl(t1, src >= 0 && src < WAVE ? src : 0, WAVE);
-        if (lane >= e0 && lane < e0 + 8) ex_score = got;
       }
+      if (sink_part && lane == nex) ex_score = sink_part[(size_t)row * 2] + sink_part[(size_t)row * 2 + 1];
     }
     const int32_t* i1 = half_idx + (size_t)row * 2 * k;
     const int32_t* i2 = i1 + k;
@@ -641,7 +673,8 @@ int cartesian_pairs(int k) {
 
 template <typename T, int NSTEP>
 static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, int H, int n, int S,
-                               int k, const float2* qstats, uint64_t* cand, uint32_t* cnts,
+                               int k, const float2* qstats, const void* sink, float* sink_part,
+                               uint64_t* cand, uint32_t* cnts,
                                int32_t* half_idx, float* half_score, uint32_t* ovf,
                                hipStream_t st) {
   const int64_t tiles = (T_ + SEARCH_TOK - 1) / SEARCH_TOK;
@@ -649,7 +682,8 @@ static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, i
   {
     LaunchTimer lt("score_topk", st);
     hipLaunchKernelGGL((k_score_topk<T, NSTEP>), dim3((unsigned)blocks), dim3(64 * SEARCH_WAVES), 0, st,
-                       (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats, cand, cnts);
+                       (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats, (const T*)sink,
+                       sink_part, cand, cnts);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -684,7 +718,8 @@ hipError_t launch_qnorm(bool bf16, const void* q, int64_t rows, int n, float eps
 }
 
 hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T_, int H,
-                              int n, int S, int k, const float2* qstats, uint64_t* cand,
+                              int n, int S, int k, const float2* qstats, const void* sink,
+                              float* sink_part, uint64_t* cand,
                               uint32_t* cnts, int32_t* half_idx, float* half_score, uint32_t* ovf,
                               hipStream_t st) {
   hipError_t e = launch_fill_u32(ovf, 0u, 1, st);
@@ -692,44 +727,44 @@ hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int
   const int d = n / 2;
   if (bf16) {
     const int steps = (d + 15) / 16;
-    if (steps <= 1) return launch_score<uint16_t, 1>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
-    if (steps <= 2) return launch_score<uint16_t, 2>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
-    if (steps <= 4) return launch_score<uint16_t, 4>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
-    if (steps <= 8) return launch_score<uint16_t, 8>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
-    return launch_score<uint16_t, 16>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+    if (steps <= 1) return launch_score<uint16_t, 1>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+    if (steps <= 2) return launch_score<uint16_t, 2>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+    if (steps <= 4) return launch_score<uint16_t, 4>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+    if (steps <= 8) return launch_score<uint16_t, 8>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+    return launch_score<uint16_t, 16>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
   }
   const int steps = (d + 1) / 2;
-  if (steps <= 2) return launch_score<float, 2>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
-  if (steps <= 4) return launch_score<float, 4>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
-  if (steps <= 8) return launch_score<float, 8>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
-  if (steps <= 16) return launch_score<float, 16>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
-  return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, qstats, cand, cnts, half_idx, half_score, ovf, st);
+  if (steps <= 2) return launch_score<float, 2>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+  if (steps <= 4) return launch_score<float, 4>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+  if (steps <= 8) return launch_score<float, 8>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+  if (steps <= 16) return launch_score<float, 16>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+  return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
 }
 
 template <int E>
 static void cart_launch(dim3 g, dim3 b, hipStream_t st, const int32_t* half_idx,
                         const float* half_score, int64_t rows, int S, int k, int np, bool bf16,
                         const void* q, const void* subkeys, int H, int n, const int64_t* ex_idx,
-                        int nex, const void* sink, int64_t sink_row0, int64_t* idx_out,
+                        int nex, const float* sink_part, int64_t sink_row0, int64_t* idx_out,
                         float* w_out, float* score_out) {
-  if (nex == 0 && !sink)
+  if (nex == 0 && !sink_part)
     hipLaunchKernelGGL((k_cartesian<E, uint16_t, false>), g, b, 0, st, half_idx, half_score, rows,
                        S, k, np, (const uint16_t*)nullptr, (const uint16_t*)nullptr, H, n,
-                       (const int64_t*)nullptr, 0, (const uint16_t*)nullptr, (int64_t)0, idx_out,
+                       (const int64_t*)nullptr, 0, (const float*)nullptr, (int64_t)0, idx_out,
                        w_out, score_out);
   else if (bf16)
     hipLaunchKernelGGL((k_cartesian<E, uint16_t, true>), g, b, 0, st, half_idx, half_score, rows, S,
                        k, np, (const uint16_t*)q, (const uint16_t*)subkeys, H, n, ex_idx, nex,
-                       (const uint16_t*)sink, sink_row0, idx_out, w_out, score_out);
+                       sink_part, sink_row0, idx_out, w_out, score_out);
   else
     hipLaunchKernelGGL((k_cartesian<E, float, true>), g, b, 0, st, half_idx, half_score, rows, S, k,
                        np, (const float*)q, (const float*)subkeys, H, n, ex_idx, nex,
-                       (const float*)sink, sink_row0, idx_out, w_out, score_out);
+                       sink_part, sink_row0, idx_out, w_out, score_out);
 }
 
 hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, int64_t T_, int H,
                             int S, int k, bool bf16, const void* q, const void* subkeys, int n,
-                            const int64_t* ex_idx, int nex, const void* sink,
+                            const int64_t* ex_idx, int nex, const float* sink_part,
                             int64_t sink_row0, int64_t* idx_out, float* w_out, float* score_out,
                             hipStream_t st) {
   const int64_t rows = T_ * H;
@@ -739,10 +774,10 @@ hipError_t launch_cartesian(const int32_t* half_idx, const float* half_score, in
   if (blocks < 1) blocks = 1;
   const dim3 g((unsigned)blocks), b(256);
   LaunchTimer lt("cartesian", st);
-  if (np <= 64) cart_launch<1>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink, sink_row0, idx_out, w_out, score_out);
-  else if (np <= 128) cart_launch<2>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink, sink_row0, idx_out, w_out, score_out);
-  else if (np <= 256) cart_launch<4>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink, sink_row0, idx_out, w_out, score_out);
-  else cart_launch<8>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink, sink_row0, idx_out, w_out, score_out);
+  if (np <= 64) cart_launch<1>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink_part, sink_row0, idx_out, w_out, score_out);
+  else if (np <= 128) cart_launch<2>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink_part, sink_row0, idx_out, w_out, score_out);
+  else if (np <= 256) cart_launch<4>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink_part, sink_row0, idx_out, w_out, score_out);
+  else cart_launch<8>(g, b, st, half_idx, half_score, rows, S, k, np, bf16, q, subkeys, H, n, ex_idx, nex, sink_part, sink_row0, idx_out, w_out, score_out);
   return hipGetLastError();
 }
 
