@@ -522,7 +522,9 @@ __global__ __launch_bounds__(256) void k_topk_fallback(const T* __restrict__ q,
 // head), one more slot follows: its score is the sum of the two halves' parts
 // of q . sink[h] that the scoring kernel left in sink_part, and its index is
 // sink_row0 + h.
-template <int E, typename T, bool EXTRA>
+// MODE: 0 = the k selected only, 1 = extra pairs (and the sink, if given),
+// 2 = the sink only.
+template <int E, typename T, int MODE>
 __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ half_idx,
                                                    const float* __restrict__ half_score,
                                                    int64_t rows, int S, int k, int npairs,
@@ -542,6 +544,7 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
   }
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr bool EXTRA = MODE != 0;
   const int nsc = EXTRA ? nex + (sink_part ? 1 : 0) : 0;  // full keys scored per row
   const int kk = k + nsc;                             // slots per row
   for (int64_t row = (int64_t)blockIdx.x * 4 + wave; row < rows; row += (int64_t)gridDim.x * 4) {
@@ -552,7 +555,7 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
       const int h = (int)(row % H);
       const int64_t N = (int64_t)S * S;
       ex_given = lane < nex ? ex_idx[(size_t)row * nex + lane] : (lane == nex ? sink_row0 + h : 0);
-      if (nex > 0) {
+      if (MODE == 1 && nex > 0) {
         const int d = n >> 1;
         const bool ql = lane * 4 < d;
         const int qo = ql ? lane * 4 : 0;
@@ -748,16 +751,21 @@ static void cart_launch(dim3 g, dim3 b, hipStream_t st, const int32_t* half_idx,
                         int nex, const float* sink_part, int64_t sink_row0, int64_t* idx_out,
                         float* w_out, float* score_out) {
   if (nex == 0 && !sink_part)
-    hipLaunchKernelGGL((k_cartesian<E, uint16_t, false>), g, b, 0, st, half_idx, half_score, rows,
+    hipLaunchKernelGGL((k_cartesian<E, uint16_t, 0>), g, b, 0, st, half_idx, half_score, rows,
                        S, k, np, (const uint16_t*)nullptr, (const uint16_t*)nullptr, H, n,
                        (const int64_t*)nullptr, 0, (const float*)nullptr, (int64_t)0, idx_out,
                        w_out, score_out);
+  else if (nex == 0)
+    hipLaunchKernelGGL((k_cartesian<E, uint16_t, 2>), g, b, 0, st, half_idx, half_score, rows,
+                       S, k, np, (const uint16_t*)nullptr, (const uint16_t*)nullptr, H, n,
+                       (const int64_t*)nullptr, 0, sink_part, sink_row0, idx_out, w_out,
+                       score_out);
   else if (bf16)
-    hipLaunchKernelGGL((k_cartesian<E, uint16_t, true>), g, b, 0, st, half_idx, half_score, rows, S,
+    hipLaunchKernelGGL((k_cartesian<E, uint16_t, 1>), g, b, 0, st, half_idx, half_score, rows, S,
                        k, np, (const uint16_t*)q, (const uint16_t*)subkeys, H, n, ex_idx, nex,
                        sink_part, sink_row0, idx_out, w_out, score_out);
   else
-    hipLaunchKernelGGL((k_cartesian<E, float, true>), g, b, 0, st, half_idx, half_score, rows, S, k,
+    hipLaunchKernelGGL((k_cartesian<E, float, 1>), g, b, 0, st, half_idx, half_score, rows, S, k,
                        np, (const float*)q, (const float*)subkeys, H, n, ex_idx, nex,
                        sink_part, sink_row0, idx_out, w_out, score_out);
 }
