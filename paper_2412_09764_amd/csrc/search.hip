@@ -69,7 +69,6 @@ struct MfmaOp<uint16_t> {  // bf16 storage
   __device__ static __forceinline__ frag zero() { return __builtin_bit_cast(frag, uint4{0, 0, 0, 0}); }
   __device__ static __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
   __device__ static __forceinline__ float stored(float v) { return round_bf16_f32(v); }
-  // Normalised fragment, rounded to bf16 (nearest, ties to even).
   // sum over the fragment's 8 elements of f[i] * s[i] (s: 8 bf16, 16-byte aligned)
   __device__ static __forceinline__ float dot(frag f, const uint16_t* s) {
     const uint4 u = __builtin_bit_cast(uint4, f);
@@ -83,6 +82,7 @@ struct MfmaOp<uint16_t> {  // bf16 storage
     a = fmaf(bf16_lo(u.w), bf16_lo(v.w), a);
     return fmaf(bf16_hi(u.w), bf16_hi(v.w), a);
   }
+  // Normalised fragment, rounded to bf16 (nearest, ties to even).
   __device__ static __forceinline__ frag normalize(frag f, float mean, float rstd) {
     uint4 u = __builtin_bit_cast(uint4, f);
     u.x = pack_bf16x2(qn_apply(bf16_lo(u.x), mean, rstd), qn_apply(bf16_hi(u.x), mean, rstd));
@@ -114,8 +114,11 @@ struct MfmaOp<float> {
 // Per (token, head) query of n elements (n * esize <= 1 KiB): mean and
 // rstd = 1 / sqrt(var + eps) of LayerNorm without affine (biased variance,
 // fp32, centred second pass; rstd = 0 where var + eps == 0), one wave per
-// query, lane l holding the 16-byte chunk l.  qhat (optional) receives the
+// four queries (their loads issued together), lane l holding the 16-byte
+// chunk l of each.  qhat (optional) receives the
 // normalised query rounded to the query dtype, exactly as the scoring uses it.
+constexpr int QNORM_ROWS = 4;  // query rows per wave
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_qnorm(const T* __restrict__ q, int64_t rows, int n,
                                                float eps, float2* __restrict__ stats,
@@ -123,43 +126,51 @@ __global__ __launch_bounds__(256) void k_qnorm(const T* __restrict__ q, int64_t 
   constexpr int EPL = 16 / (int)sizeof(T);
   using M = MfmaOp<T>;
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= rows) return;  // whole wave
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * QNORM_ROWS;
+  if (r0 >= rows) return;  // whole wave
   const bool has = lane * EPL < n;
-  float x[EPL];
-  {
-    const uint4 raw = has ? ld16(q + r * n + lane * EPL) : uint4{0, 0, 0, 0};
+  // the wave's rows loaded together, then each reduced on its own
+  float x[QNORM_ROWS][EPL];
+#pragma unroll
+  for (int j = 0; j < QNORM_ROWS; ++j) {
+    const int64_t r = r0 + j;
+    const uint4 raw = (has && r < rows) ? ld16(q + r * n + lane * EPL) : uint4{0, 0, 0, 0};
     const T* e = reinterpret_cast<const T*>(&raw);
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) x[i] = M::to_f32(e[i]);
+    for (int i = 0; i < EPL; ++i) x[j][i] = M::to_f32(e[i]);
   }
-  float sum = 0.f;
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) sum += x[i];
-  sum = group_sum<WAVE>(sum);
-  const float mean = sum / (float)n;
-  float sq = 0.f;
-  if (has) {
+  for (int j = 0; j < QNORM_ROWS; ++j) {
+    const int64_t r = r0 + j;
+    if (r >= rows) break;  // the same for the whole wave
+    float sum = 0.f;
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-      const float c = x[i] - mean;
-      sq = fmaf(c, c, sq);
+    for (int i = 0; i < EPL; ++i) sum += x[j][i];
+    sum = group_sum<WAVE>(sum);
+    const float mean = sum / (float)n;
+    float sq = 0.f;
+    if (has) {
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) {
+        const float c = x[j][i] - mean;
+        sq = fmaf(c, c, sq);
+      }
     }
-  }
-  sq = group_sum<WAVE>(sq);
-  const float ve = sq / (float)n + eps;
-  const float rstd = ve > 0.f ? 1.f / sqrtf(ve) : 0.f;
-  if (lane == 0) stats[r] = make_float2(mean, rstd);
-  if (qhat && has) {
-    uint4 o;
-    T* e = reinterpret_cast<T*>(&o);
+    sq = group_sum<WAVE>(sq);
+    const float ve = sq / (float)n + eps;
+    const float rstd = ve > 0.f ? 1.f / sqrtf(ve) : 0.f;
+    if (lane == 0) stats[r] = make_float2(mean, rstd);
+    if (qhat && has) {
+      uint4 o;
+      T* e = reinterpret_cast<T*>(&o);
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-      const float v = M::stored(qn_apply(x[i], mean, rstd));
-      if constexpr (sizeof(T) == 2) e[i] = (T)(__float_as_uint(v) >> 16);
-      else e[i] = v;
+      for (int i = 0; i < EPL; ++i) {
+        const float v = M::stored(qn_apply(x[j][i], mean, rstd));
+        if constexpr (sizeof(T) == 2) e[i] = (T)(__float_as_uint(v) >> 16);
+        else e[i] = v;
+      }
+      *reinterpret_cast<uint4*>(qhat + r * n + lane * EPL) = o;
     }
-    *reinterpret_cast<uint4*>(qhat + r * n + lane * EPL) = o;
   }
 }
 
@@ -710,7 +721,7 @@ hipError_t launch_qnorm(bool bf16, const void* q, int64_t rows, int n, float eps
                        void* qhat, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   LaunchTimer lt("qnorm", st);
-  const dim3 g((unsigned)((rows + 3) / 4)), b(256);
+  const dim3 g((unsigned)((rows + 4 * QNORM_ROWS - 1) / (4 * QNORM_ROWS))), b(256);
   if (bf16)
     hipLaunchKernelGGL(k_qnorm<uint16_t>, g, b, 0, st, (const uint16_t*)q, rows, n, eps, stats,
                        (uint16_t*)qhat);
