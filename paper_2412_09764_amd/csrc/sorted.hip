@@ -3,10 +3,12 @@
 // gradient row knows which lookups contribute to it).
 //
 //   1. Stable LSD radix sort of the L = T*H*k lookups by row: 8-bit digits,
-//      per pass a tile histogram, a device-wide exclusive scan of the
-//      digit-major histogram, and a stable scatter whose in-tile ranks come
-//      from wave ballots.  Keys are rows (< 2^26), values lookup ids.
-//   2. Segment heads (first lookup of each distinct row) -> seg_start[U + 1].
+//      per pass a tile histogram, a scan of each digit's tile counts (one
+//      workgroup per digit), and a stable scatter: each wave ranks a
+//      contiguous quarter of the tile with ballots, and the tile goes out
+//      through LDS in sorted order.  Keys are rows (< 2^26), values lookup ids.
+//   2. Segment heads (first lookup of each distinct row) -> seg_start[U + 1],
+//      the head flags computed where they are counted and placed.
 //   3. One lane group per touched row (two adjacent rows per iteration): read
 //      the value row once, then take the contributing lookups in lookup order,
 //      a few at a time with their dy rows loaded together, add w * dy into a
@@ -16,8 +18,9 @@
 //      value and gradient tables are streamed nearly sequentially, and the
 //      result is bitwise deterministic.
 //   4. A row with more than LONG_SEG lookups would hold one lane group for
-//      its whole length: the per-row kernel lists it instead, and a second
-//      kernel gives each listed row a workgroup whose lane groups take
+//      its whole length: k_list_long lists it, the per-row kernel skips it,
+//      and a second kernel gives each listed row a workgroup whose lane
+//      groups take
 //      contiguous runs of its lookups; their partial sums meet in LDS and are
 //      added in group order (still deterministic).
 #include "pk_device.h"
