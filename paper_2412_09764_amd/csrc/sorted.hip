@@ -20,9 +20,8 @@
 //   4. A row with more than LONG_SEG lookups would hold one lane group for
 //      its whole length: k_list_long lists it, the per-row kernel skips it,
 //      and a second kernel gives each listed row a workgroup whose lane
-//      groups take
-//      contiguous runs of its lookups; their partial sums meet in LDS and are
-//      added in group order (still deterministic).
+//      groups take contiguous runs of its lookups; their partial sums meet in
+//      LDS and are added in group order (still deterministic).
 #include "pk_device.h"
 #include "pk_internal.h"
 
