@@ -36,11 +36,13 @@
 //     (LayerNorm without affine, fp32, centred second pass); the scoring
 //     kernel normalises its query fragments as it loads them and rounds them
 //     to the query dtype, so the normalised queries never go through memory.
+//   * With a sink (a fixed key per head), the kernel's prologue also forms
+//     each half's part of q . sink[h] from the query fragments in registers.
 // Step 2, k_cartesian: per (token, head) the top k of the sums s1[a] + s2[b]
 //   over rank pairs with (a+1)(b+1) <= k (every other pair is beaten by at
 //   least k pairs), ordered (sum desc, composed index i1*S + i2 asc), then the
 //   softmax over the k selected sums (and over any extra key-value pairs the
-//   caller adds, scored in the same kernel).
+//   caller adds, scored in the same kernel, and the sink's score).
 #include "pk_device.h"
 #include "pk_internal.h"
 
