@@ -180,7 +180,9 @@ __global__ __launch_bounds__(256) void k_qnorm(const T* __restrict__ q, int64_t 
 // upper-half bit is kh (columns are lane & 31).
 __device__ __forceinline__ int acc_row(int j, int kh) { return 8 * (j >> 2) + 4 * kh + (j & 3); }
 
-template <typename T, int NSTEP>
+// KBIG (k > 32): records equal to the threshold are counted one by one (the
+// per-tile rule below needs 2k <= CAND_CAP / 2).
+template <typename T, int NSTEP, bool KBIG>
 __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
     const T* __restrict__ q, const T* __restrict__ subkeys, int64_t ntok, int H, int n, int S,
     int k, const float2* __restrict__ qstats, const T* __restrict__ sink,
@@ -389,28 +391,29 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   const float thl = tok_ok ? th : INFINITY;  // scores are finite
   const float strict = next_up(thl);
   float bound = thl;
+  uint32_t my_eq = 0;  // KBIG: records kept equal to the threshold
+  auto keep = [&](float z, uint32_t row) {
+    my_cand[my_cnt < (uint32_t)HALF_CAP ? my_cnt : (uint32_t)HALF_CAP - 1] =
+        (uint64_t(__float_as_uint(z)) << 32) | row;
+    ++my_cnt;
+    if constexpr (KBIG) {  // the k-th record at the threshold: only higher scores from now on
+      if (z == thl && ++my_eq == (uint32_t)k) bound = strict;
+    }
+  };
   sweep([&](const f32x16_t& acc, int c, int half) {
     const uint32_t r0 = (uint32_t)(c * CHUNK_ROWS + half * 32 + 4 * kh);
     if (c < nfull) {  // uniform
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        if (acc[j] >= bound) {
-          my_cand[my_cnt < (uint32_t)HALF_CAP ? my_cnt : (uint32_t)HALF_CAP - 1] =
-              (uint64_t(__float_as_uint(acc[j])) << 32) | (r0 + 8 * (j >> 2) + (j & 3));
-          ++my_cnt;
-        }
-      }
+      for (int j = 0; j < 16; ++j)
+        if (acc[j] >= bound) keep(acc[j], r0 + 8 * (j >> 2) + (j & 3));
     } else {
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const uint32_t row = r0 + 8 * (j >> 2) + (j & 3);
-        if (acc[j] >= bound && row < (uint32_t)S) {
-          my_cand[my_cnt < (uint32_t)HALF_CAP ? my_cnt : (uint32_t)HALF_CAP - 1] = (uint64_t(__float_as_uint(acc[j])) << 32) | row;
-          ++my_cnt;
-        }
+        if (acc[j] >= bound && row < (uint32_t)S) keep(acc[j], row);
       }
     }
-    bound = my_cnt >= 2u * (uint32_t)k ? strict : bound;
+    if constexpr (!KBIG) bound = my_cnt >= 2u * (uint32_t)k ? strict : bound;
   });
   if (tok_ok) cnts[rid * 2 + kh] = my_cnt;
 }
@@ -697,9 +700,14 @@ static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, i
   const int64_t blocks = tiles * 2 * H;
   {
     LaunchTimer lt("score_topk", st);
-    hipLaunchKernelGGL((k_score_topk<T, NSTEP>), dim3((unsigned)blocks), dim3(64 * SEARCH_WAVES), 0, st,
-                       (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats, (const T*)sink,
-                       sink_part, cand, cnts);
+    if (k > 32)
+      hipLaunchKernelGGL((k_score_topk<T, NSTEP, true>), dim3((unsigned)blocks), dim3(64 * SEARCH_WAVES),
+                         0, st, (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats,
+                         (const T*)sink, sink_part, cand, cnts);
+    else
+      hipLaunchKernelGGL((k_score_topk<T, NSTEP, false>), dim3((unsigned)blocks), dim3(64 * SEARCH_WAVES),
+                         0, st, (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats,
+                         (const T*)sink, sink_part, cand, cnts);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

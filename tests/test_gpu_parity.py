@@ -330,3 +330,33 @@ def test_search_overflow_goes_to_the_exact_rescan(gpu_lib):
     # half 0's selection is group 0's rows, the largest first
     np.testing.assert_array_equal(hidx[:, :, 0].cpu().numpy(),
                                   np.broadcast_to(np.arange(63, 63 - k, -1) * 64, (T, H, k)))
+
+
+@pytest.mark.parametrize("k", [48, 64])
+def test_search_all_ties_large_k(gpu_lib, k):
+    """k > 32: a lane counts the records equal to the threshold one by one and
+    keeps the first k; with every score tied the result is the k lowest
+    composed indices without the rescan."""
+    T, H, S, n = 1000, 2, 512, 128
+    q = normal_tensor((T, H, n), 154, torch.bfloat16).cuda()
+    K = torch.full((H, 2, S, n // 2), 0.125, dtype=torch.bfloat16, device="cuda")
+    idx, w, score, hidx = gpu_lib.mem_search(q, K, k, want_half=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(hidx.cpu().numpy(), np.broadcast_to(np.arange(k), (T, H, 2, k)))
+    np.testing.assert_array_equal(idx.cpu().numpy(), np.broadcast_to(np.arange(k), (T, H, k)))
+    np.testing.assert_allclose(w.cpu().numpy(), 1.0 / k, rtol=1e-6)
+
+
+def test_search_repeated_subkeys_integer_large_k(gpu_lib):
+    """k = 48 on sub-keys repeated in blocks of 40 equal rows: exact against the
+    oracle."""
+    T, H, S, n, k = 200, 2, 900, 64, 48
+    q = int_tensor((T, H, n), 155, torch.bfloat16)
+    base = int_tensor((H, 2, S // 40 + 1, n // 2), 156, torch.bfloat16)
+    K = base[:, :, torch.arange(S) // 40].contiguous()
+    idx, w, score, hidx = gpu_lib.mem_search(q.cuda(), K.cuda(), k, want_half=True)
+    torch.cuda.synchronize()
+    ref = oracle.search(h64(q), h64(K), k)
+    np.testing.assert_array_equal(hidx.cpu().numpy(), ref["half_idx"])
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    np.testing.assert_array_equal(h64(score), ref["score"])
