@@ -13,8 +13,9 @@
  * Conventions for every entry point
  *   - Pointers are DEVICE pointers unless marked "host".  All device buffers are
  *     allocated and owned by the caller; the library allocates no device memory
- *     and keeps no device state between calls (one exception, off by default:
- *     the 4-byte flag of the PKMEM_DEBUG index check, see Environment below).
+ *     and keeps no device state between calls (two exceptions: the 4-byte flag
+ *     of the PKMEM_DEBUG index check, off by default, see Environment below,
+ *     and the static scratch array of mem_search_noalloc).
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = null stream) and
  *     return once the work is enqueued.  mem_bag_backward_sparse is the only call
  *     that waits on the stream (it must report a row count to the host).
@@ -97,6 +98,35 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
                int64_t T, int H, int n, int S, int k,
                int64_t* idx_out, float* w_out, float* score_out, int32_t* half_idx_out,
                void* ws, size_t ws_bytes, pkmem_stream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * mem_search without a workspace argument, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops (search
+ * then mem_bag_forward, which needs no workspace), harnesses that forbid
+ * allocation.  It runs mem_search's kernels with its workspace carved from a
+ * static device array of PKMEM_NOALLOC_SCRATCH_BYTES that the library holds
+ * on each GPU it runs on until the process ends; the call itself allocates
+ * nothing (no hipMalloc, no allocating library routine).
+ *   Arguments and outputs as for mem_search.
+ *   Size limit: mem_search_workspace_size(T, H, S, k) <= PKMEM_NOALLOC_SCRATCH_BYTES
+ *   (64 MiB: about 25,000 (token, head) rows at k = 32, e.g. T = 6,400 at
+ *   H = 4); larger requests return PKMEM_ERR_UNSUPPORTED before touching the
+ *   device (use mem_search with a workspace).
+ *   Sharing: every call on one GPU uses that GPU's one array, which keeps the
+ *   last call's contents (nothing read is assumed to start at zero; the call
+ *   clears what it needs with a fill kernel).  Calls that overlap on one GPU
+ *   (different streams, or different host threads, without ordering between
+ *   them) race on the array and give undefined results: serialise them.
+ *   Set-up: the first call on a device looks up that device's address of the
+ *   array once (hipGetSymbolAddress) with the device current; a failure there
+ *   returns PKMEM_ERR_HIP.
+ * ------------------------------------------------------------------------ */
+#define PKMEM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+int mem_search_noalloc(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                       int64_t T, int H, int n, int S, int k,
+                       int64_t* idx_out, float* w_out, float* score_out, int32_t* half_idx_out,
+                       pkmem_stream_t stream);
 
 /* ------------------------------------------------------------------------ *
  * Search with extra key-value pairs beside the top-k (Sec. 5.4, model

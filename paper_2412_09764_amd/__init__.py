@@ -13,13 +13,15 @@ there is no fallback: without the built library every call raises.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
 import torch  # noqa: F401  (first: the library binds to the HIP runtime torch loads)
 
 __all__ = [
-    "PkmemError", "load", "lib_path", "mem_search", "mem_search_backward", "mem_search_qnorm",
+    "PkmemError", "load", "lib_path", "mem_search", "mem_search_noalloc", "mem_search_backward",
+    "mem_search_qnorm", "NOALLOC_SCRATCH_BYTES",
     "mem_search_backward_qnorm", "mem_search_extra", "mem_search_sink",
     "mem_search_backward_sink", "mem_bag_forward",
     "mem_bag_forward_gated", "mem_gate_backward",
@@ -29,6 +31,7 @@ __all__ = [
 ]
 
 F32, BF16 = 0, 1
+NOALLOC_SCRATCH_BYTES = 64 << 20  # PKMEM_NOALLOC_SCRATCH_BYTES
 BWD_MODES = {"auto": 0, "atomic": 1, "sorted": 2}
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
@@ -58,6 +61,8 @@ def load() -> ctypes.CDLL:
     L.mem_search_workspace_size.restype = SZ
     L.mem_search.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, SZ, P]
     L.mem_search.restype = I32
+    L.mem_search_noalloc.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P]
+    L.mem_search_noalloc.restype = I32
     L.mem_search_backward_workspace_size.argtypes = [I64, I32, I32, I32]
     L.mem_search_backward_workspace_size.restype = SZ
     L.mem_search_backward.argtypes = [P, I32, P, I32, I64, I32, I32, I32, I32, P, P, P, P, P, SZ, P]
@@ -139,6 +144,13 @@ def _stream(stream) -> int:
     return s.cuda_stream
 
 
+def _on(stream):
+    """Context making `stream` (if given) torch's current stream, so that the
+    outputs and workspaces allocated inside belong to the stream the library
+    launches on and any zero-fill is ordered before the launch."""
+    return contextlib.nullcontext() if stream is None else torch.cuda.stream(stream)
+
+
 def _workspace(nbytes: int, device, ws):
     if ws is not None:
         if ws.numel() * ws.element_size() < nbytes:
@@ -185,6 +197,34 @@ def mem_search(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None, 
     """
     return _search(q, subkeys, k, None, idx_out, w_out, score_out, half_idx_out, want_score,
                    want_half, None, None, workspace, stream)[:4]
+
+
+def mem_search_noalloc(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None,
+                       w_out=None, score_out=None, half_idx_out=None, want_score: bool = True,
+                       want_half: bool = False, stream=None):
+    """mem_search with its workspace in the library's static device scratch
+    array (no workspace argument; the C call allocates nothing).  Outputs not
+    given are allocated here with torch; pass them all to allocate nothing.
+    Requires mem_search_workspace_size(T, H, S, k) <= NOALLOC_SCRATCH_BYTES."""
+    L = load()
+    _dev(q, subkeys)
+    T, H, n = q.shape
+    S = subkeys.shape[2]
+    with _on(stream):
+        dev = q.device
+        if idx_out is None:
+            idx_out = torch.empty((T, H, k), dtype=torch.int64, device=dev)
+        if w_out is None:
+            w_out = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+        if score_out is None and want_score:
+            score_out = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+        if half_idx_out is None and want_half:
+            half_idx_out = torch.empty((T, H, 2, k), dtype=torch.int32, device=dev)
+        _dev(idx_out, w_out, score_out, half_idx_out)
+        _check(L.mem_search_noalloc(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
+                                    _ptr(idx_out), _ptr(w_out), _ptr(score_out),
+                                    _ptr(half_idx_out), _stream(None)))
+    return idx_out, w_out, score_out, half_idx_out
 
 
 def mem_search_qnorm(q: torch.Tensor, subkeys: torch.Tensor, k: int, eps: float = 1e-5, *,

@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -406,6 +407,65 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
   return search_common("mem_search", q, q_dt, subkeys, k_dt, T, H, n, S, k, false, 0.f, 0, nullptr,
                        false, nullptr, 0, idx_out, w_out, score_out, half_idx_out, nullptr, nullptr, ws, ws_bytes,
                        stream);
+}
+
+}  // extern "C"
+
+// Workspace of mem_search_noalloc: one array per GPU, part of the library's
+// code object, held until the process ends.  Host code never uses its name as
+// an address: the device address comes from hipGetSymbolAddress, looked up
+// once per device with that device current.
+static __device__ __align__(256) unsigned char scratch[PKMEM_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int SCRATCH_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[SCRATCH_DEVICES] = {};
+
+// The current device's address of the scratch array (looked up at the first
+// call on that device).
+int scratch_on_current_device(const char* fn, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, fn);
+  if (dev < 0 || dev >= SCRATCH_DEVICES) return fail(PKMEM_ERR_UNSUPPORTED, "%s: device %d", fn, dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, fn);
+    if (!p) return fail(PKMEM_ERR_HIP, "%s: no device address for the scratch array", fn);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return PKMEM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mem_search_noalloc(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
+                       int64_t T, int H, int n, int S, int k, int64_t* idx_out, float* w_out,
+                       float* score_out, int32_t* half_idx_out, pkmem_stream_t stream) {
+  const char* fn = "mem_search_noalloc";
+  int rc = check_search_shapes(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k);
+  if (rc) return rc;
+  const size_t need = search_ws(nullptr, T, H, k).bytes;
+  if (need > PKMEM_NOALLOC_SCRATCH_BYTES)
+    return fail(PKMEM_ERR_UNSUPPORTED,
+                "%s: T=%lld, H=%d, k=%d needs %zu bytes of scratch, more than its %zu "
+                "(use mem_search with a workspace)",
+                fn, (long long)T, H, k, need, (size_t)PKMEM_NOALLOC_SCRATCH_BYTES);
+  if (T > 0 && (!idx_out || !w_out)) return fail(PKMEM_ERR_INVALID, "%s: null pointer", fn);
+  if (T == 0) return PKMEM_OK;
+  void* ws = nullptr;
+  rc = scratch_on_current_device(fn, &ws);
+  if (rc) return rc;
+  return search_common(fn, q, q_dt, subkeys, k_dt, T, H, n, S, k, false, 0.f, 0, nullptr, false,
+                       nullptr, 0, idx_out, w_out, score_out, half_idx_out, nullptr, nullptr, ws,
+                       PKMEM_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int mem_search_qnorm(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
