@@ -6,15 +6,17 @@ Sec. 3, Eq. (1), and the weighted EmbeddingBag forward and backward of
 Sec. 3.1.4, as hand-written HIP kernels for gfx950.
 
 This module only marshals arguments: it checks tensor placement and dtype,
-allocates outputs and workspaces with torch on the current device, passes raw
-pointers and the current HIP stream through the C ABI, and turns a non-zero
-status into PkmemError.  Every step of the computation runs in the library;
+allocates outputs and workspaces with torch on the current device (on the
+`stream` argument when one is given, else on the current stream), passes raw
+pointers and that HIP stream through the C ABI, and turns a non-zero status
+into PkmemError.  Every step of the computation runs in the library;
 there is no fallback: without the built library every call raises.
 """
 from __future__ import annotations
 
 import contextlib
 import ctypes
+import functools
 import os
 
 import torch  # noqa: F401  (first: the library binds to the HIP runtime torch loads)
@@ -31,7 +33,7 @@ __all__ = [
 ]
 
 F32, BF16 = 0, 1
-NOALLOC_SCRATCH_BYTES = 64 << 20  # PKMEM_NOALLOC_SCRATCH_BYTES
+NOALLOC_SCRATCH_BYTES = 128 << 20  # PKMEM_NOALLOC_SCRATCH_BYTES
 BWD_MODES = {"auto": 0, "atomic": 1, "sorted": 2}
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
@@ -151,6 +153,18 @@ def _on(stream):
     return contextlib.nullcontext() if stream is None else torch.cuda.stream(stream)
 
 
+def _launches_on_stream(fn):
+    """Runs fn with its `stream` argument (if given) as torch's current stream:
+    outputs, workspaces and zero-filled accumulators allocated by the wrapper
+    then belong to the stream the library launches on, and the fills are
+    ordered before the launch on that stream."""
+    @functools.wraps(fn)
+    def wrapper(*args, stream=None, **kw):
+        with _on(stream):
+            return fn(*args, stream=stream, **kw)
+    return wrapper
+
+
 def _workspace(nbytes: int, device, ws):
     if ws is not None:
         if ws.numel() * ws.element_size() < nbytes:
@@ -187,6 +201,7 @@ def mem_bag_backward_workspace_size(T: int, H: int, k: int, N: int, D: int, mode
     return int(load().mem_bag_backward_workspace_size(T, H, k, N, D, m))
 
 
+@_launches_on_stream
 def mem_search(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None, w_out=None,
                score_out=None, half_idx_out=None, want_score: bool = True,
                want_half: bool = False, workspace=None, stream=None):
@@ -199,6 +214,7 @@ def mem_search(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None, 
                    want_half, None, None, workspace, stream)[:4]
 
 
+@_launches_on_stream
 def mem_search_noalloc(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_out=None,
                        w_out=None, score_out=None, half_idx_out=None, want_score: bool = True,
                        want_half: bool = False, stream=None):
@@ -210,23 +226,23 @@ def mem_search_noalloc(q: torch.Tensor, subkeys: torch.Tensor, k: int, *, idx_ou
     _dev(q, subkeys)
     T, H, n = q.shape
     S = subkeys.shape[2]
-    with _on(stream):
-        dev = q.device
-        if idx_out is None:
-            idx_out = torch.empty((T, H, k), dtype=torch.int64, device=dev)
-        if w_out is None:
-            w_out = torch.empty((T, H, k), dtype=torch.float32, device=dev)
-        if score_out is None and want_score:
-            score_out = torch.empty((T, H, k), dtype=torch.float32, device=dev)
-        if half_idx_out is None and want_half:
-            half_idx_out = torch.empty((T, H, 2, k), dtype=torch.int32, device=dev)
-        _dev(idx_out, w_out, score_out, half_idx_out)
-        _check(L.mem_search_noalloc(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
-                                    _ptr(idx_out), _ptr(w_out), _ptr(score_out),
-                                    _ptr(half_idx_out), _stream(None)))
+    dev = q.device
+    if idx_out is None:
+        idx_out = torch.empty((T, H, k), dtype=torch.int64, device=dev)
+    if w_out is None:
+        w_out = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    if score_out is None and want_score:
+        score_out = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+    if half_idx_out is None and want_half:
+        half_idx_out = torch.empty((T, H, 2, k), dtype=torch.int32, device=dev)
+    _dev(idx_out, w_out, score_out, half_idx_out)
+    _check(L.mem_search_noalloc(_ptr(q), _dt(q), _ptr(subkeys), _dt(subkeys), T, H, n, S, k,
+                                _ptr(idx_out), _ptr(w_out), _ptr(score_out), _ptr(half_idx_out),
+                                _stream(stream)))
     return idx_out, w_out, score_out, half_idx_out
 
 
+@_launches_on_stream
 def mem_search_qnorm(q: torch.Tensor, subkeys: torch.Tensor, k: int, eps: float = 1e-5, *,
                      idx_out=None, w_out=None, score_out=None, half_idx_out=None,
                      want_score: bool = True, want_half: bool = False, qhat_out=None,
@@ -244,6 +260,7 @@ def mem_search_qnorm(q: torch.Tensor, subkeys: torch.Tensor, k: int, eps: float 
                    want_half, qhat_out, stats_out, workspace, stream)
 
 
+@_launches_on_stream
 def mem_search_extra(q: torch.Tensor, subkeys: torch.Tensor, k: int, extra_idx: torch.Tensor, *,
                      idx_out=None, w_out=None, score_out=None, half_idx_out=None,
                      want_score: bool = True, want_half: bool = False, workspace=None,
@@ -255,6 +272,7 @@ def mem_search_extra(q: torch.Tensor, subkeys: torch.Tensor, k: int, extra_idx: 
                          half_idx_out, want_score, want_half, workspace, stream)
 
 
+@_launches_on_stream
 def mem_search_sink(q: torch.Tensor, subkeys: torch.Tensor, k: int, sink_keys: torch.Tensor,
                     sink_row0: int, extra_idx=None, *, idx_out=None, w_out=None, score_out=None,
                     half_idx_out=None, want_score: bool = True, want_half: bool = False,
@@ -335,6 +353,7 @@ def _search(q, subkeys, k, eps, idx_out, w_out, score_out, half_idx_out, want_sc
     return idx_out, w_out, score_out, half_idx_out, qhat_out, stats_out
 
 
+@_launches_on_stream
 def mem_search_backward(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tensor,
                         grad_scores: torch.Tensor, *, grad_q=None, grad_subkeys=None,
                         want_grad_q: bool = True, want_grad_subkeys: bool = True, workspace=None,
@@ -346,6 +365,7 @@ def mem_search_backward(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tenso
                             want_grad_subkeys, workspace, stream)
 
 
+@_launches_on_stream
 def mem_search_backward_qnorm(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tensor,
                               grad_scores: torch.Tensor, eps: float = 1e-5, *, grad_q=None,
                               grad_subkeys=None, want_grad_q: bool = True,
@@ -357,6 +377,7 @@ def mem_search_backward_qnorm(q: torch.Tensor, subkeys: torch.Tensor, idx: torch
                             want_grad_q, want_grad_subkeys, workspace, stream)
 
 
+@_launches_on_stream
 def mem_search_backward_sink(q: torch.Tensor, subkeys: torch.Tensor, idx: torch.Tensor,
                              grad_scores: torch.Tensor, sink_keys: torch.Tensor, *, grad_q=None,
                              grad_subkeys=None, grad_sink=None, want_grad_q: bool = True,
@@ -412,6 +433,7 @@ def _search_backward(q, subkeys, idx, grad_scores, eps, grad_q, grad_subkeys, wa
     return grad_q, grad_subkeys
 
 
+@_launches_on_stream
 def mem_bag_forward(values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor, *, y_out=None,
                     stream=None):
     """y[t] = sum_j w[t, j] values[idx[t, j]]; idx, w of shape [T, ...] (bag = rest)."""
@@ -430,6 +452,7 @@ def mem_bag_forward(values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor, *,
     return y_out
 
 
+@_launches_on_stream
 def mem_bag_forward_gated(values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor,
                           gate: torch.Tensor, *, want_y=True, out=None, y_out=None, stream=None):
     """Memory+ epilogue: out = bag * silu(gate), gate [T, D] in the value dtype.
@@ -453,6 +476,7 @@ def mem_bag_forward_gated(values: torch.Tensor, idx: torch.Tensor, w: torch.Tens
     return out, y_out
 
 
+@_launches_on_stream
 def mem_gate_backward(d_out: torch.Tensor, gate: torch.Tensor, y: torch.Tensor, *, dy_out=None,
                       grad_gate=None, stream=None):
     """Backward of out = y * silu(gate): returns (dy [value dtype], grad_gate fp32)."""
@@ -472,6 +496,7 @@ def mem_gate_backward(d_out: torch.Tensor, gate: torch.Tensor, y: torch.Tensor, 
     return dy_out, grad_gate
 
 
+@_launches_on_stream
 def mem_bag_backward(dy: torch.Tensor, values: torch.Tensor, idx: torch.Tensor, w: torch.Tensor,
                      *, grad_values=None, grad_w=None, grad_scores=None, want_grad_values=True,
                      want_grad_w=True, want_grad_scores=True, mode="auto", workspace=None,
@@ -499,6 +524,7 @@ def mem_bag_backward(dy: torch.Tensor, values: torch.Tensor, idx: torch.Tensor, 
     return grad_values, grad_w, grad_scores
 
 
+@_launches_on_stream
 def mem_bag_backward_sparse(dy: torch.Tensor, values: torch.Tensor, idx: torch.Tensor,
                             w: torch.Tensor, *, want_grad_w=True, want_grad_scores=True,
                             workspace=None, stream=None):
