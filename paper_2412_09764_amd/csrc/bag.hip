@@ -250,68 +250,78 @@ __global__ __launch_bounds__(256) void k_gate_bwd(const V* __restrict__ d_out,
 
 // Atomic strategy: per lookup, grad_w = dy . V[row] and grad_values[row] +=
 // w * dy with fp32 atomic adds (no return) resolved in L2.  The dot product
-// uses dy in the 16-byte chunk layout of the value loads; the atomics use a
-// second, lane-strided copy of dy (element cl + CL*m in slot m), so each
-// atomic instruction of a lane group covers CL consecutive floats.
-template <typename V, int CPL, int CL>
+// uses dy in the quad layout of the value loads (lane cl of a CL-lane group
+// owns quads m*CL + cl); the atomics use a second, lane-strided copy of dy
+// (element cl + CL*a in slot a), so each atomic instruction of a lane group
+// covers CL consecutive floats.  A token's bag is cut into `split` contiguous
+// parts of `per` lookups, one wave each (the token's dy row is then read by
+// `split` waves, from L2), and a persistent grid strides over the T * split
+// parts: small batches still fill the chip.
+template <typename V, int NQ, int CL>
 __global__ __launch_bounds__(256) void k_bag_bwd_atomic(const V* __restrict__ dy,
                                                         const V* __restrict__ values, int D,
                                                         const int64_t* __restrict__ idx,
                                                         const float* __restrict__ w, int64_t T,
-                                                        int bag, float* __restrict__ grad_values,
+                                                        int bag, int split, int per,
+                                                        float* __restrict__ grad_values,
                                                         float* __restrict__ grad_w) {
-  using R = Row16<V>;
+  using Q = Quad<V>;
   constexpr int G = WAVE / CL;
-  constexpr int AM = CPL * R::N;  // strided elements per lane
+  constexpr int AM = NQ * 4;  // strided elements per lane
   const int lane = threadIdx.x & 63;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
-  const int C = D / R::N;
+  const int nquad = D / 4;
   const int grp = lane / CL, cl = lane % CL;
-  const V* dyt = dy + t * D;
-
-  bool ok[CPL];
-  float g[CPL][R::N];
+  bool ok[NQ];
 #pragma unroll
-  for (int i = 0; i < CPL; ++i) {
-    ok[i] = (i * CL + cl) < C;
-    const uint4 v = ok[i] ? ld16(dyt + (size_t)(i * CL + cl) * R::N) : uint4{0, 0, 0, 0};
-    R::unpack(v, g[i]);
-  }
-  float ga[AM];
+  for (int m = 0; m < NQ; ++m) ok[m] = (m * CL + cl) < nquad;
+  const int64_t units = T * split;
+  for (int64_t u = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); u < units;
+       u += (int64_t)gridDim.x * 4) {
+    const int64_t t = u / split;
+    const int j0 = (int)(u % split) * per;
+    const int j1 = j0 + per < bag ? j0 + per : bag;
+    const V* dyt = dy + t * D;
+    float g[NQ][4];
 #pragma unroll
-  for (int m = 0; m < AM; ++m) {
-    const int e = cl + CL * m;
-    ga[m] = 0.f;
-    if (e < D) {
-      if constexpr (sizeof(V) == 2) ga[m] = bf16_to_f32(dyt[e]);
-      else ga[m] = (float)dyt[e];
+    for (int m = 0; m < NQ; ++m) {
+      const typename Q::raw r = ok[m] ? Q::load(dyt + (size_t)(m * CL + cl) * 4) : Q::zero();
+      Q::unpack(r, g[m]);
     }
-  }
-  const int64_t* ti = idx + t * bag;
-  const float* tw = w + t * bag;
-  for (int j = grp; j < bag; j += G) {
-    const int64_t r = ti[j];
-    const float ww = tw[j];
-    float part = 0.f;
+    float ga[AM];
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      if (!ok[i]) continue;
-      float f[R::N];
-      R::unpack(ld16(values + r * D + (size_t)(i * CL + cl) * R::N), f);
-#pragma unroll
-      for (int e = 0; e < R::N; ++e) part = fmaf(g[i][e], f[e], part);
-    }
-    if (grad_values) {
-      float* gr = grad_values + r * D;
-#pragma unroll
-      for (int m = 0; m < AM; ++m) {
-        const int e = cl + CL * m;
-        if (e < D) unsafeAtomicAdd(gr + e, ww * ga[m]);
+    for (int a = 0; a < AM; ++a) {
+      const int e = cl + CL * a;
+      ga[a] = 0.f;
+      if (e < D) {
+        if constexpr (sizeof(V) == 2) ga[a] = bf16_to_f32(dyt[e]);
+        else ga[a] = (float)dyt[e];
       }
     }
-    part = group_sum<CL>(part);
-    if (cl == 0 && grad_w) grad_w[t * bag + j] = part;
+    const int64_t* ti = idx + t * bag;
+    const float* tw = w + t * bag;
+    for (int j = j0 + grp; j < j1; j += G) {
+      const int64_t r = ti[j];
+      const float ww = tw[j];
+      float part = 0.f;
+#pragma unroll
+      for (int m = 0; m < NQ; ++m) {
+        if (!ok[m]) continue;
+        float f[4];
+        Q::unpack(Q::load(values + r * D + (size_t)(m * CL + cl) * 4), f);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) part = fmaf(g[m][e], f[e], part);
+      }
+      if (grad_values) {
+        float* gr = grad_values + r * D;
+#pragma unroll
+        for (int a = 0; a < AM; ++a) {
+          const int e = cl + CL * a;
+          if (e < D) unsafeAtomicAdd(gr + e, ww * ga[a]);
+        }
+      }
+      part = group_sum<CL>(part);
+      if (cl == 0 && grad_w) grad_w[t * bag + j] = part;
+    }
   }
 }
 
@@ -485,22 +495,42 @@ hipError_t launch_check_indices(const int64_t* idx, int64_t count, int64_t limit
   return launch_check_indices_strided(idx, count, 1, 1, limit, bad, st);
 }
 
+constexpr int64_t ATOMIC_WAVES = 16384;  // waves the atomic backward aims for
+constexpr int64_t ATOMIC_BLOCKS = 8192;  // its persistent grid, at most
+
 hipError_t launch_bag_backward_atomic(bool bf16, const void* dy, const void* values, int D,
                                       const int64_t* idx, const float* w, int64_t T, int bag,
                                       float* grad_values, float* grad_w, hipStream_t st) {
   if (T <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((T + 3) / 4)), block(256);
-  const int C = D * (bf16 ? 2 : 4) / 16;
+  // Parts per token: enough waves to fill the chip (ATOMIC_WAVES), each part
+  // at least 4 lookups; then a persistent grid of at most ATOMIC_BLOCKS
+  // workgroups of four waves.
+  int split = 1;
+  while ((int64_t)T * split < ATOMIC_WAVES && bag / (split * 2) >= 4) split *= 2;
+  const int per = (bag + split - 1) / split;
+  int64_t blocks = (T * split + 3) / 4;
+  if (blocks > ATOMIC_BLOCKS) blocks = ATOMIC_BLOCKS;
+  const dim3 grid((unsigned)blocks), block(256);
   LaunchTimer lt("bag_backward_atomic", st);
-#define PK_BWD(CPL, CL)                                                                         \
+#define PK_BWD(NQ, CL)                                                                          \
   if (bf16)                                                                                     \
-    hipLaunchKernelGGL((k_bag_bwd_atomic<uint16_t, CPL, CL>), grid, block, 0, st,               \
-                       (const uint16_t*)dy, (const uint16_t*)values, D, idx, w, T, bag,          \
-                       grad_values, grad_w);                                                    \
+    hipLaunchKernelGGL((k_bag_bwd_atomic<uint16_t, NQ, CL>), grid, block, 0, st,                \
+                       (const uint16_t*)dy, (const uint16_t*)values, D, idx, w, T, bag, split,   \
+                       per, grad_values, grad_w);                                               \
   else                                                                                          \
-    hipLaunchKernelGGL((k_bag_bwd_atomic<float, CPL, CL>), grid, block, 0, st, (const float*)dy, \
-                       (const float*)values, D, idx, w, T, bag, grad_values, grad_w);
-  PK_ROW_DISPATCH(C, PK_BWD);
+    hipLaunchKernelGGL((k_bag_bwd_atomic<float, NQ, CL>), grid, block, 0, st, (const float*)dy,  \
+                       (const float*)values, D, idx, w, T, bag, split, per, grad_values, grad_w);
+  const int nquad = D / 4;
+  if (nquad > 512) { PK_BWD(16, 64); }
+  else if (nquad > 256) { PK_BWD(8, 64); }
+  else if (nquad > 128) { PK_BWD(4, 64); }
+  else if (nquad > 64) { PK_BWD(2, 64); }
+  else if (nquad > 32) { PK_BWD(1, 64); }
+  else if (nquad > 16) { PK_BWD(1, 32); }
+  else if (nquad > 8) { PK_BWD(1, 16); }
+  else if (nquad > 4) { PK_BWD(1, 8); }
+  else if (nquad > 2) { PK_BWD(1, 4); }
+  else { PK_BWD(1, 2); }
 #undef PK_BWD
   return hipGetLastError();
 }

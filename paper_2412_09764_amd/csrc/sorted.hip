@@ -348,43 +348,6 @@ __global__ __launch_bounds__(256) void k_seg_place(const uint32_t* __restrict__ 
 
 
 // ------------------------------------------------------- per-row backward ----
-// Quad layout: a row of D elements is D/4 quads of 4 consecutive elements; the
-// CL lanes of a group own quads q = m*CL + cl (m < NQ).  A bf16 quad is 8 bytes
-// and an fp32 quad 16 bytes, so every instruction of a group reads or writes
-// one contiguous span of the row, for the bf16 inputs and the fp32 gradient
-// alike (no partial cache lines).
-template <typename V>
-struct Quad;
-template <>
-struct Quad<uint16_t> {
-  __device__ static __forceinline__ uint2 load(const uint16_t* p) { return *reinterpret_cast<const uint2*>(p); }
-  __device__ static __forceinline__ uint2 load_nt(const uint16_t* p) {
-#if PK_STREAM_NT
-    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-    const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
-    return uint2{v.x, v.y};
-#else
-    return load(p);
-#endif
-  }
-  __device__ static __forceinline__ void unpack(const uint2& v, float (&f)[4]) {
-    f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
-  }
-  using raw = uint2;
-  __device__ static __forceinline__ raw zero() { return uint2{0, 0}; }
-};
-template <>
-struct Quad<float> {
-  __device__ static __forceinline__ uint4 load(const float* p) { return ld16(p); }
-  __device__ static __forceinline__ uint4 load_nt(const float* p) { return ld16_nt(p); }
-  __device__ static __forceinline__ void unpack(const uint4& v, float (&f)[4]) {
-    f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
-    f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
-  }
-  using raw = uint4;
-  __device__ static __forceinline__ raw zero() { return uint4{0, 0, 0, 0}; }
-};
-
 // One lane group per touched row.  A row with more than LONG_SEG lookups is
 // taken as empty here (its gradient row is written back unchanged, or as zero
 // in the sparse form) and summed afterwards by k_bag_bwd_long, in stream
