@@ -130,10 +130,13 @@ def run_cpu_baseline(wl, q, K, V, dy, budget_s: float):
     of oracle time have been spent (at least 8 tokens).  One BLAS thread."""
     import numpy as np
     import torch
-    from threadpoolctl import threadpool_limits
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     import oracle
 
+    host_cores = len(os.sched_getaffinity(0))
+    blas_default = max((i.get("num_threads", 0) for i in threadpool_info()
+                        if i.get("user_api") == "blas"), default=None)
     Kh = K.float().cpu().double().numpy()
     spent = 0.0
     done = 0
@@ -156,9 +159,64 @@ def run_cpu_baseline(wl, q, K, V, dy, budget_s: float):
             spent += time.perf_counter() - c0
             done = t1
     return {"value": done / spent, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "host_cores_available": host_cores, "blas_threads_default": blas_default,
+            "blas_threads_used": 1,
             "sample": (f"first {done} of {wl.T} tokens of {wl.name}: search + softmax + bag "
                        f"forward + bag backward (touched rows), fp64 NumPy, one BLAS thread, "
                        f"{spent:.1f} s")}
+
+
+def bwd_sweep(args):
+    """Both value-gradient strategies of Sec. 3.1.4 (lookups sorted by row, or
+    fp32 atomic adds) timed over value widths D and token counts T at H = 4,
+    k = 32 over a table of 2^20 rows, with uniformly drawn indices and
+    softmax-like weights (seeded).  Each entry is the mean of `steps` calls of
+    mem_bag_backward (dense accumulation, grad_w and grad_scores included)
+    after one warm-up call, timed with events on the launch stream."""
+    import torch
+
+    import paper_2412_09764_amd as pk
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    N, H, k = 1 << 20, 4, 32
+    g = torch.Generator(device=dev)
+    rows = []
+    for vdt, D in (("f32", 64), ("bf16", 64), ("bf16", 128), ("bf16", 256), ("bf16", 512),
+                   ("bf16", 1024), ("bf16", 2048)):
+        dt = torch.float32 if vdt == "f32" else torch.bfloat16
+        g.manual_seed(D)
+        V = (torch.randn((N, D), generator=g, device=dev) * 0.02).to(dt)
+        gv = torch.zeros((N, D), dtype=torch.float32, device=dev)
+        for T in (256, 1024, 2048, 4096, 8192, 16384):
+            idx = torch.randint(0, N, (T, H, k), generator=g, device=dev)
+            w = torch.softmax(torch.randn((T, H, k), generator=g, device=dev), dim=-1).contiguous()
+            dy = torch.randn((T, D), generator=g, device=dev).to(dt)
+            gw = torch.empty((T, H, k), dtype=torch.float32, device=dev)
+            gz = torch.empty_like(gw)
+            ent = {"dtype": vdt, "D": D, "T": T, "lookups": T * H * k}
+            for mode in ("sorted", "atomic"):
+                ws = torch.empty(max(1, pk.mem_bag_backward_workspace_size(T, H, k, N, D, mode)),
+                                 dtype=torch.uint8, device=dev)
+                run = lambda: pk.mem_bag_backward(dy, V, idx, w, grad_values=gv, grad_w=gw,  # noqa: E731
+                                                  grad_scores=gz, mode=mode, workspace=ws)
+                run()
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                for _ in range(args.steps):
+                    run()
+                b.record()
+                torch.cuda.synchronize()
+                ent[f"{mode}_ms"] = round(a.elapsed_time(b) / args.steps, 4)
+                del ws
+            ent["faster"] = "sorted" if ent["sorted_ms"] <= ent["atomic_ms"] else "atomic"
+            log(f"[sweep] {ent}")
+            rows.append(ent)
+        del V, gv
+        torch.cuda.empty_cache()
+    print(json.dumps({"bwd_sweep": rows, "rows_N": N, "heads": H, "k": k,
+                      "index_distribution": "uniform", "steps": args.steps}), flush=True)
 
 
 def main():
@@ -173,6 +231,9 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before the steps, run one plain device copy of this many MiB "
                          "(reference for scaling memory counters)")
+    ap.add_argument("--bwd-sweep", action="store_true",
+                    help="instead of the step: time both value-gradient strategies over a "
+                         "grid of value widths and token counts (uniform indices), one JSON line")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -187,6 +248,9 @@ def main():
     from paper_2412_09764_amd.inputs import WORKLOADS, gen_dy, gen_queries, gen_subkeys, gen_values
 
     pk.load()
+    if args.bwd_sweep:
+        bwd_sweep(args)
+        return
     wl = WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -238,8 +302,38 @@ def main():
     e1.record()
     torch.cuda.synchronize()
     copy_gbps = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    # two streaming references with the backward's mix of reads and writes:
+    # c = a + b over fp32 (two reads per write), and g += v with v bf16 and g
+    # fp32 in place (the value-gradient update: 2 + 4 bytes read, 4 written)
+    c = torch.empty_like(src)
+    torch.add(src, dst, out=c)
+    e0.record()
+    for _ in range(5):
+        torch.add(src, dst, out=c)
+    e1.record()
+    torch.cuda.synchronize()
+    add_gbps = 5 * 3 * src.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del c
+    vb = torch.ones(src.numel(), dtype=torch.bfloat16, device=dev)
+    dst.add_(vb)
+    e0.record()
+    for _ in range(5):
+        dst.add_(vb)
+    e1.record()
+    torch.cuda.synchronize()
+    rmw_gbps = 5 * (2 + 4 + 4) * src.numel() / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del vb
+    # the same in place over fp32 only (g += h: 4 + 4 bytes read, 4 written)
+    dst.add_(src)
+    e0.record()
+    for _ in range(5):
+        dst.add_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    rmw32_gbps = 5 * 3 * src.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
     del src, dst
-    log(f"[bench] device copy: {copy_gbps:.0f} GB/s (read + write)")
+    log(f"[bench] device copy: {copy_gbps:.0f} GB/s (read + write); a + b: {add_gbps:.0f} GB/s; "
+        f"fp32 += bf16 in place: {rmw_gbps:.0f} GB/s; fp32 += fp32 in place: {rmw32_gbps:.0f} GB/s")
     log("[bench] inputs resident; warming up")
 
     L = pk.load()
@@ -324,6 +418,34 @@ def main():
     sb = [ms for _, ms in pk.mem_timer_read()]
     search_bwd_ms = sum(sb) / len(sb)
     del gq, gK, ws_sb
+
+    # Both value-gradient strategies of Sec. 3.1.4 (sorted by row, fp32 atomic
+    # adds) on the last step's selection, each timed on its own after the
+    # steps with events on the launch stream: the evidence behind what
+    # PKMEM_BWD_AUTO picks.  (The sparse gradient has the sorted form only.)
+    strategies = None
+    if not sparse:
+        strategies = {}
+        for mname in ("sorted", "atomic"):
+            wsm = torch.empty(max(1, pk.mem_bag_backward_workspace_size(T, H, k, N, D, mname)),
+                              dtype=torch.uint8, device=dev)
+            mm = pk.BWD_MODES[mname]
+
+            def bwd_once():
+                pk._check(L.mem_bag_backward(dy.data_ptr(), V.data_ptr(), BF, N, D, idx.data_ptr(),
+                                             w.data_ptr(), T, H, k, gv.data_ptr(), gw.data_ptr(),
+                                             gz.data_ptr(), mm, wsm.data_ptr(), wsm.numel(), st))
+            bwd_once()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(args.steps):
+                bwd_once()
+            b.record()
+            torch.cuda.synchronize()
+            strategies[f"{mname}_ms"] = round(a.elapsed_time(b) / args.steps, 4)
+            del wsm
+        log(f"[bench] value-gradient strategies: {strategies}")
 
     # Memory+ gating (the gated gather and the gate backward): measured on
     # their own after the timed steps, on the last step's selection.
@@ -466,6 +588,12 @@ def main():
         search_roof = dict(search_roof, sweeps=2,
                            executed_TFLOPs=round(2 * search_roof["achieved"], 2))
 
+    scatter = bw("bag_backward_rows") or bw("bag_backward_atomic")
+    if scatter:
+        # against the in-place fp32 += bf16 stream measured above (the same mix of
+        # reads and writes as the value-gradient update)
+        scatter = dict(scatter, frac_of_stream_rmw=round(scatter["achieved"] / rmw_gbps, 4))
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
@@ -493,7 +621,8 @@ def main():
         "stages_ms": stages,
         "kernels_ms": kernel_ms,
         "gather": bw("bag_forward"),
-        "scatter": bw("bag_backward_rows") or bw("bag_backward_atomic"),
+        "scatter": scatter,
+        "bwd_strategies_ms": strategies,
         "search": search_roof,
         "search_backward_ms": round(search_bwd_ms, 4),
         "memory_plus": {
@@ -517,6 +646,9 @@ def main():
         "sink_pair": {"cartesian_ms": round(sink_ms["cartesian"], 4),
                       "search_backward_ms": round(sink_bwd_ms["search_backward"], 4)},
         "stream_copy_GBps": round(copy_gbps, 1),
+        "stream_add_GBps": round(add_gbps, 1),
+        "stream_rmw_bf16_f32_GBps": round(rmw_gbps, 1),
+        "stream_rmw_f32_GBps": round(rmw32_gbps, 1),
         "touched_rows": U,
         "max_row_multiplicity": max_mult,
     }
