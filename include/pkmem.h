@@ -109,7 +109,7 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
  * nothing (no hipMalloc, no allocating library routine).
  *   Arguments and outputs as for mem_search.
  *   Size limit: mem_search_workspace_size(T, H, S, k) <= PKMEM_NOALLOC_SCRATCH_BYTES
- *   (64 MiB: about 25,000 (token, head) rows at k = 32, e.g. T = 6,400 at
+ *   (128 MiB: about 28,000 (token, head) rows at k = 32, e.g. T = 7,000 at
  *   H = 4); larger requests return PKMEM_ERR_UNSUPPORTED before touching the
  *   device (use mem_search with a workspace).
  *   Sharing: every call on one GPU uses that GPU's one array, which keeps the
@@ -121,7 +121,7 @@ int mem_search(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype
  *   array once (hipGetSymbolAddress) with the device current; a failure there
  *   returns PKMEM_ERR_HIP.
  * ------------------------------------------------------------------------ */
-#define PKMEM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+#define PKMEM_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
 
 int mem_search_noalloc(const void* q, pkmem_dtype q_dt, const void* subkeys, pkmem_dtype k_dt,
                        int64_t T, int H, int n, int S, int k,

@@ -40,6 +40,7 @@ inline bool dtype_ok(int t) { return t == PKMEM_F32 || t == PKMEM_BF16; }
 struct SearchWs {
   uint64_t* cand;
   uint32_t* cnts;
+  float* thr;
   int32_t* half_idx;
   float* half_score;
   uint32_t* ovf;
@@ -61,6 +62,7 @@ SearchWs search_ws(void* base, int64_t T, int H, int k) {
   SearchWs w;
   w.cand = reinterpret_cast<uint64_t*>(take(rows * pk::CAND_CAP * sizeof(uint64_t)));
   w.cnts = reinterpret_cast<uint32_t*>(take(rows * 2 * sizeof(uint32_t)));
+  w.thr = reinterpret_cast<float*>(take(rows * sizeof(float)));
   w.half_idx = reinterpret_cast<int32_t*>(take(rows * k * sizeof(int32_t)));
   w.half_score = reinterpret_cast<float*>(take(rows * k * sizeof(float)));
   w.ovf = reinterpret_cast<uint32_t*>(take((rows + 1) * sizeof(uint32_t)));
@@ -388,7 +390,7 @@ static int search_common(const char* fn, const void* q, pkmem_dtype q_dt, const 
   }
   int32_t* hidx = half_idx_out ? half_idx_out : w.half_idx;
   e = pk::launch_search_half(bf16, q, subkeys, T, H, n, S, k, qstats, has_sink ? sink : nullptr,
-                             w.sink_part, w.cand, w.cnts, hidx, w.half_score, w.ovf, st);
+                             w.sink_part, w.cand, w.cnts, w.thr, hidx, w.half_score, w.ovf, st);
   if (e != hipSuccess) return hip_status(e, fn);
   if (nex > 0) {
     rc = check_indices(fn, ex_idx, T * H * nex, (int64_t)S * S, st);

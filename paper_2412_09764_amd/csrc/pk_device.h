@@ -80,6 +80,20 @@ __device__ __forceinline__ void lds_dma16(const void* gptr, void* lds_base) {
   __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
 }
 
+// The same through a buffer resource (raw buffer of `bytes` bytes at base):
+// lane i's 16 bytes from base + voff (per lane) + soff (uniform) land at
+// lds_base + 16 * i.  Unlike the global form, the compiler tracks this copy
+// as a vector-memory access only, so LDS reads of other buffers keep precise
+// (partial) wait counts while the copy is in flight.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_buffer(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ void lds_dma16_buf(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                              void* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base, 16,
+                                           (int)voff, (int)soff, 0, 0);
+}
+
 // ---------------------------------------------------------------- bf16 ----
 // silu(x) = x * sigmoid(x) = x / (1 + exp(-x)) (Memory+ gate, Sec. 3.1.4);
 // for very negative x the denominator overflows to inf and the result is -0.
@@ -156,6 +170,43 @@ struct QQuad<float> {
     a[2] = fmaf(g, qn_apply(raw.z, mean, rstd), a[2]);
     a[3] = fmaf(g, qn_apply(raw.w, mean, rstd), a[3]);
   }
+};
+
+// Quad layout: a row of D elements is D/4 quads of 4 consecutive elements; the
+// CL lanes of a group own quads q = m*CL + cl (m < NQ).  A bf16 quad is 8 bytes
+// and an fp32 quad 16 bytes, so every instruction of a group reads or writes
+// one contiguous span of the row, for the bf16 inputs and the fp32 gradient
+// alike (no partial cache lines).  Used by the value-gradient kernels.
+template <typename V>
+struct Quad;
+template <>
+struct Quad<uint16_t> {
+  __device__ static __forceinline__ uint2 load(const uint16_t* p) { return *reinterpret_cast<const uint2*>(p); }
+  __device__ static __forceinline__ uint2 load_nt(const uint16_t* p) {
+#if PK_STREAM_NT
+    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+    const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+    return uint2{v.x, v.y};
+#else
+    return load(p);
+#endif
+  }
+  __device__ static __forceinline__ void unpack(const uint2& v, float (&f)[4]) {
+    f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
+  }
+  using raw = uint2;
+  __device__ static __forceinline__ raw zero() { return uint2{0, 0}; }
+};
+template <>
+struct Quad<float> {
+  __device__ static __forceinline__ uint4 load(const float* p) { return ld16(p); }
+  __device__ static __forceinline__ uint4 load_nt(const float* p) { return ld16_nt(p); }
+  __device__ static __forceinline__ void unpack(const uint4& v, float (&f)[4]) {
+    f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+  }
+  using raw = uint4;
+  __device__ static __forceinline__ raw zero() { return uint4{0, 0, 0, 0}; }
 };
 
 // --------------------------------------------------- ordered 64-bit keys ----
@@ -239,9 +290,31 @@ __device__ __forceinline__ float group_sum(float v) {
 }
 
 // --------------------------------------------------- sorting networks ----
+// max(a, b) and min(a, b) of finite or infinite floats as med3 against an
+// infinity passed in a register: one instruction each, where fmaxf / fminf
+// also quieten both inputs first.
+__device__ __forceinline__ float max_med3(float a, float b, float pinf) {
+  return __builtin_amdgcn_fmed3f(a, b, pinf);
+}
+__device__ __forceinline__ float min_med3(float a, float b, float ninf) {
+  return __builtin_amdgcn_fmed3f(a, b, ninf);
+}
+// +inf and -inf in scalar registers, out of the compiler's sight (with a
+// literal infinity med3 would be turned back into fmaxf / fminf).
+__device__ __forceinline__ float opaque_pinf() {
+  float x;
+  asm("s_mov_b32 %0, 0x7f800000" : "=s"(x));
+  return x;
+}
+__device__ __forceinline__ float opaque_ninf() {
+  float x;
+  asm("s_mov_b32 %0, 0xff800000" : "=s"(x));
+  return x;
+}
+
 // Bitonic sort of a register array, descending (element 0 largest).
 template <int N>
-__device__ __forceinline__ void sort_desc_regs(float (&v)[N]) {
+__device__ __forceinline__ void sort_desc_regs(float (&v)[N], float pinf, float ninf) {
 #pragma unroll
   for (int size = 2; size <= N; size <<= 1) {
 #pragma unroll
@@ -252,8 +325,8 @@ __device__ __forceinline__ void sort_desc_regs(float (&v)[N]) {
         if (j > i) {
           const bool desc = (i & size) == 0;
           const float a = v[i], b = v[j];
-          v[i] = desc ? fmaxf(a, b) : fminf(a, b);
-          v[j] = desc ? fminf(a, b) : fmaxf(a, b);
+          v[i] = desc ? max_med3(a, b, pinf) : min_med3(a, b, ninf);
+          v[j] = desc ? min_med3(a, b, ninf) : max_med3(a, b, pinf);
         }
       }
     }
@@ -262,7 +335,7 @@ __device__ __forceinline__ void sort_desc_regs(float (&v)[N]) {
 
 // Bitonic merge of a register array that is already bitonic, descending.
 template <int N>
-__device__ __forceinline__ void merge_desc_regs(float (&v)[N]) {
+__device__ __forceinline__ void merge_desc_regs(float (&v)[N], float pinf, float ninf) {
 #pragma unroll
   for (int stride = N >> 1; stride > 0; stride >>= 1) {
 #pragma unroll
@@ -270,8 +343,8 @@ __device__ __forceinline__ void merge_desc_regs(float (&v)[N]) {
       const int j = i ^ stride;
       if (j > i) {
         const float a = v[i], b = v[j];
-        v[i] = fmaxf(a, b);
-        v[j] = fminf(a, b);
+        v[i] = max_med3(a, b, pinf);
+        v[j] = min_med3(a, b, ninf);
       }
     }
   }

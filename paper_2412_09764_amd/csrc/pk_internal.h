@@ -24,7 +24,7 @@ class LaunchTimer {
 
 // Candidate slots kept per (token, head, half) between the filter pass and the
 // per-row sort of the search kernel.
-constexpr int CAND_CAP = 128;
+constexpr int CAND_CAP = 256;
 // Waves and tokens per workgroup of the scoring kernel (32 tokens per wave).
 #ifndef PK_SEARCH_WAVES
 #define PK_SEARCH_WAVES 8
@@ -38,7 +38,8 @@ int cartesian_pairs(int k);
 
 // ---- search (search.hip) -------------------------------------------------
 // rows = T*H*2 (token, head, half) rows; cand = [rows, CAND_CAP] u64;
-// cnts = [rows, 2] u32 (candidates per run);
+// cnts = [rows, 2] u32 (candidates per run); thr = [rows] fp32 (each row's
+// final threshold: no score below it can be selected);
 // ovf = [1 + rows] u32 (count, then overflowed row ids).
 // qstats (nullable) = per (token, head) query (mean, rstd): the scoring then
 // normalises the queries as it loads them (see launch_qnorm).
@@ -46,7 +47,7 @@ int cartesian_pairs(int k);
 // receives each half's part of q . sink[h].
 hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T, int H,
                               int n, int S, int k, const float2* qstats, const void* sink,
-                              float* sink_part, uint64_t* cand, uint32_t* cnts,
+                              float* sink_part, uint64_t* cand, uint32_t* cnts, float* thr,
                               int32_t* half_idx, float* half_score, uint32_t* ovf,
                               hipStream_t st);
 // LayerNorm statistics of rows = T*H queries of n elements into stats, and

@@ -9,27 +9,34 @@
 //   * Scores come from v_mfma_f32_32x32x16_bf16 (fp32 inputs: 32x32x2 f32) with
 //     sub-keys as the A operand (M = 32 sub-keys) and the wave's 32 queries as
 //     the register-resident B operand (N = 32 tokens); sub-key chunks of 64 rows
-//     are staged through LDS, double buffered.  Scores never leave registers.
-//   * Pass 1 keeps, per token, the maximum of each of 64 interleaved groups of
-//     sub-keys (group = row mod 64).  The k-th largest of those 64 maxima is a
-//     threshold with at least k distinct scores at or above it.
-//   * Pass 2 recomputes the same tiles (bitwise identical) and appends every
-//     score >= threshold, as a raw 64-bit (score, index) record, to the row's
-//     candidate list (typically about 43 of 2048 at k = 32).  Its cost is
-//     instruction issue, not MFMA: a wave issues one instruction per four
-//     cycles, so the collection is one compare and a predicated store per
-//     accumulator slot, with the lane's count in a register (the two lanes
-//     holding a token's rows own half of its CAND_CAP slots each; a count
-//     past capacity keeps writing the last slot and sends the row to the
-//     rescan) - no masks, atomics or capacity branches; the two counts go to
-//     memory.  A lane holding 2k records takes only scores above the
-//     threshold from then on (lower indices win ties), so rows of tied
+//     are copied into LDS by buffer LDS-DMA, double buffered, and read as
+//     fragments a few MFMA steps ahead of their use.  Scores never leave
+//     registers.  A 32-row tile is one chain of dependent MFMAs; the
+//     filtering of the previous tile (its 16 accumulator slots per lane) is
+//     spread over that chain, so VALU and store work overlaps matrix work.
+//   * Threshold: per token, the maximum of each of 64 interleaved groups of
+//     sub-keys (group = row mod 64); the k-th largest of those maxima has at
+//     least k distinct scores at or above it, so no score below it can be
+//     selected.
+//   * Three sweeps, 1.5 passes over the sub-keys: the first half of the rows
+//     gives group maxima and a first threshold; the second half is filtered
+//     against that threshold while the maxima are completed, which gives the
+//     final threshold; the first half is then filtered against the final one
+//     (its products recomputed bitwise alike).  Every score at or above its
+//     threshold is appended, as a raw 64-bit (score, index) record, to the
+//     row's candidate list (about 66 of 2048 at k = 32); the two lanes holding
+//     a token's rows own half of its CAND_CAP slots each.  The append is one
+//     wave ballot and one exec-masked store per accumulator slot (no branch
+//     per lane); a tile where some lane could run past its slots takes a
+//     clamped path (a count past capacity sends the row to the rescan).  A
+//     lane holding k records taken against the current threshold takes only
+//     scores above it from then on (lower indices win ties), so rows of tied
 //     scores fit their slots.
 //   * Pass 3, k_topk_sort, a kernel of its own (a sort needs few registers, so
 //     it runs at far higher occupancy than the scoring kernel, which is held
-//     to two waves per SIMD): per row a wave bitonic sort of the candidates,
-//     the first k written.  A row whose lane half overflowed its CAND_CAP / 2
-//     slots (more than that many scores above the threshold) is listed for
+//     to two waves per SIMD): per row the records below the final threshold
+//     are dropped, the rest sorted by one wave, the first k written.  A row
+//     whose lane half overflowed its CAND_CAP / 2 slots is listed for
 //     k_topk_fallback, which rescans it exactly.
 //   * With query normalisation (qk-normalisation, Sec. 3.1.4) k_qnorm first
 //     computes each (token, head) query's mean and rstd = 1/sqrt(var + eps)
@@ -52,6 +59,14 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 
 constexpr int CHUNK_ROWS = 64;  // sub-keys per LDS chunk = two MFMA tiles
+
+// Lambdas of the scoring kernel are always inlined: register arrays indexed
+// by their arguments must see those arguments as constants.
+#define PK_INLINE __attribute__((always_inline))
+
+#ifndef PK_SCORE_PREFETCH
+#define PK_SCORE_PREFETCH 2  // LDS fragments read this many MFMA steps ahead (0: none)
+#endif
 
 template <typename T>
 struct MfmaOp;
@@ -176,17 +191,36 @@ __global__ __launch_bounds__(256) void k_qnorm(const T* __restrict__ q, int64_t 
   }
 }
 
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// Stores rec (8 bytes) at ptr and advances ptr by 8 bytes in the lanes of mask
+// only, without a branch: exec is narrowed to mask for the store and the
+// increment, and restored before the block ends.  A store with no lane active
+// does nothing.
+__device__ __forceinline__ void store_masked_advance(uint64_t mask, uint64_t& ptr, u32x2_t rec) {
+  uint64_t saved;
+  asm volatile(
+      "s_and_saveexec_b64 %[sv], %[m]\n\t"
+      "global_store_dwordx2 %[p], %[r], off\n\t"
+      "v_lshl_add_u64 %[p], %[p], 0, 8\n\t"
+      "s_mov_b64 exec, %[sv]"
+      : [p] "+v"(ptr), [sv] "=&s"(saved)
+      : [m] "s"(mask), [r] "v"(rec)
+      : "memory", "scc");
+}
+
 // Row of the 32x32 MFMA result held in accumulator slot j of a lane whose
 // upper-half bit is kh (columns are lane & 31).
 __device__ __forceinline__ int acc_row(int j, int kh) { return 8 * (j >> 2) + 4 * kh + (j & 3); }
 
-// KBIG (k > 32): records equal to the threshold are counted one by one (the
-// per-tile rule below needs 2k <= CAND_CAP / 2).
+// KBIG (k > 32): records equal to the threshold are counted one by one, and
+// both thresholds come from all rows (P = all chunks: no second sweep).
 template <typename T, int NSTEP, bool KBIG>
 __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
     const T* __restrict__ q, const T* __restrict__ subkeys, int64_t ntok, int H, int n, int S,
     int k, const float2* __restrict__ qstats, const T* __restrict__ sink,
-    float* __restrict__ sink_part, uint64_t* __restrict__ cand, uint32_t* __restrict__ cnts) {
+    float* __restrict__ sink_part, uint64_t* __restrict__ cand, uint32_t* __restrict__ cnts,
+    float* __restrict__ thr) {
   using M = MfmaOp<T>;
   constexpr int DPAD = NSTEP * M::KSTEP;      // padded half dim
   constexpr int RB = DPAD * M::ESIZE;         // bytes per sub-key row in LDS
@@ -260,25 +294,27 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   // chunk: computed once, so a chunk whose rows all exist costs one address
   // add per load; the last, partial chunk clamps rows as it goes.
   constexpr int NDMA = (NCOL + SEARCH_WAVES - 1) / SEARCH_WAVES;  // loads per wave, at most
-  uint32_t src_off[NDMA];  // element offset of the lane's segment in chunk 0
-#pragma unroll
-  for (int j = 0; j < NDMA; ++j) {
+  // The (head, half) table as a raw buffer: S rows of d elements.
+  const __amdgpu_buffer_rsrc_t ktab = raw_buffer(kbase, (uint32_t)((size_t)S * d * M::ESIZE));
+  // Byte offset of the lane's segment j within a chunk (recomputed at every
+  // chunk rather than held in registers).
+  auto src_off = [&](int j) PK_INLINE {
     const int i = wave + j * SEARCH_WAVES;
     const int sidx = i * WAVE + lane;
     const int r = sidx / NCOL, pc = sidx % NCOL;
     const int lc = pc ^ (r & SWZ);
     int e0 = lc * EPS;
     e0 = e0 < d ? e0 : 0;
-    src_off[j] = (uint32_t)(r * d + e0);
-  }
+    return (uint32_t)((r * d + e0) * M::ESIZE);
+  };
   const int nfull_rows = S / CHUNK_ROWS;  // chunks whose 64 rows all exist
-  auto issue_chunk = [&](int c, unsigned char* buf) {
+  auto issue_chunk = [&](int c, unsigned char* buf) PK_INLINE {
     if (c < nfull_rows) {
-      const T* cb = kbase + (size_t)c * CHUNK_ROWS * d;
+      const uint32_t cb = (uint32_t)((size_t)c * CHUNK_ROWS * d * M::ESIZE);
 #pragma unroll
       for (int j = 0; j < NDMA; ++j) {
         const int i = wave + j * SEARCH_WAVES;
-        if (NCOL % SEARCH_WAVES == 0 || i < NCOL) lds_dma16(cb + src_off[j], &buf[i * WAVE * 16]);
+        if (NCOL % SEARCH_WAVES == 0 || i < NCOL) lds_dma16_buf(ktab, src_off(j), cb, &buf[i * WAVE * 16]);
       }
       return;
     }
@@ -290,109 +326,176 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
       row = row < S ? row : S - 1;
       int e0 = lc * EPS;
       e0 = e0 < d ? e0 : 0;
-      lds_dma16(kbase + (size_t)row * d + e0, &buf[i * WAVE * 16]);
+      lds_dma16_buf(ktab, (uint32_t)(((size_t)row * d + e0) * M::ESIZE), 0u, &buf[i * WAVE * 16]);
     }
   };
-  // Both 32-row tiles of the chunk in buffer b, accumulators interleaved.
-  auto tile_pair = [&](const unsigned char* base, f32x16_t& a0, f32x16_t& a1) {
-    a0 = f32x16_t{};
-    a1 = f32x16_t{};
-#pragma unroll
-    for (int s = 0; s < NSTEP; ++s) {
-      const int e = s * M::KSTEP + kh * M::LANE_K;  // first reduction element of the fragment
-      const int seg = (e * M::ESIZE) >> 4;
-      const int within = (e * M::ESIZE) & 15;
-      const int off = ((seg ^ (col & SWZ)) << 4) + within;
-      const auto fa = M::load(base + col * RB + off);
-      const auto fb = M::load(base + (32 + col) * RB + off);
-      a0 = M::mma(fa, bq[s], a0);
-      a1 = M::mma(fb, bq[s], a1);
-    }
+  // ---- the sweeps -----------------------------------------------------------
+  // A sweep visits every 32-row tile once, in row order.  Tile t is one chain
+  // of NSTEP dependent MFMAs into its own accumulator (fragments read from
+  // LDS LEAD steps ahead of their use), and the filtering of tile t - 1 is
+  // spread over those steps, SPS accumulator slots per step: the VALU and
+  // memory work of one tile runs while the next tile's products occupy the
+  // matrix pipe.  Chunks of two tiles alternate between the two LDS buffers
+  // (unrolled by two so every access names its buffer statically).  A pass
+  // supplies
+  //   fast(c, half)          whether tile (c, half) of a full chunk may be
+  //                          filtered slot by slot (uniform),
+  //   slot(acc, c, half, j)  slot j of such a tile,
+  //   done(c, half)          after its last slot,
+  //   whole(acc, c, half)    a whole tile at once (a partial last chunk, or
+  //                          fast() false).
+  // Byte offset in LDS of the lane's fragment of step s: row col of the tile,
+  // reduction elements from s * KSTEP + kh * LANE_K, through the swizzle.
+  // It equals lane_addr ^ step_xor(s) with a lane-independent step_xor (the
+  // lane's part, col * RB, kh and the swizzle, occupies bits the step's part
+  // does not carry into), so each step costs one XOR instead of a register
+  // held per step.
+  auto frag_off = [&](int s, int kh_, int col_) PK_INLINE {
+    const int e = s * M::KSTEP + kh_ * M::LANE_K;  // first reduction element of the fragment
+    const int seg = (e * M::ESIZE) >> 4;
+    const int within = (e * M::ESIZE) & 15;
+    return ((seg ^ (col_ & SWZ)) << 4) + within;
   };
-  // One pass over all sub-keys; body(acc, c, half) sees each 32-row tile.
+  const uint32_t lane_addr = (uint32_t)(col * RB + frag_off(0, kh, col));
+  auto step_addr = [&](int s) PK_INLINE {
+    uint32_t a;
+    // volatile: formed at its use rather than hoisted into a register per step
+    asm volatile("v_xor_b32 %0, %1, %2" : "=v"(a) : "i"(frag_off(s, 0, 0)), "v"(lane_addr));
+    return a;
+  };
+  constexpr int LEAD = PK_SCORE_PREFETCH > 0 ? PK_SCORE_PREFETCH : 1;
+  constexpr int SPS = (16 + NSTEP - 1) / NSTEP;  // slots of the pending tile per MFMA step
   const int nch = (S + CHUNK_ROWS - 1) / CHUNK_ROWS;
-  auto sweep = [&](auto&& body) {
-    // Unrolled by two so each step names its buffers statically; the LDS reads
-    // of one buffer then need not wait for the loads in flight into the other.
-    issue_chunk(0, kbuf0);
-    for (int c = 0; c < nch; c += 2) {
-      __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of chunk c have landed
-      __syncthreads();                // ... and every wave's; kbuf1 is free
-      if (c + 1 < nch) issue_chunk(c + 1, kbuf1);
-      f32x16_t a0, a1;
-      tile_pair(kbuf0, a0, a1);
-      body(a0, c, 0);
-      body(a1, c, 1);
-      if (c + 1 < nch) {
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (c + 2 < nch) issue_chunk(c + 2, kbuf0);
-        tile_pair(kbuf1, a0, a1);
-        body(a0, c + 1, 0);
-        body(a1, c + 1, 1);
-      }
-    }
-    __syncthreads();
-  };
   const int nfull = S / CHUNK_ROWS;  // chunks with all 64 rows valid
 
-  // ---- pass 1: maxima of the 64 interleaved groups (group = row mod 64) ----
+  // Rows half*32 .. half*32 + 31 of the chunk in buf into acc; pend(j) runs
+  // slot j of the pending tile (or nothing).
+  auto run_tile = [&](const unsigned char* buf, int half, f32x16_t& acc, auto&& pend) PK_INLINE {
+    const unsigned char* rp = buf + half * 32 * RB;
+    acc = f32x16_t{};
+    typename M::frag ring[LEAD + 1];
+#pragma unroll
+    for (int s = 0; s < LEAD && s < NSTEP; ++s) ring[s] = M::load(rp + step_addr(s));
+#pragma unroll
+    for (int s = 0; s < NSTEP; ++s) {
+      if (s + LEAD < NSTEP) ring[(s + LEAD) % (LEAD + 1)] = M::load(rp + step_addr(s + LEAD));
+      __builtin_amdgcn_sched_barrier(0);  // reads stay LEAD steps ahead of their use
+      acc = M::mma(ring[s % (LEAD + 1)], bq[s], acc);
+#pragma unroll
+      for (int q = 0; q < SPS; ++q)
+        if (s * SPS + q < 16) pend(s * SPS + q);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // Chunks [cb, ce) in order (any range; the two LDS buffers alternate).
+  auto sweep = [&](int cb, int ce, auto&& fast, auto&& slot, auto&& done, auto&& whole) PK_INLINE {
+    if (cb >= ce) return;
+    f32x16_t acc0, acc1;  // the chunk's two tiles
+    int pc = -1;          // chunk whose second tile (in acc1) is pending
+    auto chunk = [&](const unsigned char* buf, int c) PK_INLINE {
+      if (pc >= 0 && pc < nfull && fast(pc, 1)) {
+        run_tile(buf, 0, acc0, [&](int j) PK_INLINE { slot(acc1, pc, 1, j); });
+        done(pc, 1);
+      } else {
+        run_tile(buf, 0, acc0, [&](int) PK_INLINE {});
+        if (pc >= 0) whole(acc1, pc, 1);
+      }
+      if (c < nfull && fast(c, 0)) {
+        run_tile(buf, 1, acc1, [&](int j) PK_INLINE { slot(acc0, c, 0, j); });
+        done(c, 0);
+      } else {
+        run_tile(buf, 1, acc1, [&](int) PK_INLINE {});
+        whole(acc0, c, 0);
+      }
+      pc = c;
+    };
+    issue_chunk(cb, kbuf0);
+    for (int c = cb; c < ce; c += 2) {
+      __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of chunk c have landed
+      __syncthreads();                // ... and every wave's; kbuf1 is free
+      if (c + 1 < ce) issue_chunk(c + 1, kbuf1);
+      chunk(kbuf0, c);
+      if (c + 1 < ce) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (c + 2 < ce) issue_chunk(c + 2, kbuf0);
+        chunk(kbuf1, c + 1);
+      }
+    }
+    whole(acc1, pc, 1);
+    __syncthreads();
+  };
+
+  // ---- group maxima and the threshold ---------------------------------------
+  // 64 interleaved groups per token (group = row mod 64): 32 maxima in this
+  // lane, 32 in lane ^ 32.  Maxima and minima here are med3 against an
+  // infinity in a register (max_med3 / min_med3): one instruction each.
+  const float pinf = opaque_pinf(), ninf = opaque_ninf();
   float mx[32];
 #pragma unroll
   for (int i = 0; i < 32; ++i) mx[i] = -INFINITY;
-  sweep([&](const f32x16_t& acc, int c, int half) {
-    if (c < nfull) {
+  auto max_slot = [&](const f32x16_t& acc, int half, int j) PK_INLINE {
+    mx[half * 16 + j] = max_med3(mx[half * 16 + j], acc[j], pinf);
+  };
+  auto max_whole = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) mx[half * 16 + j] = fmaxf(mx[half * 16 + j], acc[j]);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int row = c * CHUNK_ROWS + half * 32 + acc_row(j, kh);
-        mx[half * 16 + j] = fmaxf(mx[half * 16 + j], row < S ? acc[j] : -INFINITY);
-      }
+    for (int j = 0; j < 16; ++j) {
+      const int row = c * CHUNK_ROWS + half * 32 + acc_row(j, kh);
+      mx[half * 16 + j] =
+          max_med3(mx[half * 16 + j], row < S ? acc[j] : -INFINITY, pinf);
     }
-  });
-
-  // Threshold = k-th largest of this token's 64 group maxima (32 in this lane,
-  // 32 in lane ^ 32).  Sort both halves, form the bitonic half-cleaner of the
-  // 64-element sequence (mine descending, partner's reversed) and merge.
-  float th;
-  {
-    sort_desc_regs<32>(mx);
-    float part[32];
-#pragma unroll
-    for (int i = 0; i < 32; ++i) part[i] = __shfl_xor(mx[31 - i], 32, WAVE);
+  };
+  // The k-th largest of the 64 values: each is a score of a distinct row, so
+  // at least k distinct scores lie at or above it.  Both halves are sorted in
+  // place, then the bitonic half-cleaner of the 64-element sequence (mine
+  // descending, partner's reversed) is merged.  Sorting moves maxima between
+  // groups; later updates keep every value a score of a row of its own, so
+  // the bound stays valid when the sweep continues afterwards.
+  auto kth_of_maxima = [&]() PK_INLINE -> float {
+    sort_desc_regs<32>(mx, pinf, ninf);
     float sel[32];
-    if (k <= 32) {
 #pragma unroll
-      for (int i = 0; i < 32; ++i) sel[i] = fmaxf(mx[i], part[i]);
-    } else {
-#pragma unroll
-      for (int i = 0; i < 32; ++i) sel[i] = fminf(mx[i], part[i]);
+    for (int i = 0; i < 16; ++i) {  // element i pairs with the partner's 31 - i
+      const float pa = __shfl_xor(mx[31 - i], 32, WAVE), pb = __shfl_xor(mx[i], 32, WAVE);
+      sel[i] = k <= 32 ? max_med3(mx[i], pa, pinf) : min_med3(mx[i], pa, ninf);
+      sel[31 - i] = k <= 32 ? max_med3(mx[31 - i], pb, pinf) : min_med3(mx[31 - i], pb, ninf);
     }
-    merge_desc_regs<32>(sel);
+    merge_desc_regs<32>(sel, pinf, ninf);
     const int want = (k <= 32) ? k - 1 : k - 33;
-    th = sel[0];
+    float t = sel[0];
 #pragma unroll
-    for (int i = 1; i < 32; ++i) th = (i == want) ? sel[i] : th;
-  }
+    for (int i = 1; i < 32; ++i) t = (i == want) ? sel[i] : t;
+    return t;
+  };
 
-  // ---- pass 2: collect candidates >= threshold ------------------------------
-  // A lane meets its rows in increasing index order.  Once it holds 2k
-  // records it takes only scores above the threshold: of those 2k either k
-  // equal the threshold, and a later equal one has a higher index than all
-  // of them (ties go to the lower index), or k exceed it, and then no score
-  // equal to the threshold is among the k selected.  Heavily tied rows (equal
-  // sub-keys) thus stay within their slots; the test runs once per tile.
+  // ---- candidate collection ---------------------------------------------------
+  // Every score >= bound is appended to the lane's run.  A lane meets the rows
+  // of one sweep in increasing index order, tile by tile.  Once it holds k
+  // records taken against the current threshold in earlier tiles of the
+  // sweep, it takes only scores above the threshold: a later score equal to
+  // it is beaten by each of those k (by score, or on the tie by their lower
+  // index), so it cannot be selected.  Heavily tied rows (equal sub-keys) thus
+  // stay within their slots (at most k + 15 records per lane and sweep); the
+  // test runs once per tile.  Tiles of full chunks whose records cannot overrun any lane's slots
+  // take the branch-free store (one masked store per slot); the others, and
+  // k > 32 (records equal to the threshold counted one by one), the clamped
+  // path.
   constexpr int HALF_CAP = CAND_CAP / 2;
   const size_t rid = ((size_t)(tok_ok ? tok : 0) * H + h) * 2 + p;
   uint64_t* my_cand = cand + rid * CAND_CAP + kh * HALF_CAP;
   uint32_t my_cnt = 0;
-  const float thl = tok_ok ? th : INFINITY;  // scores are finite
-  const float strict = next_up(thl);
-  float bound = thl;
-  uint32_t my_eq = 0;  // KBIG: records kept equal to the threshold
-  auto keep = [&](float z, uint32_t row) {
+  float thl = INFINITY, strict = INFINITY, bound = INFINITY;
+  uint32_t my_eq = 0;   // KBIG: records kept equal to the threshold
+  uint32_t cnt0 = 0;    // my_cnt when the threshold was last set
+  uint64_t ptr = 0;     // next record of the fast path
+  auto set_threshold = [&](float t) PK_INLINE {
+    thl = tok_ok ? t : INFINITY;  // scores are finite
+    strict = next_up(thl);
+    bound = thl;
+    my_eq = 0;
+    cnt0 = my_cnt;
+  };
+  auto keep = [&](float z, uint32_t row) PK_INLINE {
     my_cand[my_cnt < (uint32_t)HALF_CAP ? my_cnt : (uint32_t)HALF_CAP - 1] =
         (uint64_t(__float_as_uint(z)) << 32) | row;
     ++my_cnt;
@@ -400,36 +503,84 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
       if (z == thl && ++my_eq == (uint32_t)k) bound = strict;
     }
   };
-  sweep([&](const f32x16_t& acc, int c, int half) {
+  auto col_fast = [&](int, int) PK_INLINE {
+    if constexpr (KBIG) return false;
+    const bool room = my_cnt <= (uint32_t)(HALF_CAP - 16);
+    if (__builtin_amdgcn_ballot_w64(!room) != 0) return false;
+    ptr = reinterpret_cast<uint64_t>(my_cand + my_cnt);
+    return true;
+  };
+  auto col_slot = [&](const f32x16_t& acc, int c, int half, int j) PK_INLINE {
+    const uint32_t row = (uint32_t)(c * CHUNK_ROWS + half * 32 + acc_row(j, kh));
+    const uint64_t m = __builtin_amdgcn_ballot_w64(acc[j] >= bound);
+    if (m) store_masked_advance(m, ptr, u32x2_t{row, __float_as_uint(acc[j])});  // uniform
+  };
+  auto col_done = [&](int, int) PK_INLINE {
+    my_cnt = (uint32_t)((ptr - reinterpret_cast<uint64_t>(my_cand)) >> 3);
+    bound = my_cnt - cnt0 >= (uint32_t)k ? strict : bound;
+  };
+  auto col_whole = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
     const uint32_t r0 = (uint32_t)(c * CHUNK_ROWS + half * 32 + 4 * kh);
-    if (c < nfull) {  // uniform
 #pragma unroll
-      for (int j = 0; j < 16; ++j)
-        if (acc[j] >= bound) keep(acc[j], r0 + 8 * (j >> 2) + (j & 3));
-    } else {
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const uint32_t row = r0 + 8 * (j >> 2) + (j & 3);
-        if (acc[j] >= bound && row < (uint32_t)S) keep(acc[j], row);
-      }
+    for (int j = 0; j < 16; ++j) {
+      const uint32_t row = r0 + 8 * (j >> 2) + (j & 3);
+      if (acc[j] >= bound && row < (uint32_t)S) keep(acc[j], row);
     }
-    if constexpr (!KBIG) bound = my_cnt >= 2u * (uint32_t)k ? strict : bound;
-  });
+    if constexpr (!KBIG) bound = my_cnt - cnt0 >= (uint32_t)k ? strict : bound;
+  };
+
+  // ---- the three sweeps ----------------------------------------------------------
+  // 1. Chunks [0, P): group maxima only; their k-th largest is a first
+  //    threshold.  2. Chunks [P, nch): candidates against that threshold,
+  //    maxima still updated; then the final threshold (the k-th largest of
+  //    the maxima over all rows).  3. Chunks [0, P) again: candidates against
+  //    the final threshold.  Every score of the top k is at or above both
+  //    thresholds, so every one is collected; the products over [0, P) are
+  //    computed twice, bitwise alike.  P = half of the chunks (1.5 sweeps in
+  //    all); with k > 32 P = all of them (sweep 2 is empty).
+  const int P = KBIG ? nch : (nch + 1) / 2;
+  auto yes = [&](int, int) PK_INLINE { return true; };
+  auto none = [&](int, int) PK_INLINE {};
+  sweep(0, P, yes, [&](const f32x16_t& acc, int, int half, int j) PK_INLINE { max_slot(acc, half, j); },
+        none, max_whole);
+  set_threshold(kth_of_maxima());
+  if (P < nch) {
+    sweep(P, nch, col_fast,
+          [&](const f32x16_t& acc, int c, int half, int j) PK_INLINE {
+            max_slot(acc, half, j);
+            col_slot(acc, c, half, j);
+          },
+          col_done,
+          [&](const f32x16_t& acc, int c, int half) PK_INLINE {
+            max_whole(acc, c, half);
+            col_whole(acc, c, half);
+          });
+    set_threshold(kth_of_maxima());
+  }
+  sweep(0, P, col_fast, col_slot, col_done, col_whole);
+  if (tok_ok && kh == 0) thr[rid] = thl;
   if (tok_ok) cnts[rid * 2 + kh] = my_cnt;
 }
 
 // Pass 3 as a kernel of its own: one wave per (token, head, half) row at a
 // time.  The row's candidates sit in two runs (c0 records at slot 0, c1 at
-// slot CAND_CAP / 2); lane l takes record l (and l + 64) of their
-// concatenation; the wave sorts them as (score desc, index asc) keys and
-// writes the first k.  A row with an overflowed run goes to the rescan list.
+// slot CAND_CAP / 2); lane l takes records l, l + 64, ... of their
+// concatenation.  Records below the row's final threshold (taken against the
+// first, looser one) cannot be selected and are dropped; when at most 64
+// remain (the usual case) they are compacted through LDS into one record per
+// lane, otherwise all are kept.  The wave then sorts them as (score desc,
+// index asc) keys and writes the first k.  A row with an overflowed run goes
+// to the rescan list.
 __global__ __launch_bounds__(256) void k_topk_sort(const uint64_t* __restrict__ cand,
                                                    const uint32_t* __restrict__ cnts,
+                                                   const float* __restrict__ thr,
                                                    int64_t rows, int k,
                                                    int32_t* __restrict__ half_idx,
                                                    float* __restrict__ half_score,
                                                    uint32_t* __restrict__ ovf) {
   constexpr uint32_t HALF_CAP = CAND_CAP / 2;
+  constexpr int E = CAND_CAP / WAVE;
+  __shared__ uint64_t stage[4][WAVE];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   auto to_key = [](uint64_t raw) { return make_key(__uint_as_float(uint32_t(raw >> 32)), uint32_t(raw)); };
   for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < rows; r += (int64_t)gridDim.x * 4) {
@@ -443,26 +594,42 @@ __global__ __launch_bounds__(256) void k_topk_sort(const uint64_t* __restrict__ 
     }
     const uint64_t* rc = cand + (size_t)r * CAND_CAP;
     const uint32_t c = c0 + c1;
-    uint64_t raw[2] = {0ull, 0ull};
+    const float tr = thr[r];
+    uint64_t key[E];
+    bool keep[E];
+    uint32_t n = 0;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
+    for (int e = 0; e < E; ++e) {
       const uint32_t x = (uint32_t)(lane + e * WAVE);
-      if (x < c0) raw[e] = rc[x];
-      else if (x - c0 < c1) raw[e] = rc[HALF_CAP + x - c0];
+      uint64_t raw = 0;
+      if (x < c0) raw = rc[x];
+      else if (x - c0 < c1) raw = rc[HALF_CAP + x - c0];
+      const bool valid = x < c;
+      key[e] = valid ? to_key(raw) : 0ull;
+      keep[e] = valid && __uint_as_float(uint32_t(raw >> 32)) >= tr;
+      n += (uint32_t)__popcll(__ballot(keep[e]));
     }
-    uint64_t key;
-    if (c <= (uint32_t)WAVE) {
-      uint64_t v[1] = {(uint32_t)lane < c ? to_key(raw[0]) : 0ull};
+    uint64_t top;
+    if (n <= (uint32_t)WAVE) {
+      uint32_t base = 0;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const uint64_t m = __ballot(keep[e]);
+        const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        if (keep[e]) stage[wave][base + below] = key[e];
+        base += (uint32_t)__popcll(m);
+      }
+      uint64_t v[1] = {(uint32_t)lane < n ? stage[wave][lane] : 0ull};
       wave_sort_desc<1>(v, lane);
-      key = v[0];
+      top = v[0];
     } else {
-      uint64_t v[2] = {to_key(raw[0]), (uint32_t)lane + WAVE < c ? to_key(raw[1]) : 0ull};
-      wave_sort_desc<2>(v, lane);
-      key = v[0];
+      wave_sort_desc<E>(key, lane);
+      top = key[0];
     }
     if (lane < k) {
-      half_idx[r * k + lane] = (int32_t)key_index(key);
-      half_score[r * k + lane] = key_score(key);
+      half_idx[r * k + lane] = (int32_t)key_index(top);
+      half_score[r * k + lane] = key_score(top);
     }
   }
 }
@@ -693,7 +860,7 @@ int cartesian_pairs(int k) {
 template <typename T, int NSTEP>
 static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, int H, int n, int S,
                                int k, const float2* qstats, const void* sink, float* sink_part,
-                               uint64_t* cand, uint32_t* cnts,
+                               uint64_t* cand, uint32_t* cnts, float* thr,
                                int32_t* half_idx, float* half_score, uint32_t* ovf,
                                hipStream_t st) {
   const int64_t tiles = (T_ + SEARCH_TOK - 1) / SEARCH_TOK;
@@ -703,11 +870,11 @@ static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, i
     if (k > 32)
       hipLaunchKernelGGL((k_score_topk<T, NSTEP, true>), dim3((unsigned)blocks), dim3(64 * SEARCH_WAVES),
                          0, st, (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats,
-                         (const T*)sink, sink_part, cand, cnts);
+                         (const T*)sink, sink_part, cand, cnts, thr);
     else
       hipLaunchKernelGGL((k_score_topk<T, NSTEP, false>), dim3((unsigned)blocks), dim3(64 * SEARCH_WAVES),
                          0, st, (const T*)q, (const T*)subkeys, T_, H, n, S, k, qstats,
-                         (const T*)sink, sink_part, cand, cnts);
+                         (const T*)sink, sink_part, cand, cnts, thr);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -717,7 +884,7 @@ static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, i
     if (sb > 16384) sb = 16384;
     LaunchTimer lt("topk_sort", st);
     hipLaunchKernelGGL(k_topk_sort, dim3((unsigned)sb), dim3(256), 0, st, (const uint64_t*)cand,
-                       (const uint32_t*)cnts, rows, k, half_idx, half_score, ovf);
+                       (const uint32_t*)cnts, (const float*)thr, rows, k, half_idx, half_score, ovf);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -743,26 +910,26 @@ hipError_t launch_qnorm(bool bf16, const void* q, int64_t rows, int n, float eps
 
 hipError_t launch_search_half(bool bf16, const void* q, const void* subkeys, int64_t T_, int H,
                               int n, int S, int k, const float2* qstats, const void* sink,
-                              float* sink_part, uint64_t* cand,
-                              uint32_t* cnts, int32_t* half_idx, float* half_score, uint32_t* ovf,
+                              float* sink_part, uint64_t* cand, uint32_t* cnts, float* thr,
+                              int32_t* half_idx, float* half_score, uint32_t* ovf,
                               hipStream_t st) {
   hipError_t e = launch_fill_u32(ovf, 0u, 1, st);
   if (e != hipSuccess) return e;
   const int d = n / 2;
   if (bf16) {
     const int steps = (d + 15) / 16;
-    if (steps <= 1) return launch_score<uint16_t, 1>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
-    if (steps <= 2) return launch_score<uint16_t, 2>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
-    if (steps <= 4) return launch_score<uint16_t, 4>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
-    if (steps <= 8) return launch_score<uint16_t, 8>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
-    return launch_score<uint16_t, 16>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+    if (steps <= 1) return launch_score<uint16_t, 1>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
+    if (steps <= 2) return launch_score<uint16_t, 2>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
+    if (steps <= 4) return launch_score<uint16_t, 4>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
+    if (steps <= 8) return launch_score<uint16_t, 8>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
+    return launch_score<uint16_t, 16>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
   }
   const int steps = (d + 1) / 2;
-  if (steps <= 2) return launch_score<float, 2>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
-  if (steps <= 4) return launch_score<float, 4>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
-  if (steps <= 8) return launch_score<float, 8>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
-  if (steps <= 16) return launch_score<float, 16>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
-  return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, half_idx, half_score, ovf, st);
+  if (steps <= 2) return launch_score<float, 2>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
+  if (steps <= 4) return launch_score<float, 4>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
+  if (steps <= 8) return launch_score<float, 8>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
+  if (steps <= 16) return launch_score<float, 16>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
+  return launch_score<float, 32>(q, subkeys, T_, H, n, S, k, qstats, sink, sink_part, cand, cnts, thr, half_idx, half_score, ovf, st);
 }
 
 template <int E>

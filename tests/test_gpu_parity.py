@@ -360,3 +360,52 @@ def test_search_repeated_subkeys_integer_large_k(gpu_lib):
     np.testing.assert_array_equal(hidx.cpu().numpy(), ref["half_idx"])
     np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
     np.testing.assert_array_equal(h64(score), ref["score"])
+
+
+def _search_overflow_count(q, K, k):
+    """mem_search with a caller workspace; returns (idx, half_idx, number of
+    rows sent to the exact rescan).  The count is the first word of the
+    overflow list, whose offset mirrors the workspace layout of csrc/abi.hip
+    (candidate slots, run counts, thresholds, half lists, overflow list, each
+    256-byte aligned; 256 candidate slots per (token, head, half) row)."""
+    import paper_2412_09764_amd as pk
+    T, H, n = q.shape
+    S = K.shape[2]
+    rows = T * H * 2
+    a = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    off = a(rows * 256 * 8) + a(rows * 2 * 4) + a(rows * 4) + 2 * a(rows * k * 4)
+    ws = torch.zeros(pk.mem_search_workspace_size(T, H, S, k), dtype=torch.uint8, device="cuda")
+    idx, w, score, hidx = pk.mem_search(q, K, k, want_half=True, workspace=ws)
+    torch.cuda.synchronize()
+    nov = int(ws[off:off + 4].view(torch.int32).item())
+    return idx, hidx, nov
+
+
+@pytest.mark.parametrize("k", [25, 32])
+def test_search_ties_but_one_needs_no_rescan(gpu_lib, k):
+    """Every sub-key equal except one lower row: every score of a row ties but
+    one.  The k lowest indices other than that row are selected, and no row
+    goes to the exact rescan (a lane keeps at most k + 15 records per sweep
+    once it holds k at the threshold)."""
+    T, H, S, n = 512, 2, 2048, 64
+    low = 5
+    q = normal_tensor((T, H, n), 155, torch.float32).abs().to(torch.bfloat16).cuda()
+    K = torch.full((H, 2, S, n // 2), 0.0625, dtype=torch.bfloat16, device="cuda")
+    K[:, :, low, :] = 0.03125
+    idx, hidx, nov = _search_overflow_count(q, K, k)
+    assert nov == 0, f"{nov} rows went to the rescan"
+    want = np.array([i for i in range(k + 1) if i != low][:k])
+    np.testing.assert_array_equal(hidx.cpu().numpy(), np.broadcast_to(want, (T, H, 2, k)))
+    comp = np.sort((want[:, None] * S + want[None, :]).ravel(), kind="stable")[:k]
+    np.testing.assert_array_equal(idx.cpu().numpy(), np.broadcast_to(comp, (T, H, k)))
+
+
+def test_search_gaussian_rows_need_no_rescan(gpu_lib):
+    """The 4M-key workload's Gaussian queries (first 4096 tokens) fit their
+    candidate slots: no row goes to the rescan."""
+    wl = WORKLOADS["pk4m_d2048"]
+    from paper_2412_09764_amd.inputs import gen_queries, gen_subkeys
+    q = gen_queries(wl, "cuda", T=4096)
+    K = gen_subkeys(wl, "cuda")
+    _, _, nov = _search_overflow_count(q, K, wl.k)
+    assert nov == 0, f"{nov} rows went to the rescan"

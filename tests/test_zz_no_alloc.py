@@ -53,7 +53,7 @@ def test_noalloc_matches_workspace_search_twice(gpu_lib):
     dev = torch.device("cuda:0")
     wl = WORKLOADS["pk1m_d1024"]  # S = 1024, H = 4, n = 512, k = 32, bf16
     K = gen_subkeys(wl, dev)
-    # first call: 4096 tokens (about 42 MB of the 64 MiB scratch), Gaussian queries
+    # first call: 4096 tokens (about 76 MB of the 128 MiB scratch), Gaussian queries
     T1 = 4096
     assert pk.mem_search_workspace_size(T1, wl.H, wl.S, wl.k) <= pk.NOALLOC_SCRATCH_BYTES
     q1 = gen_queries(wl, dev, T=T1)
