@@ -110,21 +110,29 @@ int check_bag_shapes(const char* fn, pkmem_dtype v_dt, int64_t N, int D, int64_t
   return PKMEM_OK;
 }
 
-size_t bwd_ws_bytes(int64_t T, int H, int k, int mode) {
+// grad_w when the caller passes none; for the sorted strategy the sort, then
+// the partial rows of long rows' chunks.
+size_t bwd_ws_bytes(int64_t T, int H, int k, int D, int mode) {
   const int64_t L = T * H * k;
-  size_t b = align256((size_t)L * sizeof(float));  // grad_w when the caller passes none
-  if (mode == PKMEM_BWD_SORTED) b += pk::sorted_workspace_bytes(L);
+  size_t b = align256((size_t)L * sizeof(float));
+  if (mode == PKMEM_BWD_SORTED) b += pk::sorted_workspace_bytes(L) + pk::long_partial_bytes(L, D);
   return b;
 }
 
-// PKMEM_BWD_MODE=atomic|sorted in the environment overrides the library's
-// choice for PKMEM_BWD_AUTO (read at every call).
-int resolve_mode(int mode, int D) {
+// What PKMEM_BWD_AUTO means for L = T*H*k lookups of rows of D elements:
+// atomic adds when L*D <= 2^26 fp32 updates and D <= 1024, the sorted
+// strategy otherwise.  Measured on MI355X (uniform indices over 2^20 rows,
+// D = 64..2048, L = 32K..2M): the atomic kernel costs about 3.5 ps per
+// updated element plus one launch, the sort a fixed ~0.1 ms (eleven
+// launches) plus its row streaming, so atomics win only small batches; at
+// D = 2048 the sort wins from 256 tokens on.  PKMEM_BWD_MODE=atomic|sorted in
+// the environment overrides the choice (read at every call).
+int resolve_mode(int mode, int D, int64_t L) {
   if (mode != PKMEM_BWD_AUTO) return mode;
   const char* env = getenv("PKMEM_BWD_MODE");
   if (env && strcmp(env, "atomic") == 0) return PKMEM_BWD_ATOMIC;
   if (env && strcmp(env, "sorted") == 0) return PKMEM_BWD_SORTED;
-  return D > 128 ? PKMEM_BWD_SORTED : PKMEM_BWD_ATOMIC;
+  return (D <= 1024 && L * (int64_t)D <= (int64_t(1) << 26)) ? PKMEM_BWD_ATOMIC : PKMEM_BWD_SORTED;
 }
 
 // PKMEM_DEBUG=1 in the environment (read at every call) checks on the device
@@ -194,7 +202,7 @@ int bag_backward_common(const char* fn, const void* dy, const void* values, pkme
   if (mode != PKMEM_BWD_AUTO && mode != PKMEM_BWD_ATOMIC && mode != PKMEM_BWD_SORTED)
     return fail(PKMEM_ERR_INVALID, "%s: unknown mode %d", fn, mode);
   const bool sparse = rows_out != nullptr || num_rows_out != nullptr;
-  const int m = sparse ? PKMEM_BWD_SORTED : resolve_mode(mode, D);
+  const int m = sparse ? PKMEM_BWD_SORTED : resolve_mode(mode, D, T * H * (int64_t)k);
   if (T > 0 && (!dy || !values || !idx || !w))
     return fail(PKMEM_ERR_INVALID, "%s: null input pointer", fn);
   if (!aligned(dy, 16) || !aligned(values, 16))
@@ -210,7 +218,7 @@ int bag_backward_common(const char* fn, const void* dy, const void* values, pkme
     if (cap < need)
       return fail(PKMEM_ERR_INVALID, "%s: cap %lld < min(T*H*k, N) = %lld", fn, (long long)cap, (long long)need);
   }
-  const size_t need_ws = bwd_ws_bytes(T, H, k, m);
+  const size_t need_ws = bwd_ws_bytes(T, H, k, D, m);
   if (!ws || ws_bytes < need_ws)
     return fail(PKMEM_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need_ws, ws ? ws_bytes : (size_t)0);
   if (!aligned(ws, 256)) return fail(PKMEM_ERR_INVALID, "%s: workspace must be 256-byte aligned", fn);
@@ -229,9 +237,10 @@ int bag_backward_common(const char* fn, const void* dy, const void* values, pkme
     if (e != hipSuccess) return hip_status(e, fn);
   } else {
     uint32_t* nrows_dev = nullptr;
+    float* part = reinterpret_cast<float*>(p + pk::sorted_workspace_bytes(L));
     e = pk::launch_bag_backward_sorted(bf16, dy, values, N, D, idx, w, T, H * k,
                                        sparse ? nullptr : grad_values, sparse ? rows_out : nullptr,
-                                       grad_rows_out, gw, p, &nrows_dev, st);
+                                       grad_rows_out, gw, p, part, &nrows_dev, st);
     if (e != hipSuccess) return hip_status(e, fn);
     if (sparse) {
       uint32_t U = 0;
@@ -646,7 +655,7 @@ int mem_gate_backward(const void* d_out, const void* gate, const void* y, pkmem_
 size_t mem_bag_backward_workspace_size(int64_t T, int H, int k, int64_t N, int D, int mode) {
   (void)N;
   if (T < 0 || H < 1 || k < 1) return 0;
-  return bwd_ws_bytes(T, H, k, resolve_mode(mode, D));
+  return bwd_ws_bytes(T, H, k, D, resolve_mode(mode, D, T * H * (int64_t)k));
 }
 
 int mem_bag_backward(const void* dy, const void* values, pkmem_dtype v_dt, int64_t N, int D,

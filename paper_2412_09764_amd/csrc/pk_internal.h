@@ -110,13 +110,15 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream
 
 // ---- sorted backward (sorted.hip) ------------------------------------------
 size_t sorted_workspace_bytes(int64_t L);
+// Partial rows of the chunks of rows with many lookups (see sorted.hip).
+size_t long_partial_bytes(int64_t L, int D);
 // Sorts the L lookups by row (stable), finds the touched rows, and per row
 // computes grad_w of its lookups and the row's gradient sum.  Dense mode adds
 // the sum into grad_values[row]; sparse mode writes rows_out / grad_rows_out.
 hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* values, int64_t N,
                                       int D, const int64_t* idx, const float* w, int64_t T,
                                       int bag, float* grad_values, int64_t* rows_out,
-                                      float* grad_rows_out, float* grad_w, void* ws,
+                                      float* grad_rows_out, float* grad_w, void* ws, float* part,
                                       uint32_t** num_rows_dev, hipStream_t st);
 
 }  // namespace pk

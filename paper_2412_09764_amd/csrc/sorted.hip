@@ -33,7 +33,8 @@ constexpr int SORT_ITEMS = 16;                 // keys per thread per tile
 constexpr int SORT_TILE = 256 * SORT_ITEMS;    // keys per workgroup tile
 constexpr int SCAN_ITEMS = 8;
 constexpr uint32_t LONG_SEG = 1024;  // lookups of a row beyond which it is split
-constexpr int LONG_WAVES = 8;        // waves of the workgroup that takes a long row
+constexpr uint32_t LONG_CHUNK = 1024;  // lookups of a long row per workgroup
+constexpr int LONG_WAVES = 8;        // waves of the workgroup that takes a chunk
 constexpr int SCAN_TILE = 256 * SCAN_ITEMS;
 
 static inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -505,7 +506,8 @@ __global__ __launch_bounds__(256) void k_bag_bwd_rows(
 
 // -------------------------------------------------------------- launcher ----
 struct SortedWs {
-  uint32_t *keys_a, *vals_a, *keys_b, *vals_b, *hist, *sums, *seg, *misc, *long_list, *totals;
+  uint32_t *keys_a, *vals_a, *keys_b, *vals_b, *hist, *sums, *seg, *misc, *long_list, *totals,
+      *long_base;
 };
 static int64_t max_long(int64_t L) { return L / LONG_SEG + 1; }
 
@@ -526,6 +528,7 @@ static SortedWs carve(void* ws, int64_t L) {
   w.misc = take(256);  // [0] segments, [1] long rows listed
   w.long_list = take(4 * (size_t)max_long(L));
   w.totals = take(4 * (size_t)RADIX);  // a radix pass's count per digit
+  w.long_base = take(4 * (size_t)(max_long(L) + 1));  // first chunk of each listed long row
   return w;
 }
 
@@ -535,7 +538,14 @@ size_t sorted_workspace_bytes(int64_t L) {
   const int64_t scan_n = (hist_n > L + 1 ? hist_n : L + 1);
   return 4 * align256(4 * (size_t)L) + align256(4 * (size_t)scan_n) +
          align256(4 * (size_t)(cdiv(scan_n, SCAN_TILE) + 1)) + align256(4 * (size_t)(L + 1)) + 256 +
-         align256(4 * (size_t)max_long(L)) + align256(4 * (size_t)RADIX);
+         align256(4 * (size_t)max_long(L)) + align256(4 * (size_t)RADIX) +
+         align256(4 * (size_t)(max_long(L) + 1));
+}
+
+// Partial rows of the long-row chunks: at most L / LONG_CHUNK + max_long(L)
+// chunks of D fp32 each.
+size_t long_partial_bytes(int64_t L, int D) {
+  return align256((size_t)(L / LONG_CHUNK + max_long(L)) * (size_t)D * sizeof(float));
 }
 
 // Stable LSD radix sort of L keys (< 2^key_bits, from an int64 or a u32 array)
@@ -633,44 +643,84 @@ hipError_t launch_list_long(const uint32_t* seg_start, const uint32_t* nseg, int
   return hipGetLastError();
 }
 
-// Rows listed by k_list_long (more than LONG_SEG lookups), one workgroup
-// per row at a time: its ng lane groups (ng = LONG_WAVES * WAVE / CL, fewer
-// when the partial rows would not fit 64 KiB of LDS) take contiguous runs of
-// the row's lookups in lookup order, each writing grad_w and summing w * dy
-// into a partial row; the partials go to LDS and are added, in group order,
-// to the old gradient row (dense) or written as the row's gradient (sparse).
-template <typename V, int NQ, int CL, bool SPARSE>
+// Rows listed by k_list_long (more than LONG_SEG lookups) are cut into chunks
+// of LONG_CHUNK consecutive lookups (in lookup order), and every chunk of
+// every listed row is summed by a workgroup of its own, so a row chosen by a
+// large share of the tokens is spread over many CUs:
+//   k_long_bases    (one workgroup) the first chunk number of each listed row
+//                   (an exclusive scan of the chunk counts, in list order),
+//   k_bag_bwd_long  (persistent grid over the chunks) the chunk's lane groups
+//                   take contiguous runs of its lookups, write their grad_w and
+//                   sum w * dy into partial rows in LDS, added in group order
+//                   into the chunk's partial row in the workspace,
+//   k_long_reduce   (one workgroup per listed row) adds the row's partial rows
+//                   in chunk order to the old gradient row (dense) or writes
+//                   their sum as the row's gradient (sparse).
+// The list's order varies from run to run, but a row's value depends only on
+// its own chunks, summed in chunk order: bitwise deterministic.
+__global__ __launch_bounds__(256) void k_long_bases(const uint32_t* __restrict__ seg_start,
+                                                    const uint32_t* __restrict__ long_list,
+                                                    const uint32_t* __restrict__ long_cnt,
+                                                    uint32_t* __restrict__ long_base) {
+  __shared__ uint32_t wsum[4];
+  const uint32_t nlong = *long_cnt;
+  uint32_t carry = 0;
+  for (uint32_t i0 = 0; i0 < nlong; i0 += 256) {
+    const uint32_t i = i0 + threadIdx.x;
+    uint32_t nch = 0;
+    if (i < nlong) {
+      const uint32_t u = long_list[i];
+      nch = (seg_start[u + 1] - seg_start[u] + LONG_CHUNK - 1) / LONG_CHUNK;
+    }
+    uint32_t total;
+    const uint32_t before = block_exclusive_scan(nch, wsum, total);
+    if (i < nlong) long_base[i] = carry + before;
+    carry += total;
+  }
+  if (threadIdx.x == 0) long_base[nlong] = carry;
+}
+
+template <typename V, int NQ, int CL>
 __global__ __launch_bounds__(64 * LONG_WAVES) void k_bag_bwd_long(
     const V* __restrict__ dy, const V* __restrict__ values, int D, const float* __restrict__ w,
     int bag, const uint32_t* __restrict__ rows_sorted, const uint32_t* __restrict__ lookups,
     const uint32_t* __restrict__ seg_start, const uint32_t* __restrict__ long_list,
-    const uint32_t* __restrict__ long_cnt, float* __restrict__ grad_values,
-    int64_t* __restrict__ rows_out, float* __restrict__ grad_rows_out,
-    float* __restrict__ grad_w) {
+    const uint32_t* __restrict__ long_cnt, const uint32_t* __restrict__ long_base,
+    float* __restrict__ part, float* __restrict__ grad_w) {
   using Q = Quad<V>;
   constexpr int G = WAVE / CL;
   constexpr int PB = RowsBatch<NQ, CL>::value;
-  extern __shared__ float part[];  // [ng][D]
+  extern __shared__ float lpart[];  // [ng][D]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = wave * G + lane / CL, cl = lane % CL;
   const int nquad = D / 4;
   int ng = LONG_WAVES * G;
   if (ng > 16384 / D) ng = 16384 / D;  // 64 KiB of partial rows
   const bool mine = grp < ng;
-  const bool dense = !SPARSE && grad_values != nullptr;
   bool ok[NQ];
 #pragma unroll
   for (int m = 0; m < NQ; ++m) ok[m] = mine && (m * CL + cl) < nquad;
   const uint32_t nlong = *long_cnt;
-  for (uint32_t it = blockIdx.x; it < nlong; it += gridDim.x) {
-    const uint32_t u = long_list[it];
-    const uint32_t s0 = seg_start[u], s1 = seg_start[u + 1];
-    const int64_t row = (int64_t)rows_sorted[s0];
-    const uint32_t len = s1 - s0;
+  const uint32_t nchunk = long_base[nlong];
+  for (uint32_t g = blockIdx.x; g < nchunk; g += gridDim.x) {
+    // the listed row holding chunk g: long_base is ascending
+    uint32_t lo = 0, hi = nlong;  // long_base[lo] <= g < long_base[hi]
+    while (hi - lo > 1) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (long_base[mid] <= g) lo = mid;
+      else hi = mid;
+    }
+    const uint32_t u = long_list[lo];
+    const uint32_t c = g - long_base[lo];
+    const uint32_t s_end = seg_start[u + 1];
+    const uint32_t c0 = seg_start[u] + c * LONG_CHUNK;
+    const uint32_t c1 = c0 + LONG_CHUNK < s_end ? c0 + LONG_CHUNK : s_end;
+    const int64_t row = (int64_t)rows_sorted[c0];
+    const uint32_t len = c1 - c0;
     const uint32_t per = (len + (uint32_t)ng - 1) / (uint32_t)ng;
     uint32_t a = mine ? (uint32_t)grp * per : len, z = mine ? (uint32_t)(grp + 1) * per : len;
-    a = (a < len ? a : len) + s0;
-    z = (z < len ? z : len) + s0;
+    a = (a < len ? a : len) + c0;
+    z = (z < len ? z : len) + c0;
     typename Q::raw vraw[NQ];
     float acc[NQ][4];
 #pragma unroll
@@ -700,13 +750,13 @@ __global__ __launch_bounds__(64 * LONG_WAVES) void k_bag_bwd_long(
         part_w[pp] = 0.f;
 #pragma unroll
         for (int m = 0; m < NQ; ++m) {
-          float g[4], v[4];
-          Q::unpack(graw[pp][m], g);
+          float gg[4], v[4];
+          Q::unpack(graw[pp][m], gg);
           Q::unpack(vraw[m], v);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            acc[m][e] = fmaf(ww, g[e], acc[m][e]);
-            part_w[pp] = fmaf(g[e], v[e], part_w[pp]);
+            acc[m][e] = fmaf(ww, gg[e], acc[m][e]);
+            part_w[pp] = fmaf(gg[e], v[e], part_w[pp]);
           }
         }
       }
@@ -720,29 +770,57 @@ __global__ __launch_bounds__(64 * LONG_WAVES) void k_bag_bwd_long(
 #pragma unroll
     for (int m = 0; m < NQ; ++m)
       if (ok[m]) {
-        float* d = part + (size_t)grp * D + (size_t)(m * CL + cl) * 4;
+        float* d = lpart + (size_t)grp * D + (size_t)(m * CL + cl) * 4;
         d[0] = acc[m][0]; d[1] = acc[m][1]; d[2] = acc[m][2]; d[3] = acc[m][3];
       }
     __syncthreads();
     for (int qd = threadIdx.x; qd < nquad; qd += blockDim.x) {
       float4 tot = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (dense) tot = *reinterpret_cast<const float4*>(grad_values + row * D + (size_t)qd * 4);
       for (int gi = 0; gi < ng; ++gi) {
-        const float* sp = part + (size_t)gi * D + (size_t)qd * 4;
+        const float* sp = lpart + (size_t)gi * D + (size_t)qd * 4;
         tot.x += sp[0]; tot.y += sp[1]; tot.z += sp[2]; tot.w += sp[3];
+      }
+      *reinterpret_cast<float4*>(part + (size_t)g * D + (size_t)qd * 4) = tot;
+    }
+    __syncthreads();  // the LDS partial rows are reused for the next chunk
+  }
+}
+
+template <bool SPARSE>
+__global__ __launch_bounds__(256) void k_long_reduce(int D, const uint32_t* __restrict__ rows_sorted,
+                                                     const uint32_t* __restrict__ seg_start,
+                                                     const uint32_t* __restrict__ long_list,
+                                                     const uint32_t* __restrict__ long_cnt,
+                                                     const uint32_t* __restrict__ long_base,
+                                                     const float* __restrict__ part,
+                                                     float* __restrict__ grad_values,
+                                                     int64_t* __restrict__ rows_out,
+                                                     float* __restrict__ grad_rows_out) {
+  const uint32_t nlong = *long_cnt;
+  const int nquad = D / 4;
+  const bool dense = !SPARSE && grad_values != nullptr;
+  for (uint32_t i = blockIdx.x; i < nlong; i += gridDim.x) {
+    const uint32_t u = long_list[i];
+    const int64_t row = (int64_t)rows_sorted[seg_start[u]];
+    const uint32_t b0 = long_base[i], b1 = long_base[i + 1];
+    for (int qd = threadIdx.x; qd < nquad; qd += blockDim.x) {
+      float4 tot = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (dense) tot = *reinterpret_cast<const float4*>(grad_values + row * D + (size_t)qd * 4);
+      for (uint32_t g = b0; g < b1; ++g) {
+        const float4 pv = *reinterpret_cast<const float4*>(part + (size_t)g * D + (size_t)qd * 4);
+        tot.x += pv.x; tot.y += pv.y; tot.z += pv.z; tot.w += pv.w;
       }
       float* dst = SPARSE ? grad_rows_out + (size_t)u * D : grad_values + row * D;
       if (SPARSE || dense) *reinterpret_cast<float4*>(dst + (size_t)qd * 4) = tot;
     }
     if (SPARSE && threadIdx.x == 0) rows_out[u] = row;
-    __syncthreads();  // the partial rows are reused for the next listed row
   }
 }
 
 hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* values, int64_t N,
                                       int D, const int64_t* idx, const float* w, int64_t T,
                                       int bag, float* grad_values, int64_t* rows_out,
-                                      float* grad_rows_out, float* grad_w, void* ws,
+                                      float* grad_rows_out, float* grad_w, void* ws, float* part,
                                       uint32_t** num_rows_dev, hipStream_t st) {
   const int64_t L = T * bag;
   SortedWs b = carve(ws, L);
@@ -767,11 +845,15 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
   if (blocks > 16384) blocks = 16384;
   const dim3 grid((unsigned)blocks), block(256);
   const bool sparse = rows_out != nullptr;
-  int64_t lblocks = max_long(L);
-  if (lblocks > 512) lblocks = 512;
+  int64_t lblocks = L / LONG_CHUNK + max_long(L);  // chunks of long rows, at most
+  if (lblocks > 1024) lblocks = 1024;
+  int64_t rblocks = max_long(L);
+  if (rblocks > 512) rblocks = 512;
   const int ngrp_cap = 16384 / D;  // partial rows that fit 64 KiB
   e = launch_list_long(b.seg, b.misc, L, (uint32_t)LONG_SEG, b.long_list, b.misc + 1, st);
   if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_long_bases, dim3(1), dim3(256), 0, st, (const uint32_t*)b.seg,
+                     (const uint32_t*)b.long_list, (const uint32_t*)(b.misc + 1), b.long_base);
   LaunchTimer lt("bag_backward_rows", st);
 #define PK_ROWS_ONE(VT, NQ, CL, SP)                                                                \
   {                                                                                                \
@@ -779,10 +861,13 @@ hipError_t launch_bag_backward_sorted(bool bf16, const void* dy, const void* val
                        (const VT*)dy, (const VT*)values, D, w, bag, ks, vs, b.seg, b.misc,         \
                        grad_values, rows_out, grad_rows_out, grad_w);                             \
     const int ng = (LONG_WAVES * (WAVE / CL)) < ngrp_cap ? LONG_WAVES * (WAVE / CL) : ngrp_cap;    \
-    hipLaunchKernelGGL((k_bag_bwd_long<VT, NQ, CL, SP>), dim3((unsigned)lblocks),                  \
+    hipLaunchKernelGGL((k_bag_bwd_long<VT, NQ, CL>), dim3((unsigned)lblocks),                      \
                        dim3(64 * LONG_WAVES), (size_t)ng * D * sizeof(float), st, (const VT*)dy,   \
                        (const VT*)values, D, w, bag, ks, vs, b.seg, b.long_list, b.misc + 1,       \
-                       grad_values, rows_out, grad_rows_out, grad_w);                             \
+                       b.long_base, part, grad_w);                                                \
+    hipLaunchKernelGGL((k_long_reduce<SP>), dim3((unsigned)rblocks), dim3(256), 0, st, D, ks,      \
+                       b.seg, b.long_list, b.misc + 1, b.long_base, part, grad_values, rows_out,   \
+                       grad_rows_out);                                                             \
   }
 #define PK_ROWS(NQ, CL)                                                                           \
   if (bf16) {                                                                                     \

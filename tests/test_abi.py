@@ -238,6 +238,18 @@ def test_gating_empty_batch_is_a_noop(lib):
     assert gbwd(lib, T=0) == OK
 
 
+def test_bwd_auto_rule(lib, monkeypatch):
+    """PKMEM_BWD_AUTO: atomic when T*H*k*D <= 2^26 and D <= 1024 (the measured
+    crossover), sorted otherwise; seen through the workspace sizes."""
+    monkeypatch.delenv("PKMEM_BWD_MODE", raising=False)
+    ws = lambda T, D, m: lib.mem_bag_backward_workspace_size(T, 4, 32, 1 << 22, D, m)  # noqa: E731
+    for T, D, want in [(256, 64, 1), (8192, 64, 1), (16384, 64, 2), (4096, 128, 1),
+                       (8192, 128, 2), (256, 1024, 1), (1024, 1024, 2), (256, 2048, 2),
+                       (32768, 2048, 2)]:
+        assert ws(T, D, 0) == ws(T, D, want), (T, D, want)
+        assert ws(T, D, 1) != ws(T, D, 2)
+
+
 def test_bwd_mode_environment_override(lib, monkeypatch):
     args = (1000, 4, 32, 1 << 22, 2048, 0)
     atomic = lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 2048, 1)
@@ -246,7 +258,8 @@ def test_bwd_mode_environment_override(lib, monkeypatch):
     monkeypatch.setenv("PKMEM_BWD_MODE", "atomic")
     assert lib.mem_bag_backward_workspace_size(*args) == atomic
     monkeypatch.setenv("PKMEM_BWD_MODE", "sorted")
-    assert lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 64, 0) == sorted_
+    assert (lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 64, 0) ==
+            lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 64, 2))
     # an explicit mode is never overridden
     assert lib.mem_bag_backward_workspace_size(1000, 4, 32, 1 << 22, 2048, 1) == atomic
 

@@ -1,6 +1,7 @@
 """Rows chosen by more than 1024 lookups: the sorted backward lists them and
-splits each over a workgroup (contiguous runs of lookups per lane group,
-partial rows added in group order).  Against the fp64 oracle, dense and
+cuts each into chunks of 1024 lookups, each chunk summed by a workgroup of its
+own (contiguous runs of lookups per lane group, partial rows added in group
+order), the chunks' partial rows added in chunk order.  Against the fp64 oracle, dense and
 sparse, across row widths; bitwise deterministic run to run; lengths at and
 just past the split threshold."""
 import numpy as np
@@ -105,3 +106,33 @@ def test_backward_without_value_gradient(gpu_lib, mode):
     ref = oracle.bag_backward(h64(dy), h64(V), idx.numpy(), h64(w), H, k)
     assert normwise(h64(gw), ref["grad_w"]) <= TOL_F32
     assert normwise(h64(gz), ref["grad_z"]) <= TOL_F32
+
+
+def test_row_chosen_by_most_tokens(gpu_lib):
+    """One row chosen by about 60% of 65,536 tokens (about 39,000 lookups):
+    its lookups are cut into chunks summed by many workgroups and added in
+    chunk order.  Against the oracle, dense and sparse, bitwise deterministic."""
+    N, D, T, H, k = 1 << 16, 256, 65536, 1, 4
+    g = torch.Generator().manual_seed(31)
+    idx = torch.randint(0, N, (T, H, k), generator=g)
+    hot = torch.rand((T,), generator=g) < 0.6
+    idx[hot, 0, 0] = 7
+    V = (torch.randn((N, D), generator=g) * 0.02).to(torch.bfloat16)
+    w = torch.softmax(torch.randn((T, H, k), generator=g, dtype=torch.float64), -1).float()
+    dy = torch.randn((T, D), generator=g).to(torch.bfloat16)
+    counts = np.bincount(idx.numpy().ravel(), minlength=N)
+    assert counts[7] >= T // 2
+    print(f"[long-rows] hot row lookups {counts[7]}", flush=True)
+    args = (dy.cuda(), V.cuda(), idx.cuda(), w.cuda())
+    gv, gw, gz = gpu_lib.mem_bag_backward(*args, mode="sorted")
+    gv2, gw2, gz2 = gpu_lib.mem_bag_backward(*args, mode="sorted")
+    rows, grows, _, _ = gpu_lib.mem_bag_backward_sparse(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(gv, gv2) and torch.equal(gw, gw2) and torch.equal(gz, gz2)
+    ref = oracle.bag_backward_rows(h64(dy), h64(V), idx.numpy(), h64(w), H, k)
+    np.testing.assert_array_equal(rows.cpu().numpy(), ref["rows"])
+    assert normwise(h64(grows), ref["grad_rows"]) <= TOL_F32
+    hot_u = int(np.searchsorted(ref["rows"], 7))
+    assert normwise(h64(grows[hot_u]), ref["grad_rows"][hot_u]) <= TOL_F32
+    assert normwise(h64(gv[torch.from_numpy(ref["rows"]).cuda()]), ref["grad_rows"]) <= TOL_F32
+    assert normwise(h64(gw), ref["grad_w"]) <= TOL_F32
