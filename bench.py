@@ -384,6 +384,11 @@ def main():
     elapsed = time.perf_counter() - t0
     pk.mem_timer_stop()
     launches = pk.mem_timer_read()
+    # candidate records the scoring kernel wrote in the last step: the run
+    # counts follow the candidate slots in the search workspace (256 slots of
+    # 8 bytes per (token, head, half) row, each region 256-byte aligned)
+    cnt_off = (T * H * 2 * 256 * 8 + 255) // 256 * 256
+    records = int(ws_s[cnt_off:cnt_off + T * H * 2 * 8].view(torch.int32).sum().item())
     ms_per_step = elapsed * 1e3 / args.steps
     log(f"[bench] {ms_per_step:.3f} ms/step")
 
@@ -581,12 +586,19 @@ def main():
                 "peak": roof["peak"], "unit": roof["unit"], "frac": roof["frac"],
                 "traffic": traffic}
 
-    # the scoring kernel sweeps the sub-keys twice (threshold, then candidates):
-    # the MFMA work it executes is twice the algorithmic flops priced above
+    # the scoring kernel computes the products of the first half of the sub-key
+    # chunks twice (threshold sweep, then the final collection) and of the second
+    # half once (2 sweeps when k > 32): the MFMA work it executes is that multiple
+    # of the algorithmic flops priced above
     search_roof = bw("score_topk")
     if search_roof and search_roof["bound"] == "mfma":
-        search_roof = dict(search_roof, sweeps=2,
-                           executed_TFLOPs=round(2 * search_roof["achieved"], 2))
+        search_roof = dict(search_roof, candidate_records=records,
+                           candidates_per_row=round(records / (T * H * 2), 2))
+        nch = -(-wl.S // 64)
+        P = nch if wl.k > 32 else (nch + 1) // 2
+        sweeps = (nch + P) / nch
+        search_roof = dict(search_roof, sweeps=round(sweeps, 4),
+                           executed_TFLOPs=round(sweeps * search_roof["achieved"], 2))
 
     scatter = bw("bag_backward_rows") or bw("bag_backward_atomic")
     if scatter:

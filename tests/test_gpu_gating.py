@@ -69,8 +69,14 @@ def test_gated_forward_without_y(gpu_lib):
 
 def test_gated_chain_into_value_backward(gpu_lib):
     """gated forward -> gate backward -> bag backward, against the oracle's own
-    chain.  The GPU rounds dy to the value dtype between the two backwards, so
-    the value-side results are held to the bf16 tolerance."""
+    chain.  The GPU stores dy in the value dtype between the two backwards; the
+    oracle rounds its fp64 dy to bfloat16 the same way (round_bf16), so dy must
+    match bit for bit and the value-side results are held to 1e-5.  A dy element
+    whose exact value lies within fp32 evaluation error of a bfloat16 rounding
+    midpoint may round either way: each such element is certified as a near-tie
+    that took the other neighbour, and the tokens holding one (with every value
+    row they touch) are left out of the value-side comparison, which then
+    compares only what is unique."""
     N, D, T, H, k = 600, 512, 90, 4, 8
     V, idx, w, gate = _inputs(N, D, T, H * k, torch.bfloat16, 94)
     idx3, w3 = idx.view(T, H, k), w.view(T, H, k)
@@ -81,11 +87,25 @@ def test_gated_chain_into_value_backward(gpu_lib):
                                      mode="sorted")
     torch.cuda.synchronize()
     yref = oracle.bag_forward(h64(V), idx.numpy(), w.double().numpy())
-    dy_ref = oracle.gated_backward(h64(d_out), yref, h64(gate))["dy"]
+    dy_exact = oracle.gated_backward(h64(d_out), yref, h64(gate))["dy"]
+    dy_ref = oracle.round_bf16(dy_exact)
+    gdy = h64(dy)
+    flip = gdy != dy_ref
+    if flip.any():
+        m, e = np.frexp(dy_exact[flip])
+        frac = np.abs(m) * 256.0 - np.floor(np.abs(m) * 256.0)
+        assert np.all(np.abs(frac - 0.5) <= 2.0 ** -10), "dy differs away from a rounding midpoint"
+        assert np.all(np.abs(gdy[flip] - dy_ref[flip]) == np.ldexp(1.0, e - 8)), "not a neighbour"
+    assert flip.sum() <= 8
+    ok_t = ~flip.any(1)
+    bad_rows = np.unique(idx3.numpy()[~ok_t])
+    ok_r = np.ones(N, bool)
+    ok_r[bad_rows] = False
     b = oracle.bag_backward(dy_ref, h64(V), idx3.numpy(), w3.double().numpy(), H, k)
-    assert normwise(h64(dy), dy_ref) <= TOL_BF16
-    assert normwise(h64(gv), b["grad_values"]) <= TOL_BF16
-    assert normwise(h64(gw), b["grad_w"]) <= TOL_BF16
+    assert normwise(gdy, dy_exact) <= TOL_BF16
+    assert normwise(h64(gv)[ok_r], b["grad_values"][ok_r]) <= 1e-5
+    assert normwise(h64(gw)[ok_t], b["grad_w"][ok_t]) <= 1e-5
+    assert ok_r.sum() >= N // 2
 
 
 def test_gated_full_size_sampled(gpu_lib):
