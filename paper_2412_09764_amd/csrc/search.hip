@@ -193,19 +193,21 @@ __global__ __launch_bounds__(256) void k_qnorm(const T* __restrict__ q, int64_t 
 
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
-// Stores rec (8 bytes) at ptr and advances ptr by 8 bytes in the lanes of mask
-// only, without a branch: exec is narrowed to mask for the store and the
-// increment, and restored before the block ends.  A store with no lane active
-// does nothing.
-__device__ __forceinline__ void store_masked_advance(uint64_t mask, uint64_t& ptr, u32x2_t rec) {
+// Stores rec (8 bytes) at byte offset off of the buffer rs and advances off by
+// 8, in the lanes of mask only and without a branch: exec is narrowed to mask
+// for the store and the increment, and restored before the block ends.  A
+// store with no lane active does nothing; the buffer's bound drops any store
+// past its end.
+__device__ __forceinline__ void store_masked_advance(uint64_t mask, uint32_t& off, u32x2_t rec,
+                                                     __amdgpu_buffer_rsrc_t rs) {
   uint64_t saved;
   asm volatile(
       "s_and_saveexec_b64 %[sv], %[m]\n\t"
-      "global_store_dwordx2 %[p], %[r], off\n\t"
-      "v_lshl_add_u64 %[p], %[p], 0, 8\n\t"
+      "buffer_store_dwordx2 %[r], %[o], %[rs], 0 offen\n\t"
+      "v_add_u32 %[o], 8, %[o]\n\t"
       "s_mov_b64 exec, %[sv]"
-      : [p] "+v"(ptr), [sv] "=&s"(saved)
-      : [m] "s"(mask), [r] "v"(rec)
+      : [o] "+v"(off), [sv] "=&s"(saved)
+      : [m] "s"(mask), [r] "v"(rec), [rs] "s"(rs)
       : "memory", "scc");
 }
 
@@ -487,7 +489,15 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   float thl = INFINITY, strict = INFINITY, bound = INFINITY;
   uint32_t my_eq = 0;   // KBIG: records kept equal to the threshold
   uint32_t cnt0 = 0;    // my_cnt when the threshold was last set
-  uint64_t ptr = 0;     // next record of the fast path
+  // The workgroup's candidate rows (its tokens, every head and half) as a
+  // buffer, so the fast path's stores take 32-bit offsets.
+  const int64_t tok0 = tile * SEARCH_TOK;
+  const int64_t ntile = ntok - tok0 < SEARCH_TOK ? ntok - tok0 : SEARCH_TOK;
+  uint64_t* const wg_cand = cand + (size_t)tok0 * H * 2 * CAND_CAP;
+  const __amdgpu_buffer_rsrc_t crs =
+      raw_buffer(wg_cand, (uint32_t)((size_t)ntile * H * 2 * CAND_CAP * sizeof(uint64_t)));
+  const uint32_t my_off = (uint32_t)((my_cand - wg_cand) * sizeof(uint64_t));
+  uint32_t ptr = 0;     // byte offset of the fast path's next record in crs
   auto set_threshold = [&](float t) PK_INLINE {
     thl = tok_ok ? t : INFINITY;  // scores are finite
     strict = next_up(thl);
@@ -507,16 +517,16 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
     if constexpr (KBIG) return false;
     const bool room = my_cnt <= (uint32_t)(HALF_CAP - 16);
     if (__builtin_amdgcn_ballot_w64(!room) != 0) return false;
-    ptr = reinterpret_cast<uint64_t>(my_cand + my_cnt);
+    ptr = my_off + my_cnt * (uint32_t)sizeof(uint64_t);
     return true;
   };
   auto col_slot = [&](const f32x16_t& acc, int c, int half, int j) PK_INLINE {
     const uint32_t row = (uint32_t)(c * CHUNK_ROWS + half * 32 + acc_row(j, kh));
     const uint64_t m = __builtin_amdgcn_ballot_w64(acc[j] >= bound);
-    if (m) store_masked_advance(m, ptr, u32x2_t{row, __float_as_uint(acc[j])});  // uniform
+    if (m) store_masked_advance(m, ptr, u32x2_t{row, __float_as_uint(acc[j])}, crs);  // uniform
   };
   auto col_done = [&](int, int) PK_INLINE {
-    my_cnt = (uint32_t)((ptr - reinterpret_cast<uint64_t>(my_cand)) >> 3);
+    my_cnt = (ptr - my_off) >> 3;
     bound = my_cnt - cnt0 >= (uint32_t)k ? strict : bound;
   };
   auto col_whole = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
