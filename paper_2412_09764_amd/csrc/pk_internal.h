@@ -27,7 +27,7 @@ class LaunchTimer {
 constexpr int CAND_CAP = 256;
 // Waves and tokens per workgroup of the scoring kernel (32 tokens per wave).
 #ifndef PK_SEARCH_WAVES
-#define PK_SEARCH_WAVES 8
+#define PK_SEARCH_WAVES 16
 #endif
 constexpr int SEARCH_WAVES = PK_SEARCH_WAVES;
 constexpr int SEARCH_TOK = 32 * SEARCH_WAVES;

@@ -3,41 +3,49 @@
 //
 // Step 1, k_score_topk: for every (token, head, half) row, the top k of the S
 // half-key scores s[i] = q_half . K_half[i], ordered (score desc, index asc).
-//   * A workgroup owns SEARCH_TOK = 256 tokens (8 waves of 32) of one (head,
-//     half); the (head, half) index is blockIdx % (2H), so with 2H = 8 each XCD
-//     streams only its own 1 MiB sub-key table and keeps it in its L2.
+//   * A workgroup owns SEARCH_TOK = 512 tokens (16 waves of 32, four per SIMD)
+//     of one (head, half); the (head, half) index is blockIdx % (2H), so with
+//     2H = 8 each XCD streams only its own sub-key table and keeps it in its
+//     L2.  The kernel fits 128 registers, which is what four waves per SIMD
+//     allow.
 //   * Scores come from v_mfma_f32_32x32x16_bf16 (fp32 inputs: 32x32x2 f32) with
 //     sub-keys as the A operand (M = 32 sub-keys) and the wave's 32 queries as
 //     the register-resident B operand (N = 32 tokens); sub-key chunks of 64 rows
 //     are copied into LDS by buffer LDS-DMA, double buffered, and read as
-//     fragments a few MFMA steps ahead of their use.  Scores never leave
-//     registers.  A 32-row tile is one chain of dependent MFMAs; the
-//     filtering of the previous tile (its 16 accumulator slots per lane) is
-//     spread over that chain, so VALU and store work overlaps matrix work.
+//     fragments one MFMA step ahead of their use.  Scores never leave
+//     registers.  A 32-row tile is one chain of dependent MFMAs, then the
+//     pass works on its 16 accumulator slots per lane; half of the waves on
+//     each SIMD run one tile behind the others, so one half's vector work
+//     meets the other half's matrix work.
 //   * Threshold: per token, the maximum of each of 64 interleaved groups of
-//     sub-keys (group = row mod 64); the k-th largest of those maxima has at
-//     least k distinct scores at or above it, so no score below it can be
-//     selected.
+//     sub-keys (group = row mod 64), kept as 16-bit floats rounded toward
+//     zero, two per register; the k-th largest of those maxima, one 16-bit
+//     step down, has at least k distinct scores at or above it, so no score
+//     below it can be selected.  It is found by sorting each lane's 32
+//     maxima and a binary search for the split between the two lanes'
+//     sorted runs (left in LDS).
 //   * Three sweeps, 1.5 passes over the sub-keys: the first half of the rows
 //     gives group maxima and a first threshold; the second half is filtered
 //     against that threshold while the maxima are completed, which gives the
 //     final threshold; the first half is then filtered against the final one
 //     (its products recomputed bitwise alike).  Every score at or above its
-//     threshold is appended, as a raw 64-bit (score, index) record, to the
-//     row's candidate list (about 66 of 2048 at k = 32); the two lanes holding
-//     a token's rows own half of its CAND_CAP slots each.  The append is one
-//     wave ballot and one exec-masked store per accumulator slot (no branch
-//     per lane); a tile where some lane could run past its slots takes a
-//     clamped path (a count past capacity sends the row to the rescan).  A
-//     lane holding k records taken against the current threshold takes only
-//     scores above it from then on (lower indices win ties), so rows of tied
-//     scores fit their slots.
+//     threshold goes, as a raw 64-bit (score, index) record, to the row's
+//     candidate list (about 66 of 2048 at k = 32); the two lanes holding a
+//     token's rows own half of its CAND_CAP slots each.  A tile's candidates
+//     are found with one compare per slot into a per-lane mask and taken out
+//     in rounds (each lane its lowest remaining slot per round, the score
+//     read back from a per-wave LDS scratch), so the stores per tile are as
+//     many as the most candidates any lane has in it, not one per slot.  A
+//     count past capacity sends the row to the rescan.  A lane holding k
+//     records taken against the current threshold takes only scores above
+//     the lowest of them from then on (lower indices win ties), so rows of
+//     tied scores fit their slots.
 //   * Pass 3, k_topk_sort, a kernel of its own (a sort needs few registers, so
-//     it runs at far higher occupancy than the scoring kernel, which is held
-//     to two waves per SIMD): per row the records below the final threshold
-//     are dropped, the rest sorted by one wave, the first k written.  A row
-//     whose lane half overflowed its CAND_CAP / 2 slots is listed for
-//     k_topk_fallback, which rescans it exactly.
+//     it runs at far higher occupancy than the scoring kernel): per row the
+//     records below the final threshold are dropped, the rest sorted by one
+//     wave, the first k written.  A row whose lane half overflowed its
+//     CAND_CAP / 2 slots is listed for k_topk_fallback, which rescans it
+//     exactly.
 //   * With query normalisation (qk-normalisation, Sec. 3.1.4) k_qnorm first
 //     computes each (token, head) query's mean and rstd = 1/sqrt(var + eps)
 //     (LayerNorm without affine, fp32, centred second pass); the scoring
@@ -65,7 +73,7 @@ constexpr int CHUNK_ROWS = 64;  // sub-keys per LDS chunk = two MFMA tiles
 #define PK_INLINE __attribute__((always_inline))
 
 #ifndef PK_SCORE_PREFETCH
-#define PK_SCORE_PREFETCH 2  // LDS fragments read this many MFMA steps ahead (0: none)
+#define PK_SCORE_PREFETCH 1  // LDS fragments read this many MFMA steps ahead (0: none)
 #endif
 
 template <typename T>
@@ -191,34 +199,52 @@ __global__ __launch_bounds__(256) void k_qnorm(const T* __restrict__ q, int64_t 
   }
 }
 
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-
-// Stores rec (8 bytes) at byte offset off of the buffer rs and advances off by
-// 8, in the lanes of mask only and without a branch: exec is narrowed to mask
-// for the store and the increment, and restored before the block ends.  A
-// store with no lane active does nothing; the buffer's bound drops any store
-// past its end.
-__device__ __forceinline__ void store_masked_advance(uint64_t mask, uint32_t& off, u32x2_t rec,
-                                                     __amdgpu_buffer_rsrc_t rs) {
-  uint64_t saved;
-  asm volatile(
-      "s_and_saveexec_b64 %[sv], %[m]\n\t"
-      "buffer_store_dwordx2 %[r], %[o], %[rs], 0 offen\n\t"
-      "v_add_u32 %[o], 8, %[o]\n\t"
-      "s_mov_b64 exec, %[sv]"
-      : [o] "+v"(off), [sv] "=&s"(saved)
-      : [m] "s"(mask), [r] "v"(rec), [rs] "s"(rs)
-      : "memory", "scc");
-}
-
 // Row of the 32x32 MFMA result held in accumulator slot j of a lane whose
 // upper-half bit is kh (columns are lane & 31).
 __device__ __forceinline__ int acc_row(int j, int kh) { return 8 * (j >> 2) + 4 * kh + (j & 3); }
 
-// KBIG (k > 32): records equal to the threshold are counted one by one, and
-// both thresholds come from all rows (P = all chunks: no second sweep).
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// Group maxima of the scoring kernel: pairs of 16-bit floats rounded toward
+// zero from fp32 scores (two groups per register).
+typedef _Float16 h16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ h16x2_t pk_rtz(float lo, float hi) {
+  return __builtin_bit_cast(h16x2_t, __builtin_amdgcn_cvt_pkrtz(lo, hi));
+}
+// Element-wise maximum of two pairs (the inputs are never signalling NaNs, so
+// the instruction needs none of the quieting that maxnum would add).
+__device__ __forceinline__ void pk_max_into(h16x2_t& a, h16x2_t b) {
+  asm("v_pk_max_f16 %0, %0, %1" : "+v"(a) : "v"(b));
+}
+// The next 16-bit float below t (t holds a 16-bit float value exactly; -inf
+// stays -inf).
+__device__ __forceinline__ float f16_step_down(float t) {
+  const uint32_t hb = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)t);
+  uint32_t r = (hb & 0x8000u) ? hb + 1u : hb - 1u;  // negative (and -0): one step more negative;
+                                                     // positive: one step toward zero
+  r = hb == 0x0000u ? 0x8001u : r;                   // +0: the smallest negative value
+  r = hb == 0xFC00u ? hb : r;                        // -inf stays
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)r);
+}
+
+// (m << 1) | (z >= b): one compare into vcc and one add with carry (the two
+// wait states between them are the hardware's for a VALU read of vcc that
+// a VALU wrote).
+__device__ __forceinline__ uint32_t mask_step(uint32_t m, float z, float b) {
+  uint64_t carry;
+  asm("v_cmp_ge_f32 vcc, %[z], %[b]\n\t"
+      "s_nop 1\n\t"
+      "v_addc_co_u32_e64 %[m], %[c], %[m], %[m], vcc"
+      : [m] "+v"(m), [c] "=s"(carry)
+      : [z] "v"(z), [b] "v"(b)
+      : "vcc");
+  return m;
+}
+
+// KBIG (k > 32): the threshold comes from all rows (P = all chunks: no second
+// sweep).
 template <typename T, int NSTEP, bool KBIG>
-__global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
+__global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
     const T* __restrict__ q, const T* __restrict__ subkeys, int64_t ntok, int H, int n, int S,
     int k, const float2* __restrict__ qstats, const T* __restrict__ sink,
     float* __restrict__ sink_part, uint64_t* __restrict__ cand, uint32_t* __restrict__ cnts,
@@ -235,8 +261,15 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   // sits at row * RB + (col ^ (row & SWZ)) * 16: rows that the same fragment
   // read touches land in different banks without padding, which keeps every
   // wave's 1 KiB of a chunk contiguous for the direct global -> LDS loads.
-  __shared__ __align__(16) unsigned char kbuf0[CBYTES];
-  __shared__ __align__(16) unsigned char kbuf1[CBYTES];
+  // The two buffers are statically named arrays, so LDS accesses elsewhere
+  // never wait on the copies in flight.  Each wave also has a scratch for
+  // taking candidates out of a tile (64 lanes x 16 fp32 scores), which
+  // between sweeps holds each lane's sorted group maxima (32 16-bit floats)
+  // for the threshold.
+  constexpr int XS_WAVE = WAVE * 16 * 4;
+  __shared__ __align__(1024) unsigned char kbuf0[CBYTES];
+  __shared__ __align__(1024) unsigned char kbuf1[CBYTES];
+  __shared__ __align__(16) unsigned char xsmem[SEARCH_WAVES * XS_WAVE];
 
   const int d = n >> 1;
   const int HP = 2 * H;
@@ -333,19 +366,12 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
   };
   // ---- the sweeps -----------------------------------------------------------
   // A sweep visits every 32-row tile once, in row order.  Tile t is one chain
-  // of NSTEP dependent MFMAs into its own accumulator (fragments read from
-  // LDS LEAD steps ahead of their use), and the filtering of tile t - 1 is
-  // spread over those steps, SPS accumulator slots per step: the VALU and
-  // memory work of one tile runs while the next tile's products occupy the
-  // matrix pipe.  Chunks of two tiles alternate between the two LDS buffers
-  // (unrolled by two so every access names its buffer statically).  A pass
-  // supplies
-  //   fast(c, half)          whether tile (c, half) of a full chunk may be
-  //                          filtered slot by slot (uniform),
-  //   slot(acc, c, half, j)  slot j of such a tile,
-  //   done(c, half)          after its last slot,
-  //   whole(acc, c, half)    a whole tile at once (a partial last chunk, or
-  //                          fast() false).
+  // of NSTEP dependent MFMAs into the accumulator (fragments read from LDS
+  // LEAD steps ahead of their use), then the pass filters its 16 slots per
+  // lane.  Four waves share each SIMD (two workgroups per CU), so one wave's
+  // filtering and waits run while the others' products occupy the matrix
+  // pipe.  Chunks of two tiles alternate between the two LDS buffers
+  // (unrolled by two so every access names its buffer statically).
   // Byte offset in LDS of the lane's fragment of step s: row col of the tile,
   // reduction elements from s * KSTEP + kh * LANE_K, through the swizzle.
   // It equals lane_addr ^ step_xor(s) with a lane-independent step_xor (the
@@ -366,13 +392,11 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
     return a;
   };
   constexpr int LEAD = PK_SCORE_PREFETCH > 0 ? PK_SCORE_PREFETCH : 1;
-  constexpr int SPS = (16 + NSTEP - 1) / NSTEP;  // slots of the pending tile per MFMA step
   const int nch = (S + CHUNK_ROWS - 1) / CHUNK_ROWS;
   const int nfull = S / CHUNK_ROWS;  // chunks with all 64 rows valid
 
-  // Rows half*32 .. half*32 + 31 of the chunk in buf into acc; pend(j) runs
-  // slot j of the pending tile (or nothing).
-  auto run_tile = [&](const unsigned char* buf, int half, f32x16_t& acc, auto&& pend) PK_INLINE {
+  // Rows half*32 .. half*32 + 31 of the chunk in buf into acc.
+  auto run_tile = [&](const unsigned char* buf, int half, f32x16_t& acc) PK_INLINE {
     const unsigned char* rp = buf + half * 32 * RB;
     acc = f32x16_t{};
     typename M::frag ring[LEAD + 1];
@@ -383,34 +407,46 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
       if (s + LEAD < NSTEP) ring[(s + LEAD) % (LEAD + 1)] = M::load(rp + step_addr(s + LEAD));
       __builtin_amdgcn_sched_barrier(0);  // reads stay LEAD steps ahead of their use
       acc = M::mma(ring[s % (LEAD + 1)], bq[s], acc);
-#pragma unroll
-      for (int q = 0; q < SPS; ++q)
-        if (s * SPS + q < 16) pend(s * SPS + q);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // Chunks [cb, ce) in order (any range; the two LDS buffers alternate).
-  auto sweep = [&](int cb, int ce, auto&& fast, auto&& slot, auto&& done, auto&& whole) PK_INLINE {
+  // Rows past S (the last chunk only) score -inf: no group maximum takes
+  // them, and the candidate path checks the row as well.
+  auto mask_tail = [&](f32x16_t& acc, int c, int half) PK_INLINE {
+    const int r0 = c * CHUNK_ROWS + half * 32;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[j] = r0 + acc_row(j, kh) < S ? acc[j] : -INFINITY;
+  };
+  // Chunks [cb, ce) in order (any range; the two LDS buffers alternate);
+  // tile(acc, c, half) consumes each tile.  Half of the waves on each SIMD
+  // (waves 4-7 and 12-15, with wave w on SIMD w mod 4) lag by one tile: they
+  // consume a chunk's second tile at the start of the next chunk, so their
+  // filtering (vector ALU) runs while the other waves' products occupy the
+  // matrix pipe, and the other way round.
+  const bool lag = ((wave >> 2) & 1) != 0;
+  auto sweep = [&](int cb, int ce, auto&& tile_fn) PK_INLINE {
     if (cb >= ce) return;
-    f32x16_t acc0, acc1;  // the chunk's two tiles
-    int pc = -1;          // chunk whose second tile (in acc1) is pending
+    f32x16_t acc;
+    int pc = -1;  // lagging waves: chunk whose second tile (in acc) is pending
     auto chunk = [&](const unsigned char* buf, int c) PK_INLINE {
-      if (pc >= 0 && pc < nfull && fast(pc, 1)) {
-        run_tile(buf, 0, acc0, [&](int j) PK_INLINE { slot(acc1, pc, 1, j); });
-        done(pc, 1);
+      if (lag) {
+        if (pc >= 0) tile_fn(acc, pc, 1);
+        run_tile(buf, 0, acc);
+        if (__builtin_expect(c >= nfull, 0)) mask_tail(acc, c, 0);
+        tile_fn(acc, c, 0);
+        run_tile(buf, 1, acc);
+        if (__builtin_expect(c >= nfull, 0)) mask_tail(acc, c, 1);
+        pc = c;
       } else {
-        run_tile(buf, 0, acc0, [&](int) PK_INLINE {});
-        if (pc >= 0) whole(acc1, pc, 1);
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          run_tile(buf, half, acc);
+          if (__builtin_expect(c >= nfull, 0)) mask_tail(acc, c, half);
+          tile_fn(acc, c, half);
+        }
       }
-      if (c < nfull && fast(c, 0)) {
-        run_tile(buf, 1, acc1, [&](int j) PK_INLINE { slot(acc0, c, 0, j); });
-        done(c, 0);
-      } else {
-        run_tile(buf, 1, acc1, [&](int) PK_INLINE {});
-        whole(acc0, c, 0);
-      }
-      pc = c;
     };
+    __syncthreads();  // every wave is done with the memory (threshold, last sweep)
     issue_chunk(cb, kbuf0);
     for (int c = cb; c < ce; c += 2) {
       __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of chunk c have landed
@@ -424,151 +460,172 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES) void k_score_topk(
         chunk(kbuf1, c + 1);
       }
     }
-    whole(acc1, pc, 1);
+    if (pc >= 0) tile_fn(acc, pc, 1);
     __syncthreads();
   };
 
   // ---- group maxima and the threshold ---------------------------------------
   // 64 interleaved groups per token (group = row mod 64): 32 maxima in this
-  // lane, 32 in lane ^ 32.  Maxima and minima here are med3 against an
-  // infinity in a register (max_med3 / min_med3): one instruction each.
+  // lane, 32 in lane ^ 32, kept as 16-bit floats rounded toward zero, two
+  // groups per register (slots 2i and 2i + 1 of a tile are adjacent rows).
   const float pinf = opaque_pinf(), ninf = opaque_ninf();
-  float mx[32];
+  h16x2_t mxp[16];
 #pragma unroll
-  for (int i = 0; i < 32; ++i) mx[i] = -INFINITY;
-  auto max_slot = [&](const f32x16_t& acc, int half, int j) PK_INLINE {
-    mx[half * 16 + j] = max_med3(mx[half * 16 + j], acc[j], pinf);
-  };
-  auto max_whole = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
+  for (int i = 0; i < 16; ++i) mxp[i] = h16x2_t{(_Float16)-INFINITY, (_Float16)-INFINITY};
+  auto max_tile = [&](const f32x16_t& acc, int, int half) PK_INLINE {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int row = c * CHUNK_ROWS + half * 32 + acc_row(j, kh);
-      mx[half * 16 + j] =
-          max_med3(mx[half * 16 + j], row < S ? acc[j] : -INFINITY, pinf);
-    }
+    for (int i = 0; i < 8; ++i) pk_max_into(mxp[half * 8 + i], pk_rtz(acc[2 * i], acc[2 * i + 1]));
   };
-  // The k-th largest of the 64 values: each is a score of a distinct row, so
-  // at least k distinct scores lie at or above it.  Both halves are sorted in
-  // place, then the bitonic half-cleaner of the 64-element sequence (mine
-  // descending, partner's reversed) is merged.  Sorting moves maxima between
-  // groups; later updates keep every value a score of a row of its own, so
-  // the bound stays valid when the sweep continues afterwards.
+  // The k-th largest of the token's 64 rounded maxima, one 16-bit step down:
+  // at least k distinct scores lie at or above the result (each of the k
+  // groups whose rounded maximum reaches the k-th largest holds a score above
+  // the value one step below it, whichever way the rounding toward zero
+  // went).  Each lane sorts its 32 (in fp32, exactly) and leaves them in LDS;
+  // the k-th largest of the two sorted runs (this lane's and lane ^ 32's) is
+  // then found by a binary search for the split between them.  The sorted
+  // maxima also go back into the packed registers (exactly): sorting moves
+  // maxima between groups, but later updates keep every value the rounded
+  // score of a row of its own, so the bound stays valid when the sweep
+  // continues afterwards.  Runs between sweeps, when the chunk buffers are
+  // free.
   auto kth_of_maxima = [&]() PK_INLINE -> float {
-    sort_desc_regs<32>(mx, pinf, ninf);
-    float sel[32];
+    float mx[32];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {  // element i pairs with the partner's 31 - i
-      const float pa = __shfl_xor(mx[31 - i], 32, WAVE), pb = __shfl_xor(mx[i], 32, WAVE);
-      sel[i] = k <= 32 ? max_med3(mx[i], pa, pinf) : min_med3(mx[i], pa, ninf);
-      sel[31 - i] = k <= 32 ? max_med3(mx[31 - i], pb, pinf) : min_med3(mx[31 - i], pb, ninf);
+    for (int i = 0; i < 16; ++i) {
+      mx[2 * i] = (float)mxp[i].x;
+      mx[2 * i + 1] = (float)mxp[i].y;
     }
-    merge_desc_regs<32>(sel, pinf, ninf);
-    const int want = (k <= 32) ? k - 1 : k - 33;
-    float t = sel[0];
+    sort_desc_regs<32>(mx, pinf, ninf);
 #pragma unroll
-    for (int i = 1; i < 32; ++i) t = (i == want) ? sel[i] : t;
-    return t;
+    for (int i = 0; i < 16; ++i) mxp[i] = pk_rtz(mx[2 * i], mx[2 * i + 1]);
+    uint16_t* const runs = reinterpret_cast<uint16_t*>(xsmem);  // [64 * SEARCH_WAVES][32]
+    uint4* const mine = reinterpret_cast<uint4*>(runs + tid * 32);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      mine[i] = uint4{__builtin_bit_cast(uint32_t, mxp[4 * i]), __builtin_bit_cast(uint32_t, mxp[4 * i + 1]),
+                      __builtin_bit_cast(uint32_t, mxp[4 * i + 2]), __builtin_bit_cast(uint32_t, mxp[4 * i + 3])};
+    const uint16_t* const ra = runs + tid * 32;          // this lane's run, descending
+    const uint16_t* const rb = runs + (tid ^ 32) * 32;   // the partner's
+    auto at = [](const uint16_t* r, int i) PK_INLINE {
+      return (float)__builtin_bit_cast(_Float16, r[i]);
+    };
+    // i from this run and k - i from the other: the smallest i in
+    // [max(0, k - 32), min(k, 32)] at which taking one more from this run
+    // would not beat the last one taken from the other.
+    int lo = k > 32 ? k - 32 : 0, hi = k < 32 ? k : 32;
+#pragma unroll
+    for (int it = 0; it < 6; ++it) {
+      if (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (at(ra, mid) > at(rb, k - 1 - mid)) lo = mid + 1;  // mid < 32 and k - mid > 0 here
+        else hi = mid;
+      }
+    }
+    const int j = k - lo;
+    const float a = lo > 0 ? at(ra, lo > 0 ? lo - 1 : 0) : INFINITY;
+    const float b = j > 0 ? at(rb, j > 0 ? j - 1 : 0) : INFINITY;
+    return f16_step_down(a < b ? a : b);
   };
 
   // ---- candidate collection ---------------------------------------------------
-  // Every score >= bound is appended to the lane's run.  A lane meets the rows
-  // of one sweep in increasing index order, tile by tile.  Once it holds k
-  // records taken against the current threshold in earlier tiles of the
-  // sweep, it takes only scores above the threshold: a later score equal to
-  // it is beaten by each of those k (by score, or on the tie by their lower
-  // index), so it cannot be selected.  Heavily tied rows (equal sub-keys) thus
-  // stay within their slots (at most k + 15 records per lane and sweep); the
-  // test runs once per tile.  Tiles of full chunks whose records cannot overrun any lane's slots
-  // take the branch-free store (one masked store per slot); the others, and
-  // k > 32 (records equal to the threshold counted one by one), the clamped
-  // path.
-  constexpr int HALF_CAP = CAND_CAP / 2;
+  // A lane's candidates in a tile are the slots whose score is >= bound: one
+  // compare per slot builds the lane's 16-bit candidate mask.  When any lane
+  // has one, the lane's 16 scores go to its scratch in LDS and the wave takes
+  // the candidates out in rounds, each lane its lowest remaining slot per
+  // round (index from the mask, score read back from LDS), appending one raw
+  // 64-bit (score, row) record per round to its run in memory: a tile costs
+  // a compare per slot and a few stores, the most any lane of the wave has
+  // candidates in it, rather than work per slot.  The run holds
+  // CAND_CAP / 2 records; a count past that sends the row to the rescan.
+  //
+  // A lane meets the rows of one sweep in increasing index order, tile by
+  // tile.  Once it holds k records taken against the current threshold, the
+  // lowest of them, lo, is a bound of its own: a later score at or below lo
+  // is beaten by all k of them (by score, or on a tie by their lower index),
+  // so it cannot be selected, and the lane takes only scores above lo from
+  // then on.  Heavily tied rows (equal sub-keys) thus stay within their
+  // slots (at most k + 15 records per lane and sweep); the test runs once
+  // per tile.
+  constexpr uint32_t HALF_CAP = CAND_CAP / 2;
   const size_t rid = ((size_t)(tok_ok ? tok : 0) * H + h) * 2 + p;
-  uint64_t* my_cand = cand + rid * CAND_CAP + kh * HALF_CAP;
   uint32_t my_cnt = 0;
-  float thl = INFINITY, strict = INFINITY, bound = INFINITY;
-  uint32_t my_eq = 0;   // KBIG: records kept equal to the threshold
   uint32_t cnt0 = 0;    // my_cnt when the threshold was last set
+  float bound = INFINITY;
+  float lo = INFINITY;  // lowest record taken against the current threshold
   // The workgroup's candidate rows (its tokens, every head and half) as a
-  // buffer, so the fast path's stores take 32-bit offsets.
+  // buffer, so the stores take 32-bit offsets; this lane's run starts at
+  // my_off.
   const int64_t tok0 = tile * SEARCH_TOK;
   const int64_t ntile = ntok - tok0 < SEARCH_TOK ? ntok - tok0 : SEARCH_TOK;
   uint64_t* const wg_cand = cand + (size_t)tok0 * H * 2 * CAND_CAP;
   const __amdgpu_buffer_rsrc_t crs =
       raw_buffer(wg_cand, (uint32_t)((size_t)ntile * H * 2 * CAND_CAP * sizeof(uint64_t)));
-  const uint32_t my_off = (uint32_t)((my_cand - wg_cand) * sizeof(uint64_t));
-  uint32_t ptr = 0;     // byte offset of the fast path's next record in crs
+  const uint32_t my_off =
+      (uint32_t)((((size_t)(wave * 32 + col) * H + h) * 2 + p) * CAND_CAP + kh * HALF_CAP) * 8u;
+  // This wave's scratch: slot j of lane l at float j * 64 + l (each slot's
+  // write and each round's read are one conflict-free access).
+  float* const xs = reinterpret_cast<float*>(xsmem + wave * XS_WAVE);
+  // The last threshold set is the row's final one (what the sort keeps).
   auto set_threshold = [&](float t) PK_INLINE {
-    thl = tok_ok ? t : INFINITY;  // scores are finite
-    strict = next_up(thl);
-    bound = thl;
-    my_eq = 0;
+    bound = tok_ok ? t : INFINITY;  // scores are finite
+    lo = INFINITY;
     cnt0 = my_cnt;
+    if (tok_ok && kh == 0) thr[rid] = t;
   };
-  auto keep = [&](float z, uint32_t row) PK_INLINE {
-    my_cand[my_cnt < (uint32_t)HALF_CAP ? my_cnt : (uint32_t)HALF_CAP - 1] =
-        (uint64_t(__float_as_uint(z)) << 32) | row;
-    ++my_cnt;
-    if constexpr (KBIG) {  // the k-th record at the threshold: only higher scores from now on
-      if (z == thl && ++my_eq == (uint32_t)k) bound = strict;
-    }
-  };
-  auto col_fast = [&](int, int) PK_INLINE {
-    if constexpr (KBIG) return false;
-    const bool room = my_cnt <= (uint32_t)(HALF_CAP - 16);
-    if (__builtin_amdgcn_ballot_w64(!room) != 0) return false;
-    ptr = my_off + my_cnt * (uint32_t)sizeof(uint64_t);
-    return true;
-  };
-  auto col_slot = [&](const f32x16_t& acc, int c, int half, int j) PK_INLINE {
-    const uint32_t row = (uint32_t)(c * CHUNK_ROWS + half * 32 + acc_row(j, kh));
-    const uint64_t m = __builtin_amdgcn_ballot_w64(acc[j] >= bound);
-    if (m) store_masked_advance(m, ptr, u32x2_t{row, __float_as_uint(acc[j])}, crs);  // uniform
-  };
-  auto col_done = [&](int, int) PK_INLINE {
-    my_cnt = (ptr - my_off) >> 3;
-    bound = my_cnt - cnt0 >= (uint32_t)k ? strict : bound;
-  };
-  auto col_whole = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
+  auto collect_tile = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
     const uint32_t r0 = (uint32_t)(c * CHUNK_ROWS + half * 32 + 4 * kh);
+    uint32_t msk = 0;  // bit j: slot j is a candidate
+    if (c < nfull) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const uint32_t row = r0 + 8 * (j >> 2) + (j & 3);
-      if (acc[j] >= bound && row < (uint32_t)S) keep(acc[j], row);
+      for (int j = 15; j >= 0; --j) msk = mask_step(msk, acc[j], bound);
+    } else {  // rows past S are no candidates
+#pragma unroll
+      for (int j = 15; j >= 0; --j)
+        msk = msk * 2u + (uint32_t)(acc[j] >= bound && r0 + acc_row(j, 0) < (uint32_t)S);
     }
-    if constexpr (!KBIG) bound = my_cnt - cnt0 >= (uint32_t)k ? strict : bound;
+    if (__builtin_amdgcn_ballot_w64(msk != 0) != 0) {  // uniform
+#pragma unroll
+      for (int j = 0; j < 16; ++j) xs[j * WAVE + lane] = acc[j];
+      // a lane takes at most 16 records in the tile: unclamped when every
+      // lane has room for them
+      const bool room = __builtin_amdgcn_ballot_w64(my_cnt > HALF_CAP - 16u) == 0;
+      uint32_t ptr = my_off + my_cnt * 8u;
+      do {
+        const uint32_t j = (uint32_t)__builtin_ctz(msk | 0x8000u);  // any slot when msk is 0
+        const float z = xs[j * WAVE + lane];
+        if (msk != 0) {
+          const uint32_t at = room ? ptr : my_off + (my_cnt < HALF_CAP ? my_cnt : HALF_CAP - 1u) * 8u;
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{r0 + j + (j & 12u), __float_as_uint(z)}, crs, at, 0, 0);
+          ++my_cnt;
+          ptr += 8u;
+          lo = min_med3(lo, z, ninf);
+        }
+        msk &= msk - 1u;
+      } while (__builtin_amdgcn_ballot_w64(msk != 0) != 0);
+    }
+    bound = my_cnt - cnt0 >= (uint32_t)k ? next_up(lo) : bound;
   };
 
   // ---- the three sweeps ----------------------------------------------------------
   // 1. Chunks [0, P): group maxima only; their k-th largest is a first
   //    threshold.  2. Chunks [P, nch): candidates against that threshold,
-  //    maxima still updated; then the final threshold (the k-th largest of
-  //    the maxima over all rows).  3. Chunks [0, P) again: candidates against
-  //    the final threshold.  Every score of the top k is at or above both
-  //    thresholds, so every one is collected; the products over [0, P) are
-  //    computed twice, bitwise alike.  P = half of the chunks (1.5 sweeps in
-  //    all); with k > 32 P = all of them (sweep 2 is empty).
+  //    maxima still updated; then the final threshold (from the maxima over
+  //    all rows).  3. Chunks [0, P) again: candidates against the final
+  //    threshold.  Every score of the top k is at or above both thresholds,
+  //    so every one is collected; the products over [0, P) are computed
+  //    twice, bitwise alike.  P = half of the chunks (1.5 sweeps in all);
+  //    with k > 32 P = all of them (sweep 2 is empty).
   const int P = KBIG ? nch : (nch + 1) / 2;
-  auto yes = [&](int, int) PK_INLINE { return true; };
-  auto none = [&](int, int) PK_INLINE {};
-  sweep(0, P, yes, [&](const f32x16_t& acc, int, int half, int j) PK_INLINE { max_slot(acc, half, j); },
-        none, max_whole);
+  sweep(0, P, max_tile);
   set_threshold(kth_of_maxima());
   if (P < nch) {
-    sweep(P, nch, col_fast,
-          [&](const f32x16_t& acc, int c, int half, int j) PK_INLINE {
-            max_slot(acc, half, j);
-            col_slot(acc, c, half, j);
-          },
-          col_done,
-          [&](const f32x16_t& acc, int c, int half) PK_INLINE {
-            max_whole(acc, c, half);
-            col_whole(acc, c, half);
-          });
+    sweep(P, nch, [&](const f32x16_t& acc, int c, int half) PK_INLINE {
+      max_tile(acc, c, half);
+      collect_tile(acc, c, half);
+    });
     set_threshold(kth_of_maxima());
   }
-  sweep(0, P, col_fast, col_slot, col_done, col_whole);
-  if (tok_ok && kh == 0) thr[rid] = thl;
+  sweep(0, P, collect_tile);
   if (tok_ok) cnts[rid * 2 + kh] = my_cnt;
 }
 

@@ -80,6 +80,34 @@ def test_search_integer_inputs_exact(gpu_lib, case):
     assert normwise(h64(w), ref["w"]) <= TOL_F32
 
 
+SCORE_RANGE_CASES = [
+    # (name, q range, q scale, sub-key range, sub-key scale): integer values
+    # times powers of two, so every score is exact in fp32
+    ("beyond_f16_range", (-4, 4), 1.0, (-4, 4), 256.0),   # |score| up to 2^20
+    ("all_negative_saturating", (1, 4), 1.0, (-4, -1), 32.0),  # -131072 .. -8192
+    ("tiny_f16_subnormal", (-4, 4), 2.0 ** -12, (-4, 4), 2.0 ** -12),  # |score| <= 2^-12
+    ("near_zero_ties", (-1, 1), 1.0, (-1, 1), 1.0),
+]
+
+
+@pytest.mark.parametrize("case", SCORE_RANGE_CASES, ids=[c[0] for c in SCORE_RANGE_CASES])
+def test_search_score_ranges_exact(gpu_lib, case):
+    """The group maxima behind the threshold are 16-bit floats rounded toward
+    zero: scores past the 16-bit range, all-negative scores, scores in its
+    subnormal range and tied scores around zero still select exactly."""
+    name, (qa, qb), qs, (ka, kb), ks = case
+    S, H, n, k, T = 2048, 2, 512, 32, 48
+    print(f"[search-range] {name}", flush=True)
+    q = (int_tensor((T, H, n), 21, torch.float32, qa, qb) * qs).to(torch.bfloat16)
+    K = (int_tensor((H, 2, S, n // 2), 22, torch.float32, ka, kb) * ks).to(torch.bfloat16)
+    idx, w, score, hidx = gpu_lib.mem_search(q.cuda(), K.cuda(), k, want_half=True)
+    torch.cuda.synchronize()
+    ref = oracle.search(h64(q), h64(K), k)
+    np.testing.assert_array_equal(hidx.cpu().numpy(), ref["half_idx"])
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    np.testing.assert_array_equal(h64(score), ref["score"])
+
+
 def test_search_all_ties(gpu_lib):
     # every score equal: each lane keeps only its first k records at the
     # threshold; the result is the k lowest composed indices
