@@ -606,26 +606,37 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
     bound = my_cnt - cnt0 >= (uint32_t)k ? next_up(lo) : bound;
   };
 
-  // ---- the three sweeps ----------------------------------------------------------
-  // 1. Chunks [0, P): group maxima only; their k-th largest is a first
-  //    threshold.  2. Chunks [P, nch): candidates against that threshold,
-  //    maxima still updated; then the final threshold (from the maxima over
-  //    all rows).  3. Chunks [0, P) again: candidates against the final
-  //    threshold.  Every score of the top k is at or above both thresholds,
-  //    so every one is collected; the products over [0, P) are computed
-  //    twice, bitwise alike.  P = half of the chunks (1.5 sweeps in all);
-  //    with k > 32 P = all of them (sweep 2 is empty).
-  const int P = KBIG ? nch : (nch + 1) / 2;
-  sweep(0, P, max_tile);
+  // ---- the sweeps ------------------------------------------------------------
+  // 1. Chunks [0, P1): group maxima only; their k-th largest is a first
+  //    threshold.  2. Chunks [P1, P2): candidates against it, maxima still
+  //    updated; a second threshold from the maxima so far.  3. Chunks
+  //    [P2, nch): candidates against that one; then the final threshold (the
+  //    maxima over all rows).  4. Chunks [0, P1) again: candidates against the
+  //    final threshold.  Every score of the top k is at or above each
+  //    threshold, so every one is collected; the products over [0, P1) are
+  //    computed twice, bitwise alike.  P2 = half of the chunks; P1 = a
+  //    quarter of them from 64 chunks (4096 sub-keys) up, 1.25 sweeps in all,
+  //    else P1 = P2 (step 2 empty, 1.5 sweeps): with fewer chunks the looser
+  //    first threshold and the extra one cost more than the quarter sweep
+  //    saves (measured).  With k > 32 both are all of them (one threshold
+  //    from all rows, then one filtering sweep).
+  const int P2 = KBIG ? nch : (nch + 1) / 2;
+  const int P1 = KBIG ? nch : nch >= 64 ? (nch + 3) / 4 : P2;
+  auto max_collect = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
+    max_tile(acc, c, half);
+    collect_tile(acc, c, half);
+  };
+  sweep(0, P1, max_tile);
   set_threshold(kth_of_maxima());
-  if (P < nch) {
-    sweep(P, nch, [&](const f32x16_t& acc, int c, int half) PK_INLINE {
-      max_tile(acc, c, half);
-      collect_tile(acc, c, half);
-    });
+  if (P1 < P2) {
+    sweep(P1, P2, max_collect);
     set_threshold(kth_of_maxima());
   }
-  sweep(0, P, collect_tile);
+  if (P2 < nch) {
+    sweep(P2, nch, max_collect);
+    set_threshold(kth_of_maxima());
+  }
+  sweep(0, P1, collect_tile);
   if (tok_ok) cnts[rid * 2 + kh] = my_cnt;
 }
 
