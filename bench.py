@@ -588,15 +588,15 @@ def main():
 
     # the scoring kernel computes the products of its first P1 sub-key chunks
     # twice (first threshold, then the final collection) and of the rest once:
-    # P1 = a quarter of the chunks from 64 chunks up, else half of them, all of
-    # them when k > 32 (2 sweeps); the MFMA work it executes is that multiple
-    # of the algorithmic flops priced above
+    # P1 = an eighth of the chunks from 128 chunks up, a quarter from 64, else
+    # half of them, all of them when k > 32 (2 sweeps); the MFMA work it
+    # executes is that multiple of the algorithmic flops priced above
     search_roof = bw("score_topk")
     if search_roof and search_roof["bound"] == "mfma":
         search_roof = dict(search_roof, candidate_records=records,
                            candidates_per_row=round(records / (T * H * 2), 2))
         nch = -(-wl.S // 64)
-        P = nch if wl.k > 32 else ((nch + 3) // 4 if nch >= 64 else (nch + 1) // 2)
+        P = nch if wl.k > 32 else ((nch + 7) // 8 if nch >= 128 else (nch + 3) // 4 if nch >= 64 else (nch + 1) // 2)
         sweeps = (nch + P) / nch
         search_roof = dict(search_roof, sweeps=round(sweeps, 4),
                            executed_TFLOPs=round(sweeps * search_roof["achieved"], 2))

@@ -67,6 +67,10 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 
 constexpr int CHUNK_ROWS = 64;  // sub-keys per LDS chunk = two MFMA tiles
+#ifndef PK_SCORE_SPLIT8
+#define PK_SCORE_SPLIT8 128  // chunks from which the first threshold takes an eighth of them
+#endif
+constexpr int SPLIT8 = PK_SCORE_SPLIT8;
 
 // Lambdas of the scoring kernel are always inlined: register arrays indexed
 // by their arguments must see those arguments as constants.
@@ -608,33 +612,30 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
 
   // ---- the sweeps ------------------------------------------------------------
   // 1. Chunks [0, P1): group maxima only; their k-th largest is a first
-  //    threshold.  2. Chunks [P1, P2): candidates against it, maxima still
-  //    updated; a second threshold from the maxima so far.  3. Chunks
-  //    [P2, nch): candidates against that one; then the final threshold (the
-  //    maxima over all rows).  4. Chunks [0, P1) again: candidates against the
-  //    final threshold.  Every score of the top k is at or above each
-  //    threshold, so every one is collected; the products over [0, P1) are
-  //    computed twice, bitwise alike.  P2 = half of the chunks; P1 = a
-  //    quarter of them from 64 chunks (4096 sub-keys) up, 1.25 sweeps in all,
-  //    else P1 = P2 (step 2 empty, 1.5 sweeps): with fewer chunks the looser
-  //    first threshold and the extra one cost more than the quarter sweep
-  //    saves (measured).  With k > 32 both are all of them (one threshold
+  //    threshold.  2. The rest in segments that double, [P1, 2 P1),
+  //    [2 P1, 4 P1), ...: candidates against the current threshold, maxima
+  //    still updated, then a new threshold from the maxima so far (after the
+  //    last segment, the final one from all rows).  3. Chunks [0, P1) again:
+  //    candidates against the final threshold.  Every score of the top k is
+  //    at or above each threshold, so every one is collected; the products
+  //    over [0, P1) are computed twice, bitwise alike.  P1 = half of the
+  //    chunks (1.5 sweeps) below 64 chunks, a quarter (1.25) from 64 and an
+  //    eighth (1.125) from SPLIT8 chunks up: with fewer chunks the looser
+  //    early thresholds and the extra ones cost more than the shorter first
+  //    sweep saves (measured).  With k > 32 P1 = all of them (one threshold
   //    from all rows, then one filtering sweep).
-  const int P2 = KBIG ? nch : (nch + 1) / 2;
-  const int P1 = KBIG ? nch : nch >= 64 ? (nch + 3) / 4 : P2;
+  const int P1 = KBIG ? nch : nch >= SPLIT8 ? (nch + 7) / 8 : nch >= 64 ? (nch + 3) / 4 : (nch + 1) / 2;
   auto max_collect = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
     max_tile(acc, c, half);
     collect_tile(acc, c, half);
   };
   sweep(0, P1, max_tile);
   set_threshold(kth_of_maxima());
-  if (P1 < P2) {
-    sweep(P1, P2, max_collect);
+  for (int lo_c = P1; lo_c < nch;) {
+    const int hi_c = 2 * lo_c < nch ? 2 * lo_c : nch;
+    sweep(lo_c, hi_c, max_collect);
     set_threshold(kth_of_maxima());
-  }
-  if (P2 < nch) {
-    sweep(P2, nch, max_collect);
-    set_threshold(kth_of_maxima());
+    lo_c = hi_c;
   }
   sweep(0, P1, collect_tile);
   if (tok_ok) cnts[rid * 2 + kh] = my_cnt;
