@@ -385,10 +385,13 @@ def main():
     pk.mem_timer_stop()
     launches = pk.mem_timer_read()
     # candidate records the scoring kernel wrote in the last step: the run
-    # counts follow the candidate slots in the search workspace (256 slots of
-    # 8 bytes per (token, head, half) row, each region 256-byte aligned)
-    cnt_off = (T * H * 2 * 256 * 8 + 255) // 256 * 256
-    records = int(ws_s[cnt_off:cnt_off + T * H * 2 * 8].view(torch.int32).sum().item())
+    # counts (one per run of 32 tokens, head and half) follow the candidate
+    # slots in the search workspace (256 slots of 8 bytes per (token, head,
+    # half) row, tokens rounded up to groups of 32, each region 256-byte
+    # aligned)
+    nruns = (T + 31) // 32 * H * 2
+    cnt_off = (nruns * 32 * 256 * 8 + 255) // 256 * 256
+    records = int(ws_s[cnt_off:cnt_off + nruns * 4].view(torch.int32).sum().item())
     ms_per_step = elapsed * 1e3 / args.steps
     log(f"[bench] {ms_per_step:.3f} ms/step")
 

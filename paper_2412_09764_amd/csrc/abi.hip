@@ -59,8 +59,10 @@ SearchWs search_ws(void* base, int64_t T, int H, int k) {
     off += align256(bytes);
     return at;
   };
+  // candidate runs come in groups of 32 tokens (one per scoring wave)
+  const size_t grows = (size_t)((T + 31) / 32) * 32 * H * 2;
   SearchWs w;
-  w.cand = reinterpret_cast<uint64_t*>(take(rows * pk::CAND_CAP * sizeof(uint64_t)));
+  w.cand = reinterpret_cast<uint64_t*>(take(grows * pk::CAND_CAP * sizeof(uint64_t)));
   w.cnts = reinterpret_cast<uint32_t*>(take(rows * 2 * sizeof(uint32_t)));
   w.thr = reinterpret_cast<float*>(take(rows * sizeof(float)));
   w.half_idx = reinterpret_cast<int32_t*>(take(rows * k * sizeof(int32_t)));

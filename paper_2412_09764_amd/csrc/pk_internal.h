@@ -22,8 +22,9 @@ class LaunchTimer {
   hipEvent_t stop_ = nullptr;
 };
 
-// Candidate slots kept per (token, head, half) between the filter pass and the
-// per-row sort of the search kernel.
+// Candidate slots kept per (token, head, half) between the filter passes and
+// the per-row sort of the search; the 32 rows of a scoring wave share one run
+// of 32 * CAND_CAP records.
 constexpr int CAND_CAP = 256;
 // Waves and tokens per workgroup of the scoring kernel (32 tokens per wave).
 #ifndef PK_SEARCH_WAVES
@@ -37,8 +38,10 @@ constexpr int SEARCH_TOK = 32 * SEARCH_WAVES;
 int cartesian_pairs(int k);
 
 // ---- search (search.hip) -------------------------------------------------
-// rows = T*H*2 (token, head, half) rows; cand = [rows, CAND_CAP] u64;
-// cnts = [rows, 2] u32 (candidates per run); thr = [rows] fp32 (each row's
+// rows = T*H*2 (token, head, half) rows; cand = one run of 32 * CAND_CAP u64
+// records per group of 32 tokens, head and half (ceil(T / 32) * H * 2 runs);
+// cnts = [rows, 2] u32 (records per run, in its first entries); thr = [rows]
+// fp32 (each row's
 // final threshold: no score below it can be selected);
 // ovf = [1 + rows] u32 (count, then overflowed row ids).
 // qstats (nullable) = per (token, head) query (mean, rstd): the scoring then

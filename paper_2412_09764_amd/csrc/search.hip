@@ -536,48 +536,49 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
   // compare per slot builds the lane's 16-bit candidate mask.  When any lane
   // has one, the lane's 16 scores go to its scratch in LDS and the wave takes
   // the candidates out in rounds, each lane its lowest remaining slot per
-  // round (index from the mask, score read back from LDS), appending one raw
-  // 64-bit (score, row) record per round to its run in memory: a tile costs
-  // a compare per slot and a few stores, the most any lane of the wave has
-  // candidates in it, rather than work per slot.  The run holds
-  // CAND_CAP / 2 records; a count past that sends the row to the rescan.
+  // round (index from the mask, score read back from LDS): a tile costs a
+  // compare per slot and as many stores as the most candidates any lane of
+  // the wave has in it, not work per slot.  Each round's records go to the
+  // wave's run packed across lanes (a lane's place is the number of lanes
+  // below it with a record), so the run is written in whole lines; a record
+  // is (row | lane << 16, raw fp32 score bits).  The run holds 32 * CAND_CAP
+  // records; past that the buffer bound drops stores, the count goes on and
+  // the wave's rows are rescanned exactly later.
   //
   // A lane meets the rows of one sweep in increasing index order, tile by
   // tile.  Once it holds k records taken against the current threshold, the
   // lowest of them, lo, is a bound of its own: a later score at or below lo
   // is beaten by all k of them (by score, or on a tie by their lower index),
   // so it cannot be selected, and the lane takes only scores above lo from
-  // then on.  Heavily tied rows (equal sub-keys) thus stay within their
-  // slots (at most k + 15 records per lane and sweep); the test runs once
-  // per tile.
-  constexpr uint32_t HALF_CAP = CAND_CAP / 2;
+  // then on; this holds across the segments of one pass, whose rows keep
+  // increasing.  Heavily tied rows (equal sub-keys) thus stay within bounds
+  // (at most k + 15 records per lane and pass); the test runs once per tile.
+  constexpr uint32_t RUN = 32 * CAND_CAP;  // records per wave run
   const size_t rid = ((size_t)(tok_ok ? tok : 0) * H + h) * 2 + p;
-  uint32_t my_cnt = 0;
+  const size_t wr = (((size_t)tile * SEARCH_WAVES + wave) * H + h) * 2 + p;  // this wave's run
+  uint32_t my_cnt = 0;  // records of this lane
   uint32_t cnt0 = 0;    // my_cnt when the threshold was last set
+  uint32_t wcnt = 0;    // records of the wave (uniform)
   float bound = INFINITY;
   float lo = INFINITY;  // lowest record taken against the current threshold
-  // The workgroup's candidate rows (its tokens, every head and half) as a
-  // buffer, so the stores take 32-bit offsets; this lane's run starts at
-  // my_off.
-  const int64_t tok0 = tile * SEARCH_TOK;
-  const int64_t ntile = ntok - tok0 < SEARCH_TOK ? ntok - tok0 : SEARCH_TOK;
-  uint64_t* const wg_cand = cand + (size_t)tok0 * H * 2 * CAND_CAP;
-  const __amdgpu_buffer_rsrc_t crs =
-      raw_buffer(wg_cand, (uint32_t)((size_t)ntile * H * 2 * CAND_CAP * sizeof(uint64_t)));
-  const uint32_t my_off =
-      (uint32_t)((((size_t)(wave * 32 + col) * H + h) * 2 + p) * CAND_CAP + kh * HALF_CAP) * 8u;
+  const __amdgpu_buffer_rsrc_t crs = raw_buffer(cand + wr * RUN, RUN * (uint32_t)sizeof(uint64_t));
   // This wave's scratch: slot j of lane l at float j * 64 + l (each slot's
   // write and each round's read are one conflict-free access).
   float* const xs = reinterpret_cast<float*>(xsmem + wave * XS_WAVE);
   // The last threshold set is the row's final one (what the sort keeps).
-  auto set_threshold = [&](float t) PK_INLINE {
-    bound = tok_ok ? t : INFINITY;  // scores are finite
-    lo = INFINITY;
-    cnt0 = my_cnt;
+  // The records behind lo stay valid while the rows go on increasing (the
+  // segments of one pass); restart when the next sweep begins again at row 0.
+  auto set_threshold = [&](float t, bool restart) PK_INLINE {
+    if (restart) {
+      lo = INFINITY;
+      cnt0 = my_cnt;
+    }
+    const float tb = tok_ok ? t : INFINITY;  // scores are finite
+    bound = my_cnt - cnt0 >= (uint32_t)k ? fmaxf(tb, next_up(lo)) : tb;
     if (tok_ok && kh == 0) thr[rid] = t;
   };
   auto collect_tile = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
-    const uint32_t r0 = (uint32_t)(c * CHUNK_ROWS + half * 32 + 4 * kh);
+    const uint32_t r0 = (uint32_t)(c * CHUNK_ROWS + half * 32 + 4 * kh) | ((uint32_t)lane << 16);
     uint32_t msk = 0;  // bit j: slot j is a candidate
     if (c < nfull) {
 #pragma unroll
@@ -585,29 +586,29 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
     } else {  // rows past S are no candidates
 #pragma unroll
       for (int j = 15; j >= 0; --j)
-        msk = msk * 2u + (uint32_t)(acc[j] >= bound && r0 + acc_row(j, 0) < (uint32_t)S);
+        msk = msk * 2u + (uint32_t)(acc[j] >= bound && (r0 & 0xFFFFu) + acc_row(j, 0) < (uint32_t)S);
     }
-    if (__builtin_amdgcn_ballot_w64(msk != 0) != 0) {  // uniform
+    uint64_t m = __builtin_amdgcn_ballot_w64(msk != 0);
+    if (m != 0) {  // uniform
 #pragma unroll
       for (int j = 0; j < 16; ++j) xs[j * WAVE + lane] = acc[j];
-      // a lane takes at most 16 records in the tile: unclamped when every
-      // lane has room for them
-      const bool room = __builtin_amdgcn_ballot_w64(my_cnt > HALF_CAP - 16u) == 0;
-      uint32_t ptr = my_off + my_cnt * 8u;
       do {
         const uint32_t j = (uint32_t)__builtin_ctz(msk | 0x8000u);  // any slot when msk is 0
         const float z = xs[j * WAVE + lane];
         if (msk != 0) {
-          const uint32_t at = room ? ptr : my_off + (my_cnt < HALF_CAP ? my_cnt : HALF_CAP - 1u) * 8u;
-          __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{r0 + j + (j & 12u), __float_as_uint(z)}, crs, at, 0, 0);
+          const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{r0 + j + (j & 12u), __float_as_uint(z)}, crs,
+                                                (wcnt + below) * 8u, 0, 0);
           ++my_cnt;
-          ptr += 8u;
           lo = min_med3(lo, z, ninf);
         }
+        wcnt += (uint32_t)__popcll(m);
         msk &= msk - 1u;
-      } while (__builtin_amdgcn_ballot_w64(msk != 0) != 0);
+        m = __builtin_amdgcn_ballot_w64(msk != 0);
+      } while (m != 0);
     }
-    bound = my_cnt - cnt0 >= (uint32_t)k ? next_up(lo) : bound;
+    bound = my_cnt - cnt0 >= (uint32_t)k ? fmaxf(bound, next_up(lo)) : bound;
   };
 
   // ---- the sweeps ------------------------------------------------------------
@@ -630,86 +631,105 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
     collect_tile(acc, c, half);
   };
   sweep(0, P1, max_tile);
-  set_threshold(kth_of_maxima());
+  set_threshold(kth_of_maxima(), true);
   for (int lo_c = P1; lo_c < nch;) {
     const int hi_c = 2 * lo_c < nch ? 2 * lo_c : nch;
     sweep(lo_c, hi_c, max_collect);
-    set_threshold(kth_of_maxima());
+    set_threshold(kth_of_maxima(), hi_c >= nch);  // the last: sweep 3 restarts at row 0
     lo_c = hi_c;
   }
   sweep(0, P1, collect_tile);
-  if (tok_ok) cnts[rid * 2 + kh] = my_cnt;
+  if (lane == 0) cnts[wr] = wcnt;
 }
 
-// Pass 3 as a kernel of its own: one wave per (token, head, half) row at a
-// time.  The row's candidates sit in two runs (c0 records at slot 0, c1 at
-// slot CAND_CAP / 2); lane l takes records l, l + 64, ... of their
-// concatenation.  Records below the row's final threshold (taken against the
-// first, looser one) cannot be selected and are dropped; when at most 64
-// remain (the usual case) they are compacted through LDS into one record per
-// lane, otherwise all are kept.  The wave then sorts them as (score desc,
-// index asc) keys and writes the first k.  A row with an overflowed run goes
-// to the rescan list.
+// Pass 3 as a kernel of its own: one workgroup per wave run (32 tokens of one
+// head and half).  Its records are read in order, those below their row's
+// final threshold (taken against a looser one) dropped, and the places of the
+// rest gathered into per-token buckets in LDS (16-bit record numbers, so the
+// buckets stay small and many workgroups share a CU); then each wave takes
+// tokens in turn, reads its records again (from L2), sorts them as
+// (score desc, index asc) keys and writes the first k.  A run past
+// its capacity, or a token with more than BCAP records at or above its
+// threshold, goes to the rescan list.
+constexpr int SORT_BCAP = 4 * WAVE;  // records a token may keep for the sort
 __global__ __launch_bounds__(256) void k_topk_sort(const uint64_t* __restrict__ cand,
                                                    const uint32_t* __restrict__ cnts,
                                                    const float* __restrict__ thr,
-                                                   int64_t rows, int k,
+                                                   int64_t ntok, int H, int k,
                                                    int32_t* __restrict__ half_idx,
                                                    float* __restrict__ half_score,
                                                    uint32_t* __restrict__ ovf) {
-  constexpr uint32_t HALF_CAP = CAND_CAP / 2;
-  constexpr int E = CAND_CAP / WAVE;
-  __shared__ uint64_t stage[4][WAVE];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  auto to_key = [](uint64_t raw) { return make_key(__uint_as_float(uint32_t(raw >> 32)), uint32_t(raw)); };
-  for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < rows; r += (int64_t)gridDim.x * 4) {
-    const uint32_t c0 = cnts[r * 2], c1 = cnts[r * 2 + 1];
-    if (c0 > HALF_CAP || c1 > HALF_CAP) {
-      if (lane == 0) {
-        const uint32_t slot = atomicAdd(&ovf[0], 1u);
-        ovf[1 + slot] = (uint32_t)r;
+  constexpr uint32_t RUN = 32 * CAND_CAP;
+  __shared__ uint16_t bucket[32][SORT_BCAP];
+  __shared__ uint32_t bcnt[32];
+  __shared__ float bthr[32];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t nruns = (ntok + 31) / 32 * H * 2;
+  for (int64_t wr = blockIdx.x; wr < nruns; wr += gridDim.x) {
+    const int p = (int)(wr & 1);
+    const int h = (int)((wr >> 1) % H);
+    const int64_t tok0 = (wr >> 1) / H * 32;
+    if (tid < 32) {
+      const int64_t t = tok0 + tid;
+      bcnt[tid] = 0;
+      bthr[tid] = t < ntok ? thr[((size_t)t * H + h) * 2 + p] : INFINITY;
+    }
+    __syncthreads();
+    const uint32_t c = cnts[wr];
+    const uint64_t* run = cand + (size_t)wr * RUN;
+    if (c <= RUN) {
+      for (uint32_t i = tid; i < c; i += 256) {
+        const uint64_t rec = run[i];
+        const uint32_t col = (uint32_t)(rec >> 16) & 31u;
+        const float z = __uint_as_float(uint32_t(rec >> 32));
+        if (z >= bthr[col]) {
+          const uint32_t slot = atomicAdd(&bcnt[col], 1u);
+          if (slot < (uint32_t)SORT_BCAP) bucket[col][slot] = (uint16_t)i;
+        }
       }
-      continue;
     }
-    const uint64_t* rc = cand + (size_t)r * CAND_CAP;
-    const uint32_t c = c0 + c1;
-    const float tr = thr[r];
-    uint64_t key[E];
-    bool keep[E];
-    uint32_t n = 0;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const uint32_t x = (uint32_t)(lane + e * WAVE);
-      uint64_t raw = 0;
-      if (x < c0) raw = rc[x];
-      else if (x - c0 < c1) raw = rc[HALF_CAP + x - c0];
-      const bool valid = x < c;
-      key[e] = valid ? to_key(raw) : 0ull;
-      keep[e] = valid && __uint_as_float(uint32_t(raw >> 32)) >= tr;
-      n += (uint32_t)__popcll(__ballot(keep[e]));
-    }
-    uint64_t top;
-    if (n <= (uint32_t)WAVE) {
-      uint32_t base = 0;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const uint64_t m = __ballot(keep[e]);
-        const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-        if (keep[e]) stage[wave][base + below] = key[e];
-        base += (uint32_t)__popcll(m);
+    __syncthreads();
+    for (int col = wave; col < 32; col += 4) {
+      const int64_t t = tok0 + col;
+      if (t >= ntok) break;  // the same for the whole wave
+      const size_t r = ((size_t)t * H + h) * 2 + p;
+      const uint32_t n = bcnt[col];
+      if (c > RUN || n > (uint32_t)SORT_BCAP) {
+        if (lane == 0) {
+          const uint32_t slot = atomicAdd(&ovf[0], 1u);
+          ovf[1 + slot] = (uint32_t)r;
+        }
+        continue;
       }
-      uint64_t v[1] = {(uint32_t)lane < n ? stage[wave][lane] : 0ull};
-      wave_sort_desc<1>(v, lane);
-      top = v[0];
-    } else {
-      wave_sort_desc<E>(key, lane);
-      top = key[0];
+      auto key_at = [&](uint32_t x) -> uint64_t {
+        if (x >= n) return 0ull;
+        const uint64_t rec = run[bucket[col][x]];
+        return make_key(__uint_as_float(uint32_t(rec >> 32)), (uint32_t)rec & 0xFFFFu);
+      };
+      uint64_t top;
+      if (n <= (uint32_t)WAVE) {
+        uint64_t v[1] = {key_at((uint32_t)lane)};
+        wave_sort_desc<1>(v, lane);
+        top = v[0];
+      } else if (n <= 2u * WAVE) {
+        uint64_t v[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) v[e] = key_at((uint32_t)(lane + e * WAVE));
+        wave_sort_desc<2>(v, lane);
+        top = v[0];
+      } else {
+        uint64_t v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = key_at((uint32_t)(lane + e * WAVE));
+        wave_sort_desc<4>(v, lane);
+        top = v[0];
+      }
+      if (lane < k) {
+        half_idx[r * k + lane] = (int32_t)key_index(top);
+        half_score[r * k + lane] = key_score(top);
+      }
     }
-    if (lane < k) {
-      half_idx[r * k + lane] = (int32_t)key_index(top);
-      half_score[r * k + lane] = key_score(top);
-    }
+    __syncthreads();  // the buckets are reused by the next run
   }
 }
 
@@ -958,12 +978,11 @@ static hipError_t launch_score(const void* q, const void* subkeys, int64_t T_, i
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   {
-    const int64_t rows = T_ * H * 2;
-    int64_t sb = (rows + 3) / 4;
+    int64_t sb = (T_ + 31) / 32 * H * 2;  // one workgroup per wave run
     if (sb > 16384) sb = 16384;
     LaunchTimer lt("topk_sort", st);
     hipLaunchKernelGGL(k_topk_sort, dim3((unsigned)sb), dim3(256), 0, st, (const uint64_t*)cand,
-                       (const uint32_t*)cnts, (const float*)thr, rows, k, half_idx, half_score, ovf);
+                       (const uint32_t*)cnts, (const float*)thr, T_, H, k, half_idx, half_score, ovf);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -397,13 +397,15 @@ def _search_overflow_count(q, K, k):
     rows sent to the exact rescan).  The count is the first word of the
     overflow list, whose offset mirrors the workspace layout of csrc/abi.hip
     (candidate slots, run counts, thresholds, half lists, overflow list, each
-    256-byte aligned; 256 candidate slots per (token, head, half) row)."""
+    256-byte aligned; 256 candidate slots per (token, head, half) row, for
+    tokens rounded up to whole groups of 32)."""
     import paper_2412_09764_amd as pk
     T, H, n = q.shape
     S = K.shape[2]
     rows = T * H * 2
+    grows = (T + 31) // 32 * 32 * H * 2
     a = lambda x: (x + 255) // 256 * 256  # noqa: E731
-    off = a(rows * 256 * 8) + a(rows * 2 * 4) + a(rows * 4) + 2 * a(rows * k * 4)
+    off = a(grows * 256 * 8) + a(rows * 2 * 4) + a(rows * 4) + 2 * a(rows * k * 4)
     ws = torch.zeros(pk.mem_search_workspace_size(T, H, S, k), dtype=torch.uint8, device="cuda")
     idx, w, score, hidx = pk.mem_search(q, K, k, want_half=True, workspace=ws)
     torch.cuda.synchronize()
