@@ -24,28 +24,31 @@
 //     below it can be selected.  It is found by sorting each lane's 32
 //     maxima and a binary search for the split between the two lanes'
 //     sorted runs (left in LDS).
-//   * Three sweeps, 1.5 passes over the sub-keys: the first half of the rows
-//     gives group maxima and a first threshold; the second half is filtered
-//     against that threshold while the maxima are completed, which gives the
-//     final threshold; the first half is then filtered against the final one
-//     (its products recomputed bitwise alike).  Every score at or above its
-//     threshold goes, as a raw 64-bit (score, index) record, to the row's
-//     candidate list (about 66 of 2048 at k = 32); the two lanes holding a
-//     token's rows own half of its CAND_CAP slots each.  A tile's candidates
-//     are found with one compare per slot into a per-lane mask and taken out
-//     in rounds (each lane its lowest remaining slot per round, the score
-//     read back from a per-wave LDS scratch), so the stores per tile are as
-//     many as the most candidates any lane has in it, not one per slot.  A
-//     count past capacity sends the row to the rescan.  A lane holding k
-//     records taken against the current threshold takes only scores above
-//     the lowest of them from then on (lower indices win ties), so rows of
-//     tied scores fit their slots.
+//   * Sweeps: the first P1 chunks of rows give group maxima and a first
+//     threshold; the rest, in doubling segments, are filtered against the
+//     current threshold while the maxima are completed (a new threshold
+//     after each segment, the last from all rows); the first P1 chunks are
+//     then filtered against the final one (their products recomputed bitwise
+//     alike).  P1 is half of the chunks (1.5 sweeps in all), a quarter from
+//     64 chunks and an eighth from SPLIT8 chunks up.  Every score at or above
+//     its threshold goes, as a raw 64-bit (row | lane << 16, score) record,
+//     to the wave's candidate run (about 65 per row of 2048 at k = 32).  A
+//     tile's candidates are found with one compare per slot into a per-lane
+//     mask and taken out in rounds (each lane its lowest remaining slot per
+//     round, the score read back from a per-wave LDS scratch), a round's
+//     records packed across lanes, so a tile costs as many stores as the most
+//     candidates any lane has in it, and the run is written in whole lines.
+//     A lane holding k records taken against the current threshold (within
+//     one pass over increasing rows) takes only scores above the lowest of
+//     them from then on (lower indices win ties), so rows of tied scores stay
+//     within bounds.
 //   * Pass 3, k_topk_sort, a kernel of its own (a sort needs few registers, so
-//     it runs at far higher occupancy than the scoring kernel): per row the
-//     records below the final threshold are dropped, the rest sorted by one
-//     wave, the first k written.  A row whose lane half overflowed its
-//     CAND_CAP / 2 slots is listed for k_topk_fallback, which rescans it
-//     exactly.
+//     it runs at far higher occupancy than the scoring kernel): per wave run
+//     the records below their row's final threshold are dropped, the rest
+//     bucketed by token in LDS, and each token's sorted by one wave, the
+//     first k written.  A run past its capacity, or a token with more than
+//     256 records at its threshold, is listed for k_topk_fallback, which
+//     rescans the row exactly.
 //   * With query normalisation (qk-normalisation, Sec. 3.1.4) k_qnorm first
 //     computes each (token, head) query's mean and rstd = 1/sqrt(var + eps)
 //     (LayerNorm without affine, fp32, centred second pass); the scoring
