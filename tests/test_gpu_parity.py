@@ -362,6 +362,29 @@ def test_search_overflow_goes_to_the_exact_rescan(gpu_lib):
                                   np.broadcast_to(np.arange(63, 63 - k, -1) * 64, (T, H, k)))
 
 
+def test_search_run_overflow_is_rescanned(gpu_lib):
+    """Every row of the 32 best groups scores just below its group's maximum,
+    so about 2,000 scores per row lie at or above the final threshold: each
+    wave's candidate run (32 * 256 records) overflows and each token's rows
+    exceed the sort's 256, and every row goes to the exact rescan, which must
+    still select exactly.  fp32 keys make every score distinct."""
+    T, H, S, n, k = 64, 1, 4096, 8, 32
+    d = n // 2
+    q = torch.zeros((T, H, n), dtype=torch.float32)
+    q[:, :, 0] = 1.0
+    q[:, :, d] = 1.0
+    rows = torch.arange(S, dtype=torch.float32)
+    K = torch.zeros((H, 2, S, d), dtype=torch.float32)
+    K[:, 0, :, 0] = 100.0 * (rows % 64) + rows / 4096
+    K[:, 1, :, 0] = 100.0 * (rows % 64) - rows / 4096
+    print("[search-run-overflow]", flush=True)
+    idx, hidx, nov = _search_overflow_count(q.cuda(), K.cuda(), k)
+    ref = oracle.search(h64(q), h64(K), k)
+    assert nov == T * H * 2, f"{nov} of {T * H * 2} rows rescanned"
+    np.testing.assert_array_equal(hidx.cpu().numpy(), ref["half_idx"])
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+
+
 @pytest.mark.parametrize("k", [48, 64])
 def test_search_all_ties_large_k(gpu_lib, k):
     """k > 32: a lane counts the records equal to the threshold one by one and
