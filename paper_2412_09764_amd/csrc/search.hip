@@ -234,16 +234,50 @@ __device__ __forceinline__ float f16_step_down(float t) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)r);
 }
 
-// (m << 1) | (z >= b): one compare into vcc and one add with carry (the two
-// wait states between them are the hardware's for a VALU read of vcc that
-// a VALU wrote).
-__device__ __forceinline__ uint32_t mask_step(uint32_t m, float z, float b) {
-  uint64_t carry;
-  asm("v_cmp_ge_f32 vcc, %[z], %[b]\n\t"
-      "s_nop 1\n\t"
-      "v_addc_co_u32_e64 %[m], %[c], %[m], %[m], vcc"
-      : [m] "+v"(m), [c] "=s"(carry)
-      : [z] "v"(z), [b] "v"(b)
+// Bit j of the result is acc[j] >= b. Sixteen compares into three rotating
+// SGPR pairs, each consumed by an add with carry (m + m + c) two VALU
+// instructions after it was written: the hardware's wait states between a
+// VALU write of an SGPR and a VALU read of it are covered by independent work
+// instead of s_nop.
+__device__ __forceinline__ uint32_t mask16(const f32x16_t& acc, float b) {
+  uint32_t m;
+  uint64_t c0, c1, c2;
+  asm(
+      "v_cmp_ge_f32_e64 %[c0], %[z15], %[b]\n\t"
+      "v_cmp_ge_f32_e64 %[c1], %[z14], %[b]\n\t"
+      "v_cmp_ge_f32_e64 %[c2], %[z13], %[b]\n\t"
+      "v_cndmask_b32_e64 %[m], 0, 1, %[c0]\n\t"
+      "v_cmp_ge_f32_e64 %[c0], %[z12], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c1]\n\t"
+      "v_cmp_ge_f32_e64 %[c1], %[z11], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c2]\n\t"
+      "v_cmp_ge_f32_e64 %[c2], %[z10], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c0]\n\t"
+      "v_cmp_ge_f32_e64 %[c0], %[z9], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c1]\n\t"
+      "v_cmp_ge_f32_e64 %[c1], %[z8], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c2]\n\t"
+      "v_cmp_ge_f32_e64 %[c2], %[z7], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c0]\n\t"
+      "v_cmp_ge_f32_e64 %[c0], %[z6], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c1]\n\t"
+      "v_cmp_ge_f32_e64 %[c1], %[z5], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c2]\n\t"
+      "v_cmp_ge_f32_e64 %[c2], %[z4], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c0]\n\t"
+      "v_cmp_ge_f32_e64 %[c0], %[z3], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c1]\n\t"
+      "v_cmp_ge_f32_e64 %[c1], %[z2], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c2]\n\t"
+      "v_cmp_ge_f32_e64 %[c2], %[z1], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c0]\n\t"
+      "v_cmp_ge_f32_e64 %[c0], %[z0], %[b]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c1]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c2]\n\t"
+      "v_addc_co_u32_e64 %[m], vcc, %[m], %[m], %[c0]"
+      : [m] "=&v"(m), [c0] "=&s"(c0), [c1] "=&s"(c1), [c2] "=&s"(c2)
+      : [b] "v"(b),
+        [z0] "v"(acc[0]), [z1] "v"(acc[1]), [z2] "v"(acc[2]), [z3] "v"(acc[3]), [z4] "v"(acc[4]), [z5] "v"(acc[5]), [z6] "v"(acc[6]), [z7] "v"(acc[7]), [z8] "v"(acc[8]), [z9] "v"(acc[9]), [z10] "v"(acc[10]), [z11] "v"(acc[11]), [z12] "v"(acc[12]), [z13] "v"(acc[13]), [z14] "v"(acc[14]), [z15] "v"(acc[15])
       : "vcc");
   return m;
 }
@@ -332,14 +366,18 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
   // lane's 16 bytes going to LDS at base + 16*lane.  Rows past S and padded
   // columns read a valid (finite) sub-key element instead: padded columns
   // meet zero query entries and rows past S are masked out.
-  // The lane's source element offsets within a chunk are the same for every
-  // chunk: computed once, so a chunk whose rows all exist costs one address
-  // add per load; the last, partial chunk clamps rows as it goes.
+  // The lane's source offsets within a chunk are the same for every chunk.
+  // When load j's rows are load 0's moved down by a multiple of the swizzle
+  // period (true for the usual sizes), its lane offset is load 0's and the
+  // move goes into the scalar offset: a chunk whose rows all exist costs one
+  // lane offset for all its loads.  The last, partial chunk clamps rows as it
+  // goes.
   constexpr int NDMA = (NCOL + SEARCH_WAVES - 1) / SEARCH_WAVES;  // loads per wave, at most
+  constexpr int RSTEP = (SEARCH_WAVES * WAVE) / NCOL;             // rows between loads j and j + 1
+  constexpr bool SHIFTED = (SEARCH_WAVES * WAVE) % NCOL == 0 && (RSTEP & SWZ) == 0;
   // The (head, half) table as a raw buffer: S rows of d elements.
   const __amdgpu_buffer_rsrc_t ktab = raw_buffer(kbase, (uint32_t)((size_t)S * d * M::ESIZE));
-  // Byte offset of the lane's segment j within a chunk (recomputed at every
-  // chunk rather than held in registers).
+  // Byte offset of the lane's segment j within a chunk.
   auto src_off = [&](int j) PK_INLINE {
     const int i = wave + j * SEARCH_WAVES;
     const int sidx = i * WAVE + lane;
@@ -353,10 +391,20 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
   auto issue_chunk = [&](int c, unsigned char* buf) PK_INLINE {
     if (c < nfull_rows) {
       const uint32_t cb = (uint32_t)((size_t)c * CHUNK_ROWS * d * M::ESIZE);
+      if constexpr (SHIFTED) {
+        const uint32_t o0 = src_off(0);
 #pragma unroll
-      for (int j = 0; j < NDMA; ++j) {
-        const int i = wave + j * SEARCH_WAVES;
-        if (NCOL % SEARCH_WAVES == 0 || i < NCOL) lds_dma16_buf(ktab, src_off(j), cb, &buf[i * WAVE * 16]);
+        for (int j = 0; j < NDMA; ++j) {
+          const int i = wave + j * SEARCH_WAVES;
+          if (NCOL % SEARCH_WAVES == 0 || i < NCOL)
+            lds_dma16_buf(ktab, o0, cb + (uint32_t)(j * RSTEP * d * M::ESIZE), &buf[i * WAVE * 16]);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < NDMA; ++j) {
+          const int i = wave + j * SEARCH_WAVES;
+          if (NCOL % SEARCH_WAVES == 0 || i < NCOL) lds_dma16_buf(ktab, src_off(j), cb, &buf[i * WAVE * 16]);
+        }
       }
       return;
     }
@@ -559,8 +607,7 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
   constexpr uint32_t RUN = 32 * CAND_CAP;  // records per wave run
   const size_t rid = ((size_t)(tok_ok ? tok : 0) * H + h) * 2 + p;
   const size_t wr = (((size_t)tile * SEARCH_WAVES + wave) * H + h) * 2 + p;  // this wave's run
-  uint32_t my_cnt = 0;  // records of this lane
-  uint32_t cnt0 = 0;    // my_cnt when the threshold was last set
+  uint32_t taken = 0;   // records of this lane since the last restart
   uint32_t wcnt = 0;    // records of the wave (uniform)
   float bound = INFINITY;
   float lo = INFINITY;  // lowest record taken against the current threshold
@@ -574,18 +621,17 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
   auto set_threshold = [&](float t, bool restart) PK_INLINE {
     if (restart) {
       lo = INFINITY;
-      cnt0 = my_cnt;
+      taken = 0;
     }
     const float tb = tok_ok ? t : INFINITY;  // scores are finite
-    bound = my_cnt - cnt0 >= (uint32_t)k ? fmaxf(tb, next_up(lo)) : tb;
+    bound = taken >= (uint32_t)k ? fmaxf(tb, next_up(lo)) : tb;
     if (tok_ok && kh == 0) thr[rid] = t;
   };
   auto collect_tile = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
     const uint32_t r0 = (uint32_t)(c * CHUNK_ROWS + half * 32 + 4 * kh) | ((uint32_t)lane << 16);
     uint32_t msk = 0;  // bit j: slot j is a candidate
     if (c < nfull) {
-#pragma unroll
-      for (int j = 15; j >= 0; --j) msk = mask_step(msk, acc[j], bound);
+      msk = mask16(acc, bound);
     } else {  // rows past S are no candidates
 #pragma unroll
       for (int j = 15; j >= 0; --j)
@@ -603,7 +649,7 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
           __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{r0 + j + (j & 12u), __float_as_uint(z)}, crs,
                                                 (wcnt + below) * 8u, 0, 0);
-          ++my_cnt;
+          ++taken;
           lo = min_med3(lo, z, ninf);
         }
         wcnt += (uint32_t)__popcll(m);
@@ -611,7 +657,7 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
         m = __builtin_amdgcn_ballot_w64(msk != 0);
       } while (m != 0);
     }
-    bound = my_cnt - cnt0 >= (uint32_t)k ? fmaxf(bound, next_up(lo)) : bound;
+    bound = taken >= (uint32_t)k ? fmaxf(bound, next_up(lo)) : bound;
   };
 
   // ---- the sweeps ------------------------------------------------------------
