@@ -292,25 +292,32 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
     float* __restrict__ thr) {
   using M = MfmaOp<T>;
   constexpr int DPAD = NSTEP * M::KSTEP;      // padded half dim
-  constexpr int RB = DPAD * M::ESIZE;         // bytes per sub-key row in LDS
+  constexpr int RB = DPAD * M::ESIZE;         // bytes of a sub-key row
   constexpr int NCOL = RB / 16;               // 16-byte segments per row
-  constexpr int SWZ = (NCOL < 16 ? NCOL : 16) - 1;
+  constexpr int NSLOT = NCOL + 1;             // 16-byte slots per row in LDS (one spare)
+  constexpr int RBP = NSLOT * 16;             // row pitch in LDS
   constexpr int EPS = 16 / M::ESIZE;          // elements per segment
-  constexpr int CBYTES = CHUNK_ROWS * RB;
+  constexpr int CBYTES = CHUNK_ROWS * RBP;
+  constexpr int NDMA = (NSLOT + SEARCH_WAVES - 1) / SEARCH_WAVES;  // loads per wave and chunk, at most
 
-  // Sub-key chunks of 64 rows, double buffered.  Segment (row, col) of a chunk
-  // sits at row * RB + (col ^ (row & SWZ)) * 16: rows that the same fragment
-  // read touches land in different banks without padding, which keeps every
-  // wave's 1 KiB of a chunk contiguous for the direct global -> LDS loads.
-  // The two buffers are statically named arrays, so LDS accesses elsewhere
-  // never wait on the copies in flight.  Each wave also has a scratch for
-  // taking candidates out of a tile (64 lanes x 16 fp32 scores), which
-  // between sweeps holds each lane's sorted group maxima (32 16-bit floats)
-  // for the threshold.
+  // Sub-key chunks of 64 rows, double buffered, each row followed by a spare
+  // 16-byte slot: with a pitch of an odd number of 16-byte slots, the 16
+  // consecutive rows that one fragment read touches start in 16 different
+  // bank groups, and a fragment's address is the lane's row address plus a
+  // constant per step (the instruction's offset field: no address arithmetic
+  // in the product loop).  The direct global -> LDS loads fill 64 consecutive
+  // slots each, spare ones included (they receive a copy of the row's last
+  // segment, never read).  The two buffers are statically named arrays, so
+  // LDS accesses elsewhere never wait on the copies in flight.  Each wave
+  // also has a scratch for taking candidates out of a tile (64 lanes x 16
+  // fp32 scores), which between sweeps holds each lane's sorted group maxima
+  // (32 16-bit floats) for the threshold, and a table of its lanes' source
+  // offsets for the loads.
   constexpr int XS_WAVE = WAVE * 16 * 4;
   __shared__ __align__(1024) unsigned char kbuf0[CBYTES];
   __shared__ __align__(1024) unsigned char kbuf1[CBYTES];
   __shared__ __align__(16) unsigned char xsmem[SEARCH_WAVES * XS_WAVE];
+  __shared__ uint32_t dtab[NDMA * SEARCH_WAVES * WAVE];
 
   const int d = n >> 1;
   const int HP = 2 * H;
@@ -362,104 +369,81 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
     if (kh == 0 && tok_ok) sink_part[((size_t)tok * H + h) * 2 + p] = part;
   }
 
-  // Chunk c into buffer b: 64*NCOL segments, 64 per wave instruction, each
-  // lane's 16 bytes going to LDS at base + 16*lane.  Rows past S and padded
-  // columns read a valid (finite) sub-key element instead: padded columns
-  // meet zero query entries and rows past S are masked out.
-  // The lane's source offsets within a chunk are the same for every chunk.
-  // When load j's rows are load 0's moved down by a multiple of the swizzle
-  // period (true for the usual sizes), its lane offset is load 0's and the
-  // move goes into the scalar offset: a chunk whose rows all exist costs one
-  // lane offset for all its loads.  The last, partial chunk clamps rows as it
-  // goes.
-  constexpr int NDMA = (NCOL + SEARCH_WAVES - 1) / SEARCH_WAVES;  // loads per wave, at most
-  constexpr int RSTEP = (SEARCH_WAVES * WAVE) / NCOL;             // rows between loads j and j + 1
-  constexpr bool SHIFTED = (SEARCH_WAVES * WAVE) % NCOL == 0 && (RSTEP & SWZ) == 0;
+  // Chunk c into buffer b: 64*NSLOT slots, 64 per wave instruction, each
+  // lane's 16 bytes going to LDS at base + 16*lane.  Padded columns read a
+  // valid (finite) sub-key element instead (they meet zero query entries);
+  // the last, partial chunk reads row S - 1 in place of rows past S (masked
+  // out later).
   // The (head, half) table as a raw buffer: S rows of d elements.
   const __amdgpu_buffer_rsrc_t ktab = raw_buffer(kbase, (uint32_t)((size_t)S * d * M::ESIZE));
-  // Byte offset of the lane's segment j within a chunk.
-  auto src_off = [&](int j) PK_INLINE {
-    const int i = wave + j * SEARCH_WAVES;
-    const int sidx = i * WAVE + lane;
-    const int r = sidx / NCOL, pc = sidx % NCOL;
-    const int lc = pc ^ (r & SWZ);
-    int e0 = lc * EPS;
+  // Offset in a chunk of the sub-key bytes for slot t (row t / NSLOT, spare
+  // slots repeating the row's last segment).
+  auto slot_src = [&](int t, int& r) PK_INLINE {
+    r = t / NSLOT;
+    int g = t - r * NSLOT;
+    g = g < NCOL ? g : NCOL - 1;
+    int e0 = g * EPS;
     e0 = e0 < d ? e0 : 0;
-    return (uint32_t)((r * d + e0) * M::ESIZE);
+    return e0 * M::ESIZE;
   };
+  // The lane's source offsets within a chunk are the same for every chunk:
+  // computed once into the table in LDS (read back by the lane itself), so a
+  // chunk whose rows all exist costs one LDS read per load and no vector
+  // arithmetic.
+#pragma unroll
+  for (int j = 0; j < NDMA; ++j) {
+    const int i = wave + j * SEARCH_WAVES;
+    if (i < NSLOT) {
+      int r;
+      const int eb = slot_src(i * WAVE + lane, r);
+      dtab[j * SEARCH_WAVES * WAVE + tid] = (uint32_t)(r * d * M::ESIZE + eb);
+    }
+  }
   const int nfull_rows = S / CHUNK_ROWS;  // chunks whose 64 rows all exist
   auto issue_chunk = [&](int c, unsigned char* buf) PK_INLINE {
     if (c < nfull_rows) {
       const uint32_t cb = (uint32_t)((size_t)c * CHUNK_ROWS * d * M::ESIZE);
-      if constexpr (SHIFTED) {
-        const uint32_t o0 = src_off(0);
 #pragma unroll
-        for (int j = 0; j < NDMA; ++j) {
-          const int i = wave + j * SEARCH_WAVES;
-          if (NCOL % SEARCH_WAVES == 0 || i < NCOL)
-            lds_dma16_buf(ktab, o0, cb + (uint32_t)(j * RSTEP * d * M::ESIZE), &buf[i * WAVE * 16]);
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < NDMA; ++j) {
-          const int i = wave + j * SEARCH_WAVES;
-          if (NCOL % SEARCH_WAVES == 0 || i < NCOL) lds_dma16_buf(ktab, src_off(j), cb, &buf[i * WAVE * 16]);
-        }
+      for (int j = 0; j < NDMA; ++j) {
+        const int i = wave + j * SEARCH_WAVES;
+        if (NSLOT % SEARCH_WAVES == 0 || i < NSLOT)
+          lds_dma16_buf(ktab, dtab[j * SEARCH_WAVES * WAVE + tid], cb, &buf[i * WAVE * 16]);
       }
       return;
     }
-    for (int i = wave; i < NCOL; i += SEARCH_WAVES) {
-      const int sidx = i * WAVE + lane;
-      const int r = sidx / NCOL, pc = sidx % NCOL;
-      const int lc = pc ^ (r & SWZ);
+    for (int i = wave; i < NSLOT; i += SEARCH_WAVES) {
+      int r;
+      const int eb = slot_src(i * WAVE + lane, r);
       int row = c * CHUNK_ROWS + r;
       row = row < S ? row : S - 1;
-      int e0 = lc * EPS;
-      e0 = e0 < d ? e0 : 0;
-      lds_dma16_buf(ktab, (uint32_t)(((size_t)row * d + e0) * M::ESIZE), 0u, &buf[i * WAVE * 16]);
+      lds_dma16_buf(ktab, (uint32_t)((size_t)row * d * M::ESIZE + eb), 0u, &buf[i * WAVE * 16]);
     }
   };
   // ---- the sweeps -----------------------------------------------------------
   // A sweep visits every 32-row tile once, in row order.  Tile t is one chain
   // of NSTEP dependent MFMAs into the accumulator (fragments read from LDS
   // LEAD steps ahead of their use), then the pass filters its 16 slots per
-  // lane.  Four waves share each SIMD (two workgroups per CU), so one wave's
-  // filtering and waits run while the others' products occupy the matrix
-  // pipe.  Chunks of two tiles alternate between the two LDS buffers
+  // lane.  Four waves share each SIMD (one 16-wave workgroup per CU), so one
+  // wave's filtering and waits run while the others' products occupy the
+  // matrix pipe.  Chunks of two tiles alternate between the two LDS buffers
   // (unrolled by two so every access names its buffer statically).
-  // Byte offset in LDS of the lane's fragment of step s: row col of the tile,
-  // reduction elements from s * KSTEP + kh * LANE_K, through the swizzle.
-  // It equals lane_addr ^ step_xor(s) with a lane-independent step_xor (the
-  // lane's part, col * RB, kh and the swizzle, occupies bits the step's part
-  // does not carry into), so each step costs one XOR instead of a register
-  // held per step.
-  auto frag_off = [&](int s, int kh_, int col_) PK_INLINE {
-    const int e = s * M::KSTEP + kh_ * M::LANE_K;  // first reduction element of the fragment
-    const int seg = (e * M::ESIZE) >> 4;
-    const int within = (e * M::ESIZE) & 15;
-    return ((seg ^ (col_ & SWZ)) << 4) + within;
-  };
-  const uint32_t lane_addr = (uint32_t)(col * RB + frag_off(0, kh, col));
-  auto step_addr = [&](int s) PK_INLINE {
-    uint32_t a;
-    // volatile: formed at its use rather than hoisted into a register per step
-    asm volatile("v_xor_b32 %0, %1, %2" : "=v"(a) : "i"(frag_off(s, 0, 0)), "v"(lane_addr));
-    return a;
-  };
+  // The lane's fragment of step s: row col of the tile, reduction elements
+  // from s * KSTEP + kh * LANE_K, at lane_addr + s * KSTEP * ESIZE.
+  const uint32_t lane_addr = (uint32_t)(col * RBP + kh * M::LANE_K * M::ESIZE);
   constexpr int LEAD = PK_SCORE_PREFETCH > 0 ? PK_SCORE_PREFETCH : 1;
   const int nch = (S + CHUNK_ROWS - 1) / CHUNK_ROWS;
   const int nfull = S / CHUNK_ROWS;  // chunks with all 64 rows valid
 
   // Rows half*32 .. half*32 + 31 of the chunk in buf into acc.
   auto run_tile = [&](const unsigned char* buf, int half, f32x16_t& acc) PK_INLINE {
-    const unsigned char* rp = buf + half * 32 * RB;
+    const unsigned char* rp = buf + half * 32 * RBP + lane_addr;
     acc = f32x16_t{};
     typename M::frag ring[LEAD + 1];
 #pragma unroll
-    for (int s = 0; s < LEAD && s < NSTEP; ++s) ring[s] = M::load(rp + step_addr(s));
+    for (int s = 0; s < LEAD && s < NSTEP; ++s) ring[s] = M::load(rp + s * M::KSTEP * M::ESIZE);
 #pragma unroll
     for (int s = 0; s < NSTEP; ++s) {
-      if (s + LEAD < NSTEP) ring[(s + LEAD) % (LEAD + 1)] = M::load(rp + step_addr(s + LEAD));
+      if (s + LEAD < NSTEP) ring[(s + LEAD) % (LEAD + 1)] = M::load(rp + (s + LEAD) * M::KSTEP * M::ESIZE);
       __builtin_amdgcn_sched_barrier(0);  // reads stay LEAD steps ahead of their use
       acc = M::mma(ring[s % (LEAD + 1)], bq[s], acc);
       __builtin_amdgcn_sched_barrier(0);
