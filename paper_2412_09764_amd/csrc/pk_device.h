@@ -350,9 +350,29 @@ __device__ __forceinline__ void merge_desc_regs(float (&v)[N], float pinf, float
   }
 }
 
+// Lanes l with (l & m) == 0, for m a power of two up to 32.
+__device__ __forceinline__ constexpr uint64_t lanes_bit_clear(int m) {
+  return m == 1    ? 0x5555555555555555ull
+         : m == 2  ? 0x3333333333333333ull
+         : m == 4  ? 0x0F0F0F0F0F0F0F0Full
+         : m == 8  ? 0x00FF00FF00FF00FFull
+         : m == 16 ? 0x0000FFFF0000FFFFull
+                   : 0x00000000FFFFFFFFull;
+}
+// Per-lane choice between a (bit clear) and b (bit set) by a lane mask held
+// in scalar registers.
+__device__ __forceinline__ uint32_t sel_lanes(uint32_t a, uint32_t b, uint64_t m) {
+  uint32_t r;
+  asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "s"(m));
+  return r;
+}
+
 // Bitonic sort, descending, of 64*E keys held by one wave: element
 // e = r * 64 + lane lives in v[r] of that lane.  Afterwards element 0
-// (lane 0, v[0]) is the largest.
+// (lane 0, v[0]) is the largest.  A compare-exchange across lanes is one
+// 64-bit compare into a lane mask, a scalar XNOR with the constant mask of
+// lanes that keep the larger key, and two selects.  Every lane of the wave
+// must be active.
 template <int E>
 __device__ __forceinline__ void wave_sort_desc(uint64_t (&v)[E], int lane) {
 #pragma unroll
@@ -376,9 +396,16 @@ __device__ __forceinline__ void wave_sort_desc(uint64_t (&v)[E], int lane) {
 #pragma unroll
         for (int r = 0; r < E; ++r) {
           const uint64_t p = shfl_xor_u64(v[r], stride);
-          const bool desc = ((r * WAVE + lane) & size) == 0;
-          const bool lower = (lane & stride) == 0;
-          v[r] = (lower == desc) ? umax64(v[r], p) : umin64(v[r], p);
+          // lanes sorting their group of `size` descending; the lower lane of
+          // each pair keeps the larger key there, the upper one elsewhere
+          const uint64_t desc = size < WAVE ? lanes_bit_clear(size)
+                                            : (((r * WAVE) & size) == 0 ? ~0ull : 0ull);
+          const uint64_t keep_max = ~(lanes_bit_clear(stride) ^ desc);
+          const uint64_t gt = __builtin_amdgcn_ballot_w64(v[r] > p);
+          const uint64_t own = ~(gt ^ keep_max);
+          const uint32_t lo = sel_lanes(uint32_t(p), uint32_t(v[r]), own);
+          const uint32_t hi = sel_lanes(uint32_t(p >> 32), uint32_t(v[r] >> 32), own);
+          v[r] = (uint64_t(hi) << 32) | lo;
         }
       }
     }
