@@ -240,7 +240,9 @@ __device__ __forceinline__ uint32_t key_index(uint64_t key) { return ~uint32_t(k
 
 // ---------------------------------------------------------- shuffles ----
 // Value of lane (lane ^ MASK) for a constant MASK.  Distances 1 and 2 are DPP
-// quad permutations (a VALU operand modifier), 4, 8 and 16 are ds_swizzle in
+// quad permutations (a VALU operand modifier); 4 is two DPP row shifts, each
+// writing the 4-lane banks that take it (+4 for banks 0 and 2, -4 for 1 and
+// 3); 8 is a DPP rotation of each 16-lane row by 8; 16 is ds_swizzle in
 // bit-mask mode (xor within 32 lanes: no address operand, no LDS access);
 // only 32 takes a ds_bpermute.
 template <int MASK>
@@ -250,7 +252,12 @@ __device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
   } else if constexpr (MASK == 2) {
     return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
-  } else if constexpr (MASK <= 16) {
+  } else if constexpr (MASK == 4) {
+    const int up = __builtin_amdgcn_update_dpp((int)v, (int)v, 0x104, 0xF, 0x5, false);  // row_shl:4
+    return (uint32_t)__builtin_amdgcn_update_dpp(up, (int)v, 0x114, 0xF, 0xA, false);    // row_shr:4
+  } else if constexpr (MASK == 8) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, false);  // row_ror:8
+  } else if constexpr (MASK == 16) {
     return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x1F | (MASK << 10));  // and 0x1f, xor MASK
   } else {
     return __shfl_xor(v, MASK, WAVE);
