@@ -590,7 +590,9 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
   // (at most k + 15 records per lane and pass); the test runs once per tile.
   constexpr uint32_t RUN = 32 * CAND_CAP;  // records per wave run
   const size_t rid = ((size_t)(tok_ok ? tok : 0) * H + h) * 2 + p;
-  const size_t wr = (((size_t)tile * SEARCH_WAVES + wave) * H + h) * 2 + p;  // this wave's run
+  // this wave's run (the wave index taken as uniform, so the run's buffer
+  // resource lives in scalar registers as the store instruction needs)
+  const size_t wr = (((size_t)tile * SEARCH_WAVES + __builtin_amdgcn_readfirstlane(wave)) * H + h) * 2 + p;
   uint32_t taken = 0;   // records of this lane since the last restart
   uint32_t wcnt = 0;    // records of the wave (uniform)
   float bound = INFINITY;
