@@ -627,19 +627,34 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
     if (m != 0) {  // uniform
 #pragma unroll
       for (int j = 0; j < 16; ++j) xs[j * WAVE + lane] = acc[j];
-      do {
-        const uint32_t j = (uint32_t)__builtin_ctz(msk | 0x8000u);  // any slot when msk is 0
-        const float z = xs[j * WAVE + lane];
+      do {  // two candidates per lane and round: their LDS reads in flight together
+        const uint32_t m1 = msk & (msk - 1u);
+        const uint32_t j0 = (uint32_t)__builtin_ctz(msk | 0x8000u);  // any slot when none
+        const uint32_t j1 = (uint32_t)__builtin_ctz(m1 | 0x8000u);
+        const float z0 = xs[j0 * WAVE + lane];
+        const float z1 = xs[j1 * WAVE + lane];
+        const uint64_t m2 = __builtin_amdgcn_ballot_w64(m1 != 0);  // lanes with a second one
+        // records of the lanes below: one per lane with a candidate, one more
+        // per lane with a second
+        const uint32_t below =
+            __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u)) +
+            __builtin_amdgcn_mbcnt_hi((uint32_t)(m2 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m2, 0u));
+        const uint32_t at = (wcnt + below) * 8u;
+        asm volatile("" ::"v"(z0), "v"(z1));  // both reads issued before either store
         if (msk != 0) {
-          const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-          __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{r0 + j + (j & 12u), __float_as_uint(z)}, crs,
-                                                (wcnt + below) * 8u, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{r0 + j0 + (j0 & 12u), __float_as_uint(z0)}, crs, at,
+                                                0, 0);
           ++taken;
-          lo = min_med3(lo, z, ninf);
+          lo = min_med3(lo, z0, ninf);
         }
-        wcnt += (uint32_t)__popcll(m);
-        msk &= msk - 1u;
+        if (m1 != 0) {
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{r0 + j1 + (j1 & 12u), __float_as_uint(z1)}, crs,
+                                                at + 8u, 0, 0);
+          ++taken;
+          lo = min_med3(lo, z1, ninf);
+        }
+        wcnt += (uint32_t)(__popcll(m) + __popcll(m2));
+        msk = m1 & (m1 - 1u);
         m = __builtin_amdgcn_ballot_w64(msk != 0);
       } while (m != 0);
     }
