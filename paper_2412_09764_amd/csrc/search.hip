@@ -728,13 +728,23 @@ __global__ __launch_bounds__(256) void k_topk_sort(const uint64_t* __restrict__ 
     const uint32_t c = cnts[wr];
     const uint64_t* run = cand + (size_t)wr * RUN;
     if (c <= RUN) {
-      for (uint32_t i = tid; i < c; i += 256) {
-        const uint64_t rec = run[i];
-        const uint32_t col = (uint32_t)(rec >> 16) & 31u;
-        const float z = __uint_as_float(uint32_t(rec >> 32));
-        if (z >= bthr[col]) {
-          const uint32_t slot = atomicAdd(&bcnt[col], 1u);
-          if (slot < (uint32_t)SORT_BCAP) bucket[col][slot] = (uint16_t)i;
+      // four records per thread and pass, their loads in flight together
+      for (uint32_t i0 = tid; i0 < c; i0 += 4 * 256) {
+        uint64_t rec[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t i = i0 + (uint32_t)u * 256u;
+          rec[u] = i < c ? run[i] : 0ull;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t i = i0 + (uint32_t)u * 256u;
+          const uint32_t col = (uint32_t)(rec[u] >> 16) & 31u;
+          const float z = __uint_as_float(uint32_t(rec[u] >> 32));
+          if (i < c && z >= bthr[col]) {
+            const uint32_t slot = atomicAdd(&bcnt[col], 1u);
+            if (slot < (uint32_t)SORT_BCAP) bucket[col][slot] = (uint16_t)i;
+          }
         }
       }
     }
