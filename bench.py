@@ -591,7 +591,7 @@ def main():
 
     # the scoring kernel computes the products of its first P1 sub-key chunks
     # twice (first threshold, then the final collection) and of the rest once:
-    # P1 = an eighth of the chunks from 128 chunks up, a quarter from 64, else
+    # P1 = an eighth of the chunks from 128 chunks up, a quarter from 32, else
     # half of them, all of them when k > 32 (2 sweeps); the MFMA work it
     # executes is that multiple of the algorithmic flops priced above
     search_roof = bw("score_topk")
@@ -599,7 +599,7 @@ def main():
         search_roof = dict(search_roof, candidate_records=records,
                            candidates_per_row=round(records / (T * H * 2), 2))
         nch = -(-wl.S // 64)
-        P = nch if wl.k > 32 else ((nch + 7) // 8 if nch >= 128 else (nch + 3) // 4 if nch >= 64 else (nch + 1) // 2)
+        P = nch if wl.k > 32 else ((nch + 7) // 8 if nch >= 128 else (nch + 3) // 4 if nch >= 32 else (nch + 1) // 2)
         sweeps = (nch + P) / nch
         search_roof = dict(search_roof, sweeps=round(sweeps, 4),
                            executed_TFLOPs=round(sweeps * search_roof["achieved"], 2))

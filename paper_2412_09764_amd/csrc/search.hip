@@ -30,7 +30,7 @@
 //     after each segment, the last from all rows); the first P1 chunks are
 //     then filtered against the final one (their products recomputed bitwise
 //     alike).  P1 is half of the chunks (1.5 sweeps in all), a quarter from
-//     64 chunks and an eighth from SPLIT8 chunks up.  Every score at or above
+//     32 chunks and an eighth from SPLIT8 chunks up.  Every score at or above
 //     its threshold goes, as a raw 64-bit (row | lane << 16, score) record,
 //     to the wave's candidate run (about 65 per row of 2048 at k = 32).  A
 //     tile's candidates are found with one compare per slot into a per-lane
@@ -670,12 +670,12 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
   //    candidates against the final threshold.  Every score of the top k is
   //    at or above each threshold, so every one is collected; the products
   //    over [0, P1) are computed twice, bitwise alike.  P1 = half of the
-  //    chunks (1.5 sweeps) below 64 chunks, a quarter (1.25) from 64 and an
+  //    chunks (1.5 sweeps) below 32 chunks, a quarter (1.25) from 32 and an
   //    eighth (1.125) from SPLIT8 chunks up: with fewer chunks the looser
   //    early thresholds and the extra ones cost more than the shorter first
-  //    sweep saves (measured).  With k > 32 P1 = all of them (one threshold
+  //    sweep saves, counting the candidate sort's share (measured).  With k > 32 P1 = all of them (one threshold
   //    from all rows, then one filtering sweep).
-  const int P1 = KBIG ? nch : nch >= SPLIT8 ? (nch + 7) / 8 : nch >= 64 ? (nch + 3) / 4 : (nch + 1) / 2;
+  const int P1 = KBIG ? nch : nch >= SPLIT8 ? (nch + 7) / 8 : nch >= 32 ? (nch + 3) / 4 : (nch + 1) / 2;
   auto max_collect = [&](const f32x16_t& acc, int c, int half) PK_INLINE {
     max_tile(acc, c, half);
     collect_tile(acc, c, half);

@@ -58,6 +58,7 @@ SEARCH_CASES = [
     ("bf16_S3000_d256_ragged_chunk", 3000, 2, 512, 32, 33, torch.bfloat16),
     ("bf16_S4100_quarter_first_sweep", 4100, 2, 512, 32, 45, torch.bfloat16),
     ("bf16_S4096_k24_quarter_first_sweep", 4096, 1, 256, 24, 70, torch.bfloat16),
+    ("bf16_S2050_quarter_from_32_chunks", 2050, 1, 512, 32, 41, torch.bfloat16),
     ("bf16_T1", 1024, 4, 512, 32, 1, torch.bfloat16),
     ("f32_d4_k3", 90, 2, 8, 3, 47, torch.float32),
     ("bf16_S1_k1", 1, 2, 16, 1, 70, torch.bfloat16),
