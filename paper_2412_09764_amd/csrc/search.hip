@@ -223,6 +223,83 @@ __device__ __forceinline__ h16x2_t pk_rtz(float lo, float hi) {
 __device__ __forceinline__ void pk_max_into(h16x2_t& a, h16x2_t b) {
   asm("v_pk_max_f16 %0, %0, %1" : "+v"(a) : "v"(b));
 }
+__device__ __forceinline__ h16x2_t pk_max2(h16x2_t a, h16x2_t b) {
+  h16x2_t r;
+  asm("v_pk_max_f16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ h16x2_t pk_min2(h16x2_t a, h16x2_t b) {
+  h16x2_t r;
+  asm("v_pk_min_f16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+// (max(a.lo, b.hi), max(a.hi, b.lo)) and the same with min: b's halves
+// crossed by the operand selects.
+__device__ __forceinline__ h16x2_t pk_max_x(h16x2_t a, h16x2_t b) {
+  h16x2_t r;
+  asm("v_pk_max_f16 %0, %1, %2 op_sel:[0,1] op_sel_hi:[1,0]" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ h16x2_t pk_min_x(h16x2_t a, h16x2_t b) {
+  h16x2_t r;
+  asm("v_pk_min_f16 %0, %1, %2 op_sel:[0,1] op_sel_hi:[1,0]" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+// (a.lo, b.lo)
+__device__ __forceinline__ h16x2_t pk_pack_lo(h16x2_t a, h16x2_t b) {
+  h16x2_t r;
+  asm("v_pack_b32_f16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Sorts the 32 16-bit floats of r descending, in place: afterwards r[m] holds
+// elements 2m (low half) and 2m + 1 (high half) of the order.  Two operations
+// per pair of compare-exchanges: the low halves and the high halves are
+// first sorted as two sequences of 16 by one bitonic network applied to both
+// at once; X (the low halves) followed by Y (the high halves) reversed is
+// then a bitonic sequence whose mirror pairs (element j, element 31 - j) are
+// exactly the registers (X[j], Y[j]).  Each half-cleaner step of its merge
+// keeps that form for the two halves it produces (one max and one min with
+// the second register's halves crossed per pair of registers), down to
+// groups of two, which are ordered within their register.  272 instructions
+// in all, no conversion to 32-bit floats.
+__device__ __forceinline__ void sort_desc_f16x32(h16x2_t (&r)[16]) {
+#pragma unroll
+  for (int size = 2; size <= 16; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int j = i ^ stride;
+        if (j > i) {
+          const h16x2_t mx = pk_max2(r[i], r[j]), mn = pk_min2(r[i], r[j]);
+          const bool desc = (i & size) == 0;
+          r[i] = desc ? mx : mn;
+          r[j] = desc ? mn : mx;
+        }
+      }
+    }
+  }
+  // merge: groups of G elements held as G / 2 mirror-pair registers
+  // (element j, element G - 1 - j), group g at registers g * G / 2 ...
+#pragma unroll
+  for (int G = 32; G > 2; G >>= 1) {
+    h16x2_t n[16];
+#pragma unroll
+    for (int g = 0; g < 32 / G; ++g) {
+#pragma unroll
+      for (int j = 0; j < G / 4; ++j) {
+        const h16x2_t a = r[g * (G / 2) + j], b = r[g * (G / 2) + G / 2 - 1 - j];
+        n[(2 * g) * (G / 4) + j] = pk_max_x(a, b);      // the larger half of the group
+        n[(2 * g + 1) * (G / 4) + j] = pk_min_x(a, b);  // the smaller half
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) r[i] = n[i];
+  }
+#pragma unroll
+  for (int m = 0; m < 16; ++m) r[m] = pk_pack_lo(pk_max_x(r[m], r[m]), pk_min_x(r[m], r[m]));
+}
 // The next 16-bit float below t (t holds a 16-bit float value exactly; -inf
 // stays -inf).
 __device__ __forceinline__ float f16_step_down(float t) {
@@ -519,24 +596,16 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
   // at least k distinct scores lie at or above the result (each of the k
   // groups whose rounded maximum reaches the k-th largest holds a score above
   // the value one step below it, whichever way the rounding toward zero
-  // went).  Each lane sorts its 32 (in fp32, exactly) and leaves them in LDS;
-  // the k-th largest of the two sorted runs (this lane's and lane ^ 32's) is
-  // then found by a binary search for the split between them.  The sorted
-  // maxima also go back into the packed registers (exactly): sorting moves
-  // maxima between groups, but later updates keep every value the rounded
-  // score of a row of its own, so the bound stays valid when the sweep
-  // continues afterwards.  Runs between sweeps, when the chunk buffers are
-  // free.
+  // went).  Each lane sorts its 32 in place (as 16-bit floats, two per
+  // instruction) and leaves them in LDS; the k-th largest of the two sorted
+  // runs (this lane's and lane ^ 32's) is then found by a binary search for
+  // the split between them.  Sorting moves maxima between groups, but later
+  // updates keep every value the maximum over rows of its own (each old
+  // maximum and each new row goes to exactly one register half), so the
+  // bound stays valid when the sweep continues afterwards.  Runs between
+  // sweeps, when the chunk buffers are free.
   auto kth_of_maxima = [&]() PK_INLINE -> float {
-    float mx[32];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      mx[2 * i] = (float)mxp[i].x;
-      mx[2 * i + 1] = (float)mxp[i].y;
-    }
-    sort_desc_regs<32>(mx, pinf, ninf);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) mxp[i] = pk_rtz(mx[2 * i], mx[2 * i + 1]);
+    sort_desc_f16x32(mxp);
     uint16_t* const runs = reinterpret_cast<uint16_t*>(xsmem);  // [64 * SEARCH_WAVES][32]
     uint4* const mine = reinterpret_cast<uint4*>(runs + tid * 32);
 #pragma unroll
