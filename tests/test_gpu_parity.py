@@ -456,6 +456,33 @@ def test_search_ties_but_one_needs_no_rescan(gpu_lib, k):
     np.testing.assert_array_equal(idx.cpu().numpy(), np.broadcast_to(comp, (T, H, k)))
 
 
+def test_search_gaussian_records_per_row_bounded(gpu_lib):
+    """Threshold quality on the 4M-key workload's Gaussian queries (first 4096
+    tokens): with a first sweep over a quarter of the 2048 sub-keys and
+    thresholds from 64 group maxima per row, the scoring kernel leaves about
+    96 candidate records per (token, head, half) row at k = 32 (a CPU
+    simulation of the schedule on Gaussian scores gives 96).  A threshold set
+    too low (maxima left unsorted, a step too far down) shows up as many
+    more; one set too high fails the parity tests instead.  The records are
+    counted from the per-run counts after the candidate slots in the caller's
+    workspace (layout of csrc/abi.hip)."""
+    import paper_2412_09764_amd as pk
+    wl = WORKLOADS["pk4m_d2048"]
+    from paper_2412_09764_amd.inputs import gen_queries, gen_subkeys
+    q = gen_queries(wl, "cuda", T=4096)
+    K = gen_subkeys(wl, "cuda")
+    T, H, _ = q.shape
+    grows = (T + 31) // 32 * 32 * H * 2
+    nruns = grows // 32
+    off = (grows * 256 * 8 + 255) // 256 * 256
+    ws = torch.zeros(pk.mem_search_workspace_size(T, H, wl.S, wl.k), dtype=torch.uint8, device="cuda")
+    pk.mem_search(q, K, wl.k, workspace=ws)
+    torch.cuda.synchronize()
+    per_row = int(ws[off:off + nruns * 4].view(torch.int32).sum().item()) / (T * H * 2)
+    print(f"[records] {per_row:.2f} per row", flush=True)
+    assert wl.k <= per_row <= 110, per_row
+
+
 def test_search_gaussian_rows_need_no_rescan(gpu_lib):
     """The 4M-key workload's Gaussian queries (first 4096 tokens) fit their
     candidate slots: no row goes to the rescan."""
