@@ -83,6 +83,30 @@ def test_search_integer_inputs_exact(gpu_lib, case):
     assert normwise(h64(w), ref["w"]) <= TOL_F32
 
 
+# Sub-key counts around 32, 64 and 128 chunks of 64 sub-keys (the first sweep
+# takes a half of the chunks below 32, a quarter from 32 and an eighth from
+# 128), with ragged last chunks; 8192 is the largest S.
+SCHEDULE_S = [1984, 2048, 2049, 4032, 4096, 4160, 8128, 8191, 8192]
+
+
+@pytest.mark.parametrize("k", [1, 17, 32])
+@pytest.mark.parametrize("S", SCHEDULE_S)
+def test_search_schedule_boundaries_exact(gpu_lib, S, k):
+    """Integer inputs in [-64, 64] (every score exact in fp32, few ties):
+    selection, scores and weights against the oracle at every sweep split."""
+    T, H, n = 37, 2, 32
+    print(f"[schedule] S={S} k={k}", flush=True)
+    q = int_tensor((T, H, n), 3000 + S + k, torch.bfloat16, -64, 64)
+    K = int_tensor((H, 2, S, n // 2), 4000 + S + k, torch.bfloat16, -64, 64)
+    idx, w, score, hidx = gpu_lib.mem_search(q.cuda(), K.cuda(), k, want_half=True)
+    torch.cuda.synchronize()
+    ref = oracle.search(h64(q), h64(K), k)
+    np.testing.assert_array_equal(hidx.cpu().numpy(), ref["half_idx"])
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    np.testing.assert_array_equal(h64(score), ref["score"])
+    assert normwise(h64(w), ref["w"]) <= TOL_F32
+
+
 SCORE_RANGE_CASES = [
     # (name, q range, q scale, sub-key range, sub-key scale): integer values
     # times powers of two, so every score is exact in fp32
