@@ -32,12 +32,13 @@
 //     alike).  P1 is half of the chunks (1.5 sweeps in all), a quarter from
 //     32 chunks and an eighth from SPLIT8 chunks up.  Every score at or above
 //     its threshold goes, as a raw 64-bit (row | lane << 16, score) record,
-//     to the wave's candidate run (about 65 per row of 2048 at k = 32).  A
+//     to the wave's candidate run (about 96 per row of 2048 at k = 32).  A
 //     tile's candidates are found with one compare per slot into a per-lane
-//     mask and taken out in rounds (each lane its lowest remaining slot per
-//     round, the score read back from a per-wave LDS scratch), a round's
-//     records packed across lanes, so a tile costs as many stores as the most
-//     candidates any lane has in it, and the run is written in whole lines.
+//     mask and taken out in rounds (each lane its two lowest remaining slots
+//     per round, the scores read back from a per-wave LDS scratch), a
+//     round's records packed across lanes, so a tile costs about as many
+//     stores as the most candidates any lane has in it, and the run is
+//     written in whole lines.
 //     A lane holding k records taken against the current threshold (within
 //     one pass over increasing rows) takes only scores above the lowest of
 //     them from then on (lower indices win ties), so rows of tied scores stay
@@ -694,6 +695,7 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
     }
     uint64_t m = __builtin_amdgcn_ballot_w64(msk != 0);
     if (m != 0) {  // uniform
+      taken += (uint32_t)__builtin_popcount(msk);  // every candidate becomes a record
 #pragma unroll
       for (int j = 0; j < 16; ++j) xs[j * WAVE + lane] = acc[j];
       do {  // two candidates per lane and round: their LDS reads in flight together
@@ -713,13 +715,11 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
         if (msk != 0) {
           __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{r0 + j0 + (j0 & 12u), __float_as_uint(z0)}, crs, at,
                                                 0, 0);
-          ++taken;
           lo = min_med3(lo, z0, ninf);
         }
         if (m1 != 0) {
           __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{r0 + j1 + (j1 & 12u), __float_as_uint(z1)}, crs,
                                                 at + 8u, 0, 0);
-          ++taken;
           lo = min_med3(lo, z1, ninf);
         }
         wcnt += (uint32_t)(__popcll(m) + __popcll(m2));
