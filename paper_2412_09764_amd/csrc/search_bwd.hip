@@ -29,8 +29,8 @@
 namespace pk {
 
 // Per (token, head) wave, per half: lane j holds rank j's sub-key; each lane
-// finds the leader of its sub-key group (lowest rank with the same sub-key)
-// and the group's gradient sum, in rank order.  Then
+// finds the ranks sharing its sub-key (one ballot per index bit), the lowest
+// of them leads the group and adds the group's gradients in rank order.  Then
 //   * grad_q (if wanted): the distinct sub-key rows are read QU at a time (all
 //     loads in flight together), lane l owning elements 4l..4l+3;
 //   * sort input (if wanted): row rp = (t*H + h)*2 + half gets its leaders'
@@ -74,19 +74,31 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
   const float g = okl ? gz[r * kst + lane] : 0.f;
   const float gsink = sink ? gz[r * kst + k] : 0.f;
   const uint64_t below = (1ull << lane) - 1ull;
+  const int nbits = S > 1 ? 32 - __builtin_clz((unsigned)(S - 1)) : 0;  // bits of a sub-key index
   float gh[2][4];  // with qstats: both halves' gradients with respect to qhat
 
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     const int mine = okl ? (int)(p == 0 ? ix / S : ix % S) : -1;
+    // the ranks sharing this lane's sub-key, as a mask over the wave's lanes:
+    // one ballot per bit of the sub-key index
+    uint64_t peers = __ballot(okl);
+    for (int bt = 0; bt < nbits; ++bt) {
+      const bool bit = (mine >> bt) & 1;
+      const uint64_t set = __ballot(bit);
+      peers &= bit ? set : ~set;
+    }
+    const bool leader = okl && (peers & below) == 0ull;
+    // the leader's group sum, added in rank order; every lane takes part in
+    // each exchange, the leaders keep what their own mask asks for
     float gsum = 0.f;
-    bool leader = okl;
-    for (int j = 0; j < k; ++j) {
-      const int oi = __builtin_amdgcn_readlane(mine, j);
-      const float og = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), j));
-      if (oi == mine) {
-        gsum += og;
-        if (j < lane) leader = false;
+    uint64_t pm = leader ? peers : 0ull;
+    while (__ballot(pm != 0ull) != 0ull) {
+      const int j = pm != 0ull ? __builtin_ctzll(pm) : 0;
+      const float v = __shfl(g, j, WAVE);
+      if (pm != 0ull) {
+        gsum += v;
+        pm &= pm - 1ull;
       }
     }
     if (keys) {
