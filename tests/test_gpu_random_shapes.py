@@ -113,3 +113,38 @@ def test_random_shape_extra_and_sink(gpu_lib, seed):
     # against one token's contribution to a key gradient as well
     scale = max(np.abs(s["grad_sink"]).max(), np.abs(b["grad_z"]).max() * np.abs(h64(q)).max())
     assert np.abs(h64(gs) - s["grad_sink"]).max() <= TOL_F32 * scale
+
+
+@pytest.mark.parametrize("seed", list(range(3000, 3012)))
+def test_random_large_S_search_and_backward(gpu_lib, seed):
+    """Search and search backward at random S from 1500 to 8192 (every first
+    sweep split: a half, a quarter or an eighth of the chunks, ragged last
+    chunks), random k <= 64, H, d and dtype: integer inputs in [-32, 32]
+    (scores exact in fp32), selection bit for bit and gradients within 1e-5
+    against the oracle."""
+    rng = np.random.default_rng(seed)
+    f32 = rng.random() < 0.3
+    S = int(rng.integers(1500, 8193))
+    H = int(rng.integers(1, 5))
+    d = int(rng.choice([8, 16, 32])) if f32 else int(8 * rng.integers(1, 17))
+    k = int(rng.integers(1, 65))
+    T = int(rng.integers(1, 40))
+    dt = torch.float32 if f32 else torch.bfloat16
+    n = 2 * d
+    print(f"[random large S] seed {seed}: S={S} H={H} n={n} k={k} T={T} {dt}", flush=True)
+    q = int_tensor((T, H, n), seed + 1, dt, -32, 32)
+    K = int_tensor((H, 2, S, d), seed + 2, dt, -32, 32)
+    idx, w, score, hidx = pk.mem_search(q.cuda(), K.cuda(), k, want_half=True)
+    torch.cuda.synchronize()
+    ref = oracle.search(h64(q), h64(K), k)
+    np.testing.assert_array_equal(hidx.cpu().numpy(), ref["half_idx"])
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    np.testing.assert_array_equal(h64(score), ref["score"])
+    assert normwise(h64(w), ref["w"]) <= TOL_F32
+    g = torch.Generator().manual_seed(seed + 3)
+    gz = torch.randn((T, H, k), generator=g)
+    gq, gK = pk.mem_search_backward(q.cuda(), K.cuda(), idx, gz.cuda())
+    torch.cuda.synchronize()
+    s = oracle.search_backward(h64(q), h64(K), ref["idx"], gz.double().numpy())
+    assert normwise(h64(gq), s["grad_q"]) <= TOL_F32
+    assert normwise(h64(gK), s["grad_K"]) <= TOL_F32
