@@ -979,6 +979,9 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
           qb.to_f32(fb);
         }
         const int64_t ex_safe = (ex_given >= 0 && ex_given < N) ? ex_given : 0;
+        // each lane splits its own extra index once (S * S <= 2^26 fits 32 bits)
+        const uint32_t exu = (uint32_t)ex_safe;
+        const uint32_t ex1 = exu / (uint32_t)S, ex2 = exu - ex1 * (uint32_t)S;
         const T* k1 = subkeys + (size_t)(h * 2) * S * d + qo;
         const T* k2 = k1 + (size_t)S * d;
         // eight extras at a time: their sub-key loads in flight together, then
@@ -989,9 +992,7 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const int e = e0 + j < nex ? e0 + j : nex - 1;
-            const uint64_t ie = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)ex_safe, e) |
-                                ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(ex_safe >> 32), e) << 32);
-            const int i1 = (int)(ie / (uint64_t)S), i2 = (int)(ie % (uint64_t)S);
+            const int i1 = __builtin_amdgcn_readlane((int)ex1, e), i2 = __builtin_amdgcn_readlane((int)ex2, e);
             ka[j].load(k1 + (size_t)i1 * d);
             kb[j].load(k2 + (size_t)i2 * d);
           }
