@@ -71,6 +71,9 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
   const size_t r = (size_t)t * H + h;
   const int64_t ix = lane < k ? idx[r * kst + lane] : -1;
   const bool okl = ix >= 0 && ix < (int64_t)S * S;
+  // the two sub-key indices (S * S <= 2^26: a 32-bit division)
+  const int ix1 = okl ? (int)((uint32_t)ix / (uint32_t)S) : 0;
+  const int ix2 = okl ? (int)((uint32_t)ix - (uint32_t)ix1 * (uint32_t)S) : 0;
   const float g = okl ? gz[r * kst + lane] : 0.f;
   const float gsink = sink ? gz[r * kst + k] : 0.f;
   const uint64_t below = (1ull << lane) - 1ull;
@@ -79,7 +82,7 @@ __global__ __launch_bounds__(256) void k_search_bwd_q(const T* __restrict__ q,
 
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
-    const int mine = okl ? (int)(p == 0 ? ix / S : ix % S) : -1;
+    const int mine = okl ? (p == 0 ? ix1 : ix2) : -1;
     // the ranks sharing this lane's sub-key, as a mask over the wave's lanes:
     // one ballot per bit of the sub-key index
     uint64_t peers = __ballot(okl);
