@@ -541,8 +541,10 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
   // filtering (vector ALU) runs while the other waves' products occupy the
   // matrix pipe, and the other way round.
   const bool lag = ((wave >> 2) & 1) != 0;
+  // Chunk cb must already be on its way into kbuf0 (issued once both buffers
+  // were free): the caller issues it before forming a threshold, so the load
+  // runs under that work.
   auto sweep = [&](int cb, int ce, auto&& tile_fn) PK_INLINE {
-    if (cb >= ce) return;
     f32x16_t acc;
     int pc = -1;  // lagging waves: chunk whose second tile (in acc) is pending
     auto chunk = [&](const unsigned char* buf, int c) PK_INLINE {
@@ -563,8 +565,6 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
         }
       }
     };
-    __syncthreads();  // every wave is done with the memory (threshold, last sweep)
-    issue_chunk(cb, kbuf0);
     for (int c = cb; c < ce; c += 2) {
       __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of chunk c have landed
       __syncthreads();                // ... and every wave's; kbuf1 is free
@@ -578,7 +578,7 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
       }
     }
     if (pc >= 0) tile_fn(acc, pc, 1);
-    __syncthreads();
+    __syncthreads();  // every wave is done with both buffers
   };
 
   // ---- group maxima and the threshold ---------------------------------------
@@ -749,11 +749,14 @@ __global__ __launch_bounds__(64 * SEARCH_WAVES, 4) void k_score_topk(
     max_tile(acc, c, half);
     collect_tile(acc, c, half);
   };
+  issue_chunk(0, kbuf0);
   sweep(0, P1, max_tile);
+  issue_chunk(P1 < nch ? P1 : 0, kbuf0);  // the next sweep's first chunk, under the threshold
   set_threshold(kth_of_maxima(), true);
   for (int lo_c = P1; lo_c < nch;) {
     const int hi_c = 2 * lo_c < nch ? 2 * lo_c : nch;
     sweep(lo_c, hi_c, max_collect);
+    issue_chunk(hi_c < nch ? hi_c : 0, kbuf0);
     set_threshold(kth_of_maxima(), hi_c >= nch);  // the last: sweep 3 restarts at row 0
     lo_c = hi_c;
   }
