@@ -821,44 +821,64 @@ __global__ __launch_bounds__(256) void k_topk_sort(const uint64_t* __restrict__ 
       }
     }
     __syncthreads();
-    for (int col = wave; col < 32; col += 4) {
-      const int64_t t = tok0 + col;
-      if (t >= ntok) break;  // the same for the whole wave
-      const size_t r = ((size_t)t * H + h) * 2 + p;
+    auto key_at = [&](int col, uint32_t n, uint32_t x) PK_INLINE -> uint64_t {
+      if (x >= n) return 0ull;
+      const uint64_t rec = run[bucket[col][x]];
+      return make_key(__uint_as_float(uint32_t(rec >> 32)), (uint32_t)rec & 0xFFFFu);
+    };
+    auto write_top = [&](size_t r, uint64_t top) PK_INLINE {
+      if (lane < k) {
+        half_idx[r * k + lane] = (int32_t)key_index(top);
+        half_score[r * k + lane] = key_score(top);
+      }
+    };
+    auto row_of = [&](int col) PK_INLINE { return ((size_t)(tok0 + col) * H + h) * 2 + p; };
+    // one token: its records sorted 64, 128 or 256 wide, or the rescan list
+    auto one = [&](int col) PK_INLINE {
+      const size_t r = row_of(col);
       const uint32_t n = bcnt[col];
       if (c > RUN || n > (uint32_t)SORT_BCAP) {
         if (lane == 0) {
           const uint32_t slot = atomicAdd(&ovf[0], 1u);
           ovf[1 + slot] = (uint32_t)r;
         }
-        continue;
+        return;
       }
-      auto key_at = [&](uint32_t x) -> uint64_t {
-        if (x >= n) return 0ull;
-        const uint64_t rec = run[bucket[col][x]];
-        return make_key(__uint_as_float(uint32_t(rec >> 32)), (uint32_t)rec & 0xFFFFu);
-      };
-      uint64_t top;
       if (n <= (uint32_t)WAVE) {
-        uint64_t v[1] = {key_at((uint32_t)lane)};
+        uint64_t v[1] = {key_at(col, n, (uint32_t)lane)};
         wave_sort_desc<1>(v, lane);
-        top = v[0];
+        write_top(r, v[0]);
       } else if (n <= 2u * WAVE) {
         uint64_t v[2];
 #pragma unroll
-        for (int e = 0; e < 2; ++e) v[e] = key_at((uint32_t)(lane + e * WAVE));
+        for (int e = 0; e < 2; ++e) v[e] = key_at(col, n, (uint32_t)(lane + e * WAVE));
         wave_sort_desc<2>(v, lane);
-        top = v[0];
+        write_top(r, v[0]);
       } else {
         uint64_t v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = key_at((uint32_t)(lane + e * WAVE));
+        for (int e = 0; e < 4; ++e) v[e] = key_at(col, n, (uint32_t)(lane + e * WAVE));
         wave_sort_desc<4>(v, lane);
-        top = v[0];
+        write_top(r, v[0]);
       }
-      if (lane < k) {
-        half_idx[r * k + lane] = (int32_t)key_index(top);
-        half_score[r * k + lane] = key_score(top);
+    };
+    // Tokens col and col + 4 per pass: when both keep at most 64 records (the
+    // usual case), their reads and their two sorts run side by side.
+    for (int col = wave; col < 32; col += 8) {
+      if (tok0 + col >= ntok) break;  // the same for the whole wave
+      const int colB = col + 4;
+      const bool hasB = tok0 + colB < ntok;
+      const uint32_t nA = bcnt[col], nB = hasB ? bcnt[colB] : 0u;
+      if (c <= RUN && hasB && nA <= (uint32_t)WAVE && nB <= (uint32_t)WAVE) {
+        uint64_t va[1] = {key_at(col, nA, (uint32_t)lane)};
+        uint64_t vb[1] = {key_at(colB, nB, (uint32_t)lane)};
+        wave_sort_desc<1>(va, lane);
+        wave_sort_desc<1>(vb, lane);
+        write_top(row_of(col), va[0]);
+        write_top(row_of(colB), vb[0]);
+      } else {
+        one(col);
+        if (hasB) one(colB);
       }
     }
     __syncthreads();  // the buckets are reused by the next run
