@@ -981,6 +981,53 @@ __global__ __launch_bounds__(256) void k_cartesian(const int32_t* __restrict__ h
   constexpr bool EXTRA = MODE != 0;
   const int nsc = EXTRA ? nex + (sink_part ? 1 : 0) : 0;  // full keys scored per row
   const int kk = k + nsc;                             // slots per row
+  if constexpr (!EXTRA) {
+    // Two rows per pass (this wave's next grid-stride row beside it): their
+    // loads, their candidate keys and their two sorts run side by side.
+    auto build = [&](int64_t row, uint64_t (&v)[E]) PK_INLINE {
+      const int32_t* i1 = half_idx + (size_t)row * 2 * k;
+      const float* s1 = half_score + (size_t)row * 2 * k;
+      const float s1v = lane < k ? s1[lane] : 0.f;
+      const float s2v = lane < k ? s1[k + lane] : 0.f;
+      const int i1v = lane < k ? i1[lane] : 0;
+      const int i2v = lane < k ? i1[k + lane] : 0;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int m = e * WAVE + lane;
+        const uint32_t pr = pairs[m < npairs ? m : 0];
+        const int a = (int)(pr >> 16), b = (int)(pr & 0xFFFFu);
+        const float sa = __shfl(s1v, a, WAVE), sb = __shfl(s2v, b, WAVE);
+        const int ia = __shfl(i1v, a, WAVE), ib = __shfl(i2v, b, WAVE);
+        v[e] = m < npairs ? make_key(sa + sb, (uint32_t)ia * (uint32_t)S + (uint32_t)ib) : 0ull;
+      }
+    };
+    auto finish = [&](int64_t row, const uint64_t (&v)[E]) PK_INLINE {
+      const float z = key_score(v[0]);
+      const int64_t ci = (int64_t)key_index(v[0]);
+      const float zmax = __shfl(z, 0, WAVE);
+      const float ex = lane < k ? expf(z - zmax) : 0.f;
+      const float sum = group_sum<WAVE>(ex);
+      if (lane < k) {
+        const size_t o = (size_t)row * k + lane;
+        idx_out[o] = ci;
+        w_out[o] = ex / sum;
+        if (score_out) score_out[o] = z;
+      }
+    };
+    const int64_t stride = (int64_t)gridDim.x * 4;
+    for (int64_t row = (int64_t)blockIdx.x * 4 + wave; row < rows; row += 2 * stride) {
+      const bool two = row + stride < rows;             // the same for the whole wave
+      const int64_t row2 = two ? row + stride : row;  // a repeated row is sorted, not written
+      uint64_t va[E], vb[E];
+      build(row, va);
+      build(row2, vb);
+      wave_sort_desc<E>(va, lane);
+      wave_sort_desc<E>(vb, lane);
+      finish(row, va);
+      if (two) finish(row2, vb);
+    }
+    return;
+  }
   for (int64_t row = (int64_t)blockIdx.x * 4 + wave; row < rows; row += (int64_t)gridDim.x * 4) {
     // extra pairs first: their loads overlap the candidate sort below
     float ex_score = 0.f;
